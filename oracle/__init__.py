@@ -1,0 +1,137 @@
+"""CPU oracle of the LAMB (Algorithm 2) and LARS (Algorithm 1) steps.
+
+TEST INFRASTRUCTURE ONLY: the test suite, ``__graft_entry__.smoke()`` and the
+CPU-baseline leg of ``bench.py`` are the only users. It imports nothing from
+the HIP library package and shares no code with it. The arithmetic lives in
+``lamb_oracle.c`` (plain C, double); this module only marshals numpy arrays.
+
+Inputs are lists of per-tensor numpy arrays: x, m, v are float32 and updated
+in place; g is float32, or uint16 holding bf16 bit patterns.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from typing import Optional, Sequence
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+SOURCE = os.path.join(HERE, "lamb_oracle.c")
+LIBRARY = os.path.join(HERE, "liblamb_oracle.so")
+
+CFLAGS = ["-O2", "-std=c11", "-fno-fast-math", "-ffp-contract=off", "-fPIC", "-shared"]
+
+
+def build(source: str = SOURCE, output: str = LIBRARY) -> str:
+    """Compile the oracle with gcc (single-threaded, no fast-math, no FMA contraction)."""
+    tmp = output + ".tmp%d" % os.getpid()
+    subprocess.check_call(["gcc", *CFLAGS, source, "-o", tmp, "-lm"])
+    os.replace(tmp, output)
+    return output
+
+
+_DP = ctypes.POINTER(ctypes.c_double)
+
+
+def _ptr(a: np.ndarray) -> ctypes.c_void_p:
+    return ctypes.c_void_p(a.ctypes.data)
+
+
+def _check_state(a: np.ndarray, n: int, what: str) -> None:
+    if a.dtype != np.float32 or not a.flags.c_contiguous or not a.flags.writeable:
+        raise TypeError("%s must be a writeable contiguous float32 array" % what)
+    if a.size != n:
+        raise ValueError("%s has %d elements, expected %d" % (what, a.size, n))
+
+
+def _grad_kind(g: np.ndarray, n: int) -> int:
+    if not g.flags.c_contiguous or g.size != n:
+        raise ValueError("gradient must be contiguous with %d elements" % n)
+    if g.dtype == np.float32:
+        return 0
+    if g.dtype == np.uint16:
+        return 1
+    raise TypeError("gradient dtype must be float32 or uint16 (bf16 bits)")
+
+
+class Oracle:
+    """Handle on one compiled oracle library (the default one, or a test variant)."""
+
+    def __init__(self, path: str = LIBRARY):
+        self.path = path
+        lib = ctypes.CDLL(path)
+        lib.oracle_lamb_layer.restype = ctypes.c_int
+        lib.oracle_lamb_layer.argtypes = [
+            ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int,
+            ctypes.c_void_p, ctypes.c_void_p,
+            ctypes.c_double, ctypes.c_double, ctypes.c_double, ctypes.c_double,
+            ctypes.c_double, ctypes.c_int, ctypes.c_double, ctypes.c_double,
+            ctypes.c_int64, ctypes.c_int, _DP]
+        lib.oracle_lars_layer.restype = ctypes.c_int
+        lib.oracle_lars_layer.argtypes = [
+            ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int,
+            ctypes.c_void_p, ctypes.c_double, ctypes.c_double, ctypes.c_double,
+            ctypes.c_int, ctypes.c_double, ctypes.c_double, ctypes.c_double, _DP]
+        self._lib = lib
+
+    def lamb_step(self, xs: Sequence[np.ndarray], gs: Sequence[np.ndarray],
+                  ms: Sequence[np.ndarray], vs: Sequence[np.ndarray],
+                  wd_mask: Sequence[bool], *, lr: float, beta1: float, beta2: float,
+                  eps: float, weight_decay: float, gamma_l: float, gamma_u: float,
+                  step: int, bias_correction: bool = True) -> np.ndarray:
+        """One LAMB step over every block; returns (n, 3) [ratio, ||x||, ||u||]."""
+        n = len(xs)
+        out = np.zeros((n, 3), dtype=np.float64)
+        for i in range(n):
+            d = xs[i].size
+            _check_state(xs[i], d, "x[%d]" % i)
+            _check_state(ms[i], d, "m[%d]" % i)
+            _check_state(vs[i], d, "v[%d]" % i)
+            kind = _grad_kind(gs[i], d)
+            res = out[i]
+            rc = self._lib.oracle_lamb_layer(
+                d, _ptr(xs[i]), _ptr(gs[i]), kind, _ptr(ms[i]), _ptr(vs[i]),
+                lr, beta1, beta2, eps, weight_decay, int(bool(wd_mask[i])),
+                gamma_l, gamma_u, int(step), int(bool(bias_correction)),
+                res.ctypes.data_as(_DP))
+            if rc != 0:
+                raise RuntimeError("oracle_lamb_layer failed on tensor %d (%d)" % (i, rc))
+        return out
+
+    def lars_step(self, xs: Sequence[np.ndarray], gs: Sequence[np.ndarray],
+                  ms: Sequence[np.ndarray], wd_mask: Sequence[bool], *, lr: float,
+                  momentum: float, weight_decay: float, gamma_l: float, gamma_u: float,
+                  trust_coef: float) -> np.ndarray:
+        """One LARS step over every block; returns (n, 3) [ratio, ||x||, ||m||]."""
+        n = len(xs)
+        out = np.zeros((n, 3), dtype=np.float64)
+        for i in range(n):
+            d = xs[i].size
+            _check_state(xs[i], d, "x[%d]" % i)
+            _check_state(ms[i], d, "m[%d]" % i)
+            kind = _grad_kind(gs[i], d)
+            res = out[i]
+            rc = self._lib.oracle_lars_layer(
+                d, _ptr(xs[i]), _ptr(gs[i]), kind, _ptr(ms[i]), lr, momentum,
+                weight_decay, int(bool(wd_mask[i])), gamma_l, gamma_u, trust_coef,
+                res.ctypes.data_as(_DP))
+            if rc != 0:
+                raise RuntimeError("oracle_lars_layer failed on tensor %d (%d)" % (i, rc))
+        return out
+
+
+_default: Optional[Oracle] = None
+
+
+def load() -> Oracle:
+    """The oracle built from ``lamb_oracle.c`` (compiled here first if missing or stale)."""
+    global _default
+    if _default is None:
+        if (not os.path.exists(LIBRARY)
+                or os.path.getmtime(LIBRARY) < os.path.getmtime(SOURCE)):
+            build()
+        _default = Oracle(LIBRARY)
+    return _default

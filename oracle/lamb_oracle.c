@@ -1,0 +1,191 @@
+/*
+ * CPU oracle for one LAMB step and one LARS step.
+ *
+ * You, Li, Reddi, Hseu, Kumar, Bhojanapalli, Song, Demmel, Keutzer, Hsieh:
+ * "Large Batch Optimization for Deep Learning: Training BERT in 76 minutes",
+ * ICLR 2020 (arXiv:1904.00962).
+ *
+ * TEST INFRASTRUCTURE ONLY. This file is the reference the HIP library is
+ * checked against; it is not part of the product. Only the test suite, the
+ * smoke check and the CPU-baseline leg of the benchmark may load it. It shares
+ * no code, header, table or helper with the HIP library, and it includes
+ * nothing from it.
+ *
+ * Plain single-threaded C. Every quantity of the method is computed in
+ * double; inputs are widened exactly (fp32 -> double, bf16 -> fp32 -> double)
+ * and each stored value (x, m, v) is rounded to fp32 once per step, with the
+ * C conversion's round-to-nearest-even. One call handles one layer block
+ * x^(i) (Section 2, Notation): blocks never interact within a step, so a
+ * multi-tensor step is a loop over blocks in any order.
+ *
+ * Readings of the paper taken here (the paper is silent or ambiguous):
+ *  - m_hat and v_hat of Algorithm 2 are temporaries; the stored moments stay
+ *    uncorrected (Appendix E names the division "adam-correction", as in
+ *    Adam, where the corrected values are not stored).
+ *  - epsilon is added after the square root of the bias-corrected v_hat.
+ *  - the weight-decay term lambda * x uses the pre-update x_t, and lambda is
+ *    replaced by 0 for blocks whose mask is 0 (biases and norm parameters).
+ *  - a zero update norm (||r + lambda x|| = 0, or ||m|| = 0 for LARS) means
+ *    every element of the update is 0: the step leaves x unchanged and the
+ *    reported trust ratio is 0. Any other norm, NaN included, is divided by
+ *    as written, so NaN and Inf propagate by IEEE rules.
+ *  - phi(z) = min(max(z, gamma_l), gamma_u) (Section 3), evaluated with
+ *    comparisons so that a NaN norm stays NaN.
+ *  - LARS: the trust coefficient kappa multiplies phi (kappa = 1 is
+ *    Algorithm 1 exactly); the epsilon listed among Algorithm 1's inputs is
+ *    never used by the algorithm and is not taken here.
+ *
+ * Parity is pinned by the closed forms, invariants and hand-worked examples
+ * in the test suite; no function here is unpinned.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define ORACLE_OK 0
+#define ORACLE_EINVAL (-1)
+#define ORACLE_ENOMEM (-2)
+
+/* Exact widening of a bf16 bit pattern: it is the high half of an fp32. */
+static double widen_bf16(uint16_t bits)
+{
+    uint32_t word = (uint32_t)bits << 16;
+    float f;
+    memcpy(&f, &word, sizeof f);
+    return (double)f;
+}
+
+static double gradient_at(const void *g, int g_is_bf16, int64_t j)
+{
+    if (g_is_bf16)
+        return widen_bf16(((const uint16_t *)g)[j]);
+    return (double)((const float *)g)[j];
+}
+
+/* Round a double to the fp32 stored state (round to nearest, ties to even). */
+static float store_f32(double a)
+{
+    return (float)a;
+}
+
+/* Section 3: phi(z) = min{max{z, gamma_l}, gamma_u}. */
+static double phi(double z, double gamma_l, double gamma_u)
+{
+    double p = z;
+    if (p < gamma_l)
+        p = gamma_l;
+    if (p > gamma_u)
+        p = gamma_u;
+    return p;
+}
+
+/*
+ * One LAMB step (Algorithm 2) on one layer block of d elements.
+ *
+ *   m_t   = beta1 m_{t-1} + (1 - beta1) g_t
+ *   v_t   = beta2 v_{t-1} + (1 - beta2) g_t^2
+ *   m_hat = m_t / (1 - beta1^t),  v_hat = v_t / (1 - beta2^t)
+ *   r_t   = m_hat / (sqrt(v_hat) + eps)
+ *   u     = r_t + lambda x_t
+ *   x_{t+1} = x_t - eta_t phi(||x_t||) / ||u|| * u
+ *
+ * bias_correction = 0 drops the two divisions (Appendix E).
+ * x, m, v are updated in place; g is fp32 or, with g_is_bf16, bf16 bits.
+ * out[0] = trust ratio phi(||x_t||)/||u||, out[1] = ||x_t||, out[2] = ||u||.
+ */
+int oracle_lamb_layer(int64_t d, float *x, const void *g, int g_is_bf16,
+                      float *m, float *v,
+                      double lr, double beta1, double beta2, double eps,
+                      double weight_decay, int wd, double gamma_l,
+                      double gamma_u, int64_t t, int bias_correction,
+                      double *out)
+{
+    if (d < 1 || !x || !g || !m || !v || !out || t < 1)
+        return ORACLE_EINVAL;
+    double *u = (double *)malloc((size_t)d * sizeof(double));
+    if (!u)
+        return ORACLE_ENOMEM;
+
+    double c1 = 1.0, c2 = 1.0;
+    if (bias_correction) {
+        c1 = 1.0 - pow(beta1, (double)t);
+        c2 = 1.0 - pow(beta2, (double)t);
+    }
+    double lam = wd ? weight_decay : 0.0;
+
+    double sum_xx = 0.0, sum_uu = 0.0;
+    for (int64_t j = 0; j < d; ++j) {
+        double gj = gradient_at(g, g_is_bf16, j);
+        double xj = (double)x[j];
+        double mj = beta1 * (double)m[j] + (1.0 - beta1) * gj;
+        double vj = beta2 * (double)v[j] + (1.0 - beta2) * (gj * gj);
+        double m_hat = mj / c1;
+        double v_hat = vj / c2;
+        double r = m_hat / (sqrt(v_hat) + eps);
+        u[j] = r + lam * xj;
+        sum_xx += xj * xj;
+        sum_uu += u[j] * u[j];
+        m[j] = store_f32(mj);
+        v[j] = store_f32(vj);
+    }
+
+    double norm_x = sqrt(sum_xx);
+    double norm_u = sqrt(sum_uu);
+    double ratio = (norm_u == 0.0) ? 0.0 : phi(norm_x, gamma_l, gamma_u) / norm_u;
+    for (int64_t j = 0; j < d; ++j)
+        x[j] = store_f32((double)x[j] - lr * ratio * u[j]);
+
+    out[0] = ratio;
+    out[1] = norm_x;
+    out[2] = norm_u;
+    free(u);
+    return ORACLE_OK;
+}
+
+/*
+ * One LARS step (Algorithm 1) on one layer block of d elements.
+ *
+ *   m_t     = beta1 m_{t-1} + (1 - beta1) (g_t + lambda x_t)
+ *   x_{t+1} = x_t - eta_t kappa phi(||x_t||) / ||m_t|| * m_t
+ *
+ * x and m are updated in place. out[0] = trust ratio kappa phi/||m_t||,
+ * out[1] = ||x_t||, out[2] = ||m_t||.
+ */
+int oracle_lars_layer(int64_t d, float *x, const void *g, int g_is_bf16,
+                      float *m, double lr, double beta1, double weight_decay,
+                      int wd, double gamma_l, double gamma_u,
+                      double trust_coef, double *out)
+{
+    if (d < 1 || !x || !g || !m || !out)
+        return ORACLE_EINVAL;
+    double *mt = (double *)malloc((size_t)d * sizeof(double));
+    if (!mt)
+        return ORACLE_ENOMEM;
+
+    double lam = wd ? weight_decay : 0.0;
+    double sum_xx = 0.0, sum_mm = 0.0;
+    for (int64_t j = 0; j < d; ++j) {
+        double gj = gradient_at(g, g_is_bf16, j);
+        double xj = (double)x[j];
+        mt[j] = beta1 * (double)m[j] + (1.0 - beta1) * (gj + lam * xj);
+        sum_xx += xj * xj;
+        sum_mm += mt[j] * mt[j];
+    }
+
+    double norm_x = sqrt(sum_xx);
+    double norm_m = sqrt(sum_mm);
+    double ratio = (norm_m == 0.0)
+                       ? 0.0
+                       : trust_coef * phi(norm_x, gamma_l, gamma_u) / norm_m;
+    for (int64_t j = 0; j < d; ++j) {
+        x[j] = store_f32((double)x[j] - lr * ratio * mt[j]);
+        m[j] = store_f32(mt[j]);
+    }
+
+    out[0] = ratio;
+    out[1] = norm_x;
+    out[2] = norm_m;
+    free(mt);
+    return ORACLE_OK;
+}

@@ -1,0 +1,240 @@
+"""Seeded synthetic parameter sets shaped like the paper's workloads.
+
+This module only draws inputs: tensor shapes, weight-decay masks, initial
+parameters x and gradients g. It holds none of the optimizer's arithmetic and
+imports nothing from the HIP library or from the oracle, so both sides of a
+parity test can take their inputs from it.
+
+The paper trains BERT (Section 4.1) and ResNet-50 on ImageNet (Section 4.2);
+an optimizer step only reads parameter, gradient and state tensors, so these
+sets keep the models' parameter shapes and replace values with i.i.d.
+Gaussians: x ~ N(0, sigma_x) and g ~ N(0, 1e-3) (second argument = standard
+deviation). Moments start at zero, as Algorithms 1 and 2 set m_0 = v_0 = 0.
+
+Seeds: x uses ``1000 * cfg``; the gradient of step t uses ``1000 * cfg + t``.
+Values are drawn tensor by tensor in canonical order with torch's CPU
+generator in fp32; bf16 gradients are the round-to-nearest-even cast of the
+fp32 draw, handed out as their raw uint16 bit patterns.
+"""
+
+from __future__ import annotations
+
+import dataclasses
+from typing import List, Sequence, Tuple
+
+import numpy as np
+
+Shape = Tuple[int, ...]
+
+
+@dataclasses.dataclass(frozen=True)
+class TensorSpec:
+    name: str
+    shape: Shape
+    wd: bool  # decoupled weight decay applies (False for biases and norms)
+
+    @property
+    def numel(self) -> int:
+        n = 1
+        for s in self.shape:
+            n *= s
+        return n
+
+
+@dataclasses.dataclass(frozen=True)
+class ParamSet:
+    cfg: int
+    name: str
+    tensors: Tuple[TensorSpec, ...]
+    sigma_x: float
+    sigma_g: float
+    g_dtype: str  # "f32" or "bf16"
+    # LAMB hyperparameters (defaults follow Section 4 / Appendix H)
+    lr: float
+    beta1: float
+    beta2: float
+    eps: float
+    weight_decay: float
+    gamma_l: float
+    gamma_u: float
+    # LARS hyperparameters (used where the workload is run with LARS)
+    lars_lr: float = 1e-3
+    lars_momentum: float = 0.9
+    lars_trust_coef: float = 1e-3
+
+    @property
+    def numel(self) -> int:
+        return sum(t.numel for t in self.tensors)
+
+    @property
+    def n_tensors(self) -> int:
+        return len(self.tensors)
+
+    def numels(self) -> List[int]:
+        return [t.numel for t in self.tensors]
+
+    def wd_mask(self) -> List[bool]:
+        return [t.wd for t in self.tensors]
+
+
+def _linear(prefix: str, out_f: int, in_f: int, bias: bool = True) -> List[TensorSpec]:
+    specs = [TensorSpec(prefix + ".weight", (out_f, in_f), True)]
+    if bias:
+        specs.append(TensorSpec(prefix + ".bias", (out_f,), False))
+    return specs
+
+
+def _norm(prefix: str, width: int) -> List[TensorSpec]:
+    return [TensorSpec(prefix + ".gamma", (width,), False),
+            TensorSpec(prefix + ".beta", (width,), False)]
+
+
+def tiny_tensors() -> List[TensorSpec]:
+    shapes = [(256, 256), (256,), (256, 1024), (1024,), (1024, 256), (256,), (64, 256), (256,)]
+    return [TensorSpec("t%d" % i, s, len(s) > 1) for i, s in enumerate(shapes)]
+
+
+def bert_tensors(hidden: int, ffn: int, layers: int, vocab: int = 30522,
+                 positions: int = 512, types: int = 2) -> List[TensorSpec]:
+    """BERT encoder parameter list: embeddings, encoder layers, pooler."""
+    t: List[TensorSpec] = [
+        TensorSpec("emb.token", (vocab, hidden), True),
+        TensorSpec("emb.position", (positions, hidden), True),
+        TensorSpec("emb.type", (types, hidden), True),
+    ]
+    t += _norm("emb.ln", hidden)
+    for i in range(layers):
+        p = "layer%d." % i
+        for proj in ("q", "k", "v", "o"):
+            t += _linear(p + proj, hidden, hidden)
+        t += _norm(p + "ln1", hidden)
+        t.append(TensorSpec(p + "ffn_in.weight", (hidden, ffn), True))
+        t.append(TensorSpec(p + "ffn_in.bias", (ffn,), False))
+        t.append(TensorSpec(p + "ffn_out.weight", (ffn, hidden), True))
+        t.append(TensorSpec(p + "ffn_out.bias", (hidden,), False))
+        t += _norm(p + "ln2", hidden)
+    t += _linear("pooler", hidden, hidden)
+    return t
+
+
+def resnet50_tensors() -> List[TensorSpec]:
+    """ResNet-50 (bottleneck v1) convolution, batch-norm and classifier tensors."""
+    t: List[TensorSpec] = [TensorSpec("stem.conv", (64, 3, 7, 7), True)]
+    t += _norm("stem.bn", 64)
+    c_in = 64
+    for s, (w, n) in enumerate([(64, 3), (128, 4), (256, 6), (512, 3)]):
+        for b in range(n):
+            p = "stage%d.block%d." % (s + 1, b)
+            t.append(TensorSpec(p + "conv1", (w, c_in, 1, 1), True))
+            t += _norm(p + "bn1", w)
+            t.append(TensorSpec(p + "conv2", (w, w, 3, 3), True))
+            t += _norm(p + "bn2", w)
+            t.append(TensorSpec(p + "conv3", (4 * w, w, 1, 1), True))
+            t += _norm(p + "bn3", 4 * w)
+            if b == 0:
+                t.append(TensorSpec(p + "proj", (4 * w, c_in, 1, 1), True))
+                t += _norm(p + "proj_bn", 4 * w)
+            c_in = 4 * w
+    t += _linear("fc", 1000, 2048)
+    return t
+
+
+def gpt_tensors(hidden: int = 1600, ffn: int = 6400, layers: int = 48,
+                vocab: int = 50257, positions: int = 1024) -> List[TensorSpec]:
+    """Decoder-only transformer with a fused QKV projection (1.5B at defaults)."""
+    t: List[TensorSpec] = [
+        TensorSpec("emb.token", (vocab, hidden), True),
+        TensorSpec("emb.position", (positions, hidden), True),
+    ]
+    for i in range(layers):
+        p = "layer%d." % i
+        t += _norm(p + "ln1", hidden)
+        t.append(TensorSpec(p + "qkv.weight", (hidden, 3 * hidden), True))
+        t.append(TensorSpec(p + "qkv.bias", (3 * hidden,), False))
+        t += _linear(p + "o", hidden, hidden)
+        t += _norm(p + "ln2", hidden)
+        t.append(TensorSpec(p + "ffn_in.weight", (hidden, ffn), True))
+        t.append(TensorSpec(p + "ffn_in.bias", (ffn,), False))
+        t.append(TensorSpec(p + "ffn_out.weight", (ffn, hidden), True))
+        t.append(TensorSpec(p + "ffn_out.bias", (hidden,), False))
+    t += _norm("final_ln", hidden)
+    return t
+
+
+_COMMON = dict(beta1=0.9, beta2=0.999, eps=1e-6, weight_decay=0.01, gamma_l=0.0, gamma_u=10.0)
+
+CONFIGS = {
+    0: ParamSet(0, "tiny", tuple(tiny_tensors()), 0.02, 1e-3, "f32", lr=1e-3, **_COMMON),
+    1: ParamSet(1, "bert-base", tuple(bert_tensors(768, 3072, 12)), 0.02, 1e-3, "f32",
+                lr=1e-3, **_COMMON),
+    2: ParamSet(2, "bert-large", tuple(bert_tensors(1024, 4096, 24)), 0.02, 1e-3, "bf16",
+                lr=6e-3, **_COMMON),
+    3: ParamSet(3, "resnet50", tuple(resnet50_tensors()), 0.05, 1e-3, "f32", lr=1e-3,
+                lars_lr=1e-3, lars_momentum=0.9, lars_trust_coef=1e-3, **_COMMON),
+    4: ParamSet(4, "gpt-1.5b", tuple(gpt_tensors()), 0.02, 1e-3, "bf16", lr=6e-3, **_COMMON),
+}
+
+
+def get(cfg: int) -> ParamSet:
+    return CONFIGS[cfg]
+
+
+def _torch():
+    import torch  # local import: shape queries need no torch
+    return torch
+
+
+def draw_params(ps: ParamSet, indices: Sequence[int] | None = None) -> List[np.ndarray]:
+    """Initial x for every tensor (or the listed ones), fp32, seed 1000*cfg.
+
+    Tensors are always drawn in canonical order from one generator, so a
+    tensor's values do not depend on which subset is requested.
+    """
+    torch = _torch()
+    gen = torch.Generator().manual_seed(1000 * ps.cfg)
+    want = set(range(ps.n_tensors)) if indices is None else set(indices)
+    out: List[np.ndarray] = []
+    for i, spec in enumerate(ps.tensors):
+        a = torch.randn(spec.numel, generator=gen, dtype=torch.float32)
+        if i in want:
+            out.append((a * ps.sigma_x).numpy())
+    return out
+
+
+def draw_grads(ps: ParamSet, step: int, indices: Sequence[int] | None = None) -> List[np.ndarray]:
+    """Gradient of step ``step`` (>= 1): fp32 arrays, or bf16 bit patterns (uint16)."""
+    torch = _torch()
+    gen = torch.Generator().manual_seed(1000 * ps.cfg + step)
+    want = set(range(ps.n_tensors)) if indices is None else set(indices)
+    out: List[np.ndarray] = []
+    for i, spec in enumerate(ps.tensors):
+        a = torch.randn(spec.numel, generator=gen, dtype=torch.float32)
+        if i in want:
+            a = a * ps.sigma_g
+            if ps.g_dtype == "bf16":
+                out.append(a.to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16))
+            else:
+                out.append(a.numpy())
+    return out
+
+
+def bf16_bits_to_f32(bits: np.ndarray) -> np.ndarray:
+    """Exact widening of bf16 bit patterns to fp32 (for building test inputs)."""
+    return (bits.astype(np.uint32) << 16).view(np.float32)
+
+
+def f32_to_bf16_bits(a: np.ndarray) -> np.ndarray:
+    """Round-to-nearest-even cast of fp32 values to bf16 bit patterns."""
+    torch = _torch()
+    t = torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32))
+    return t.to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+
+
+def random_case(rng: np.random.Generator, numels: Sequence[int], sigma_x: float = 0.02,
+                sigma_g: float = 1e-3, g_dtype: str = "f32"):
+    """Small ad-hoc case for edge tests: (x list, g list) drawn from ``rng``."""
+    xs = [(rng.standard_normal(n) * sigma_x).astype(np.float32) for n in numels]
+    gs = [(rng.standard_normal(n) * sigma_g).astype(np.float32) for n in numels]
+    if g_dtype == "bf16":
+        gs = [f32_to_bf16_bits(g) for g in gs]
+    return xs, gs

@@ -1,0 +1,102 @@
+"""The pins are strong enough: every planted slip in the oracle is caught.
+
+Each mutant is a copy of ``oracle/lamb_oracle.c`` with one textual edit (a
+dropped term, a wrong sign, coefficient or exponent, swapped operands, a
+missing clamp branch, ...). It is compiled into a temporary library and run
+against every pin; at least one pin must fail. Mistakes are planted only in
+this CPU-side copy, never in the shipped oracle or on a GPU.
+"""
+
+import os
+import shutil
+
+import pytest
+
+import oracle
+import oracle_pins
+
+# (name, original text, replacement, which occurrence: 0 = first, 1 = second)
+MUTANTS = [
+    ("lamb_m_no_dampening", "+ (1.0 - beta1) * gj;", "+ gj;", 0),
+    ("lamb_v_uses_beta1", "double vj = beta2 * (double)v[j] + (1.0 - beta2)",
+     "double vj = beta1 * (double)v[j] + (1.0 - beta1)", 0),
+    ("lamb_v_abs_not_square", "(gj * gj)", "fabs(gj)", 0),
+    ("lamb_c1_exponent_plus_one", "pow(beta1, (double)t)", "pow(beta1, (double)(t + 1))", 0),
+    ("lamb_c2_exponent_plus_one", "pow(beta2, (double)t)", "pow(beta2, (double)(t + 1))", 0),
+    ("lamb_c1_c2_swapped", "double m_hat = mj / c1;", "double m_hat = mj / c2;", 0),
+    ("lamb_no_m_correction", "double m_hat = mj / c1;", "double m_hat = mj;", 0),
+    ("lamb_no_v_correction", "double v_hat = vj / c2;", "double v_hat = vj;", 0),
+    ("lamb_eps_inside_sqrt", "(sqrt(v_hat) + eps)", "sqrt(v_hat + eps)", 0),
+    ("lamb_eps_dropped", "(sqrt(v_hat) + eps)", "(sqrt(v_hat))", 0),
+    ("lamb_eps_before_correction", "double r = m_hat / (sqrt(v_hat) + eps);",
+     "double r = (mj / (sqrt(vj) + eps)) / c1 * sqrt(c2);", 0),
+    ("lamb_lambda_dropped", "u[j] = r + lam * xj;", "u[j] = r;", 0),
+    ("lamb_lambda_sign", "u[j] = r + lam * xj;", "u[j] = r - lam * xj;", 0),
+    ("lamb_mask_ignored", "double lam = wd ? weight_decay : 0.0;",
+     "double lam = weight_decay;", 0),
+    ("lamb_norm_of_r", "sum_uu += u[j] * u[j];", "sum_uu += r * r;", 0),
+    ("lamb_phi_of_norm_u", "phi(norm_x, gamma_l, gamma_u) / norm_u;",
+     "phi(norm_u, gamma_l, gamma_u) / norm_u;", 0),
+    ("lamb_not_normalised", "phi(norm_x, gamma_l, gamma_u) / norm_u;",
+     "phi(norm_x, gamma_l, gamma_u);", 0),
+    ("lamb_update_sign", "(double)x[j] - lr * ratio * u[j]", "(double)x[j] + lr * ratio * u[j]", 0),
+    ("lamb_stores_corrected_m", "m[j] = store_f32(mj);", "m[j] = store_f32(m_hat);", 0),
+    ("lamb_stores_corrected_v", "v[j] = store_f32(vj);", "v[j] = store_f32(v_hat);", 0),
+    ("lamb_zero_norm_not_guarded", "(norm_u == 0.0) ? 0.0 :", "", 0),
+    ("phi_no_lower_clamp", "if (p < gamma_l)\n        p = gamma_l;", "", 0),
+    ("phi_no_upper_clamp", "if (p > gamma_u)\n        p = gamma_u;", "", 0),
+    ("phi_bounds_swapped", "p = gamma_l;\n    if (p > gamma_u)\n        p = gamma_u;",
+     "p = gamma_u;\n    if (p > gamma_u)\n        p = gamma_l;", 0),
+    ("bf16_wrong_shift", "(uint32_t)bits << 16", "(uint32_t)bits << 15", 0),
+    ("lars_no_dampening", "(1.0 - beta1) * (gj + lam * xj)", "(gj + lam * xj)", 0),
+    ("lars_lambda_dropped", "(1.0 - beta1) * (gj + lam * xj)", "(1.0 - beta1) * gj", 0),
+    ("lars_lambda_after_momentum", "mt[j] = beta1 * (double)m[j] + (1.0 - beta1) * (gj + lam * xj);",
+     "mt[j] = beta1 * (double)m[j] + (1.0 - beta1) * gj + lam * xj;", 0),
+    ("lars_mask_ignored", "double lam = wd ? weight_decay : 0.0;",
+     "double lam = weight_decay;", 1),
+    ("lars_no_trust_coef", "trust_coef * phi(norm_x, gamma_l, gamma_u) / norm_m",
+     "phi(norm_x, gamma_l, gamma_u) / norm_m", 0),
+    ("lars_norm_of_g", "sum_mm += mt[j] * mt[j];", "sum_mm += gj * gj;", 0),
+    ("lars_phi_of_norm_m", "phi(norm_x, gamma_l, gamma_u) / norm_m",
+     "phi(norm_m, gamma_l, gamma_u) / norm_m", 0),
+    ("lars_update_sign", "(double)x[j] - lr * ratio * mt[j]", "(double)x[j] + lr * ratio * mt[j]", 0),
+    ("lars_stores_undamped_m", "m[j] = store_f32(mt[j]);",
+     "m[j] = store_f32(mt[j] / (1.0 - beta1));", 0),
+    ("lars_zero_norm_not_guarded", "(norm_m == 0.0)\n                       ? 0.0\n                       :", "", 0),
+]
+
+
+def _in_comment(text, pos):
+    line = text[text.rfind("\n", 0, pos) + 1:pos].lstrip()
+    return line.startswith(("*", "/*", "//"))
+
+
+def _mutate(text, old, new, occurrence):
+    """Replace the ``occurrence``-th appearance of ``old`` in code (not comments)."""
+    pos, seen = -1, -1
+    while seen < occurrence:
+        pos = text.find(old, pos + 1)
+        assert pos >= 0, "mutation anchor not found in code: %r" % old
+        if not _in_comment(text, pos):
+            seen += 1
+    return text[:pos] + new + text[pos + len(old):]
+
+
+@pytest.mark.parametrize("name,old,new,occ", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_mutant_is_caught(tmp_path, name, old, new, occ):
+    if shutil.which("gcc") is None:
+        pytest.skip("gcc not available")
+    with open(oracle.SOURCE) as f:
+        text = f.read()
+    src = tmp_path / (name + ".c")
+    src.write_text(_mutate(text, old, new, occ))
+    lib = oracle.build(str(src), str(tmp_path / ("lib" + name + ".so")))
+    mutant = oracle.Oracle(lib)
+    caught = []
+    for pin in oracle_pins.ALL_PINS:
+        try:
+            pin(mutant)
+        except (AssertionError, RuntimeError, FloatingPointError):
+            caught.append(pin.__name__)
+    assert caught, "no pin catches mutant %s" % name
+    os.remove(lib)

@@ -1,0 +1,59 @@
+"""Shapes, counts, masks and seeding of the synthetic parameter sets."""
+
+import numpy as np
+import pytest
+
+from paper_1904_00962_amd import paramsets
+
+# (tensors, parameters, 1-D tensors without weight decay, largest tensor)
+EXPECTED = {
+    0: (8, 608_000, 4, 262_144),
+    1: (199, 109_482_240, 123, 23_440_896),
+    2: (391, 335_141_888, 243, 31_254_528),
+    3: (161, 25_557_032, 107, 2_359_296),
+    4: (580, 1_557_611_200, 386, 80_411_200),
+}
+
+
+@pytest.mark.parametrize("cfg", sorted(EXPECTED))
+def test_counts(cfg):
+    ps = paramsets.get(cfg)
+    n, p, masked, largest = EXPECTED[cfg]
+    assert ps.n_tensors == n
+    assert ps.numel == p
+    assert sum(1 for t in ps.tensors if not t.wd) == masked
+    assert all((len(t.shape) == 1) == (not t.wd) for t in ps.tensors)
+    assert max(t.numel for t in ps.tensors) == largest
+
+
+def test_gradient_dtypes():
+    assert [paramsets.get(c).g_dtype for c in range(5)] == ["f32", "f32", "bf16", "f32", "bf16"]
+
+
+def test_seeded_draws_are_reproducible_and_subset_stable():
+    ps = paramsets.get(0)
+    a = paramsets.draw_params(ps)
+    b = paramsets.draw_params(ps, indices=[2, 5])
+    assert np.array_equal(a[2], b[0]) and np.array_equal(a[5], b[1])
+    g1 = paramsets.draw_grads(ps, 1)
+    g1b = paramsets.draw_grads(ps, 1)
+    g2 = paramsets.draw_grads(ps, 2)
+    assert all(np.array_equal(p, q) for p, q in zip(g1, g1b))
+    assert not np.array_equal(g1[0], g2[0])
+    assert abs(float(np.std(a[2])) - ps.sigma_x) < 1e-3
+    assert abs(float(np.std(g1[2])) - ps.sigma_g) < 1e-4
+
+
+def test_bf16_gradients_round_to_nearest_even():
+    ps = paramsets.get(2)
+    idx = [3]  # emb.ln.gamma, 1024 elements
+    bits = paramsets.draw_grads(ps, 1, indices=idx)[0]
+    assert bits.dtype == np.uint16 and bits.size == 1024
+    import torch
+    gen = torch.Generator().manual_seed(1000 * 2 + 1)
+    for spec in ps.tensors[:3]:
+        torch.randn(spec.numel, generator=gen)
+    ref = torch.randn(1024, generator=gen) * ps.sigma_g
+    widened = paramsets.bf16_bits_to_f32(bits)
+    err = np.abs(widened - ref.numpy())
+    assert np.all(err <= np.abs(ref.numpy()) * 2.0 ** -8 + 1e-30)
