@@ -1,0 +1,263 @@
+"""Benchmark: one multi-tensor LAMB (or LARS) step per timed iteration.
+
+Default workload: the BERT-Large-shaped parameter set (391 tensors,
+335,141,888 fp32 parameters, bf16 gradients), LAMB with the paper's
+hyperparameters. Inputs are synthetic, seeded, drawn on the GPU and resident
+in HBM before timing starts. Prints ONE JSON line on stdout; diagnostics go
+to stderr.
+
+  python bench.py [--steps K] [--warmup W] [--config 2] [--algo lamb|lars]
+                  [--chunk ELEMS] [--cpu-seconds S | --no-cpu-baseline]
+  python bench.py --copy-probe      # plain copy of known size (counter scale)
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "LAMB step: params updated/sec + achieved HBM GB/s (% peak), BERT-Large fp32"
+HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, published
+PROFILES = os.path.join(ROOT, "profiles")
+
+
+def eprint(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def bytes_per_param(algo: str, g_bytes: int):
+    """Algorithmic HBM bytes per parameter of (moment pass, apply pass).
+
+    LAMB moment pass reads x, g, m, v and writes m, v; apply reads x, m, v and
+    writes x. LARS moment pass reads x, g, m and writes m; apply reads x, m
+    and writes x.
+    """
+    if algo == "lamb":
+        return 4 + g_bytes + 4 + 4 + 4 + 4, 4 + 4 + 4 + 4
+    return 4 + g_bytes + 4 + 4, 4 + 4 + 4
+
+
+def kernel_source_hash() -> str:
+    from paper_1904_00962_amd import build as hb
+    h = hashlib.sha256()
+    for p in hb.SOURCES + hb.HEADERS:
+        with open(p, "rb") as f:
+            h.update(f.read())
+    h.update(" ".join(hb.HIPCC_FLAGS).encode())
+    return h.hexdigest()[:16]
+
+
+def counter_traffic(workload: str, src_hash: str):
+    """HBM bytes per launch of the moment kernel from the committed rocprofv3
+    counter summary for this workload, or None if absent or stale."""
+    path = os.path.join(PROFILES, "lamb_moments_%s_traffic.md" % workload)
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    m = re.search(r"kernel_source_hash:\s*(\w+)", text)
+    t = re.search(r"hbm_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    if not m or not t or m.group(1) != src_hash:
+        return None
+    return float(t.group(1))
+
+
+def copy_probe(args) -> None:
+    """A plain device-to-device copy of known size: FETCH_SIZE / WRITE_SIZE of
+    this kernel calibrate the counters (bytes per counted KiB)."""
+    import torch
+    n = args.copy_elems
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(args.steps):
+        dst.copy_(src)
+    end.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(end) / args.steps
+    print(json.dumps({"probe": "copy", "bytes_read": 4 * n, "bytes_written": 4 * n,
+                      "ms": ms, "GBps": 8 * n / ms / 1e6}), flush=True)
+
+
+def cpu_baseline(ps, xs, grads, algo, budget_s: float):
+    """Time the oracle (single-threaded C, as it stands) on a bounded sample of
+    this workload: whole steps over the leading tensors, covering at least a
+    third of the parameters; stop once ``budget_s`` seconds have been spent."""
+    import numpy as np
+
+    import oracle
+    from paper_1904_00962_amd import paramsets
+
+    o = oracle.load()
+    target = ps.numel // 3
+    idx, total = [], 0
+    for i, spec in enumerate(ps.tensors):
+        idx.append(i)
+        total += spec.numel
+        if total >= target:
+            break
+    hx = [paramsets.host_array(xs[i]).copy() for i in idx]
+    hg = [paramsets.host_array(grads[i]).copy() for i in idx]
+    hm = [np.zeros_like(h) for h in hx]
+    hv = [np.zeros_like(h) for h in hx]
+    wd = [ps.wd_mask()[i] for i in idx]
+    f = lambda a: float(np.float32(a))  # noqa: E731
+    done, spent = 0, 0.0
+    while done == 0 or (spent < budget_s and done < 5):
+        t0 = time.perf_counter()
+        if algo == "lamb":
+            o.lamb_step(hx, hg, hm, hv, wd, lr=f(ps.lr), beta1=f(ps.beta1), beta2=f(ps.beta2),
+                        eps=f(ps.eps), weight_decay=f(ps.weight_decay), gamma_l=f(ps.gamma_l),
+                        gamma_u=f(ps.gamma_u), step=done + 1)
+        else:
+            o.lars_step(hx, hg, hm, wd, lr=f(ps.lars_lr), momentum=f(ps.lars_momentum),
+                        weight_decay=f(ps.weight_decay), gamma_l=f(ps.gamma_l),
+                        gamma_u=f(ps.gamma_u), trust_coef=f(ps.lars_trust_coef))
+        spent += time.perf_counter() - t0
+        done += 1
+    return {"value": total * done / spent, "unit": "params/s", "cores": 1, "kind": "oracle",
+            "sample": "%d %s step(s) over the first %d of %d tensors (%d of %d params), "
+                      "single-threaded C oracle, %.1f s" % (done, algo.upper(), len(idx),
+                                                            ps.n_tensors, total, ps.numel, spent),
+            "host_cpus": os.cpu_count()}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawTextHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", type=int, default=2)
+    ap.add_argument("--algo", choices=("lamb", "lars"), default="lamb")
+    ap.add_argument("--chunk", type=int, default=0, help="elements per chunk (0 = default)")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe", action="store_true")
+    ap.add_argument("--copy-elems", type=int, default=1 << 28)
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print("bench.py measures one GPU: the optimizer step runs on a single MI355X; "
+              "--gpus %d is not supported" % args.gpus, file=sys.stderr)
+        return 2
+
+    import torch
+    if not torch.cuda.is_available():
+        eprint("bench.py needs a GPU")
+        return 1
+    if args.copy_probe:
+        copy_probe(args)
+        return 0
+
+    from paper_1904_00962_amd import _lib, paramsets
+    from paper_1904_00962_amd.optim import LAMB, LARS
+
+    _lib.load()  # fail loudly before any work if the HIP library is missing
+    ps = paramsets.get(args.config)
+    eprint("drawing %s: %d tensors, %d params (g %s)" % (ps.name, ps.n_tensors, ps.numel,
+                                                          ps.g_dtype))
+    xs = paramsets.draw_params(ps, device="cuda")
+    grads = paramsets.draw_grads(ps, 1, device="cuda")
+    if args.algo == "lamb":
+        opt = LAMB(xs, grads, lr=ps.lr, betas=(ps.beta1, ps.beta2), eps=ps.eps,
+                   weight_decay=ps.weight_decay, clamp=(ps.gamma_l, ps.gamma_u),
+                   wd_mask=ps.wd_mask(), chunk_elems=args.chunk)
+    else:
+        opt = LARS(xs, grads, lr=ps.lars_lr, momentum=ps.lars_momentum,
+                   weight_decay=ps.weight_decay, clamp=(ps.gamma_l, ps.gamma_u),
+                   trust_coef=ps.lars_trust_coef, wd_mask=ps.wd_mask(), chunk_elems=args.chunk)
+    n_tensors, n_chunks, chunk = _lib.lamb_plan_info(opt.plan)
+
+    # host copies for the CPU baseline are taken before the GPU steps move x
+    cpu = None
+    if not args.no_cpu_baseline:
+        eprint("timing the CPU oracle (budget %.0f s)" % args.cpu_seconds)
+        cpu = cpu_baseline(ps, xs, grads, args.algo, args.cpu_seconds)
+        eprint("cpu baseline: %.3e params/s (%s)" % (cpu["value"], cpu["sample"]))
+
+    for _ in range(args.warmup):
+        opt.step()
+    torch.cuda.synchronize()
+    _lib.lamb_plan_set_timing(opt.plan, args.steps)
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for _ in range(args.steps):
+        opt.step()
+    end.record()
+    torch.cuda.synchronize()
+    total_ms = start.elapsed_time(end)
+    (k_mom, k_fin, k_app), recorded = _lib.lamb_plan_timing(opt.plan)
+    _lib.lamb_plan_set_timing(opt.plan, 0)
+    ratios = opt.ratios.cpu()
+    if not torch.isfinite(ratios).all():
+        eprint("non-finite trust ratio after the timed steps")
+        return 1
+
+    ms_step = total_ms / args.steps
+    P = ps.numel
+    g_bytes = 2 if ps.g_dtype == "bf16" else 4
+    b_mom, b_app = bytes_per_param(args.algo, g_bytes)
+    avg_mom = k_mom / recorded
+    avg_app = k_app / recorded
+    avg_fin = k_fin / recorded
+    mom_gbps = b_mom * P / avg_mom / 1e6
+    app_gbps = b_app * P / avg_app / 1e6
+    step_gbps = (b_mom + b_app) * P / ms_step / 1e6
+    workload = ps.name
+    src_hash = kernel_source_hash()
+    traffic = counter_traffic(workload, src_hash) if args.algo == "lamb" else None
+    kernel = "%s_moments_kernel<%s>" % (args.algo, "bf16" if g_bytes == 2 else "f32")
+    eprint("step %.4f ms | moments %.4f ms (%.0f GB/s) | finalize %.4f ms | apply %.4f ms "
+           "(%.0f GB/s) | whole step %.0f GB/s" % (ms_step, avg_mom, mom_gbps, avg_fin, avg_app,
+                                                   app_gbps, step_gbps))
+    line = {
+        "metric": METRIC,
+        "value": P / (ms_step / 1e3),
+        "unit": "params/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": "%s %s step: %d tensors, %d fp32 params, %s gradients"
+                        % (workload, args.algo.upper(), n_tensors, P, ps.g_dtype),
+            "algo": args.algo, "tensors": n_tensors, "params": P, "grad_dtype": ps.g_dtype,
+            "chunk_elems": chunk, "chunks": n_chunks, "seed_x": 1000 * ps.cfg,
+            "seed_g": 1000 * ps.cfg + 1,
+        },
+        "hbm_GBps": step_gbps,
+        "hbm_frac_of_peak": step_gbps / HBM_PEAK_GBPS,
+        "bytes_per_param": b_mom + b_app,
+        "kernels_ms": {"moments": avg_mom, "finalize": avg_fin, "apply": avg_app},
+        "roofline": {
+            "bound": "hbm", "kernel": kernel, "achieved": mom_gbps, "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s", "frac": mom_gbps / HBM_PEAK_GBPS, "traffic": traffic,
+            "bytes_per_launch": b_mom * P, "kernel_source_hash": src_hash,
+        },
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+    opt.close()
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

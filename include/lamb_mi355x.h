@@ -1,0 +1,193 @@
+/*
+ * lamb_mi355x.h -- C ABI of the multi-tensor LAMB / LARS optimizer step for
+ * AMD Instinct MI355X (gfx950).
+ *
+ * Method: You et al., "Large Batch Optimization for Deep Learning: Training
+ * BERT in 76 minutes" (arXiv:1904.00962). LAMB is Algorithm 2 (Section 3.2),
+ * LARS is Algorithm 1 (Section 3.1); the scaling function
+ * phi(z) = min(max(z, gamma_l), gamma_u) is defined in Section 3, and a
+ * "layer" x^(i) is one block of the parameter vector (Section 2, Notation),
+ * here one tensor of the table.
+ *
+ * Conventions for every entry point:
+ *  - Tensor pointers are DEVICE pointers on the device that is current when
+ *    the plan is created; host arrays are marked "host".
+ *  - All state (x, g, m, v) is owned by the caller. The plan owns only its
+ *    own small device buffers (tensor and chunk tables, per-chunk partial
+ *    sums, per-tensor step scales), allocated in lamb_plan_create and freed
+ *    in lamb_plan_destroy.
+ *  - Arguments are validated on the host before any HIP call. A call that
+ *    fails validation returns a negative lamb_status, launches nothing and
+ *    changes no state. lamb_last_error() then describes the failure.
+ *  - Step calls enqueue work on `stream` (a hipStream_t; NULL = the null
+ *    stream) and return without synchronising, allocating or copying to the
+ *    host. Device faults surface at the caller's next synchronisation.
+ *  - One step may be in flight per plan (its partials buffer is reused);
+ *    a plan is not thread-safe. Distinct plans are independent.
+ *  - NaN and Inf in the inputs propagate by IEEE rules; nothing is masked.
+ */
+#ifndef LAMB_MI355X_H
+#define LAMB_MI355X_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Entry points are the only symbols the shared library exports. */
+#if defined(__GNUC__) || defined(__clang__)
+#define LAMB_API __attribute__((visibility("default")))
+#else
+#define LAMB_API
+#endif
+
+typedef enum lamb_status {
+    LAMB_OK = 0,
+    LAMB_EINVAL = -1,   /* a size or scalar is outside its documented range  */
+    LAMB_ENULL = -2,    /* a required pointer is NULL                         */
+    LAMB_EALIGN = -3,   /* a tensor pointer is not 16-byte aligned            */
+    LAMB_EOVERLAP = -4, /* two tensor buffers of the table overlap            */
+    LAMB_EHIP = -5,     /* a HIP runtime call failed                          */
+    LAMB_ENOMEM = -6,   /* a host or device allocation failed                 */
+    LAMB_EPLAN = -7     /* the plan was built for the other algorithm         */
+} lamb_status;
+
+typedef enum lamb_grad_dtype {
+    LAMB_GRAD_F32 = 0,  /* g is float                                         */
+    LAMB_GRAD_BF16 = 1  /* g is bfloat16 (raw 16-bit patterns), widened exactly */
+} lamb_grad_dtype;
+
+typedef enum lamb_algo {
+    LAMB_ALGO_LAMB = 0, /* Algorithm 2: needs m and v                          */
+    LAMB_ALGO_LARS = 1  /* Algorithm 1: needs m only; v is ignored            */
+} lamb_algo;
+
+/*
+ * One layer block x^(i) (Section 2). Every buffer holds `numel` contiguous
+ * elements and is 16-byte aligned; no two buffers of a table may overlap.
+ *   x  fp32 parameters, updated in place
+ *   g  gradient g_t (fp32 or bf16, fixed per plan), read only
+ *   m  fp32 first moment (LAMB) / momentum (LARS), updated in place; start at 0
+ *   v  fp32 second moment (LAMB), updated in place; start at 0. NULL for LARS.
+ *   wd weight-decay mask: 1 applies lambda to this block, 0 uses lambda = 0
+ */
+typedef struct lamb_tensor {
+    float *x;
+    const void *g;
+    float *m;
+    float *v;
+    int64_t numel;
+    int32_t wd;
+    int32_t reserved; /* must be 0 */
+} lamb_tensor;
+
+typedef struct lamb_plan lamb_plan; /* opaque */
+
+/*
+ * Build a plan for a fixed table of blocks (Section 2's decomposition of x).
+ * The table is copied; the tensor pointers must stay valid and unchanged for
+ * the plan's life (rebuild the plan if the buffers move).
+ *   tensors      host array of n_tensors descriptors, n_tensors >= 1
+ *   g_dtype      dtype of every g
+ *   algo         which step the plan serves
+ *   chunk_elems  elements per work chunk: 0 picks the default, otherwise a
+ *                multiple of 8 in [8, 2^30]. Results are deterministic for a
+ *                given chunk size and agree across sizes to rounding.
+ *   out          receives the plan
+ * Errors: LAMB_ENULL (tensors/out/x/g/m, or v for LAMB), LAMB_EINVAL (sizes,
+ * dtype, algo, reserved != 0), LAMB_EALIGN, LAMB_EOVERLAP, LAMB_ENOMEM,
+ * LAMB_EHIP (device allocation or copy failed).
+ */
+LAMB_API lamb_status lamb_plan_create(const lamb_tensor *tensors, int32_t n_tensors,
+                             lamb_grad_dtype g_dtype, lamb_algo algo,
+                             int32_t chunk_elems, lamb_plan **out);
+
+/* Free the plan's device buffers. NULL is accepted. Waits for nothing: the
+ * caller must not destroy a plan whose step is still running. */
+LAMB_API lamb_status lamb_plan_destroy(lamb_plan *plan);
+
+/* Sizes of a plan (host outputs; any may be NULL). */
+LAMB_API lamb_status lamb_plan_info(const lamb_plan *plan, int32_t *n_tensors,
+                           int32_t *n_chunks, int32_t *chunk_elems);
+
+/*
+ * One LAMB step (Algorithm 2) over every block of the plan, at step t = step:
+ *   m <- beta1 m + (1 - beta1) g ;  v <- beta2 v + (1 - beta2) g^2
+ *   r  = (m / c1) / (sqrt(v / c2) + eps),  c1 = 1 - beta1^t, c2 = 1 - beta2^t
+ *        (c1 = c2 = 1 when bias_correction == 0, Appendix E)
+ *   u  = r + lambda_i x,  lambda_i = wd_i ? weight_decay : 0
+ *   x <- x - lr * phi(||x_i||) / ||u_i|| * u      per block i
+ * A block with ||u_i|| = 0 is left unchanged and reports ratio 0.
+ * Scalars: step >= 1; 0 <= beta1, beta2 < 1; eps >= 0; 0 <= gamma_l <=
+ * gamma_u (gamma_u may be +inf); lr and weight_decay finite.
+ *   ratio_out  device, n_tensors doubles: phi(||x_i||)/||u_i||, or NULL
+ *   norms_out  device, 2*n_tensors doubles {||x_i||, ||u_i||}, or NULL
+ * Errors: LAMB_ENULL (plan), LAMB_EPLAN (a LARS plan), LAMB_EINVAL, LAMB_EHIP.
+ */
+LAMB_API lamb_status lamb_step(lamb_plan *plan, float lr, float beta1, float beta2,
+                      float eps, float weight_decay, float gamma_l,
+                      float gamma_u, int64_t step, int32_t bias_correction,
+                      void *stream, double *ratio_out, double *norms_out);
+
+/*
+ * One LARS step (Algorithm 1) over every block of the plan:
+ *   m <- momentum m + (1 - momentum) (g + lambda_i x)
+ *   x <- x - lr * trust_coef * phi(||x_i||) / ||m_i|| * m      per block i
+ * trust_coef (kappa) scales the ratio; kappa = 1 is Algorithm 1 as printed.
+ * A block with ||m_i|| = 0 is left unchanged and reports ratio 0.
+ * Scalars: 0 <= momentum < 1; 0 <= gamma_l <= gamma_u; lr, weight_decay and
+ * trust_coef finite.
+ *   ratio_out  device, n_tensors doubles kappa phi/||m_i||, or NULL
+ *   norms_out  device, 2*n_tensors doubles {||x_i||, ||m_i||}, or NULL
+ * Errors: LAMB_ENULL, LAMB_EPLAN (a LAMB plan), LAMB_EINVAL, LAMB_EHIP.
+ */
+LAMB_API lamb_status lars_step(lamb_plan *plan, float lr, float momentum,
+                      float weight_decay, float gamma_l, float gamma_u,
+                      float trust_coef, void *stream, double *ratio_out,
+                      double *norms_out);
+
+/*
+ * The chunk table a plan would use (host only, no HIP call). Tensor i is cut
+ * into ceil(numel[i] / chunk_elems) chunks in table order; chunk k of it
+ * starts at k * chunk_elems and holds min(chunk_elems, numel[i] - start)
+ * elements. chunk_elems = 0 picks the default.
+ *   numel        host, n_tensors sizes (>= 1 each)
+ *   capacity     length of the three host output arrays (may be 0 with NULL
+ *                outputs to query the count)
+ *   n_chunks     receives the number of chunks
+ * Errors: LAMB_ENULL, LAMB_EINVAL (including capacity too small, in which
+ * case *n_chunks still receives the count).
+ */
+LAMB_API lamb_status lamb_chunk_table(const int64_t *numel, int32_t n_tensors,
+                             int32_t chunk_elems, int32_t capacity,
+                             int32_t *chunk_tensor, int64_t *chunk_start,
+                             int32_t *chunk_len, int32_t *n_chunks);
+
+/*
+ * Per-kernel timing with HIP events, for measurement. max_steps > 0 creates
+ * event pairs for that many steps and makes each later step record them
+ * around its three kernels on the step's stream; 0 turns timing off and
+ * frees the events. A step beyond max_steps records nothing.
+ */
+LAMB_API lamb_status lamb_plan_set_timing(lamb_plan *plan, int32_t max_steps);
+
+/*
+ * Synchronise on the recorded events and return the summed durations in
+ * milliseconds of the moment kernel, the finalize kernel and the apply
+ * kernel (kernel_ms[0..2], host) over `steps` recorded steps (host); then
+ * start a new recording window.
+ */
+LAMB_API lamb_status lamb_plan_timing(lamb_plan *plan, double *kernel_ms, int64_t *steps);
+
+/* Static description of a status code. */
+LAMB_API const char *lamb_status_str(lamb_status status);
+
+/* Detail of the calling thread's last failure ("" if none). */
+LAMB_API const char *lamb_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LAMB_MI355X_H */

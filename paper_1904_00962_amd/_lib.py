@@ -1,0 +1,203 @@
+"""ctypes binding of ``liblamb_mi355x.so`` (include/lamb_mi355x.h).
+
+Argument marshalling only: every step of the optimizer runs in the HIP
+kernels behind these calls. The functions keep the C names; failures raise
+:class:`LambError` carrying the status code and the library's error detail.
+The library is loaded on first use and its absence is an error: there is no
+fallback implementation.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence, Tuple
+
+import numpy as np
+
+from . import build as _build
+
+LIBRARY = _build.LIBRARY
+
+LAMB_OK = 0
+LAMB_EINVAL = -1
+LAMB_ENULL = -2
+LAMB_EALIGN = -3
+LAMB_EOVERLAP = -4
+LAMB_EHIP = -5
+LAMB_ENOMEM = -6
+LAMB_EPLAN = -7
+
+LAMB_GRAD_F32 = 0
+LAMB_GRAD_BF16 = 1
+LAMB_ALGO_LAMB = 0
+LAMB_ALGO_LARS = 1
+
+# Every symbol the header declares (checked by the test suite).
+EXPORTS = ("lamb_plan_create", "lamb_plan_destroy", "lamb_plan_info", "lamb_step",
+           "lars_step", "lamb_chunk_table", "lamb_plan_set_timing", "lamb_plan_timing",
+           "lamb_status_str", "lamb_last_error")
+
+
+class LambError(RuntimeError):
+    def __init__(self, status: int, func: str, detail: str):
+        self.status = status
+        super().__init__("%s failed with status %d (%s): %s"
+                         % (func, status, status_str(status), detail))
+
+
+class lamb_tensor(ctypes.Structure):
+    _fields_ = [("x", ctypes.c_void_p), ("g", ctypes.c_void_p), ("m", ctypes.c_void_p),
+                ("v", ctypes.c_void_p), ("numel", ctypes.c_int64), ("wd", ctypes.c_int32),
+                ("reserved", ctypes.c_int32)]
+
+
+_lib: Optional[ctypes.CDLL] = None
+
+
+def load(path: str = LIBRARY) -> ctypes.CDLL:
+    """Open the HIP library (once). Raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError("HIP library %s is missing; run `python -m paper_1904_00962_amd.build` "
+                           "(there is no CPU fallback)" % path)
+    lib = ctypes.CDLL(path)
+    i32, i64, f32, vp = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_void_p
+    P = ctypes.POINTER
+    lib.lamb_plan_create.argtypes = [P(lamb_tensor), i32, i32, i32, i32, P(vp)]
+    lib.lamb_plan_destroy.argtypes = [vp]
+    lib.lamb_plan_info.argtypes = [vp, P(i32), P(i32), P(i32)]
+    lib.lamb_step.argtypes = [vp, f32, f32, f32, f32, f32, f32, f32, i64, i32, vp, vp, vp]
+    lib.lars_step.argtypes = [vp, f32, f32, f32, f32, f32, f32, vp, vp, vp]
+    lib.lamb_chunk_table.argtypes = [P(i64), i32, i32, i32, P(i32), P(i64), P(i32), P(i32)]
+    lib.lamb_plan_set_timing.argtypes = [vp, i32]
+    lib.lamb_plan_timing.argtypes = [vp, P(ctypes.c_double), P(i64)]
+    lib.lamb_status_str.argtypes = [i32]
+    lib.lamb_status_str.restype = ctypes.c_char_p
+    lib.lamb_last_error.argtypes = []
+    lib.lamb_last_error.restype = ctypes.c_char_p
+    for name in EXPORTS:
+        if name not in ("lamb_status_str", "lamb_last_error"):
+            getattr(lib, name).restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def status_str(status: int) -> str:
+    return load().lamb_status_str(status).decode()
+
+
+def last_error() -> str:
+    return load().lamb_last_error().decode()
+
+
+def _check(status: int, func: str) -> None:
+    if status != LAMB_OK:
+        raise LambError(status, func, last_error())
+
+
+def _vp(p) -> ctypes.c_void_p:
+    return ctypes.c_void_p(int(p) if p else 0)
+
+
+class Plan:
+    """Owning handle on a ``lamb_plan``; destroyed with :meth:`close` or on collection."""
+
+    def __init__(self, handle: int):
+        self.handle = handle
+
+    def close(self) -> None:
+        if self.handle:
+            h, self.handle = self.handle, 0
+            _check(load().lamb_plan_destroy(_vp(h)), "lamb_plan_destroy")
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+
+def lamb_plan_create(tensors: Sequence[Tuple[int, int, int, int, int, int]], g_dtype: int,
+                     algo: int, chunk_elems: int = 0) -> Plan:
+    """tensors: (x_ptr, g_ptr, m_ptr, v_ptr, numel, wd) per block, device pointers."""
+    lib = load()
+    n = len(tensors)
+    arr = (lamb_tensor * max(n, 1))()
+    for i, (x, g, m, v, numel, wd) in enumerate(tensors):
+        arr[i] = lamb_tensor(int(x) or None, int(g) or None, int(m) or None,
+                             int(v) if v else None, int(numel), int(wd), 0)
+    out = ctypes.c_void_p()
+    _check(lib.lamb_plan_create(arr, n, int(g_dtype), int(algo), int(chunk_elems),
+                                ctypes.byref(out)), "lamb_plan_create")
+    return Plan(out.value)
+
+
+def lamb_plan_destroy(plan: Plan) -> None:
+    plan.close()
+
+
+def lamb_plan_info(plan: Plan) -> Tuple[int, int, int]:
+    a, b, c = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
+    _check(load().lamb_plan_info(_vp(plan.handle), ctypes.byref(a), ctypes.byref(b),
+                                 ctypes.byref(c)), "lamb_plan_info")
+    return a.value, b.value, c.value
+
+
+def lamb_step(plan: Plan, lr: float, beta1: float, beta2: float, eps: float,
+              weight_decay: float, gamma_l: float, gamma_u: float, step: int,
+              bias_correction: bool = True, stream: int = 0, ratio_out: int = 0,
+              norms_out: int = 0) -> None:
+    _check(load().lamb_step(_vp(plan.handle), lr, beta1, beta2, eps, weight_decay, gamma_l,
+                            gamma_u, int(step), int(bool(bias_correction)), _vp(stream),
+                            _vp(ratio_out), _vp(norms_out)), "lamb_step")
+
+
+def lars_step(plan: Plan, lr: float, momentum: float, weight_decay: float, gamma_l: float,
+              gamma_u: float, trust_coef: float, stream: int = 0, ratio_out: int = 0,
+              norms_out: int = 0) -> None:
+    _check(load().lars_step(_vp(plan.handle), lr, momentum, weight_decay, gamma_l, gamma_u,
+                            trust_coef, _vp(stream), _vp(ratio_out), _vp(norms_out)),
+           "lars_step")
+
+
+def lamb_chunk_table(numel: Sequence[int], chunk_elems: int = 0):
+    """(tensor, start, len) arrays of the chunk table a plan would build."""
+    lib = load()
+    n = len(numel)
+    sizes = np.ascontiguousarray(np.asarray(numel, dtype=np.int64))
+    count = ctypes.c_int32()
+    p64 = sizes.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)) if n else None
+    _check(lib.lamb_chunk_table(p64, n, int(chunk_elems), 0, None, None, None,
+                                ctypes.byref(count)), "lamb_chunk_table")
+    k = count.value
+    ct = np.zeros(k, np.int32)
+    cs = np.zeros(k, np.int64)
+    cl = np.zeros(k, np.int32)
+    _check(lib.lamb_chunk_table(p64, n, int(chunk_elems), k,
+                                ct.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
+                                cs.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)),
+                                cl.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
+                                ctypes.byref(count)), "lamb_chunk_table")
+    return ct, cs, cl
+
+
+def lamb_plan_set_timing(plan: Plan, max_steps: int) -> None:
+    _check(load().lamb_plan_set_timing(_vp(plan.handle), int(max_steps)), "lamb_plan_set_timing")
+
+
+def lamb_plan_timing(plan: Plan) -> Tuple[Tuple[float, float, float], int]:
+    """Summed (moments, finalize, apply) kernel milliseconds and the step count."""
+    ms = (ctypes.c_double * 3)()
+    steps = ctypes.c_int64()
+    _check(load().lamb_plan_timing(_vp(plan.handle), ms, ctypes.byref(steps)),
+           "lamb_plan_timing")
+    return (ms[0], ms[1], ms[2]), steps.value

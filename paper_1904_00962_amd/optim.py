@@ -1,0 +1,146 @@
+"""LAMB and LARS optimizers over lists of torch tensors on an MI355X.
+
+PyTorch supplies device memory and the current stream only; the step itself
+is the HIP library (``_lib``). The plan binds the buffers' addresses, so
+parameters and gradients must be persistent, contiguous device tensors: write
+each step's gradient into the same ``grads`` tensors (e.g. ``g.copy_(...)``).
+
+Defaults follow the paper: beta1 = 0.9, beta2 = 0.999, eps = 1e-6,
+lambda = 0.01 (Section 4 and Appendix H); phi clamps to [0, 10].
+"""
+
+from __future__ import annotations
+
+from typing import Optional, Sequence, Tuple
+
+from . import _lib
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _check_tensors(params, grads):
+    torch = _torch()
+    if len(params) == 0 or len(params) != len(grads):
+        raise ValueError("need one gradient per parameter tensor (got %d and %d)"
+                         % (len(params), len(grads)))
+    g_dtype = grads[0].dtype
+    if g_dtype not in (torch.float32, torch.bfloat16):
+        raise TypeError("gradients must be float32 or bfloat16")
+    device = params[0].device
+    if device.type != "cuda":
+        raise ValueError("parameters must live on a GPU")
+    for i, (p, g) in enumerate(zip(params, grads)):
+        if p.dtype != torch.float32:
+            raise TypeError("parameter %d is %s; the step keeps fp32 master weights" % (i, p.dtype))
+        if g.dtype != g_dtype:
+            raise TypeError("all gradients must share one dtype")
+        if p.device != device or g.device != device:
+            raise ValueError("tensor %d is on another device" % i)
+        if not p.is_contiguous() or not g.is_contiguous():
+            raise ValueError("tensor %d is not contiguous" % i)
+        if p.numel() != g.numel() or p.numel() == 0:
+            raise ValueError("tensor %d: parameter and gradient sizes differ or are empty" % i)
+    return g_dtype, device
+
+
+class _LayerwiseOptimizer:
+    algo = _lib.LAMB_ALGO_LAMB
+
+    def __init__(self, params: Sequence, grads: Sequence, lr: float, weight_decay: float,
+                 clamp: Tuple[float, float], wd_mask: Optional[Sequence[bool]],
+                 chunk_elems: int, with_v: bool):
+        torch = _torch()
+        self.params = list(params)
+        self.grads = list(grads)
+        g_dtype, self.device = _check_tensors(self.params, self.grads)
+        self.lr = float(lr)
+        self.weight_decay = float(weight_decay)
+        self.gamma_l, self.gamma_u = float(clamp[0]), float(clamp[1])
+        if wd_mask is None:
+            wd_mask = [p.dim() > 1 for p in self.params]
+        self.wd_mask = [bool(w) for w in wd_mask]
+        if len(self.wd_mask) != len(self.params):
+            raise ValueError("wd_mask needs one entry per tensor")
+        self.m = [torch.zeros_like(p) for p in self.params]
+        self.v = [torch.zeros_like(p) for p in self.params] if with_v else None
+        n = len(self.params)
+        self.ratios = torch.zeros(n, dtype=torch.float64, device=self.device)
+        self.norms = torch.zeros(2 * n, dtype=torch.float64, device=self.device)
+        rows = []
+        for i, (p, g) in enumerate(zip(self.params, self.grads)):
+            v = self.v[i].data_ptr() if with_v else 0
+            rows.append((p.data_ptr(), g.data_ptr(), self.m[i].data_ptr(), v, p.numel(),
+                         int(self.wd_mask[i])))
+        kind = _lib.LAMB_GRAD_BF16 if g_dtype == torch.bfloat16 else _lib.LAMB_GRAD_F32
+        with torch.cuda.device(self.device):
+            self.plan = _lib.lamb_plan_create(rows, kind, self.algo, chunk_elems)
+        self.t = 0
+
+    def _stream(self) -> int:
+        return _torch().cuda.current_stream(self.device).cuda_stream
+
+    def close(self) -> None:
+        self.plan.close()
+
+
+class LAMB(_LayerwiseOptimizer):
+    """Algorithm 2: Adam moments with bias correction, then a per-layer trust ratio."""
+
+    algo = _lib.LAMB_ALGO_LAMB
+
+    def __init__(self, params, grads, lr: float = 1e-3, betas=(0.9, 0.999), eps: float = 1e-6,
+                 weight_decay: float = 0.01, clamp=(0.0, 10.0), wd_mask=None,
+                 bias_correction: bool = True, chunk_elems: int = 0):
+        super().__init__(params, grads, lr, weight_decay, clamp, wd_mask, chunk_elems, True)
+        self.beta1, self.beta2 = float(betas[0]), float(betas[1])
+        self.eps = float(eps)
+        self.bias_correction = bool(bias_correction)
+
+    def step(self, lr: Optional[float] = None) -> None:
+        """Advance t and apply one step; per-tensor ratios and norms land in
+        ``self.ratios`` and ``self.norms`` (device, float64)."""
+        self.t += 1
+        _lib.lamb_step(self.plan, self.lr if lr is None else float(lr), self.beta1, self.beta2,
+                       self.eps, self.weight_decay, self.gamma_l, self.gamma_u, self.t,
+                       self.bias_correction, self._stream(), self.ratios.data_ptr(),
+                       self.norms.data_ptr())
+
+    def state_dict(self):
+        return {"step": self.t, "m": [m.clone() for m in self.m], "v": [v.clone() for v in self.v]}
+
+    def load_state_dict(self, state) -> None:
+        self.t = int(state["step"])
+        for dst, src in zip(self.m, state["m"]):
+            dst.copy_(src)
+        for dst, src in zip(self.v, state["v"]):
+            dst.copy_(src)
+
+
+class LARS(_LayerwiseOptimizer):
+    """Algorithm 1: momentum with weight decay, then a per-layer trust ratio."""
+
+    algo = _lib.LAMB_ALGO_LARS
+
+    def __init__(self, params, grads, lr: float = 1e-3, momentum: float = 0.9,
+                 weight_decay: float = 0.01, clamp=(0.0, 10.0), trust_coef: float = 1e-3,
+                 wd_mask=None, chunk_elems: int = 0):
+        super().__init__(params, grads, lr, weight_decay, clamp, wd_mask, chunk_elems, False)
+        self.momentum = float(momentum)
+        self.trust_coef = float(trust_coef)
+
+    def step(self, lr: Optional[float] = None) -> None:
+        self.t += 1
+        _lib.lars_step(self.plan, self.lr if lr is None else float(lr), self.momentum,
+                       self.weight_decay, self.gamma_l, self.gamma_u, self.trust_coef,
+                       self._stream(), self.ratios.data_ptr(), self.norms.data_ptr())
+
+    def state_dict(self):
+        return {"step": self.t, "m": [m.clone() for m in self.m]}
+
+    def load_state_dict(self, state) -> None:
+        self.t = int(state["step"])
+        for dst, src in zip(self.m, state["m"]):
+            dst.copy_(src)

@@ -12,9 +12,10 @@ Gaussians: x ~ N(0, sigma_x) and g ~ N(0, 1e-3) (second argument = standard
 deviation). Moments start at zero, as Algorithms 1 and 2 set m_0 = v_0 = 0.
 
 Seeds: x uses ``1000 * cfg``; the gradient of step t uses ``1000 * cfg + t``.
-Values are drawn tensor by tensor in canonical order with torch's CPU
-generator in fp32; bf16 gradients are the round-to-nearest-even cast of the
-fp32 draw, handed out as their raw uint16 bit patterns.
+Values are drawn tensor by tensor in canonical order with a seeded torch
+generator in fp32 (on the CPU, or on the GPU for the large sets); bf16
+gradients are the round-to-nearest-even cast of the fp32 draw. The oracle
+side receives the same bits through ``host_array``.
 """
 
 from __future__ import annotations
@@ -184,38 +185,54 @@ def _torch():
     return torch
 
 
-def draw_params(ps: ParamSet, indices: Sequence[int] | None = None) -> List[np.ndarray]:
-    """Initial x for every tensor (or the listed ones), fp32, seed 1000*cfg.
+def _generator(seed: int, device):
+    torch = _torch()
+    return torch.Generator(device=torch.device(device)).manual_seed(seed)
 
-    Tensors are always drawn in canonical order from one generator, so a
-    tensor's values do not depend on which subset is requested.
+
+def draw_params(ps: ParamSet, indices: Sequence[int] | None = None, device="cpu") -> list:
+    """Initial x (fp32 torch tensors, flat) for every tensor or the listed ones.
+
+    Seed ``1000 * cfg`` on a torch generator of ``device``. Tensors are always
+    drawn in canonical order from that one generator, so a tensor's values do
+    not depend on which subset is requested. CPU and GPU generators give
+    different (equally valid) draws; a parity test draws once and hands the
+    same bits to both sides.
     """
     torch = _torch()
-    gen = torch.Generator().manual_seed(1000 * ps.cfg)
+    gen = _generator(1000 * ps.cfg, device)
     want = set(range(ps.n_tensors)) if indices is None else set(indices)
-    out: List[np.ndarray] = []
+    out = []
     for i, spec in enumerate(ps.tensors):
-        a = torch.randn(spec.numel, generator=gen, dtype=torch.float32)
+        a = torch.randn(spec.numel, generator=gen, dtype=torch.float32, device=device)
         if i in want:
-            out.append((a * ps.sigma_x).numpy())
+            out.append(a.mul_(ps.sigma_x))
     return out
 
 
-def draw_grads(ps: ParamSet, step: int, indices: Sequence[int] | None = None) -> List[np.ndarray]:
-    """Gradient of step ``step`` (>= 1): fp32 arrays, or bf16 bit patterns (uint16)."""
+def draw_grads(ps: ParamSet, step: int, indices: Sequence[int] | None = None,
+               device="cpu") -> list:
+    """Gradient of step ``step`` (>= 1), seed ``1000 * cfg + step``: flat fp32
+    tensors, or bf16 tensors rounded to nearest even from the fp32 draw."""
     torch = _torch()
-    gen = torch.Generator().manual_seed(1000 * ps.cfg + step)
+    gen = _generator(1000 * ps.cfg + step, device)
     want = set(range(ps.n_tensors)) if indices is None else set(indices)
-    out: List[np.ndarray] = []
+    out = []
     for i, spec in enumerate(ps.tensors):
-        a = torch.randn(spec.numel, generator=gen, dtype=torch.float32)
+        a = torch.randn(spec.numel, generator=gen, dtype=torch.float32, device=device)
         if i in want:
-            a = a * ps.sigma_g
-            if ps.g_dtype == "bf16":
-                out.append(a.to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16))
-            else:
-                out.append(a.numpy())
+            a.mul_(ps.sigma_g)
+            out.append(a.to(torch.bfloat16) if ps.g_dtype == "bf16" else a)
     return out
+
+
+def host_array(t) -> np.ndarray:
+    """A torch tensor's bits as a host numpy array (bf16 as uint16 patterns)."""
+    torch = _torch()
+    t = t.detach().contiguous()
+    if t.dtype == torch.bfloat16:
+        return t.view(torch.int16).cpu().numpy().view(np.uint16)
+    return t.cpu().numpy()
 
 
 def bf16_bits_to_f32(bits: np.ndarray) -> np.ndarray:

@@ -1,0 +1,232 @@
+"""Run the HIP step and the CPU oracle side by side on identical inputs.
+
+Comparison rule for fp32 state (x, m, v), per tensor and per step:
+    err_j = |gpu_j - ref_j| / max(|ref_j|, rms(ref))
+must stay <= 1e-5, where rms(ref) is the oracle's root-mean-square of that
+quantity over the tensor. The RMS floor keeps the relative test meaningful
+for elements that land near zero (a step of ~1e-5 moving x through 0 makes a
+pure relative error ill-posed there). NaN positions must match exactly.
+Trust ratios (and the norms behind them) must agree to 1e-6 relative, and be
+exactly 0 wherever the oracle reports 0.
+"""
+
+from __future__ import annotations
+
+import dataclasses
+from typing import Callable, List, Optional, Sequence
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_1904_00962_amd import _lib, paramsets
+
+STATE_TOL = 1e-5
+RATIO_TOL = 1e-6
+
+
+def torch_cuda():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU visible")
+    return torch
+
+
+def log(msg: str) -> None:
+    print(msg, flush=True)
+
+
+@dataclasses.dataclass
+class Report:
+    max_err: float = 0.0
+    max_abs: float = 0.0
+    max_rel: float = 0.0
+    n_rel_over: int = 0
+
+    def merge(self, other: "Report") -> None:
+        self.max_err = max(self.max_err, other.max_err)
+        self.max_abs = max(self.max_abs, other.max_abs)
+        self.max_rel = max(self.max_rel, other.max_rel)
+        self.n_rel_over += other.n_rel_over
+
+
+def compare_state(gpu: np.ndarray, ref: np.ndarray, what: str, tol: float = STATE_TOL) -> Report:
+    a = gpu.astype(np.float64)
+    b = ref.astype(np.float64)
+    nan_a, nan_b = np.isnan(a), np.isnan(b)
+    if not np.array_equal(nan_a, nan_b):
+        raise AssertionError("%s: NaN positions differ (%d vs %d)"
+                             % (what, int(nan_a.sum()), int(nan_b.sum())))
+    ok = ~nan_b
+    a, b = a[ok], b[ok]
+    if a.size == 0:
+        return Report()
+    inf_b = np.isinf(b)
+    if np.any(inf_b):
+        if not np.array_equal(a[inf_b], b[inf_b]):
+            raise AssertionError("%s: infinite values differ" % what)
+        a, b = a[~inf_b], b[~inf_b]
+        if a.size == 0:
+            return Report()
+    rms = float(np.sqrt(np.mean(b * b)))
+    floor = max(rms, np.finfo(np.float32).tiny)
+    diff = np.abs(a - b)
+    err = diff / np.maximum(np.abs(b), floor)
+    with np.errstate(divide="ignore", invalid="ignore"):
+        rel = np.where(b != 0, diff / np.abs(b), np.where(diff == 0, 0.0, np.inf))
+    r = Report(float(err.max()), float(diff.max()), float(rel.max()), int((rel > tol).sum()))
+    if r.max_err > tol:
+        j = int(np.argmax(err))
+        raise AssertionError("%s: error %.3e > %.1e at element %d (gpu %r, oracle %r, rms %.3e)"
+                             % (what, r.max_err, tol, j, a[j], b[j], rms))
+    return r
+
+
+def compare_ratios(gpu: np.ndarray, ref: np.ndarray, what: str, tol: float = RATIO_TOL) -> float:
+    gpu = np.asarray(gpu, np.float64)
+    ref = np.asarray(ref, np.float64)
+    if not np.array_equal(np.isnan(gpu), np.isnan(ref)):
+        raise AssertionError("%s: NaN positions differ" % what)
+    ok = ~np.isnan(ref)
+    g, r = gpu[ok], ref[ok]
+    zero = r == 0
+    if not np.all(g[zero] == 0):
+        raise AssertionError("%s: GPU reports a nonzero value where the oracle has 0" % what)
+    if np.any(~zero):
+        rel = np.abs(g[~zero] - r[~zero]) / np.abs(r[~zero])
+        worst = float(rel.max())
+        if worst > tol:
+            k = int(np.argmax(rel))
+            raise AssertionError("%s: relative error %.3e > %.1e (gpu %r, oracle %r)"
+                                 % (what, worst, tol, g[~zero][k], r[~zero][k]))
+        return worst
+    return 0.0
+
+
+class Pair:
+    """Device state + plan for the HIP path, and host state for the oracle."""
+
+    def __init__(self, xs: Sequence, wd: Sequence[bool], g_dtype: str, algo: str,
+                 chunk_elems: int = 0, oracle_subset: Optional[Sequence[int]] = None):
+        torch = torch_cuda()
+        self.torch = torch
+        self.algo = algo
+        self.n = len(xs)
+        self.wd = [bool(w) for w in wd]
+        dev = torch.device("cuda")
+        gt = torch.bfloat16 if g_dtype == "bf16" else torch.float32
+        self.X = [torch.as_tensor(x).to(dev, torch.float32).contiguous() for x in xs]
+        self.G = [torch.zeros(x.numel(), dtype=gt, device=dev) for x in self.X]
+        self.M = [torch.zeros_like(x) for x in self.X]
+        self.V = [torch.zeros_like(x) for x in self.X] if algo == "lamb" else None
+        self.subset = list(range(self.n)) if oracle_subset is None else list(oracle_subset)
+        self.hx = [paramsets.host_array(self.X[i]).copy() for i in self.subset]
+        self.hm = [np.zeros(self.X[i].numel(), np.float32) for i in self.subset]
+        self.hv = [np.zeros(self.X[i].numel(), np.float32) for i in self.subset]
+        self.ratio = torch.zeros(self.n, dtype=torch.float64, device=dev)
+        self.norms = torch.zeros(2 * self.n, dtype=torch.float64, device=dev)
+        rows = [(self.X[i].data_ptr(), self.G[i].data_ptr(), self.M[i].data_ptr(),
+                 self.V[i].data_ptr() if self.V is not None else 0, self.X[i].numel(),
+                 int(self.wd[i])) for i in range(self.n)]
+        kind = _lib.LAMB_GRAD_BF16 if g_dtype == "bf16" else _lib.LAMB_GRAD_F32
+        algo_id = _lib.LAMB_ALGO_LAMB if algo == "lamb" else _lib.LAMB_ALGO_LARS
+        self.plan = _lib.lamb_plan_create(rows, kind, algo_id, chunk_elems)
+        self.oracle = oracle.load()
+
+    def set_grads(self, grads: Sequence) -> List[np.ndarray]:
+        for G, g in zip(self.G, grads):
+            G.copy_(self.torch.as_tensor(g).reshape(-1).to(G.device))
+        return [paramsets.host_array(self.G[i]).copy() for i in self.subset]
+
+    def gpu_lamb(self, hp: dict, step: int, bias_correction: bool = True) -> None:
+        _lib.lamb_step(self.plan, hp["lr"], hp["beta1"], hp["beta2"], hp["eps"],
+                       hp["weight_decay"], hp["gamma_l"], hp["gamma_u"], step, bias_correction,
+                       self.torch.cuda.current_stream().cuda_stream, self.ratio.data_ptr(),
+                       self.norms.data_ptr())
+
+    def gpu_lars(self, hp: dict) -> None:
+        _lib.lars_step(self.plan, hp["lr"], hp["momentum"], hp["weight_decay"], hp["gamma_l"],
+                       hp["gamma_u"], hp["trust_coef"],
+                       self.torch.cuda.current_stream().cuda_stream, self.ratio.data_ptr(),
+                       self.norms.data_ptr())
+
+    def oracle_lamb(self, hg, hp: dict, step: int, bias_correction: bool = True) -> np.ndarray:
+        return self.oracle.lamb_step(self.hx, hg, self.hm, self.hv,
+                                     [self.wd[i] for i in self.subset], step=step,
+                                     bias_correction=bias_correction, **f32_scalars(hp))
+
+    def oracle_lars(self, hg, hp: dict) -> np.ndarray:
+        return self.oracle.lars_step(self.hx, hg, self.hm, [self.wd[i] for i in self.subset],
+                                     **f32_scalars(hp))
+
+    def compare(self, ref: np.ndarray, label: str) -> Report:
+        """Element-wise state and per-tensor ratio/norm comparison for the subset."""
+        self.torch.cuda.synchronize()
+        rep = Report()
+        ratio = self.ratio.cpu().numpy()
+        norms = self.norms.cpu().numpy().reshape(-1, 2)
+        for k, i in enumerate(self.subset):
+            rep.merge(compare_state(paramsets.host_array(self.X[i]), self.hx[k],
+                                    "%s x[%d]" % (label, i)))
+            rep.merge(compare_state(paramsets.host_array(self.M[i]), self.hm[k],
+                                    "%s m[%d]" % (label, i)))
+            if self.V is not None:
+                rep.merge(compare_state(paramsets.host_array(self.V[i]), self.hv[k],
+                                        "%s v[%d]" % (label, i)))
+        idx = np.asarray(self.subset)
+        compare_ratios(ratio[idx], ref[:, 0], label + " trust ratio")
+        compare_ratios(norms[idx, 0], ref[:, 1], label + " ||x||")
+        compare_ratios(norms[idx, 1], ref[:, 2], label + " ||u||")
+        return rep
+
+    def close(self) -> None:
+        self.plan.close()
+
+
+SCALAR_KEYS = ("lr", "beta1", "beta2", "eps", "weight_decay", "gamma_l", "gamma_u", "momentum",
+               "trust_coef")
+
+
+def f32_scalars(hp: dict) -> dict:
+    """The oracle takes the same fp32-rounded scalars the C ABI receives."""
+    out = {}
+    for k, v in hp.items():
+        out[k] = float(np.float32(v)) if k in SCALAR_KEYS else v
+    return out
+
+
+def lamb_hp(ps: paramsets.ParamSet) -> dict:
+    return dict(lr=ps.lr, beta1=ps.beta1, beta2=ps.beta2, eps=ps.eps,
+                weight_decay=ps.weight_decay, gamma_l=ps.gamma_l, gamma_u=ps.gamma_u)
+
+
+def lars_hp(ps: paramsets.ParamSet) -> dict:
+    return dict(lr=ps.lars_lr, momentum=ps.lars_momentum, weight_decay=ps.weight_decay,
+                gamma_l=ps.gamma_l, gamma_u=ps.gamma_u, trust_coef=ps.lars_trust_coef)
+
+
+def run_config(cfg: int, steps: int, algo: str = "lamb", chunk_elems: int = 0,
+               device: str = "cuda", oracle_subset: Optional[Sequence[int]] = None) -> Report:
+    """Parity over ``steps`` steps of a named parameter set, compared every step."""
+    ps = paramsets.get(cfg)
+    log("parity cfg=%d (%s) algo=%s steps=%d chunk=%d" % (cfg, ps.name, algo, steps, chunk_elems))
+    pair = Pair(paramsets.draw_params(ps, device=device), ps.wd_mask(), ps.g_dtype, algo,
+                chunk_elems, oracle_subset)
+    rep = Report()
+    hp = lamb_hp(ps) if algo == "lamb" else lars_hp(ps)
+    try:
+        for t in range(1, steps + 1):
+            hg = pair.set_grads(paramsets.draw_grads(ps, t, device=device))
+            if algo == "lamb":
+                pair.gpu_lamb(hp, t)
+                ref = pair.oracle_lamb(hg, hp, t)
+            else:
+                pair.gpu_lars(hp)
+                ref = pair.oracle_lars(hg, hp)
+            r = pair.compare(ref, "cfg%d %s step %d" % (cfg, algo, t))
+            log("  step %d: max err %.3e, max abs %.3e, max rel %.3e, rel>1e-5: %d"
+                % (t, r.max_err, r.max_abs, r.max_rel, r.n_rel_over))
+            rep.merge(r)
+    finally:
+        pair.close()
+    return rep

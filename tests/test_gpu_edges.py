@@ -1,0 +1,221 @@
+"""Edge cases of the HIP step against the oracle: ragged sizes around every
+tile boundary, degenerate blocks, special values, flags and validation."""
+
+import math
+
+import numpy as np
+import pytest
+
+import gpu_harness as H
+from paper_1904_00962_amd import _lib
+
+pytestmark = pytest.mark.gpu
+
+DEFAULT = dict(lr=1e-2, beta1=0.9, beta2=0.999, eps=1e-6, weight_decay=0.01, gamma_l=0.0,
+               gamma_u=10.0)
+LARS = dict(lr=1e-2, momentum=0.9, weight_decay=0.01, gamma_l=0.0, gamma_u=10.0, trust_coef=0.01)
+
+
+def _xs(rng, sizes, scale=0.5):
+    return [(rng.standard_normal(n) * scale).astype(np.float32) for n in sizes]
+
+
+def _gs(rng, sizes, g_dtype="f32", scale=1e-3):
+    import torch
+    out = []
+    for n in sizes:
+        t = torch.from_numpy((rng.standard_normal(n) * scale).astype(np.float32))
+        out.append(t.to(torch.bfloat16) if g_dtype == "bf16" else t)
+    return out
+
+
+def _run(xs, wd, g_dtype, algo, chunk, steps, hp, rng, grads=None, bias_correction=True):
+    pair = H.Pair(xs, wd, g_dtype, algo, chunk)
+    try:
+        for t in range(1, steps + 1):
+            gs = grads(t) if grads else _gs(rng, [x.size for x in xs], g_dtype)
+            hg = pair.set_grads(gs)
+            if algo == "lamb":
+                pair.gpu_lamb(hp, t, bias_correction)
+                ref = pair.oracle_lamb(hg, hp, t, bias_correction)
+            else:
+                pair.gpu_lars(hp)
+                ref = pair.oracle_lars(hg, hp)
+            pair.compare(ref, "%s %s chunk=%d step %d" % (algo, g_dtype, chunk, t))
+        return pair
+    finally:
+        pair.close()
+
+
+RAGGED = [1, 2, 3, 4, 5, 7, 8, 9, 15, 16, 17, 255, 256, 257, 1023, 1024, 1025, 1031, 2047,
+          2048, 2049, 4095, 4096, 4097, 8191, 8193]
+
+
+@pytest.mark.parametrize("algo,g_dtype", [("lamb", "f32"), ("lamb", "bf16"), ("lars", "f32"),
+                                          ("lars", "bf16")])
+@pytest.mark.parametrize("chunk", [8, 64, 1024, 0])
+def test_ragged_sizes(algo, g_dtype, chunk):
+    """Every tensor length around the 4-element group, the 256-thread tile,
+    the unrolled loop trip and the chunk boundary."""
+    rng = np.random.default_rng(1000 + chunk)
+    sizes = list(RAGGED)
+    if chunk:
+        sizes += [chunk - 1, chunk, chunk + 1, 4 * chunk + 5]
+    else:
+        sizes += [32767, 32768, 32769, 4 * 32768 + 5]
+    xs = _xs(rng, sizes)
+    wd = [i % 3 != 0 for i in range(len(sizes))]
+    hp = DEFAULT if algo == "lamb" else LARS
+    H.log("ragged algo=%s g=%s chunk=%d tensors=%d" % (algo, g_dtype, chunk, len(sizes)))
+    _run(xs, wd, g_dtype, algo, chunk, 3, hp, rng)
+
+
+def test_zero_gradient_block_does_not_move():
+    """||u|| = 0: ratio exactly 0, x bit for bit unchanged, no NaN."""
+    torch = H.torch_cuda()
+    rng = np.random.default_rng(5)
+    xs = _xs(rng, [100, 37])
+    pair = H.Pair(xs, [False, True], "f32", "lamb")
+    try:
+        hg = pair.set_grads([torch.zeros(100), torch.from_numpy(rng.standard_normal(37).astype(np.float32) * 1e-3)])
+        x0 = pair.X[0].clone()
+        pair.gpu_lamb(DEFAULT, 1)
+        ref = pair.oracle_lamb(hg, DEFAULT, 1)
+        pair.compare(ref, "zero grad")
+        assert torch.equal(pair.X[0], x0)
+        assert float(pair.ratio[0]) == 0.0 and ref[0, 0] == 0.0
+    finally:
+        pair.close()
+
+
+@pytest.mark.parametrize("gamma_l", [0.0, 0.25])
+def test_zero_parameter_block(gamma_l):
+    """phi(0) = gamma_l: a zero block stays put at gamma_l = 0, else moves."""
+    rng = np.random.default_rng(6)
+    xs = [np.zeros(513, np.float32), _xs(rng, [300])[0]]
+    hp = dict(DEFAULT, gamma_l=gamma_l)
+    _run(xs, [True, True], "f32", "lamb", 0, 2, hp, rng)
+    _run(xs, [True, True], "f32", "lars", 0, 2, dict(LARS, gamma_l=gamma_l), rng)
+
+
+def test_nan_gradient_propagates_like_the_oracle():
+    torch = H.torch_cuda()
+    rng = np.random.default_rng(7)
+    xs = _xs(rng, [64, 65])
+    g0 = torch.from_numpy((rng.standard_normal(64) * 1e-3).astype(np.float32))
+    g0[17] = float("nan")
+    g1 = torch.from_numpy((rng.standard_normal(65) * 1e-3).astype(np.float32))
+    pair = H.Pair(xs, [True, True], "f32", "lamb")
+    try:
+        hg = pair.set_grads([g0, g1])
+        pair.gpu_lamb(DEFAULT, 1)
+        ref = pair.oracle_lamb(hg, DEFAULT, 1)
+        pair.compare(ref, "nan grad")
+        assert np.isnan(ref[0, 0]) and math.isnan(float(pair.ratio[0]))
+    finally:
+        pair.close()
+
+
+@pytest.mark.parametrize("hp", [
+    dict(DEFAULT, gamma_u=float("inf")),
+    dict(DEFAULT, gamma_l=5.0, gamma_u=5.0),
+    dict(DEFAULT, beta1=0.0, beta2=0.0, eps=0.0, weight_decay=0.0),
+    dict(DEFAULT, eps=0.0),
+    dict(DEFAULT, weight_decay=0.5, lr=0.3),
+], ids=["no-upper-clamp", "phi-const", "sign-sgd", "eps0", "big-lr-wd"])
+def test_scalar_settings(hp):
+    rng = np.random.default_rng(8)
+    xs = _xs(rng, [4096, 333, 9, 1], scale=2.0)
+    _run(xs, [True, False, True, True], "f32", "lamb", 1024, 4, hp, rng)
+
+
+def test_without_bias_correction():
+    rng = np.random.default_rng(9)
+    xs = _xs(rng, [5000, 77])
+    _run(xs, [True, False], "bf16", "lamb", 2048, 4, DEFAULT, rng, bias_correction=False)
+
+
+def test_lars_trust_coefficient_one_and_no_momentum():
+    rng = np.random.default_rng(10)
+    xs = _xs(rng, [3000, 5])
+    _run(xs, [True, False], "f32", "lars", 0, 3, dict(LARS, trust_coef=1.0, momentum=0.0), rng)
+
+
+def test_guard_bands_untouched():
+    """Tensors carved out of one buffer with canary gaps between them: no
+    kernel writes outside its tensors."""
+    torch = H.torch_cuda()
+    sizes = [1, 7, 1000, 4097, 33]
+    gap = 64
+    total = sum(sizes) + gap * (len(sizes) + 1)
+    bufs = {k: torch.full((total,), -7.25, device="cuda") for k in "xgmv"}
+    views = {k: [] for k in "xgmv"}
+    off = gap
+    rng = np.random.default_rng(11)
+    for n in sizes:
+        for k in "xgmv":
+            views[k].append(bufs[k][off:off + n])
+        views["x"][-1].copy_(torch.from_numpy(rng.standard_normal(n).astype(np.float32)))
+        views["g"][-1].copy_(torch.from_numpy(rng.standard_normal(n).astype(np.float32) * 1e-3))
+        views["m"][-1].zero_()
+        views["v"][-1].zero_()
+        off += n + gap
+        off = (off + 3) // 4 * 4  # keep every tensor 16-byte aligned
+    canary = {k: bufs[k].clone() for k in "xgmv"}
+    mask = torch.ones(total, dtype=torch.bool, device="cuda")
+    for k in "xgmv":
+        for v in views[k]:
+            start = (v.data_ptr() - bufs[k].data_ptr()) // 4
+            mask[start:start + v.numel()] = False
+    rows = [(views["x"][i].data_ptr(), views["g"][i].data_ptr(), views["m"][i].data_ptr(),
+             views["v"][i].data_ptr(), sizes[i], 1) for i in range(len(sizes))]
+    with _lib.lamb_plan_create(rows, _lib.LAMB_GRAD_F32, _lib.LAMB_ALGO_LAMB, 8) as plan:
+        for t in range(1, 4):
+            _lib.lamb_step(plan, 0.01, 0.9, 0.999, 1e-6, 0.01, 0.0, 10.0, t, True,
+                           torch.cuda.current_stream().cuda_stream)
+        torch.cuda.synchronize()
+    for k in "xgmv":
+        assert torch.equal(bufs[k][mask], canary[k][mask]), "canary overwritten in " + k
+    assert not torch.equal(bufs["x"], canary["x"])
+
+
+def test_validation_leaves_state_untouched():
+    torch = H.torch_cuda()
+    rng = np.random.default_rng(12)
+    pair = H.Pair(_xs(rng, [100]), [True], "f32", "lamb")
+    lars = H.Pair(_xs(rng, [100]), [True], "f32", "lars")
+    try:
+        pair.set_grads(_gs(rng, [100]))
+        x0 = pair.X[0].clone()
+        s = torch.cuda.current_stream().cuda_stream
+        bad = [
+            dict(step=0), dict(beta1=1.0), dict(beta2=-0.1), dict(eps=-1e-6),
+            dict(lr=float("nan")), dict(weight_decay=float("inf")), dict(gamma_l=2.0, gamma_u=1.0),
+            dict(gamma_l=-1.0), dict(gamma_u=float("nan")), dict(bias_correction=2),
+        ]
+        for b in bad:
+            a = dict(DEFAULT, step=1, bias_correction=1)
+            a.update(b)
+            with pytest.raises(_lib.LambError) as e:
+                _lib.load()
+                st = _lib.load().lamb_step(_lib._vp(pair.plan.handle), a["lr"], a["beta1"],
+                                          a["beta2"], a["eps"], a["weight_decay"], a["gamma_l"],
+                                          a["gamma_u"], a["step"], a["bias_correction"],
+                                          _lib._vp(s), None, None)
+                _lib._check(st, "lamb_step")
+            assert e.value.status == _lib.LAMB_EINVAL, b
+        with pytest.raises(_lib.LambError) as e:
+            _lib.lars_step(pair.plan, 0.01, 0.9, 0.01, 0.0, 10.0, 0.01, s)
+        assert e.value.status == _lib.LAMB_EPLAN
+        with pytest.raises(_lib.LambError) as e:
+            _lib.lamb_step(lars.plan, 0.01, 0.9, 0.999, 1e-6, 0.01, 0.0, 10.0, 1, True, s)
+        assert e.value.status == _lib.LAMB_EPLAN
+        with pytest.raises(_lib.LambError) as e:
+            _lib.lars_step(lars.plan, 0.01, 1.5, 0.01, 0.0, 10.0, 0.01, s)
+        assert e.value.status == _lib.LAMB_EINVAL
+        torch.cuda.synchronize()
+        assert torch.equal(pair.X[0], x0)
+        assert not torch.any(pair.M[0] != 0)
+    finally:
+        pair.close()
+        lars.close()

@@ -1,0 +1,156 @@
+"""Properties of the HIP step that need no oracle: bitwise determinism,
+chunk-size invariance, per-layer independence, resume, timing hooks and
+the optimizer facade."""
+
+import numpy as np
+import pytest
+
+import gpu_harness as H
+from paper_1904_00962_amd import _lib, paramsets
+
+pytestmark = pytest.mark.gpu
+
+
+def _state(pair):
+    out = [x.clone() for x in pair.X] + [m.clone() for m in pair.M]
+    if pair.V is not None:
+        out += [v.clone() for v in pair.V]
+    return out + [pair.ratio.clone()]
+
+
+def _steps(cfg, algo, chunk, steps, device="cuda", subset=None):
+    ps = paramsets.get(cfg)
+    xs = paramsets.draw_params(ps, indices=subset, device=device)
+    wd = ps.wd_mask() if subset is None else [ps.wd_mask()[i] for i in subset]
+    pair = H.Pair(xs, wd, ps.g_dtype, algo, chunk, oracle_subset=[])
+    hp = H.lamb_hp(ps) if algo == "lamb" else H.lars_hp(ps)
+    for t in range(1, steps + 1):
+        pair.set_grads(paramsets.draw_grads(ps, t, indices=subset, device=device))
+        if algo == "lamb":
+            pair.gpu_lamb(hp, t)
+        else:
+            pair.gpu_lars(hp)
+    return pair
+
+
+@pytest.mark.parametrize("cfg,algo", [(2, "lamb"), (3, "lars")])
+def test_bitwise_deterministic(cfg, algo):
+    torch = H.torch_cuda()
+    runs = []
+    for _ in range(2):
+        pair = _steps(cfg, algo, 0, 2)
+        runs.append(_state(pair))
+        pair.close()
+    for a, b in zip(*runs):
+        assert torch.equal(a, b)
+
+
+def test_chunk_size_invariance():
+    """m and v are elementwise, so they do not depend on the chunking at all;
+    x and the ratios agree to rounding of the reduction order."""
+    torch = H.torch_cuda()
+    runs = [_state(_steps(1, "lamb", c, 2)) for c in (0, 4096, 65536)]
+    n = paramsets.get(1).n_tensors
+    for other in runs[1:]:
+        for k in range(n, 3 * n):
+            assert torch.equal(runs[0][k], other[k])
+        for k in range(n):
+            H.compare_state(other[k].cpu().numpy(), runs[0][k].cpu().numpy(), "x[%d]" % k)
+        H.compare_ratios(other[-1].cpu().numpy(), runs[0][-1].cpu().numpy(), "ratio")
+
+
+def test_layer_independence():
+    """A step on {A, B} equals a step on {A} and a step on {B}, bit for bit."""
+    torch = H.torch_cuda()
+    ps = paramsets.get(0)
+    joint = _steps(0, "lamb", 1024, 3)
+    parts = [_steps(0, "lamb", 1024, 3, subset=[i]) for i in range(ps.n_tensors)]
+    for i, p in enumerate(parts):
+        assert torch.equal(joint.X[i], p.X[0])
+        assert torch.equal(joint.M[i], p.M[0])
+        assert torch.equal(joint.V[i], p.V[0])
+        assert torch.equal(joint.ratio[i], p.ratio[0])
+
+
+def test_resume_is_bitwise():
+    """The caller owns x, m, v and t: 6 steps equal 3 steps, a copy out and
+    into a fresh optimizer, and 3 more."""
+    torch = H.torch_cuda()
+    from paper_1904_00962_amd.optim import LAMB
+    ps = paramsets.get(3)
+    x0 = paramsets.draw_params(ps, device="cuda")
+    grads = [torch.zeros(x.numel(), device="cuda") for x in x0]
+
+    def run(opt, t0, t1):
+        for t in range(t0, t1):
+            for g, d in zip(grads, paramsets.draw_grads(ps, t, device="cuda")):
+                g.copy_(d)
+            opt.step()
+
+    p1 = [x.clone() for x in x0]
+    a = LAMB(p1, grads, lr=ps.lr)
+    run(a, 1, 7)
+    p2 = [x.clone() for x in x0]
+    b = LAMB(p2, grads, lr=ps.lr)
+    run(b, 1, 4)
+    saved = ([x.clone() for x in p2], b.state_dict())
+    b.close()
+    p3 = [x.clone() for x in saved[0]]
+    c = LAMB(p3, grads, lr=ps.lr)
+    c.load_state_dict(saved[1])
+    run(c, 4, 7)
+    torch.cuda.synchronize()
+    for u, w in zip(p1, p3):
+        assert torch.equal(u, w)
+    a.close()
+    c.close()
+
+
+def test_timing_hooks_record_each_kernel():
+    torch = H.torch_cuda()
+    pair = _steps(0, "lamb", 0, 0)
+    ps = paramsets.get(0)
+    _lib.lamb_plan_set_timing(pair.plan, 8)
+    pair.set_grads(paramsets.draw_grads(ps, 1, device="cuda"))
+    for t in range(1, 6):
+        pair.gpu_lamb(H.lamb_hp(ps), t)
+    ms, steps = _lib.lamb_plan_timing(pair.plan)
+    assert steps == 5 and all(v > 0 for v in ms)
+    ms2, steps2 = _lib.lamb_plan_timing(pair.plan)
+    assert steps2 == 0
+    _lib.lamb_plan_set_timing(pair.plan, 0)
+    pair.close()
+
+
+def test_facade_matches_oracle():
+    torch = H.torch_cuda()
+    import oracle
+    from paper_1904_00962_amd.optim import LAMB, LARS
+    ps = paramsets.get(0)
+    for cls in (LAMB, LARS):
+        xs = paramsets.draw_params(ps, device="cuda")
+        grads = [torch.zeros(x.numel(), device="cuda") for x in xs]
+        hx = [paramsets.host_array(x).copy() for x in xs]
+        hm = [np.zeros_like(h) for h in hx]
+        hv = [np.zeros_like(h) for h in hx]
+        if cls is LAMB:
+            opt = LAMB(xs, grads, lr=ps.lr)
+        else:
+            opt = LARS(xs, grads, lr=ps.lars_lr, trust_coef=ps.lars_trust_coef)
+        for t in (1, 2):
+            for g, d in zip(grads, paramsets.draw_grads(ps, t, device="cuda")):
+                g.copy_(d)
+            hg = [paramsets.host_array(g).copy() for g in grads]
+            opt.step()
+            if cls is LAMB:
+                ref = oracle.load().lamb_step(hx, hg, hm, hv, ps.wd_mask(), step=t,
+                                              **H.f32_scalars(H.lamb_hp(ps)))
+            else:
+                hp = dict(lr=ps.lars_lr, momentum=0.9, weight_decay=0.01, gamma_l=0.0,
+                          gamma_u=10.0, trust_coef=ps.lars_trust_coef)
+                ref = oracle.load().lars_step(hx, hg, hm, ps.wd_mask(), **H.f32_scalars(hp))
+            torch.cuda.synchronize()
+            for i in range(ps.n_tensors):
+                H.compare_state(paramsets.host_array(xs[i]), hx[i], "facade x")
+            H.compare_ratios(opt.ratios.cpu().numpy(), ref[:, 0], "facade ratio")
+        opt.close()
