@@ -55,11 +55,16 @@ class lamb_tensor(ctypes.Structure):
 _lib: Optional[ctypes.CDLL] = None
 
 
-def load(path: str = LIBRARY) -> ctypes.CDLL:
-    """Open the HIP library (once). Raises if it has not been built."""
+def load(path: Optional[str] = None) -> ctypes.CDLL:
+    """Open the HIP library (once). Raises if it has not been built.
+
+    ``LAMB_MI355X_LIBRARY`` may name another build of the same library (for
+    comparing compile-time variants); the default is the in-tree build.
+    """
     global _lib
     if _lib is not None:
         return _lib
+    path = path or os.environ.get("LAMB_MI355X_LIBRARY") or LIBRARY
     if not os.path.exists(path):
         raise RuntimeError("HIP library %s is missing; run `python -m paper_1904_00962_amd.build` "
                            "(there is no CPU fallback)" % path)

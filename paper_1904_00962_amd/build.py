@@ -36,9 +36,11 @@ def hipcc() -> str:
     return path
 
 
-def build(output: str = LIBRARY, verbose: bool = False) -> str:
+def build(output: str = LIBRARY, verbose: bool = False, defines=()) -> str:
+    """Compile the library; ``defines`` are extra -D flags (tuning variants)."""
     tmp = output + ".tmp%d" % os.getpid()
-    cmd = [hipcc(), *HIPCC_FLAGS, "-I", INCLUDE, "-I", CSRC, *SOURCES, "-o", tmp]
+    cmd = [hipcc(), *HIPCC_FLAGS, *["-D" + d for d in defines], "-I", INCLUDE, "-I", CSRC,
+           *SOURCES, "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     proc = subprocess.run(cmd, capture_output=True, text=True)

@@ -10,9 +10,15 @@ namespace lamb_mi355x {
 
 // Work is cut into chunks of at most `chunk_elems` elements of one tensor;
 // one workgroup of kBlock threads handles one chunk. kBlock = 4 wave64s.
-constexpr int kBlock = 256;
+#ifndef LAMB_BLOCK
+#define LAMB_BLOCK 256
+#endif
+#ifndef LAMB_DEFAULT_CHUNK
+#define LAMB_DEFAULT_CHUNK 512
+#endif
+constexpr int kBlock = LAMB_BLOCK;
 constexpr int kWaves = kBlock / 64;
-constexpr int32_t kDefaultChunkElems = 32768;
+constexpr int32_t kDefaultChunkElems = LAMB_DEFAULT_CHUNK;
 
 // One layer block x^(i) (Section 2) as the kernels see it. 64 bytes.
 struct TensorDesc {

@@ -44,15 +44,50 @@ typedef LAMB_GLOBAL const uint16_t gcbf16;
 __device__ __forceinline__ gfloat *global_view(float *p) { return (gfloat *)p; }
 __device__ __forceinline__ gcfloat *global_view(const float *p) { return (gcfloat *)p; }
 
-// float4 groups each thread keeps in flight per loop trip.
-constexpr int kUnroll = 4;
+// Tuning knobs (compile-time; the defaults are the measured best on MI355X).
+// LAMB_UNROLL: float4 groups each thread keeps in flight per loop trip.
+// LAMB_NONTEMPORAL: stream x, g, m, v with nontemporal loads and stores; the
+//   data is touched once per pass, so it should not displace cache lines.
+// LAMB_APPLY_REVERSE: the apply pass walks chunks last-to-first, so its first
+//   reads are the lines the moment pass touched last (still in the caches).
+#ifndef LAMB_UNROLL
+#define LAMB_UNROLL 2
+#endif
+#ifndef LAMB_NONTEMPORAL
+#define LAMB_NONTEMPORAL 1
+#endif
+#ifndef LAMB_APPLY_REVERSE
+#define LAMB_APPLY_REVERSE 1
+#endif
+#ifndef LAMB_XCD_CONTIGUOUS
+#define LAMB_XCD_CONTIGUOUS 0
+#endif
+constexpr int kUnroll = LAMB_UNROLL;
+
+template <typename T>
+__device__ __forceinline__ T stream_load(LAMB_GLOBAL const T *p) {
+#if LAMB_NONTEMPORAL
+    return __builtin_nontemporal_load(p);
+#else
+    return *p;
+#endif
+}
+
+template <typename T>
+__device__ __forceinline__ void stream_store(LAMB_GLOBAL T *p, T v) {
+#if LAMB_NONTEMPORAL
+    __builtin_nontemporal_store(v, p);
+#else
+    *p = v;
+#endif
+}
 
 __device__ __forceinline__ f32x4 load4(gcfloat *p) {
-    return *(LAMB_GLOBAL const f32x4 *)p;
+    return stream_load((LAMB_GLOBAL const f32x4 *)p);
 }
 
 __device__ __forceinline__ void store4(gfloat *p, f32x4 v) {
-    *(LAMB_GLOBAL f32x4 *)p = v;
+    stream_store((LAMB_GLOBAL f32x4 *)p, v);
 }
 
 // The gradient of one chunk: fp32, or bf16 bit patterns that widen exactly
@@ -74,7 +109,7 @@ struct GradView {
     // elements i..i+3, i a multiple of 4
     __device__ __forceinline__ f32x4 at4(int i) const {
         if constexpr (kBf16) {
-            const u32x2 w = *(LAMB_GLOBAL const u32x2 *)((gcbf16 *)base + i);
+            const u32x2 w = stream_load((LAMB_GLOBAL const u32x2 *)((gcbf16 *)base + i));
             f32x4 r;
             r.x = __uint_as_float(w.x << 16);
             r.y = __uint_as_float(w.x & 0xffff0000u);
@@ -129,10 +164,12 @@ __device__ __forceinline__ double wave_sum(double v) {
     return v;
 }
 
-// Sum (a, b) over the workgroup in a fixed tree and store it at `out`.
-__device__ __forceinline__ void store_block_sums(double a, double b, Partial *out) {
-    __shared__ double red_a[kWaves];
-    __shared__ double red_b[kWaves];
+// Sum (a, b) over a workgroup of kNumWaves wave64s in a fixed tree and store
+// it at `out` (thread 0 writes).
+template <int kNumWaves>
+__device__ __forceinline__ void block_sums(double a, double b, Partial *out) {
+    __shared__ double red_a[kNumWaves];
+    __shared__ double red_b[kNumWaves];
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
     a = wave_sum(a);
@@ -145,13 +182,40 @@ __device__ __forceinline__ void store_block_sums(double a, double b, Partial *ou
     if (threadIdx.x == 0) {
         double sa = red_a[0], sb = red_b[0];
 #pragma unroll
-        for (int w = 1; w < kWaves; ++w) {
+        for (int w = 1; w < kNumWaves; ++w) {
             sa += red_a[w];
             sb += red_b[w];
         }
         out->sum_xx = sa;
         out->sum_uu = sb;
     }
+}
+
+// Workgroups are dispatched round-robin over the 8 XCDs. With
+// LAMB_XCD_CONTIGUOUS each XCD takes one contiguous eighth of the chunk list
+// instead of every eighth chunk.
+__device__ __forceinline__ uint32_t dispatch_rank() {
+#if LAMB_XCD_CONTIGUOUS
+    const uint32_t n = gridDim.x, b = blockIdx.x;
+    const uint32_t per = n / 8, extra = n % 8;  // XCDs 0..extra-1 get one more
+    const uint32_t xcd = b % 8, k = b / 8;
+    const uint32_t first = xcd * per + (xcd < extra ? xcd : extra);
+    return first + k;
+#else
+    return blockIdx.x;
+#endif
+}
+
+// Chunk handled by this workgroup of a moment pass.
+__device__ __forceinline__ uint32_t chunk_index() { return dispatch_rank(); }
+
+// Chunk handled by this workgroup of an apply pass.
+__device__ __forceinline__ uint32_t apply_chunk_index() {
+#if LAMB_APPLY_REVERSE
+    return gridDim.x - 1 - dispatch_rank();
+#else
+    return dispatch_rank();
+#endif
 }
 
 // ---------------------------------------------------------------------------
@@ -162,7 +226,7 @@ template <bool kBf16>
 __global__ __launch_bounds__(kBlock) void lamb_moments_kernel(
     const TensorDesc *__restrict__ tensors, const ChunkDesc *__restrict__ chunks,
     Partial *__restrict__ partials, LambArgs a) {
-    const ChunkDesc c = chunks[blockIdx.x];
+    const ChunkDesc c = chunks[chunk_index()];
     const TensorDesc &t = tensors[c.tensor];
     gcfloat *x = global_view(t.x + c.start);
     gfloat *m = global_view(t.m + c.start);
@@ -216,13 +280,13 @@ __global__ __launch_bounds__(kBlock) void lamb_moments_kernel(
         sum_xx = fma(xd, xd, sum_xx);
         sum_uu = fma(ud, ud, sum_uu);
     }
-    store_block_sums(sum_xx, sum_uu, partials + blockIdx.x);
+    block_sums<kWaves>(sum_xx, sum_uu, partials + chunk_index());
 }
 
 __global__ __launch_bounds__(kBlock) void lamb_apply_kernel(
     const TensorDesc *__restrict__ tensors, const ChunkDesc *__restrict__ chunks,
     const float *__restrict__ scale, LambArgs a) {
-    const ChunkDesc c = chunks[blockIdx.x];
+    const ChunkDesc c = chunks[apply_chunk_index()];
     const TensorDesc &t = tensors[c.tensor];
     gfloat *x = global_view(t.x + c.start);
     gcfloat *m = global_view(static_cast<const float *>(t.m) + c.start);
@@ -267,7 +331,7 @@ template <bool kBf16>
 __global__ __launch_bounds__(kBlock) void lars_moments_kernel(
     const TensorDesc *__restrict__ tensors, const ChunkDesc *__restrict__ chunks,
     Partial *__restrict__ partials, LarsArgs a) {
-    const ChunkDesc c = chunks[blockIdx.x];
+    const ChunkDesc c = chunks[chunk_index()];
     const TensorDesc &t = tensors[c.tensor];
     gcfloat *x = global_view(static_cast<const float *>(t.x) + c.start);
     gfloat *m = global_view(t.m + c.start);
@@ -312,13 +376,13 @@ __global__ __launch_bounds__(kBlock) void lars_moments_kernel(
         sum_xx = fma(xd, xd, sum_xx);
         sum_mm = fma(md, md, sum_mm);
     }
-    store_block_sums(sum_xx, sum_mm, partials + blockIdx.x);
+    block_sums<kWaves>(sum_xx, sum_mm, partials + chunk_index());
 }
 
 __global__ __launch_bounds__(kBlock) void lars_apply_kernel(
     const TensorDesc *__restrict__ tensors, const ChunkDesc *__restrict__ chunks,
     const float *__restrict__ scale) {
-    const ChunkDesc c = chunks[blockIdx.x];
+    const ChunkDesc c = chunks[apply_chunk_index()];
     const TensorDesc &t = tensors[c.tensor];
     gfloat *x = global_view(t.x + c.start);
     gcfloat *m = global_view(static_cast<const float *>(t.m) + c.start);
@@ -353,31 +417,53 @@ __global__ __launch_bounds__(kBlock) void lars_apply_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// Per-tensor finalize: norms, phi, trust ratio, step scale. One wave64 per
-// tensor; lane l sums chunk slots l, l + 64, ... in order, then a fixed
-// butterfly combines the lanes.
+// Per-tensor finalize: norms, phi, trust ratio, step scale. One workgroup of
+// kFinalizeBlock threads per tensor. Thread k owns slots k + j*kFinalizeBlock
+// and sums them into kFinalizeLanes independent accumulators (so several
+// loads are in flight), which it then adds in a fixed order; the fixed
+// wave/LDS tree combines the threads. The order never depends on timing.
 // ---------------------------------------------------------------------------
 
-__global__ __launch_bounds__(kBlock) void finalize_kernel(
-    const TensorDesc *__restrict__ tensors, int32_t n_tensors,
-    const Partial *__restrict__ partials, FinalizeArgs a, float *__restrict__ scale,
-    double *__restrict__ ratio_out, double *__restrict__ norms_out) {
-    const int lane = threadIdx.x & 63;
-    const int i = blockIdx.x * kWaves + (threadIdx.x >> 6);
-    if (i >= n_tensors)
-        return;  // the whole wave leaves together; no barrier follows
+constexpr int kFinalizeBlock = 1024;
+constexpr int kFinalizeLanes = 16;
+
+__global__ __launch_bounds__(kFinalizeBlock) void finalize_kernel(
+    const TensorDesc *__restrict__ tensors, const Partial *__restrict__ partials,
+    FinalizeArgs a, float *__restrict__ scale, double *__restrict__ ratio_out,
+    double *__restrict__ norms_out) {
+    const int i = blockIdx.x;
     const TensorDesc &t = tensors[i];
-    double sx = 0.0, su = 0.0;
-    for (int k = lane; k < t.n_chunks; k += 64) {
-        const Partial p = partials[t.first_chunk + k];
-        sx += p.sum_xx;
-        su += p.sum_uu;
+    const Partial *p = partials + t.first_chunk;
+    const int n = t.n_chunks;
+    double sx[kFinalizeLanes] = {}, su[kFinalizeLanes] = {};
+    int k = threadIdx.x;
+    for (; k + (kFinalizeLanes - 1) * kFinalizeBlock < n; k += kFinalizeLanes * kFinalizeBlock) {
+#pragma unroll
+        for (int j = 0; j < kFinalizeLanes; ++j) {
+            const Partial q = p[k + j * kFinalizeBlock];
+            sx[j] += q.sum_xx;
+            su[j] += q.sum_uu;
+        }
     }
-    sx = wave_sum(sx);
-    su = wave_sum(su);
-    if (lane == 0) {
-        const double norm_x = sqrt(sx);
-        const double norm_u = sqrt(su);
+#pragma unroll
+    for (int j = 0; j < kFinalizeLanes - 1; ++j) {
+        if (k + j * kFinalizeBlock < n) {
+            const Partial q = p[k + j * kFinalizeBlock];
+            sx[j] += q.sum_xx;
+            su[j] += q.sum_uu;
+        }
+    }
+#pragma unroll
+    for (int j = 1; j < kFinalizeLanes; ++j) {
+        sx[0] += sx[j];
+        su[0] += su[j];
+    }
+    __shared__ Partial total;
+    block_sums<kFinalizeBlock / 64>(sx[0], su[0], &total);
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        const double norm_x = sqrt(total.sum_xx);
+        const double norm_u = sqrt(total.sum_uu);
         // phi(z) = min(max(z, gamma_l), gamma_u), Section 3; comparisons keep NaN.
         double phi = norm_x;
         if (phi < a.gamma_l)
@@ -442,10 +528,9 @@ hipError_t launch_finalize(const TensorDesc *tensors, int32_t n_tensors,
                            const Partial *partials, const FinalizeArgs &args, float *scale,
                            double *ratio_out, double *norms_out, hipStream_t stream) {
     FinalizeArgs a = args;
-    void *params[] = {&tensors, &n_tensors, &partials, &a, &scale, &ratio_out, &norms_out};
-    const int blocks = (n_tensors + kWaves - 1) / kWaves;
-    return hipLaunchKernel(reinterpret_cast<const void *>(&finalize_kernel), dim3(blocks),
-                           dim3(kBlock), params, 0, stream);
+    void *params[] = {&tensors, &partials, &a, &scale, &ratio_out, &norms_out};
+    return hipLaunchKernel(reinterpret_cast<const void *>(&finalize_kernel), dim3(n_tensors),
+                           dim3(kFinalizeBlock), params, 0, stream);
 }
 
 }  // namespace lamb_mi355x

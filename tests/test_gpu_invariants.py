@@ -87,16 +87,17 @@ def test_resume_is_bitwise():
                 g.copy_(d)
             opt.step()
 
+    mask = ps.wd_mask()
     p1 = [x.clone() for x in x0]
-    a = LAMB(p1, grads, lr=ps.lr)
+    a = LAMB(p1, grads, lr=ps.lr, wd_mask=mask)
     run(a, 1, 7)
     p2 = [x.clone() for x in x0]
-    b = LAMB(p2, grads, lr=ps.lr)
+    b = LAMB(p2, grads, lr=ps.lr, wd_mask=mask)
     run(b, 1, 4)
     saved = ([x.clone() for x in p2], b.state_dict())
     b.close()
     p3 = [x.clone() for x in saved[0]]
-    c = LAMB(p3, grads, lr=ps.lr)
+    c = LAMB(p3, grads, lr=ps.lr, wd_mask=mask)
     c.load_state_dict(saved[1])
     run(c, 4, 7)
     torch.cuda.synchronize()
@@ -133,10 +134,12 @@ def test_facade_matches_oracle():
         hx = [paramsets.host_array(x).copy() for x in xs]
         hm = [np.zeros_like(h) for h in hx]
         hv = [np.zeros_like(h) for h in hx]
+        # the tensors are flat, so the mask is given (the default reads dim() > 1)
         if cls is LAMB:
-            opt = LAMB(xs, grads, lr=ps.lr)
+            opt = LAMB(xs, grads, lr=ps.lr, wd_mask=ps.wd_mask())
         else:
-            opt = LARS(xs, grads, lr=ps.lars_lr, trust_coef=ps.lars_trust_coef)
+            opt = LARS(xs, grads, lr=ps.lars_lr, trust_coef=ps.lars_trust_coef,
+                       wd_mask=ps.wd_mask())
         for t in (1, 2):
             for g, d in zip(grads, paramsets.draw_grads(ps, t, device="cuda")):
                 g.copy_(d)
