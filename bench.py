@@ -28,6 +28,7 @@ if ROOT not in sys.path:
 METRIC = "LAMB step: params updated/sec + achieved HBM GB/s (% peak), BERT-Large fp32"
 HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, published
 PROFILES = os.path.join(ROOT, "profiles")
+NLAMB_BETA1, NLAMB_EPS = 0.975, 1e-8  # N-LAMB / NN-LAMB settings (Appendix D)
 
 
 def eprint(*a):
@@ -38,11 +39,13 @@ def bytes_per_param(algo: str, g_bytes: int):
     """Algorithmic HBM bytes per parameter of (moment pass, apply pass).
 
     LAMB moment pass reads x, g, m, v and writes m, v; apply reads x, m, v and
-    writes x. LARS moment pass reads x, g, m and writes m; apply reads x, m
-    and writes x.
+    writes x (N-LAMB and NN-LAMB also read g there). LARS moment pass reads x,
+    g, m and writes m; apply reads x, m and writes x.
     """
     if algo == "lamb":
         return 4 + g_bytes + 4 + 4 + 4 + 4, 4 + 4 + 4 + 4
+    if algo in ("nlamb", "nnlamb"):  # the Nesterov update also needs g in the apply pass
+        return 4 + g_bytes + 4 + 4 + 4 + 4, 4 + g_bytes + 4 + 4 + 4
     return 4 + g_bytes + 4 + 4, 4 + 4 + 4
 
 
@@ -129,6 +132,11 @@ def cpu_baseline(ps, sample, algo, budget_s: float):
             o.lamb_step(hx, hg, hm, hv, wd, lr=f(ps.lr), beta1=f(ps.beta1), beta2=f(ps.beta2),
                         eps=f(ps.eps), weight_decay=f(ps.weight_decay), gamma_l=f(ps.gamma_l),
                         gamma_u=f(ps.gamma_u), step=done + 1)
+        elif algo in ("nlamb", "nnlamb"):
+            o.nlamb_step(hx, hg, hm, hv, wd, lr=f(ps.lr), beta1=f(NLAMB_BETA1), beta2=f(ps.beta2),
+                         eps=f(NLAMB_EPS), weight_decay=f(ps.weight_decay),
+                         gamma_l=f(ps.gamma_l), gamma_u=f(ps.gamma_u), step=done + 1,
+                         nesterov_v=algo == "nnlamb")
         else:
             o.lars_step(hx, hg, hm, wd, lr=f(ps.lars_lr), momentum=f(ps.lars_momentum),
                         weight_decay=f(ps.weight_decay), gamma_l=f(ps.gamma_l),
@@ -148,7 +156,7 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--config", type=int, default=2)
-    ap.add_argument("--algo", choices=("lamb", "lars"), default="lamb")
+    ap.add_argument("--algo", choices=("lamb", "lars", "nlamb", "nnlamb"), default="lamb")
     ap.add_argument("--chunk", type=int, default=0, help="elements per chunk (0 = default)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -182,6 +190,11 @@ def main() -> int:
         opt = LAMB(xs, grads, lr=ps.lr, betas=(ps.beta1, ps.beta2), eps=ps.eps,
                    weight_decay=ps.weight_decay, clamp=(ps.gamma_l, ps.gamma_u),
                    wd_mask=ps.wd_mask(), chunk_elems=args.chunk)
+    elif args.algo in ("nlamb", "nnlamb"):
+        opt = LAMB(xs, grads, lr=ps.lr, betas=(NLAMB_BETA1, ps.beta2), eps=NLAMB_EPS,
+                   weight_decay=ps.weight_decay, clamp=(ps.gamma_l, ps.gamma_u),
+                   wd_mask=ps.wd_mask(), chunk_elems=args.chunk,
+                   variant="n-lamb" if args.algo == "nlamb" else "nn-lamb")
     else:
         opt = LARS(xs, grads, lr=ps.lars_lr, momentum=ps.lars_momentum,
                    weight_decay=ps.weight_decay, clamp=(ps.gamma_l, ps.gamma_u),
@@ -230,7 +243,9 @@ def main() -> int:
     workload = ps.name
     src_hash = kernel_source_hash()
     traffic = counter_traffic(workload, src_hash) if args.algo == "lamb" else None
-    kernel = "%s_moments_kernel<%s>" % (args.algo, "bf16" if g_bytes == 2 else "f32")
+    algo_name = {"lamb": "LAMB", "lars": "LARS", "nlamb": "N-LAMB", "nnlamb": "NN-LAMB"}[args.algo]
+    kernel = "%s_moments_kernel<%s>" % ("lars" if args.algo == "lars" else "lamb",
+                                        "bf16" if g_bytes == 2 else "f32")
     eprint("step %.4f ms | moments %.4f ms (%.0f GB/s) | finalize %.4f ms | apply %.4f ms "
            "(%.0f GB/s) | whole step %.0f GB/s" % (ms_step, avg_mom, mom_gbps, avg_fin, avg_app,
                                                    app_gbps, step_gbps))
@@ -249,7 +264,7 @@ def main() -> int:
         "data": "synthetic",
         "config": {
             "workload": "%s %s step: %d tensors, %d fp32 params, %s gradients"
-                        % (workload, args.algo.upper(), n_tensors, P, ps.g_dtype),
+                        % (workload, algo_name, n_tensors, P, ps.g_dtype),
             "algo": args.algo, "tensors": n_tensors, "params": P, "grad_dtype": ps.g_dtype,
             "chunk_elems": chunk, "chunks": n_chunks, "seed_x": 1000 * ps.cfg,
             "seed_g": 1000 * ps.cfg + 1,

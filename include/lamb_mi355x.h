@@ -131,6 +131,25 @@ LAMB_API lamb_status lamb_step(lamb_plan *plan, float lr, float beta1, float bet
                       void *stream, double *ratio_out, double *norms_out);
 
 /*
+ * One N-LAMB step (Algorithm 3, Appendix D) or, with nesterov_v = 1, one
+ * NN-LAMB step (Algorithm 4) over every block of a LAMB plan, at step t:
+ *   m <- beta1 m + (1 - beta1) g ;  v <- beta2 v + (1 - beta2) g^2
+ *   m_hat = beta1 m / (1 - beta1^(t+1)) + (1 - beta1) g / (1 - beta1^t)
+ *   v_hat = beta2 v / (1 - beta2^t)                                  (N-LAMB)
+ *   v_hat = beta2 v / (1 - beta2^(t+1)) + (1 - beta2) g^2 / (1 - beta2^t)
+ *                                                                    (NN-LAMB)
+ *   u = m_hat / (sqrt(v_hat) + eps) + lambda_i x ; x as in lamb_step.
+ * The algorithms take a per-step sequence {beta1^t}; this entry point uses
+ * the constant sequence beta1^t = beta1 (the paper's setting, beta1 = 0.975),
+ * whose running products are the powers above. The apply pass also reads g.
+ * Scalars, outputs and errors as lamb_step (nesterov_v must be 0 or 1).
+ */
+LAMB_API lamb_status nlamb_step(lamb_plan *plan, float lr, float beta1, float beta2,
+                       float eps, float weight_decay, float gamma_l,
+                       float gamma_u, int64_t step, int32_t nesterov_v,
+                       void *stream, double *ratio_out, double *norms_out);
+
+/*
  * One LARS step (Algorithm 1) over every block of the plan:
  *   m <- momentum m + (1 - momentum) (g + lambda_i x)
  *   x <- x - lr * trust_coef * phi(||x_i||) / ||m_i|| * m      per block i

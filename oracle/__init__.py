@@ -1,4 +1,5 @@
-"""CPU oracle of the LAMB (Algorithm 2) and LARS (Algorithm 1) steps.
+"""CPU oracle of the LAMB (Algorithm 2), N-LAMB / NN-LAMB (Algorithms 3 and
+4) and LARS (Algorithm 1) steps.
 
 TEST INFRASTRUCTURE ONLY: the test suite, ``__graft_entry__.smoke()`` and the
 CPU-baseline leg of ``bench.py`` are the only users. It imports nothing from
@@ -70,6 +71,13 @@ class Oracle:
             ctypes.c_double, ctypes.c_double, ctypes.c_double, ctypes.c_double,
             ctypes.c_double, ctypes.c_int, ctypes.c_double, ctypes.c_double,
             ctypes.c_int64, ctypes.c_int, _DP]
+        lib.oracle_nlamb_layer.restype = ctypes.c_int
+        lib.oracle_nlamb_layer.argtypes = [
+            ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int,
+            ctypes.c_void_p, ctypes.c_void_p,
+            ctypes.c_double, ctypes.c_double, ctypes.c_double, ctypes.c_double,
+            ctypes.c_double, ctypes.c_int, ctypes.c_double, ctypes.c_double,
+            ctypes.c_int64, ctypes.c_int, _DP]
         lib.oracle_lars_layer.restype = ctypes.c_int
         lib.oracle_lars_layer.argtypes = [
             ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int,
@@ -99,6 +107,31 @@ class Oracle:
                 res.ctypes.data_as(_DP))
             if rc != 0:
                 raise RuntimeError("oracle_lamb_layer failed on tensor %d (%d)" % (i, rc))
+        return out
+
+    def nlamb_step(self, xs: Sequence[np.ndarray], gs: Sequence[np.ndarray],
+                   ms: Sequence[np.ndarray], vs: Sequence[np.ndarray],
+                   wd_mask: Sequence[bool], *, lr: float, beta1: float, beta2: float,
+                   eps: float, weight_decay: float, gamma_l: float, gamma_u: float,
+                   step: int, nesterov_v: bool = False) -> np.ndarray:
+        """One N-LAMB (Algorithm 3) or NN-LAMB (Algorithm 4, nesterov_v) step;
+        returns (n, 3) [ratio, ||x||, ||u||]."""
+        n = len(xs)
+        out = np.zeros((n, 3), dtype=np.float64)
+        for i in range(n):
+            d = xs[i].size
+            _check_state(xs[i], d, "x[%d]" % i)
+            _check_state(ms[i], d, "m[%d]" % i)
+            _check_state(vs[i], d, "v[%d]" % i)
+            kind = _grad_kind(gs[i], d)
+            res = out[i]
+            rc = self._lib.oracle_nlamb_layer(
+                d, _ptr(xs[i]), _ptr(gs[i]), kind, _ptr(ms[i]), _ptr(vs[i]),
+                lr, beta1, beta2, eps, weight_decay, int(bool(wd_mask[i])),
+                gamma_l, gamma_u, int(step), int(bool(nesterov_v)),
+                res.ctypes.data_as(_DP))
+            if rc != 0:
+                raise RuntimeError("oracle_nlamb_layer failed on tensor %d (%d)" % (i, rc))
         return out
 
     def lars_step(self, xs: Sequence[np.ndarray], gs: Sequence[np.ndarray],

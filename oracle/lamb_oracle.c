@@ -1,5 +1,5 @@
 /*
- * CPU oracle for one LAMB step and one LARS step.
+ * CPU oracle for one step of LAMB, N-LAMB, NN-LAMB and LARS.
  *
  * You, Li, Reddi, Hseu, Kumar, Bhojanapalli, Song, Demmel, Keutzer, Hsieh:
  * "Large Batch Optimization for Deep Learning: Training BERT in 76 minutes",
@@ -34,6 +34,12 @@
  *  - LARS: the trust coefficient kappa multiplies phi (kappa = 1 is
  *    Algorithm 1 exactly); the epsilon listed among Algorithm 1's inputs is
  *    never used by the algorithm and is not taken here.
+ *
+ *  - N-LAMB / NN-LAMB (Appendix D): the inputs {beta1^t} form a per-step
+ *    sequence of momentum parameters; the paper's experiments hold it
+ *    constant (beta1 = 0.975), and that constant sequence is what is taken
+ *    here, so the products prod_{i<=k} beta1^i are the powers beta1^k. The
+ *    moment recursions use the constant beta1 and beta2 as printed.
  *
  * Parity is pinned by the closed forms, invariants and hand-worked examples
  * in the test suite; no function here is unpinned.
@@ -187,5 +193,73 @@ int oracle_lars_layer(int64_t d, float *x, const void *g, int g_is_bf16,
     out[1] = norm_x;
     out[2] = norm_m;
     free(mt);
+    return ORACLE_OK;
+}
+
+/*
+ * One N-LAMB step (Algorithm 3) or, with nesterov_v, one NN-LAMB step
+ * (Algorithm 4) on one layer block of d elements, at step t:
+ *
+ *   m_t   = beta1 m_{t-1} + (1 - beta1) g_t
+ *   m_hat = beta1 m_t / (1 - beta1^(t+1)) + (1 - beta1) g_t / (1 - beta1^t)
+ *   v_t   = beta2 v_{t-1} + (1 - beta2) g_t^2
+ *   v_hat = beta2 v_t / (1 - beta2^t)                               (N-LAMB)
+ *   v_hat = beta2 v_t / (1 - beta2^(t+1))
+ *           + (1 - beta2) g_t^2 / (1 - beta2^t)                     (NN-LAMB)
+ *   r_t   = m_hat / (sqrt(v_hat) + eps)
+ *   u     = r_t + lambda x_t
+ *   x_{t+1} = x_t - eta_t phi(||x_t||) / ||u|| * u
+ *
+ * Arguments and outputs as oracle_lamb_layer (bias correction is part of
+ * these algorithms and always on).
+ */
+int oracle_nlamb_layer(int64_t d, float *x, const void *g, int g_is_bf16,
+                       float *m, float *v,
+                       double lr, double beta1, double beta2, double eps,
+                       double weight_decay, int wd, double gamma_l,
+                       double gamma_u, int64_t t, int nesterov_v, double *out)
+{
+    if (d < 1 || !x || !g || !m || !v || !out || t < 1)
+        return ORACLE_EINVAL;
+    double *u = (double *)malloc((size_t)d * sizeof(double));
+    if (!u)
+        return ORACLE_ENOMEM;
+
+    double b1_t = pow(beta1, (double)t);
+    double b1_next = pow(beta1, (double)(t + 1));
+    double b2_t = pow(beta2, (double)t);
+    double b2_next = pow(beta2, (double)(t + 1));
+    double lam = wd ? weight_decay : 0.0;
+
+    double sum_xx = 0.0, sum_uu = 0.0;
+    for (int64_t j = 0; j < d; ++j) {
+        double gj = gradient_at(g, g_is_bf16, j);
+        double xj = (double)x[j];
+        double mj = beta1 * (double)m[j] + (1.0 - beta1) * gj;
+        double m_hat = beta1 * mj / (1.0 - b1_next) + (1.0 - beta1) * gj / (1.0 - b1_t);
+        double vj = beta2 * (double)v[j] + (1.0 - beta2) * (gj * gj);
+        double v_hat;
+        if (nesterov_v)
+            v_hat = beta2 * vj / (1.0 - b2_next) + (1.0 - beta2) * (gj * gj) / (1.0 - b2_t);
+        else
+            v_hat = beta2 * vj / (1.0 - b2_t);
+        double r = m_hat / (sqrt(v_hat) + eps);
+        u[j] = r + lam * xj;
+        sum_xx += xj * xj;
+        sum_uu += u[j] * u[j];
+        m[j] = store_f32(mj);
+        v[j] = store_f32(vj);
+    }
+
+    double norm_x = sqrt(sum_xx);
+    double norm_u = sqrt(sum_uu);
+    double ratio = (norm_u == 0.0) ? 0.0 : phi(norm_x, gamma_l, gamma_u) / norm_u;
+    for (int64_t j = 0; j < d; ++j)
+        x[j] = store_f32((double)x[j] - lr * ratio * u[j]);
+
+    out[0] = ratio;
+    out[1] = norm_x;
+    out[2] = norm_u;
+    free(u);
     return ORACLE_OK;
 }

@@ -35,7 +35,7 @@ LAMB_ALGO_LARS = 1
 
 # Every symbol the header declares (checked by the test suite).
 EXPORTS = ("lamb_plan_create", "lamb_plan_destroy", "lamb_plan_info", "lamb_step",
-           "lars_step", "lamb_chunk_table", "lamb_plan_set_timing", "lamb_plan_timing",
+           "nlamb_step", "lars_step", "lamb_chunk_table", "lamb_plan_set_timing", "lamb_plan_timing",
            "lamb_status_str", "lamb_last_error")
 
 
@@ -75,6 +75,7 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
     lib.lamb_plan_destroy.argtypes = [vp]
     lib.lamb_plan_info.argtypes = [vp, P(i32), P(i32), P(i32)]
     lib.lamb_step.argtypes = [vp, f32, f32, f32, f32, f32, f32, f32, i64, i32, vp, vp, vp]
+    lib.nlamb_step.argtypes = [vp, f32, f32, f32, f32, f32, f32, f32, i64, i32, vp, vp, vp]
     lib.lars_step.argtypes = [vp, f32, f32, f32, f32, f32, f32, vp, vp, vp]
     lib.lamb_chunk_table.argtypes = [P(i64), i32, i32, i32, P(i32), P(i64), P(i32), P(i32)]
     lib.lamb_plan_set_timing.argtypes = [vp, i32]
@@ -164,6 +165,15 @@ def lamb_step(plan: Plan, lr: float, beta1: float, beta2: float, eps: float,
     _check(load().lamb_step(_vp(plan.handle), lr, beta1, beta2, eps, weight_decay, gamma_l,
                             gamma_u, int(step), int(bool(bias_correction)), _vp(stream),
                             _vp(ratio_out), _vp(norms_out)), "lamb_step")
+
+
+def nlamb_step(plan: Plan, lr: float, beta1: float, beta2: float, eps: float,
+               weight_decay: float, gamma_l: float, gamma_u: float, step: int,
+               nesterov_v: bool = False, stream: int = 0, ratio_out: int = 0,
+               norms_out: int = 0) -> None:
+    _check(load().nlamb_step(_vp(plan.handle), lr, beta1, beta2, eps, weight_decay, gamma_l,
+                             gamma_u, int(step), int(bool(nesterov_v)), _vp(stream),
+                             _vp(ratio_out), _vp(norms_out)), "nlamb_step")
 
 
 def lars_step(plan: Plan, lr: float, momentum: float, weight_decay: float, gamma_l: float,

@@ -343,14 +343,18 @@ lamb_status lamb_plan_info(const lamb_plan *plan, int32_t *n_tensors, int32_t *n
     return LAMB_OK;
 }
 
-lamb_status lamb_step(lamb_plan *plan, float lr, float beta1, float beta2, float eps,
-                      float weight_decay, float gamma_l, float gamma_u, int64_t step,
-                      int32_t bias_correction, void *stream, double *ratio_out,
-                      double *norms_out) {
+}  // extern "C"
+
+namespace {
+
+// Scalar checks shared by the LAMB family (Algorithms 2, 3 and 4).
+lamb_status check_lamb_scalars(const lamb_plan *plan, float lr, float beta1, float beta2,
+                               float eps, float weight_decay, float gamma_l, float gamma_u,
+                               int64_t step) {
     if (!plan)
         return fail(LAMB_ENULL, "plan must not be NULL");
     if (plan->algo != LAMB_ALGO_LAMB)
-        return fail(LAMB_EPLAN, "lamb_step needs a plan created for LAMB");
+        return fail(LAMB_EPLAN, "the LAMB family needs a plan created for LAMB");
     if (step < 1)
         return fail(LAMB_EINVAL, "step = %lld, need >= 1", static_cast<long long>(step));
     lamb_status st = check_beta(beta1, "beta1");
@@ -362,29 +366,26 @@ lamb_status lamb_step(lamb_plan *plan, float lr, float beta1, float beta2, float
         return fail(LAMB_EINVAL, "eps = %g, need finite and >= 0", double(eps));
     if (!finite(lr) || !finite(weight_decay))
         return fail(LAMB_EINVAL, "lr and weight_decay must be finite");
-    if (bias_correction != 0 && bias_correction != 1)
-        return fail(LAMB_EINVAL, "bias_correction must be 0 or 1");
-    st = check_phi_bounds(gamma_l, gamma_u);
-    if (st != LAMB_OK)
-        return st;
+    return check_phi_bounds(gamma_l, gamma_u);
+}
 
-    // Bias-correction denominators 1 - beta^t in double (Algorithm 2).
-    double c1 = 1.0, c2 = 1.0;
-    if (bias_correction) {
-        c1 = 1.0 - std::pow(double(beta1), double(step));
-        c2 = 1.0 - std::pow(double(beta2), double(step));
-    }
+LambArgs lamb_args(float beta1, float beta2, float eps, float weight_decay) {
     LambArgs a;
     a.beta1 = beta1;
     a.one_minus_beta1 = float(1.0 - double(beta1));
     a.beta2 = beta2;
     a.one_minus_beta2 = float(1.0 - double(beta2));
-    a.inv_c1 = float(1.0 / c1);
-    a.inv_c2 = float(1.0 / c2);
+    a.m_scale = a.v_scale = 1.0f;
+    a.m_grad = a.v_grad = 0.0f;
     a.eps = eps;
     a.weight_decay = weight_decay;
-    FinalizeArgs f{double(lr), double(gamma_l), double(gamma_u), 1.0};
+    return a;
+}
 
+// Enqueue moment pass, finalize and apply pass of the LAMB family.
+lamb_status launch_lamb_family(lamb_plan *plan, LambVariant variant, const LambArgs &a,
+                               const FinalizeArgs &f, void *stream, double *ratio_out,
+                               double *norms_out) {
     DeviceGuard guard(plan->device);
     if (guard.status != hipSuccess)
         return fail_hip(guard.status, "selecting the plan's device");
@@ -392,7 +393,7 @@ lamb_status lamb_step(lamb_plan *plan, float lr, float beta1, float beta2, float
     const bool bf16 = plan->g_dtype == LAMB_GRAD_BF16;
     record(plan, 0, s);
     hipError_t err = launch_lamb_moments(plan->tensors, plan->chunks, plan->partials,
-                                         plan->n_chunks, bf16, a, s);
+                                         plan->n_chunks, bf16, variant, a, s);
     if (err != hipSuccess)
         return fail_hip(err, "launching the LAMB moment kernel");
     record(plan, 1, s);
@@ -401,13 +402,70 @@ lamb_status lamb_step(lamb_plan *plan, float lr, float beta1, float beta2, float
     if (err != hipSuccess)
         return fail_hip(err, "launching the finalize kernel");
     record(plan, 2, s);
-    err = launch_lamb_apply(plan->tensors, plan->chunks, plan->scale, plan->n_chunks, a, s);
+    err = launch_lamb_apply(plan->tensors, plan->chunks, plan->scale, plan->n_chunks, bf16,
+                            variant, a, s);
     if (err != hipSuccess)
         return fail_hip(err, "launching the LAMB apply kernel");
     record(plan, 3, s);
     if (plan->timing_used < plan->timing_capacity)
         ++plan->timing_used;
     return LAMB_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+lamb_status lamb_step(lamb_plan *plan, float lr, float beta1, float beta2, float eps,
+                      float weight_decay, float gamma_l, float gamma_u, int64_t step,
+                      int32_t bias_correction, void *stream, double *ratio_out,
+                      double *norms_out) {
+    lamb_status st = check_lamb_scalars(plan, lr, beta1, beta2, eps, weight_decay, gamma_l,
+                                        gamma_u, step);
+    if (st != LAMB_OK)
+        return st;
+    if (bias_correction != 0 && bias_correction != 1)
+        return fail(LAMB_EINVAL, "bias_correction must be 0 or 1");
+    // Bias-correction denominators 1 - beta^t in double (Algorithm 2).
+    double c1 = 1.0, c2 = 1.0;
+    if (bias_correction) {
+        c1 = 1.0 - std::pow(double(beta1), double(step));
+        c2 = 1.0 - std::pow(double(beta2), double(step));
+    }
+    LambArgs a = lamb_args(beta1, beta2, eps, weight_decay);
+    a.m_scale = float(1.0 / c1);
+    a.v_scale = float(1.0 / c2);
+    const FinalizeArgs f{double(lr), double(gamma_l), double(gamma_u), 1.0};
+    return launch_lamb_family(plan, kLamb, a, f, stream, ratio_out, norms_out);
+}
+
+lamb_status nlamb_step(lamb_plan *plan, float lr, float beta1, float beta2, float eps,
+                       float weight_decay, float gamma_l, float gamma_u, int64_t step,
+                       int32_t nesterov_v, void *stream, double *ratio_out,
+                       double *norms_out) {
+    lamb_status st = check_lamb_scalars(plan, lr, beta1, beta2, eps, weight_decay, gamma_l,
+                                        gamma_u, step);
+    if (st != LAMB_OK)
+        return st;
+    if (nesterov_v != 0 && nesterov_v != 1)
+        return fail(LAMB_EINVAL, "nesterov_v must be 0 or 1");
+    // Algorithms 3 and 4 with the constant sequence beta1^t = beta1, whose
+    // products are powers: coefficients in double, rounded once to fp32.
+    const double b1 = beta1, b2 = beta2, t = double(step);
+    const double b1_t = std::pow(b1, t), b1_next = std::pow(b1, t + 1.0);
+    const double b2_t = std::pow(b2, t), b2_next = std::pow(b2, t + 1.0);
+    LambArgs a = lamb_args(beta1, beta2, eps, weight_decay);
+    a.m_scale = float(b1 / (1.0 - b1_next));
+    a.m_grad = float((1.0 - b1) / (1.0 - b1_t));
+    if (nesterov_v) {
+        a.v_scale = float(b2 / (1.0 - b2_next));
+        a.v_grad = float((1.0 - b2) / (1.0 - b2_t));
+    } else {
+        a.v_scale = float(b2 / (1.0 - b2_t));
+    }
+    const FinalizeArgs f{double(lr), double(gamma_l), double(gamma_u), 1.0};
+    return launch_lamb_family(plan, nesterov_v ? kNNLamb : kNLamb, a, f, stream, ratio_out,
+                              norms_out);
 }
 
 lamb_status lars_step(lamb_plan *plan, float lr, float momentum, float weight_decay,

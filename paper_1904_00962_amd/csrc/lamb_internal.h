@@ -49,11 +49,21 @@ struct Partial {
     double sum_uu;  // sum of u^2 (LAMB) or m_t^2 (LARS) over the chunk
 };
 
-// fp32 scalars of the elementwise LAMB passes (Algorithm 2).
+// Which corrected moments the update uses.
+enum LambVariant : int {
+    kLamb = 0,    // Algorithm 2: m_hat = m_t / c1, v_hat = v_t / c2
+    kNLamb = 1,   // Algorithm 3: Nesterov m_hat, v_hat = beta2 v_t / c2
+    kNNLamb = 2,  // Algorithm 4: Nesterov m_hat and v_hat
+};
+
+// fp32 scalars of the elementwise LAMB-family passes. The corrected moments
+// are m_hat = m_scale * m_t + m_grad * g_t and v_hat = v_scale * v_t +
+// v_grad * g_t^2; Algorithm 2 has m_grad = v_grad = 0.
 struct LambArgs {
     float beta1, one_minus_beta1;
     float beta2, one_minus_beta2;
-    float inv_c1, inv_c2;  // 1 / (1 - beta^t), or 1 without bias correction
+    float m_scale, m_grad;
+    float v_scale, v_grad;
     float eps;
     float weight_decay;
 };
@@ -74,10 +84,10 @@ struct FinalizeArgs {
 // Kernel launchers (lamb_kernels.hip). Each returns the launch status.
 hipError_t launch_lamb_moments(const TensorDesc *tensors, const ChunkDesc *chunks,
                                Partial *partials, int32_t n_chunks, bool bf16_grad,
-                               const LambArgs &args, hipStream_t stream);
+                               LambVariant variant, const LambArgs &args, hipStream_t stream);
 hipError_t launch_lamb_apply(const TensorDesc *tensors, const ChunkDesc *chunks,
-                             const float *scale, int32_t n_chunks, const LambArgs &args,
-                             hipStream_t stream);
+                             const float *scale, int32_t n_chunks, bool bf16_grad,
+                             LambVariant variant, const LambArgs &args, hipStream_t stream);
 hipError_t launch_lars_moments(const TensorDesc *tensors, const ChunkDesc *chunks,
                                Partial *partials, int32_t n_chunks, bool bf16_grad,
                                const LarsArgs &args, hipStream_t stream);

@@ -136,13 +136,26 @@ __device__ __forceinline__ float lamb_second_moment(float v, float g, const Lamb
     return fmaf(a.beta2, v, a.one_minus_beta2 * (g * g));
 }
 
-// u = r + lambda x with r = m_hat / (sqrt(v_hat) + eps), from the NEW moments.
-// The moment and apply passes both call this, so their u agree bit for bit;
-// division and square root are the correctly rounded IEEE operations.
-__device__ __forceinline__ float lamb_update(float x, float m, float v, float lam,
+// u = r + lambda x with r = m_hat / (sqrt(v_hat) + eps), from the NEW moments
+// m = m_t, v = v_t. Algorithm 2 corrects by 1 / (1 - beta^t); Algorithms 3
+// and 4 add the Nesterov gradient terms, which is why their apply pass also
+// reads g. The moment and apply passes both call this, so their u agree bit
+// for bit; division and square root are the correctly rounded IEEE
+// operations.
+template <int kVariant>
+__device__ __forceinline__ float lamb_update(float x, float g, float m, float v, float lam,
                                              const LambArgs &a) {
-    const float m_hat = m * a.inv_c1;
-    const float v_hat = v * a.inv_c2;
+    float m_hat, v_hat;
+    if constexpr (kVariant == kLamb) {
+        m_hat = m * a.m_scale;
+        v_hat = v * a.v_scale;
+    } else {
+        m_hat = fmaf(a.m_scale, m, a.m_grad * g);
+        if constexpr (kVariant == kNNLamb)
+            v_hat = fmaf(a.v_scale, v, a.v_grad * (g * g));
+        else
+            v_hat = v * a.v_scale;
+    }
     const float r = __fdiv_rn(m_hat, __fadd_rn(__fsqrt_rn(v_hat), a.eps));
     return fmaf(lam, x, r);
 }
@@ -222,7 +235,7 @@ __device__ __forceinline__ uint32_t apply_chunk_index() {
 // LAMB passes.
 // ---------------------------------------------------------------------------
 
-template <bool kBf16>
+template <bool kBf16, int kVariant>
 __global__ __launch_bounds__(kBlock) void lamb_moments_kernel(
     const TensorDesc *__restrict__ tensors, const ChunkDesc *__restrict__ chunks,
     Partial *__restrict__ partials, LambArgs a) {
@@ -257,7 +270,7 @@ __global__ __launch_bounds__(kBlock) void lamb_moments_kernel(
                 for (int e = 0; e < 4; ++e) {
                     mn[e] = lamb_first_moment(mr[k][e], gr[k][e], a);
                     vn[e] = lamb_second_moment(vr[k][e], gr[k][e], a);
-                    const float u = lamb_update(xr[k][e], mn[e], vn[e], lam, a);
+                    const float u = lamb_update<kVariant>(xr[k][e], gr[k][e], mn[e], vn[e], lam, a);
                     const double xd = xr[k][e], ud = u;
                     sum_xx = fma(xd, xd, sum_xx);
                     sum_uu = fma(ud, ud, sum_uu);
@@ -273,7 +286,7 @@ __global__ __launch_bounds__(kBlock) void lamb_moments_kernel(
         const float gj = g.at(tail);
         const float mj = lamb_first_moment(m[tail], gj, a);
         const float vj = lamb_second_moment(v[tail], gj, a);
-        const float u = lamb_update(xj, mj, vj, lam, a);
+        const float u = lamb_update<kVariant>(xj, gj, mj, vj, lam, a);
         m[tail] = mj;
         v[tail] = vj;
         const double xd = xj, ud = u;
@@ -283,25 +296,33 @@ __global__ __launch_bounds__(kBlock) void lamb_moments_kernel(
     block_sums<kWaves>(sum_xx, sum_uu, partials + chunk_index());
 }
 
+// kVariant = kLamb never reads g (the template flag kBf16 is then unused).
+template <bool kBf16, int kVariant>
 __global__ __launch_bounds__(kBlock) void lamb_apply_kernel(
     const TensorDesc *__restrict__ tensors, const ChunkDesc *__restrict__ chunks,
     const float *__restrict__ scale, LambArgs a) {
+    constexpr bool kReadsGrad = kVariant != kLamb;
     const ChunkDesc c = chunks[apply_chunk_index()];
     const TensorDesc &t = tensors[c.tensor];
     gfloat *x = global_view(t.x + c.start);
     gcfloat *m = global_view(static_cast<const float *>(t.m) + c.start);
     gcfloat *v = global_view(static_cast<const float *>(t.v) + c.start);
+    const GradView<kBf16> g(t.g, c.start);
     const float lam = t.wd ? a.weight_decay : 0.0f;
     const float s = scale[c.tensor];
 
     const int n4 = c.len >> 2;
     for (int base = threadIdx.x; base < n4; base += kBlock * kUnroll) {
-        f32x4 xr[kUnroll], mr[kUnroll], vr[kUnroll];
+        f32x4 xr[kUnroll], gr[kUnroll], mr[kUnroll], vr[kUnroll];
 #pragma unroll
         for (int k = 0; k < kUnroll; ++k) {
             const int q = base + k * kBlock;
             if (q < n4) {
                 xr[k] = load4(x + 4 * q);
+                if constexpr (kReadsGrad)
+                    gr[k] = g.at4(4 * q);
+                else
+                    gr[k] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
                 mr[k] = load4(m + 4 * q);
                 vr[k] = load4(v + 4 * q);
             }
@@ -313,14 +334,18 @@ __global__ __launch_bounds__(kBlock) void lamb_apply_kernel(
                 f32x4 xn;
 #pragma unroll
                 for (int e = 0; e < 4; ++e)
-                    xn[e] = fmaf(-s, lamb_update(xr[k][e], mr[k][e], vr[k][e], lam, a), xr[k][e]);
+                    xn[e] = fmaf(-s, lamb_update<kVariant>(xr[k][e], gr[k][e], mr[k][e],
+                                                           vr[k][e], lam, a),
+                                 xr[k][e]);
                 store4(x + 4 * q, xn);
             }
         }
     }
     const int tail = 4 * n4 + threadIdx.x;
-    if (tail < c.len)
-        x[tail] = fmaf(-s, lamb_update(x[tail], m[tail], v[tail], lam, a), x[tail]);
+    if (tail < c.len) {
+        const float gj = kReadsGrad ? g.at(tail) : 0.0f;
+        x[tail] = fmaf(-s, lamb_update<kVariant>(x[tail], gj, m[tail], v[tail], lam, a), x[tail]);
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -488,23 +513,38 @@ __global__ __launch_bounds__(kFinalizeBlock) void finalize_kernel(
 // Launchers.
 // ---------------------------------------------------------------------------
 
+template <int kVariant>
+const void *moments_fn(bool bf16) {
+    return bf16 ? reinterpret_cast<const void *>(&lamb_moments_kernel<true, kVariant>)
+                : reinterpret_cast<const void *>(&lamb_moments_kernel<false, kVariant>);
+}
+
 hipError_t launch_lamb_moments(const TensorDesc *tensors, const ChunkDesc *chunks,
                                Partial *partials, int32_t n_chunks, bool bf16_grad,
-                               const LambArgs &args, hipStream_t stream) {
+                               LambVariant variant, const LambArgs &args, hipStream_t stream) {
     LambArgs a = args;
     void *params[] = {&tensors, &chunks, &partials, &a};
-    const void *fn = bf16_grad ? reinterpret_cast<const void *>(&lamb_moments_kernel<true>)
-                               : reinterpret_cast<const void *>(&lamb_moments_kernel<false>);
+    const void *fn = variant == kNLamb    ? moments_fn<kNLamb>(bf16_grad)
+                     : variant == kNNLamb ? moments_fn<kNNLamb>(bf16_grad)
+                                          : moments_fn<kLamb>(bf16_grad);
     return hipLaunchKernel(fn, dim3(n_chunks), dim3(kBlock), params, 0, stream);
 }
 
 hipError_t launch_lamb_apply(const TensorDesc *tensors, const ChunkDesc *chunks,
-                             const float *scale, int32_t n_chunks, const LambArgs &args,
-                             hipStream_t stream) {
+                             const float *scale, int32_t n_chunks, bool bf16_grad,
+                             LambVariant variant, const LambArgs &args, hipStream_t stream) {
     LambArgs a = args;
     void *params[] = {&tensors, &chunks, &scale, &a};
-    return hipLaunchKernel(reinterpret_cast<const void *>(&lamb_apply_kernel), dim3(n_chunks),
-                           dim3(kBlock), params, 0, stream);
+    const void *fn;
+    if (variant == kNLamb)
+        fn = bf16_grad ? reinterpret_cast<const void *>(&lamb_apply_kernel<true, kNLamb>)
+                       : reinterpret_cast<const void *>(&lamb_apply_kernel<false, kNLamb>);
+    else if (variant == kNNLamb)
+        fn = bf16_grad ? reinterpret_cast<const void *>(&lamb_apply_kernel<true, kNNLamb>)
+                       : reinterpret_cast<const void *>(&lamb_apply_kernel<false, kNNLamb>);
+    else
+        fn = reinterpret_cast<const void *>(&lamb_apply_kernel<false, kLamb>);
+    return hipLaunchKernel(fn, dim3(n_chunks), dim3(kBlock), params, 0, stream);
 }
 
 hipError_t launch_lars_moments(const TensorDesc *tensors, const ChunkDesc *chunks,

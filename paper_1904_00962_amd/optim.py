@@ -91,22 +91,36 @@ class LAMB(_LayerwiseOptimizer):
 
     algo = _lib.LAMB_ALGO_LAMB
 
+    VARIANTS = ("lamb", "n-lamb", "nn-lamb")
+
     def __init__(self, params, grads, lr: float = 1e-3, betas=(0.9, 0.999), eps: float = 1e-6,
                  weight_decay: float = 0.01, clamp=(0.0, 10.0), wd_mask=None,
-                 bias_correction: bool = True, chunk_elems: int = 0):
+                 bias_correction: bool = True, chunk_elems: int = 0, variant: str = "lamb"):
+        """``variant``: "lamb" (Algorithm 2), "n-lamb" (Algorithm 3) or "nn-lamb"
+        (Algorithm 4; the paper pairs both with betas=(0.975, 0.999), eps=1e-8)."""
+        if variant not in self.VARIANTS:
+            raise ValueError("variant must be one of %s" % (self.VARIANTS,))
+        if variant != "lamb" and not bias_correction:
+            raise ValueError("N-LAMB and NN-LAMB carry their own bias correction")
         super().__init__(params, grads, lr, weight_decay, clamp, wd_mask, chunk_elems, True)
         self.beta1, self.beta2 = float(betas[0]), float(betas[1])
         self.eps = float(eps)
         self.bias_correction = bool(bias_correction)
+        self.variant = variant
 
     def step(self, lr: Optional[float] = None) -> None:
         """Advance t and apply one step; per-tensor ratios and norms land in
         ``self.ratios`` and ``self.norms`` (device, float64)."""
         self.t += 1
-        _lib.lamb_step(self.plan, self.lr if lr is None else float(lr), self.beta1, self.beta2,
-                       self.eps, self.weight_decay, self.gamma_l, self.gamma_u, self.t,
-                       self.bias_correction, self._stream(), self.ratios.data_ptr(),
-                       self.norms.data_ptr())
+        lr = self.lr if lr is None else float(lr)
+        if self.variant == "lamb":
+            _lib.lamb_step(self.plan, lr, self.beta1, self.beta2, self.eps, self.weight_decay,
+                           self.gamma_l, self.gamma_u, self.t, self.bias_correction,
+                           self._stream(), self.ratios.data_ptr(), self.norms.data_ptr())
+        else:
+            _lib.nlamb_step(self.plan, lr, self.beta1, self.beta2, self.eps, self.weight_decay,
+                            self.gamma_l, self.gamma_u, self.t, self.variant == "nn-lamb",
+                            self._stream(), self.ratios.data_ptr(), self.norms.data_ptr())
 
     def state_dict(self):
         return {"step": self.t, "m": [m.clone() for m in self.m], "v": [v.clone() for v in self.v]}

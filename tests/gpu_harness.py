@@ -118,7 +118,7 @@ class Pair:
         self.X = [torch.as_tensor(x).to(dev, torch.float32).contiguous() for x in xs]
         self.G = [torch.zeros(x.numel(), dtype=gt, device=dev) for x in self.X]
         self.M = [torch.zeros_like(x) for x in self.X]
-        self.V = [torch.zeros_like(x) for x in self.X] if algo == "lamb" else None
+        self.V = [torch.zeros_like(x) for x in self.X] if algo != "lars" else None
         self.subset = list(range(self.n)) if oracle_subset is None else list(oracle_subset)
         self.hx = [paramsets.host_array(self.X[i]).copy() for i in self.subset]
         self.hm = [np.zeros(self.X[i].numel(), np.float32) for i in self.subset]
@@ -129,7 +129,7 @@ class Pair:
                  self.V[i].data_ptr() if self.V is not None else 0, self.X[i].numel(),
                  int(self.wd[i])) for i in range(self.n)]
         kind = _lib.LAMB_GRAD_BF16 if g_dtype == "bf16" else _lib.LAMB_GRAD_F32
-        algo_id = _lib.LAMB_ALGO_LAMB if algo == "lamb" else _lib.LAMB_ALGO_LARS
+        algo_id = _lib.LAMB_ALGO_LARS if algo == "lars" else _lib.LAMB_ALGO_LAMB
         self.plan = _lib.lamb_plan_create(rows, kind, algo_id, chunk_elems)
         self.oracle = oracle.load()
 
@@ -144,6 +144,12 @@ class Pair:
                        self.torch.cuda.current_stream().cuda_stream, self.ratio.data_ptr(),
                        self.norms.data_ptr())
 
+    def gpu_nlamb(self, hp: dict, step: int, nesterov_v: bool) -> None:
+        _lib.nlamb_step(self.plan, hp["lr"], hp["beta1"], hp["beta2"], hp["eps"],
+                        hp["weight_decay"], hp["gamma_l"], hp["gamma_u"], step, nesterov_v,
+                        self.torch.cuda.current_stream().cuda_stream, self.ratio.data_ptr(),
+                        self.norms.data_ptr())
+
     def gpu_lars(self, hp: dict) -> None:
         _lib.lars_step(self.plan, hp["lr"], hp["momentum"], hp["weight_decay"], hp["gamma_l"],
                        hp["gamma_u"], hp["trust_coef"],
@@ -154,6 +160,11 @@ class Pair:
         return self.oracle.lamb_step(self.hx, hg, self.hm, self.hv,
                                      [self.wd[i] for i in self.subset], step=step,
                                      bias_correction=bias_correction, **f32_scalars(hp))
+
+    def oracle_nlamb(self, hg, hp: dict, step: int, nesterov_v: bool) -> np.ndarray:
+        return self.oracle.nlamb_step(self.hx, hg, self.hm, self.hv,
+                                      [self.wd[i] for i in self.subset], step=step,
+                                      nesterov_v=nesterov_v, **f32_scalars(hp))
 
     def oracle_lars(self, hg, hp: dict) -> np.ndarray:
         return self.oracle.lars_step(self.hx, hg, self.hm, [self.wd[i] for i in self.subset],
@@ -200,9 +211,27 @@ def lamb_hp(ps: paramsets.ParamSet) -> dict:
                 weight_decay=ps.weight_decay, gamma_l=ps.gamma_l, gamma_u=ps.gamma_u)
 
 
+def nlamb_hp(ps: paramsets.ParamSet) -> dict:
+    """N-LAMB / NN-LAMB settings of Appendix D (beta1 0.975, beta2 0.999, eps 1e-8)."""
+    return dict(lamb_hp(ps), beta1=0.975, beta2=0.999, eps=1e-8)
+
+
 def lars_hp(ps: paramsets.ParamSet) -> dict:
     return dict(lr=ps.lars_lr, momentum=ps.lars_momentum, weight_decay=ps.weight_decay,
                 gamma_l=ps.gamma_l, gamma_u=ps.gamma_u, trust_coef=ps.lars_trust_coef)
+
+
+def step_both(pair: Pair, algo: str, hg, hp: dict, t: int, bias_correction: bool = True):
+    """One step of ``algo`` on the GPU and in the oracle; returns the oracle's
+    per-tensor [ratio, ||x||, ||u||]."""
+    if algo == "lamb":
+        pair.gpu_lamb(hp, t, bias_correction)
+        return pair.oracle_lamb(hg, hp, t, bias_correction)
+    if algo in ("nlamb", "nnlamb"):
+        pair.gpu_nlamb(hp, t, algo == "nnlamb")
+        return pair.oracle_nlamb(hg, hp, t, algo == "nnlamb")
+    pair.gpu_lars(hp)
+    return pair.oracle_lars(hg, hp)
 
 
 def run_config(cfg: int, steps: int, algo: str = "lamb", chunk_elems: int = 0,
@@ -213,16 +242,11 @@ def run_config(cfg: int, steps: int, algo: str = "lamb", chunk_elems: int = 0,
     pair = Pair(paramsets.draw_params(ps, device=device), ps.wd_mask(), ps.g_dtype, algo,
                 chunk_elems, oracle_subset)
     rep = Report()
-    hp = lamb_hp(ps) if algo == "lamb" else lars_hp(ps)
+    hp = {"lamb": lamb_hp, "lars": lars_hp, "nlamb": nlamb_hp, "nnlamb": nlamb_hp}[algo](ps)
     try:
         for t in range(1, steps + 1):
             hg = pair.set_grads(paramsets.draw_grads(ps, t, device=device))
-            if algo == "lamb":
-                pair.gpu_lamb(hp, t)
-                ref = pair.oracle_lamb(hg, hp, t)
-            else:
-                pair.gpu_lars(hp)
-                ref = pair.oracle_lars(hg, hp)
+            ref = step_both(pair, algo, hg, hp, t)
             r = pair.compare(ref, "cfg%d %s step %d" % (cfg, algo, t))
             log("  step %d: max err %.3e, max abs %.3e, max rel %.3e, rel>1e-5: %d"
                 % (t, r.max_err, r.max_abs, r.max_rel, r.n_rel_over))

@@ -8,10 +8,10 @@ anywhere in the oracle (a dropped term, a wrong sign, index or coefficient,
 swapped operands) breaks at least one of them. ``test_oracle_mutants`` plants
 such slips in a copy of the oracle and checks that each one is caught.
 
-Sources: Algorithm 1 (LARS) and Algorithm 2 (LAMB) of You et al., the
-scaling function phi of Section 3, the sign-SGD remark of Section 3.2, the
-bound on ||r|| used in the proof of Theorem 3 (Appendix B) and the bias
-correction remark of Appendix E.
+Sources: Algorithm 1 (LARS), Algorithm 2 (LAMB) and Algorithms 3 and 4
+(N-LAMB, NN-LAMB, Appendix D) of You et al., the scaling function phi of
+Section 3, the sign-SGD remark of Section 3.2, the bound on ||r|| used in the
+proof of Theorem 3 (Appendix B) and the bias correction remark of Appendix E.
 """
 
 from __future__ import annotations
@@ -444,10 +444,82 @@ def pin_lars_step_length(o):
             _close(length, lr * kappa * _phi(np.linalg.norm(xo), gl, gu), 2e-5)
 
 
+# ---------------------------------------------------------------------------
+# N-LAMB (Algorithm 3) and NN-LAMB (Algorithm 4)
+# ---------------------------------------------------------------------------
+
+def _nlamb(o, xs, gs, ms, vs, wd, step, nesterov_v, **hp):
+    kw = dict(LAMB_DEFAULTS)
+    kw.update(hp)
+    return o.nlamb_step(xs, gs, ms, vs, wd, step=step, nesterov_v=nesterov_v, **kw)
+
+
+def _nesterov_factor(beta, t):
+    """Coefficient of g in the Nesterov-corrected moment when g_t is constant:
+    beta (1 - beta^t) / (1 - beta^(t+1)) + (1 - beta) / (1 - beta^t)."""
+    return beta * (1 - beta ** t) / (1 - beta ** (t + 1)) + (1 - beta) / (1 - beta ** t)
+
+
+def pin_nlamb_constant_gradient(o):
+    """Constant g from zero moments: m_t = (1 - b1^t) g and v_t = (1 - b2^t) g^2
+    (geometric series). Substituted into Algorithms 3 and 4, m_hat = c_m(t) g
+    with c_m the Nesterov factor of b1; v_hat = b2 g^2 (N-LAMB) or c_v(t) g^2
+    with the factor of b2 (NN-LAMB). So u = c_m g / (sqrt(c_v) |g| + eps) +
+    lambda_i x_t, at every t."""
+    rng = np.random.default_rng(41)
+    b1, b2, eps, lam, lr = 0.7, 0.9, 2e-4, 0.05, 0.05
+    for nesterov_v in (False, True):
+        xs, wd = _three_blocks(rng)
+        gs = [_f32(rng.standard_normal(x.size) * 1e-3) for x in xs]
+        ms, vs = _zeros_like(xs), _zeros_like(xs)
+        for t in range(1, 7):
+            x_old = [x.astype(np.float64) for x in xs]
+            out = _nlamb(o, xs, gs, ms, vs, wd, t, nesterov_v, lr=lr, beta1=b1, beta2=b2,
+                         eps=eps, weight_decay=lam, gamma_l=1.0, gamma_u=10.0)
+            cm = _nesterov_factor(b1, t)
+            cv = _nesterov_factor(b2, t) if nesterov_v else b2
+            for i, (g, xo) in enumerate(zip(gs, x_old)):
+                gd = g.astype(np.float64)
+                _close(ms[i], (1 - b1 ** t) * gd, 1e-6, what="N-LAMB m_t")
+                _close(vs[i], (1 - b2 ** t) * gd * gd, 1e-6, what="N-LAMB v_t")
+                u = cm * gd / (math.sqrt(cv) * np.abs(gd) + eps) + (lam if wd[i] else 0.0) * xo
+                nx, nu = np.linalg.norm(xo), np.linalg.norm(u)
+                what = "%s t=%d block %d" % ("NN-LAMB" if nesterov_v else "N-LAMB", t, i)
+                _close(out[i, 2], nu, 1e-6, what=what + " ||u||")
+                _close(out[i, 0], _phi(nx, 1.0, 10.0) / nu, 1e-6, what=what + " ratio")
+                expect = xo - lr * _phi(nx, 1.0, 10.0) * u / nu
+                step = np.max(np.abs(expect - xo))
+                _close(xs[i], expect, 0, atol=2e-7 * np.max(np.abs(xo)) + 1e-6 * step, what=what)
+
+
+def pin_nnlamb_lookahead(o):
+    """Nesterov's look-ahead: once the bias corrections have decayed (large t),
+    NN-LAMB's m_hat and v_hat are the moments one further update with the same
+    gradient would give. Its step from (m, v) therefore equals the uncorrected
+    LAMB step (Appendix E) taken from the moments after one LAMB update."""
+    rng = np.random.default_rng(42)
+    b1, b2, t = 0.6, 0.7, 4000          # b^t underflows: corrections are exactly 1
+    x0 = _f32(rng.standard_normal(50))
+    m0 = _f32(rng.standard_normal(50) * 1e-3)
+    v0 = _f32(np.abs(rng.standard_normal(50)) * 1e-6)
+    g = [_f32(rng.standard_normal(50) * 1e-3)]
+    xa, ma, va = [x0.copy()], [m0.copy()], [v0.copy()]
+    oa = _nlamb(o, xa, g, ma, va, [True], t, True, beta1=b1, beta2=b2, eps=1e-6,
+                weight_decay=0.02)
+    # advance the moments once with the same gradient, then an uncorrected LAMB step
+    xb, mb, vb = [x0.copy()], [m0.copy()], [v0.copy()]
+    _lamb(o, [x0.copy()], g, mb, vb, [True], 1, beta1=b1, beta2=b2, bias_correction=False)
+    ob = _lamb(o, xb, g, mb, vb, [True], 1, beta1=b1, beta2=b2, eps=1e-6, weight_decay=0.02,
+               bias_correction=False)
+    _close(oa[0], ob[0], 1e-6, what="look-ahead ratio/norms")
+    _close(xa[0], xb[0], 1e-7, what="look-ahead x")
+
+
 LAMB_PINS = [pin_hand_cases, pin_constant_gradient, pin_step_length, pin_sign_sgd,
              pin_scalar_sign, pin_first_step, pin_bias_correction_factor,
              pin_no_correction_first_step, pin_ratio_bound, pin_mask, pin_scale_invariance,
              pin_zero_block, pin_zero_update, pin_permutation, pin_bf16_gradient]
+NLAMB_PINS = [pin_nlamb_constant_gradient, pin_nnlamb_lookahead]
 LARS_PINS = [pin_lars_normalized_sgd, pin_lars_constant_gradient, pin_lars_weight_decay,
              pin_lars_step_length]
-ALL_PINS = LAMB_PINS + LARS_PINS
+ALL_PINS = LAMB_PINS + NLAMB_PINS + LARS_PINS

@@ -130,6 +130,8 @@ def test_null_plan_and_outputs(lib):
     assert lib.lamb_step(None, 1e-3, 0.9, 0.999, 1e-6, 0.01, 0.0, 10.0, 1, 1, None, None,
                          None) == _lib.LAMB_ENULL
     assert lib.lars_step(None, 1e-3, 0.9, 0.01, 0.0, 10.0, 1e-3, None, None, None) == _lib.LAMB_ENULL
+    assert lib.nlamb_step(None, 1e-3, 0.975, 0.999, 1e-8, 0.01, 0.0, 10.0, 1, 0, None, None,
+                          None) == _lib.LAMB_ENULL
     assert lib.lamb_plan_destroy(None) == _lib.LAMB_OK
     assert lib.lamb_plan_info(None, None, None, None) == _lib.LAMB_ENULL
     assert lib.lamb_plan_set_timing(None, 4) == _lib.LAMB_ENULL

@@ -35,12 +35,7 @@ def _run(xs, wd, g_dtype, algo, chunk, steps, hp, rng, grads=None, bias_correcti
         for t in range(1, steps + 1):
             gs = grads(t) if grads else _gs(rng, [x.size for x in xs], g_dtype)
             hg = pair.set_grads(gs)
-            if algo == "lamb":
-                pair.gpu_lamb(hp, t, bias_correction)
-                ref = pair.oracle_lamb(hg, hp, t, bias_correction)
-            else:
-                pair.gpu_lars(hp)
-                ref = pair.oracle_lars(hg, hp)
+            ref = H.step_both(pair, algo, hg, hp, t, bias_correction)
             pair.compare(ref, "%s %s chunk=%d step %d" % (algo, g_dtype, chunk, t))
         return pair
     finally:
@@ -51,8 +46,12 @@ RAGGED = [1, 2, 3, 4, 5, 7, 8, 9, 15, 16, 17, 255, 256, 257, 1023, 1024, 1025, 1
           2048, 2049, 4095, 4096, 4097, 8191, 8193]
 
 
+NLAMB = dict(DEFAULT, beta1=0.975, eps=1e-8)
+
+
 @pytest.mark.parametrize("algo,g_dtype", [("lamb", "f32"), ("lamb", "bf16"), ("lars", "f32"),
-                                          ("lars", "bf16")])
+                                          ("lars", "bf16"), ("nlamb", "bf16"),
+                                          ("nnlamb", "f32")])
 @pytest.mark.parametrize("chunk", [8, 64, 1024, 0])
 def test_ragged_sizes(algo, g_dtype, chunk):
     """Every tensor length around the 4-element group, the 256-thread tile,
@@ -65,7 +64,7 @@ def test_ragged_sizes(algo, g_dtype, chunk):
         sizes += [32767, 32768, 32769, 4 * 32768 + 5]
     xs = _xs(rng, sizes)
     wd = [i % 3 != 0 for i in range(len(sizes))]
-    hp = DEFAULT if algo == "lamb" else LARS
+    hp = {"lamb": DEFAULT, "lars": LARS, "nlamb": NLAMB, "nnlamb": NLAMB}[algo]
     H.log("ragged algo=%s g=%s chunk=%d tensors=%d" % (algo, g_dtype, chunk, len(sizes)))
     _run(xs, wd, g_dtype, algo, chunk, 3, hp, rng)
 
@@ -210,6 +209,12 @@ def test_validation_leaves_state_untouched():
         with pytest.raises(_lib.LambError) as e:
             _lib.lamb_step(lars.plan, 0.01, 0.9, 0.999, 1e-6, 0.01, 0.0, 10.0, 1, True, s)
         assert e.value.status == _lib.LAMB_EPLAN
+        with pytest.raises(_lib.LambError) as e:
+            _lib.nlamb_step(lars.plan, 0.01, 0.975, 0.999, 1e-8, 0.01, 0.0, 10.0, 1, True, s)
+        assert e.value.status == _lib.LAMB_EPLAN
+        with pytest.raises(_lib.LambError) as e:
+            _lib.nlamb_step(pair.plan, 0.01, 0.975, 0.999, 1e-8, 0.01, 0.0, 10.0, 0, True, s)
+        assert e.value.status == _lib.LAMB_EINVAL
         with pytest.raises(_lib.LambError) as e:
             _lib.lars_step(lars.plan, 0.01, 1.5, 0.01, 0.0, 10.0, 0.01, s)
         assert e.value.status == _lib.LAMB_EINVAL

@@ -42,6 +42,22 @@ def test_resnet50_lars():
     H.run_config(3, 3, "lars")
 
 
+@pytest.mark.parametrize("algo", ["nlamb", "nnlamb"])
+def test_tiny_nesterov_variants(algo):
+    H.run_config(0, 10, algo)
+    H.run_config(0, 4, algo, chunk_elems=64)
+
+
+@pytest.mark.parametrize("algo", ["nlamb", "nnlamb"])
+def test_bert_large_nesterov_variants_bf16_grad(algo):
+    H.run_config(2, 2, algo)
+
+
+@pytest.mark.parametrize("algo", ["nlamb", "nnlamb"])
+def test_resnet50_nesterov_variants(algo):
+    H.run_config(3, 3, algo)
+
+
 def test_bert_large_lars_bf16_grad():
     ps = paramsets.get(2)
     H.run_config(2, 2, "lars", oracle_subset=[0, 3, 4, 5, 6, ps.n_tensors - 1])

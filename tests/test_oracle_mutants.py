@@ -62,6 +62,26 @@ MUTANTS = [
     ("lars_update_sign", "(double)x[j] - lr * ratio * mt[j]", "(double)x[j] + lr * ratio * mt[j]", 0),
     ("lars_stores_undamped_m", "m[j] = store_f32(mt[j]);",
      "m[j] = store_f32(mt[j] / (1.0 - beta1));", 0),
+    ("nlamb_m_next_power", "double b1_next = pow(beta1, (double)(t + 1));",
+     "double b1_next = pow(beta1, (double)t);", 0),
+    ("nlamb_m_power_index", "double b1_t = pow(beta1, (double)t);",
+     "double b1_t = pow(beta1, (double)(t + 1));", 0),
+    ("nlamb_m_drops_gradient_term",
+     "double m_hat = beta1 * mj / (1.0 - b1_next) + (1.0 - beta1) * gj / (1.0 - b1_t);",
+     "double m_hat = beta1 * mj / (1.0 - b1_next);", 0),
+    ("nlamb_m_no_beta_factor",
+     "double m_hat = beta1 * mj / (1.0 - b1_next) + (1.0 - beta1) * gj / (1.0 - b1_t);",
+     "double m_hat = mj / (1.0 - b1_next) + (1.0 - beta1) * gj / (1.0 - b1_t);", 0),
+    ("nlamb_v_no_beta_factor", "v_hat = beta2 * vj / (1.0 - b2_t);", "v_hat = vj / (1.0 - b2_t);", 0),
+    ("nnlamb_v_next_power", "double b2_next = pow(beta2, (double)(t + 1));",
+     "double b2_next = pow(beta2, (double)t);", 0),
+    ("nnlamb_v_drops_gradient_term",
+     "v_hat = beta2 * vj / (1.0 - b2_next) + (1.0 - beta2) * (gj * gj) / (1.0 - b2_t);",
+     "v_hat = beta2 * vj / (1.0 - b2_next);", 0),
+    ("nlamb_flags_swapped", "if (nesterov_v)", "if (!nesterov_v)", 0),
+    ("nlamb_mask_ignored", "double lam = wd ? weight_decay : 0.0;", "double lam = weight_decay;", 2),
+    ("nlamb_eps_inside_sqrt", "double r = m_hat / (sqrt(v_hat) + eps);",
+     "double r = m_hat / sqrt(v_hat + eps);", 1),
     ("lars_zero_norm_not_guarded", "(norm_m == 0.0)\n                       ? 0.0\n                       :", "", 0),
 ]
 
