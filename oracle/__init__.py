@@ -7,7 +7,11 @@ the HIP library package and shares no code with it. The arithmetic lives in
 ``lamb_oracle.c`` (plain C, double); this module only marshals numpy arrays.
 
 Inputs are lists of per-tensor numpy arrays: x, m, v are float32 and updated
-in place; g is float32, or uint16 holding bf16 bit patterns.
+in place; g is float32, or uint16 holding bf16 bit patterns. Every step takes
+``grad_scale`` (g_t = grad_scale * g), ``norm`` ("l2", "l1" or "linf", the
+layer norm of Appendix F) and ``skip_nonfinite``: when set and any scaled
+gradient element of any tensor is NaN or infinite, the step changes nothing
+and returns NaN ratios and norms.
 """
 
 from __future__ import annotations
@@ -35,6 +39,7 @@ def build(source: str = SOURCE, output: str = LIBRARY) -> str:
 
 
 _DP = ctypes.POINTER(ctypes.c_double)
+NORMS = {"l2": 0, "l1": 1, "linf": 2}
 
 
 def _ptr(a: np.ndarray) -> ctypes.c_void_p:
@@ -70,27 +75,48 @@ class Oracle:
             ctypes.c_void_p, ctypes.c_void_p,
             ctypes.c_double, ctypes.c_double, ctypes.c_double, ctypes.c_double,
             ctypes.c_double, ctypes.c_int, ctypes.c_double, ctypes.c_double,
-            ctypes.c_int64, ctypes.c_int, _DP]
+            ctypes.c_int64, ctypes.c_int, ctypes.c_double, ctypes.c_int, _DP]
         lib.oracle_nlamb_layer.restype = ctypes.c_int
         lib.oracle_nlamb_layer.argtypes = [
             ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int,
             ctypes.c_void_p, ctypes.c_void_p,
             ctypes.c_double, ctypes.c_double, ctypes.c_double, ctypes.c_double,
             ctypes.c_double, ctypes.c_int, ctypes.c_double, ctypes.c_double,
-            ctypes.c_int64, ctypes.c_int, _DP]
+            ctypes.c_int64, ctypes.c_int, ctypes.c_double, ctypes.c_int, _DP]
         lib.oracle_lars_layer.restype = ctypes.c_int
         lib.oracle_lars_layer.argtypes = [
             ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int,
             ctypes.c_void_p, ctypes.c_double, ctypes.c_double, ctypes.c_double,
-            ctypes.c_int, ctypes.c_double, ctypes.c_double, ctypes.c_double, _DP]
+            ctypes.c_int, ctypes.c_double, ctypes.c_double, ctypes.c_double,
+            ctypes.c_double, ctypes.c_int, _DP]
+        lib.oracle_gradient_finite.restype = ctypes.c_int
+        lib.oracle_gradient_finite.argtypes = [ctypes.c_int64, ctypes.c_void_p, ctypes.c_int,
+                                               ctypes.c_double]
         self._lib = lib
+
+    def gradients_finite(self, gs: Sequence[np.ndarray], grad_scale: float = 1.0) -> bool:
+        """True unless some fp32(g_j) * fp32(grad_scale) of some tensor is NaN or infinite."""
+        for g in gs:
+            kind = _grad_kind(g, g.size)
+            if not self._lib.oracle_gradient_finite(g.size, _ptr(g), kind, grad_scale):
+                return False
+        return True
+
+    def _skipped(self, gs, grad_scale, skip_nonfinite):
+        if skip_nonfinite and not self.gradients_finite(gs, grad_scale):
+            return np.full((len(gs), 3), np.nan)
+        return None
 
     def lamb_step(self, xs: Sequence[np.ndarray], gs: Sequence[np.ndarray],
                   ms: Sequence[np.ndarray], vs: Sequence[np.ndarray],
                   wd_mask: Sequence[bool], *, lr: float, beta1: float, beta2: float,
                   eps: float, weight_decay: float, gamma_l: float, gamma_u: float,
-                  step: int, bias_correction: bool = True) -> np.ndarray:
+                  step: int, bias_correction: bool = True, grad_scale: float = 1.0,
+                  norm: str = "l2", skip_nonfinite: bool = False) -> np.ndarray:
         """One LAMB step over every block; returns (n, 3) [ratio, ||x||, ||u||]."""
+        skipped = self._skipped(gs, grad_scale, skip_nonfinite)
+        if skipped is not None:
+            return skipped
         n = len(xs)
         out = np.zeros((n, 3), dtype=np.float64)
         for i in range(n):
@@ -103,8 +129,8 @@ class Oracle:
             rc = self._lib.oracle_lamb_layer(
                 d, _ptr(xs[i]), _ptr(gs[i]), kind, _ptr(ms[i]), _ptr(vs[i]),
                 lr, beta1, beta2, eps, weight_decay, int(bool(wd_mask[i])),
-                gamma_l, gamma_u, int(step), int(bool(bias_correction)),
-                res.ctypes.data_as(_DP))
+                gamma_l, gamma_u, int(step), int(bool(bias_correction)), grad_scale,
+                NORMS[norm], res.ctypes.data_as(_DP))
             if rc != 0:
                 raise RuntimeError("oracle_lamb_layer failed on tensor %d (%d)" % (i, rc))
         return out
@@ -113,9 +139,13 @@ class Oracle:
                    ms: Sequence[np.ndarray], vs: Sequence[np.ndarray],
                    wd_mask: Sequence[bool], *, lr: float, beta1: float, beta2: float,
                    eps: float, weight_decay: float, gamma_l: float, gamma_u: float,
-                   step: int, nesterov_v: bool = False) -> np.ndarray:
+                   step: int, nesterov_v: bool = False, grad_scale: float = 1.0,
+                   norm: str = "l2", skip_nonfinite: bool = False) -> np.ndarray:
         """One N-LAMB (Algorithm 3) or NN-LAMB (Algorithm 4, nesterov_v) step;
         returns (n, 3) [ratio, ||x||, ||u||]."""
+        skipped = self._skipped(gs, grad_scale, skip_nonfinite)
+        if skipped is not None:
+            return skipped
         n = len(xs)
         out = np.zeros((n, 3), dtype=np.float64)
         for i in range(n):
@@ -128,8 +158,8 @@ class Oracle:
             rc = self._lib.oracle_nlamb_layer(
                 d, _ptr(xs[i]), _ptr(gs[i]), kind, _ptr(ms[i]), _ptr(vs[i]),
                 lr, beta1, beta2, eps, weight_decay, int(bool(wd_mask[i])),
-                gamma_l, gamma_u, int(step), int(bool(nesterov_v)),
-                res.ctypes.data_as(_DP))
+                gamma_l, gamma_u, int(step), int(bool(nesterov_v)), grad_scale,
+                NORMS[norm], res.ctypes.data_as(_DP))
             if rc != 0:
                 raise RuntimeError("oracle_nlamb_layer failed on tensor %d (%d)" % (i, rc))
         return out
@@ -137,8 +167,12 @@ class Oracle:
     def lars_step(self, xs: Sequence[np.ndarray], gs: Sequence[np.ndarray],
                   ms: Sequence[np.ndarray], wd_mask: Sequence[bool], *, lr: float,
                   momentum: float, weight_decay: float, gamma_l: float, gamma_u: float,
-                  trust_coef: float) -> np.ndarray:
+                  trust_coef: float, grad_scale: float = 1.0, norm: str = "l2",
+                  skip_nonfinite: bool = False) -> np.ndarray:
         """One LARS step over every block; returns (n, 3) [ratio, ||x||, ||m||]."""
+        skipped = self._skipped(gs, grad_scale, skip_nonfinite)
+        if skipped is not None:
+            return skipped
         n = len(xs)
         out = np.zeros((n, 3), dtype=np.float64)
         for i in range(n):
@@ -150,7 +184,7 @@ class Oracle:
             rc = self._lib.oracle_lars_layer(
                 d, _ptr(xs[i]), _ptr(gs[i]), kind, _ptr(ms[i]), lr, momentum,
                 weight_decay, int(bool(wd_mask[i])), gamma_l, gamma_u, trust_coef,
-                res.ctypes.data_as(_DP))
+                grad_scale, NORMS[norm], res.ctypes.data_as(_DP))
             if rc != 0:
                 raise RuntimeError("oracle_lars_layer failed on tensor %d (%d)" % (i, rc))
         return out

@@ -35,6 +35,14 @@
  *    Algorithm 1 exactly); the epsilon listed among Algorithm 1's inputs is
  *    never used by the algorithm and is not taken here.
  *
+ *  - g_t is the mean of the per-sample gradients (Algorithms 1 and 2); the
+ *    caller may hand over the sum (or a loss-scaled value) and grad_scale,
+ *    so that g_t = grad_scale * g. Whether a scaled gradient is finite is
+ *    decided on the fp32 product fp32(g) * fp32(grad_scale), the precision
+ *    the GPU path computes it in.
+ *  - Layer norms (Appendix F): L2 is the default; the paper does not name
+ *    the other norms it tried, so L1 and L-infinity are offered, used for
+ *    both ||x|| and ||u||. The L-infinity maximum keeps NaN.
  *  - N-LAMB / NN-LAMB (Appendix D): the inputs {beta1^t} form a per-step
  *    sequence of momentum parameters; the paper's experiments hold it
  *    constant (beta1 = 0.975), and that constant sequence is what is taken
@@ -86,6 +94,43 @@ static double phi(double z, double gamma_l, double gamma_u)
     return p;
 }
 
+#define ORACLE_NORM_L2 0
+#define ORACLE_NORM_L1 1
+#define ORACLE_NORM_LINF 2
+
+/* Add one element to a running layer norm (Appendix F). */
+static double norm_add(int norm, double acc, double a)
+{
+    if (norm == ORACLE_NORM_L1)
+        return acc + fabs(a);
+    if (norm == ORACLE_NORM_LINF) {
+        double b = fabs(a);
+        return (isnan(b) || b > acc) ? b : acc;
+    }
+    return acc + a * a;
+}
+
+static double norm_finish(int norm, double acc)
+{
+    return norm == ORACLE_NORM_L2 ? sqrt(acc) : acc;
+}
+
+/*
+ * 1 if every scaled gradient element fp32(g_j) * fp32(grad_scale), computed
+ * in fp32, is finite; 0 if any is NaN or infinite.
+ */
+int oracle_gradient_finite(int64_t d, const void *g, int g_is_bf16, double grad_scale)
+{
+    float s = (float)grad_scale;
+    for (int64_t j = 0; j < d; ++j) {
+        float gj = (float)gradient_at(g, g_is_bf16, j);
+        float p = gj * s;
+        if (!isfinite(p))
+            return 0;
+    }
+    return 1;
+}
+
 /*
  * One LAMB step (Algorithm 2) on one layer block of d elements.
  *
@@ -97,7 +142,8 @@ static double phi(double z, double gamma_l, double gamma_u)
  *   x_{t+1} = x_t - eta_t phi(||x_t||) / ||u|| * u
  *
  * bias_correction = 0 drops the two divisions (Appendix E).
- * x, m, v are updated in place; g is fp32 or, with g_is_bf16, bf16 bits.
+ * x, m, v are updated in place; g is fp32 or, with g_is_bf16, bf16 bits, and
+ * g_t = grad_scale * g. norm selects the layer norm (ORACLE_NORM_*).
  * out[0] = trust ratio phi(||x_t||)/||u||, out[1] = ||x_t||, out[2] = ||u||.
  */
 int oracle_lamb_layer(int64_t d, float *x, const void *g, int g_is_bf16,
@@ -105,9 +151,9 @@ int oracle_lamb_layer(int64_t d, float *x, const void *g, int g_is_bf16,
                       double lr, double beta1, double beta2, double eps,
                       double weight_decay, int wd, double gamma_l,
                       double gamma_u, int64_t t, int bias_correction,
-                      double *out)
+                      double grad_scale, int norm, double *out)
 {
-    if (d < 1 || !x || !g || !m || !v || !out || t < 1)
+    if (d < 1 || !x || !g || !m || !v || !out || t < 1 || norm < 0 || norm > 2)
         return ORACLE_EINVAL;
     double *u = (double *)malloc((size_t)d * sizeof(double));
     if (!u)
@@ -122,7 +168,7 @@ int oracle_lamb_layer(int64_t d, float *x, const void *g, int g_is_bf16,
 
     double sum_xx = 0.0, sum_uu = 0.0;
     for (int64_t j = 0; j < d; ++j) {
-        double gj = gradient_at(g, g_is_bf16, j);
+        double gj = grad_scale * gradient_at(g, g_is_bf16, j);
         double xj = (double)x[j];
         double mj = beta1 * (double)m[j] + (1.0 - beta1) * gj;
         double vj = beta2 * (double)v[j] + (1.0 - beta2) * (gj * gj);
@@ -130,14 +176,14 @@ int oracle_lamb_layer(int64_t d, float *x, const void *g, int g_is_bf16,
         double v_hat = vj / c2;
         double r = m_hat / (sqrt(v_hat) + eps);
         u[j] = r + lam * xj;
-        sum_xx += xj * xj;
-        sum_uu += u[j] * u[j];
+        sum_xx = norm_add(norm, sum_xx, xj);
+        sum_uu = norm_add(norm, sum_uu, u[j]);
         m[j] = store_f32(mj);
         v[j] = store_f32(vj);
     }
 
-    double norm_x = sqrt(sum_xx);
-    double norm_u = sqrt(sum_uu);
+    double norm_x = norm_finish(norm, sum_xx);
+    double norm_u = norm_finish(norm, sum_uu);
     double ratio = (norm_u == 0.0) ? 0.0 : phi(norm_x, gamma_l, gamma_u) / norm_u;
     for (int64_t j = 0; j < d; ++j)
         x[j] = store_f32((double)x[j] - lr * ratio * u[j]);
@@ -155,15 +201,15 @@ int oracle_lamb_layer(int64_t d, float *x, const void *g, int g_is_bf16,
  *   m_t     = beta1 m_{t-1} + (1 - beta1) (g_t + lambda x_t)
  *   x_{t+1} = x_t - eta_t kappa phi(||x_t||) / ||m_t|| * m_t
  *
- * x and m are updated in place. out[0] = trust ratio kappa phi/||m_t||,
- * out[1] = ||x_t||, out[2] = ||m_t||.
+ * x and m are updated in place; g_t = grad_scale * g; norm as for LAMB.
+ * out[0] = trust ratio kappa phi/||m_t||, out[1] = ||x_t||, out[2] = ||m_t||.
  */
 int oracle_lars_layer(int64_t d, float *x, const void *g, int g_is_bf16,
                       float *m, double lr, double beta1, double weight_decay,
                       int wd, double gamma_l, double gamma_u,
-                      double trust_coef, double *out)
+                      double trust_coef, double grad_scale, int norm, double *out)
 {
-    if (d < 1 || !x || !g || !m || !out)
+    if (d < 1 || !x || !g || !m || !out || norm < 0 || norm > 2)
         return ORACLE_EINVAL;
     double *mt = (double *)malloc((size_t)d * sizeof(double));
     if (!mt)
@@ -172,15 +218,15 @@ int oracle_lars_layer(int64_t d, float *x, const void *g, int g_is_bf16,
     double lam = wd ? weight_decay : 0.0;
     double sum_xx = 0.0, sum_mm = 0.0;
     for (int64_t j = 0; j < d; ++j) {
-        double gj = gradient_at(g, g_is_bf16, j);
+        double gj = grad_scale * gradient_at(g, g_is_bf16, j);
         double xj = (double)x[j];
         mt[j] = beta1 * (double)m[j] + (1.0 - beta1) * (gj + lam * xj);
-        sum_xx += xj * xj;
-        sum_mm += mt[j] * mt[j];
+        sum_xx = norm_add(norm, sum_xx, xj);
+        sum_mm = norm_add(norm, sum_mm, mt[j]);
     }
 
-    double norm_x = sqrt(sum_xx);
-    double norm_m = sqrt(sum_mm);
+    double norm_x = norm_finish(norm, sum_xx);
+    double norm_m = norm_finish(norm, sum_mm);
     double ratio = (norm_m == 0.0)
                        ? 0.0
                        : trust_coef * phi(norm_x, gamma_l, gamma_u) / norm_m;
@@ -217,9 +263,10 @@ int oracle_nlamb_layer(int64_t d, float *x, const void *g, int g_is_bf16,
                        float *m, float *v,
                        double lr, double beta1, double beta2, double eps,
                        double weight_decay, int wd, double gamma_l,
-                       double gamma_u, int64_t t, int nesterov_v, double *out)
+                       double gamma_u, int64_t t, int nesterov_v,
+                       double grad_scale, int norm, double *out)
 {
-    if (d < 1 || !x || !g || !m || !v || !out || t < 1)
+    if (d < 1 || !x || !g || !m || !v || !out || t < 1 || norm < 0 || norm > 2)
         return ORACLE_EINVAL;
     double *u = (double *)malloc((size_t)d * sizeof(double));
     if (!u)
@@ -233,7 +280,7 @@ int oracle_nlamb_layer(int64_t d, float *x, const void *g, int g_is_bf16,
 
     double sum_xx = 0.0, sum_uu = 0.0;
     for (int64_t j = 0; j < d; ++j) {
-        double gj = gradient_at(g, g_is_bf16, j);
+        double gj = grad_scale * gradient_at(g, g_is_bf16, j);
         double xj = (double)x[j];
         double mj = beta1 * (double)m[j] + (1.0 - beta1) * gj;
         double m_hat = beta1 * mj / (1.0 - b1_next) + (1.0 - beta1) * gj / (1.0 - b1_t);
@@ -245,14 +292,14 @@ int oracle_nlamb_layer(int64_t d, float *x, const void *g, int g_is_bf16,
             v_hat = beta2 * vj / (1.0 - b2_t);
         double r = m_hat / (sqrt(v_hat) + eps);
         u[j] = r + lam * xj;
-        sum_xx += xj * xj;
-        sum_uu += u[j] * u[j];
+        sum_xx = norm_add(norm, sum_xx, xj);
+        sum_uu = norm_add(norm, sum_uu, u[j]);
         m[j] = store_f32(mj);
         v[j] = store_f32(vj);
     }
 
-    double norm_x = sqrt(sum_xx);
-    double norm_u = sqrt(sum_uu);
+    double norm_x = norm_finish(norm, sum_xx);
+    double norm_u = norm_finish(norm, sum_uu);
     double ratio = (norm_u == 0.0) ? 0.0 : phi(norm_x, gamma_l, gamma_u) / norm_u;
     for (int64_t j = 0; j < d; ++j)
         x[j] = store_f32((double)x[j] - lr * ratio * u[j]);

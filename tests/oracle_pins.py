@@ -519,7 +519,120 @@ LAMB_PINS = [pin_hand_cases, pin_constant_gradient, pin_step_length, pin_sign_sg
              pin_scalar_sign, pin_first_step, pin_bias_correction_factor,
              pin_no_correction_first_step, pin_ratio_bound, pin_mask, pin_scale_invariance,
              pin_zero_block, pin_zero_update, pin_permutation, pin_bf16_gradient]
+# ---------------------------------------------------------------------------
+# Gradient scaling, other layer norms (Appendix F), skipping non-finite steps
+# ---------------------------------------------------------------------------
+
+def pin_grad_scale(o):
+    """g_t is the scaled gradient: a step on (g, s = 2^k) is bit for bit the step
+    on (2^k g, 1) for every algorithm; for LARS with beta1 = 0 the momentum is
+    s g + lambda x (the scale never touches the decay term)."""
+    rng = np.random.default_rng(51)
+    x0 = _f32(rng.standard_normal(37))
+    g = _f32(rng.standard_normal(37) * 1e-3)
+    for algo in ("lamb", "nlamb", "lars"):
+        res = []
+        for gg, sc in ((g, 0.25), (_f32(g * 0.25), 1.0)):
+            xs, ms, vs = [x0.copy()], [np.zeros(37, np.float32)], [np.zeros(37, np.float32)]
+            for t in (1, 2):
+                if algo == "lamb":
+                    out = _lamb(o, xs, [gg], ms, vs, [True], t, eps=1e-6, weight_decay=0.02,
+                                grad_scale=sc)
+                elif algo == "nlamb":
+                    out = _nlamb(o, xs, [gg], ms, vs, [True], t, True, eps=1e-6,
+                                 weight_decay=0.02, grad_scale=sc)
+                else:
+                    out = _lars(o, xs, [gg], ms, [True], weight_decay=0.02, grad_scale=sc)
+            res.append((xs[0], ms[0], vs[0], out))
+        for a, b in zip(*res):
+            assert np.array_equal(a, b), algo
+    xs, ms = [x0.copy()], [np.zeros(37, np.float32)]
+    _lars(o, xs, [g], ms, [True], momentum=0.0, weight_decay=0.1, grad_scale=0.37)
+    _close(ms[0], 0.37 * g.astype(np.float64) + 0.1 * x0.astype(np.float64), 1.2e-7)
+
+
+def _pnorm(a, norm):
+    a = np.abs(np.asarray(a, np.float64))
+    return {"l2": np.sqrt(np.sum(a * a)), "l1": np.sum(a), "linf": np.max(a)}[norm]
+
+
+def pin_other_norms(o):
+    """Appendix F swaps the layer norm: with the L1 or L-infinity norm the
+    reported ||x|| is sum|x| or max|x|, and u / ||u|| has unit norm in that
+    norm, so the step has that norm's length eta * phi(||x||) (LAMB, N-LAMB)
+    or eta * kappa * phi(||x||) (LARS). With beta1 = beta2 = eps = lambda = 0,
+    u = sign(g): the L-infinity step is eta phi sign(g) and the L1 step is
+    eta phi sign(g) / d."""
+    rng = np.random.default_rng(52)
+    lr, gl, gu, kappa = 0.05, 0.5, 10.0, 0.3
+    for norm in ("l1", "linf"):
+        xs = [_f32(rng.standard_normal(n) * sc) for n, sc in ((120, 1.0), (40, 0.02))]
+        ms, vs = _zeros_like(xs), _zeros_like(xs)
+        for algo in ("lamb", "nlamb", "lars"):
+            for t in (1, 2):
+                gs = [_f32(rng.standard_normal(x.size) * 1e-3) for x in xs]
+                x_old = [x.astype(np.float64) for x in xs]
+                if algo == "lamb":
+                    out = _lamb(o, xs, gs, ms, vs, [True, False], t, lr=lr, eps=1e-6,
+                                weight_decay=0.05, gamma_l=gl, gamma_u=gu, norm=norm)
+                    k = 1.0
+                elif algo == "nlamb":
+                    out = _nlamb(o, xs, gs, ms, vs, [True, False], t, False, lr=lr, eps=1e-6,
+                                 weight_decay=0.05, gamma_l=gl, gamma_u=gu, norm=norm)
+                    k = 1.0
+                else:
+                    out = _lars(o, xs, gs, ms, [True, False], lr=lr, weight_decay=0.05,
+                                gamma_l=gl, gamma_u=gu, trust_coef=kappa, norm=norm)
+                    k = kappa
+                for i, xo in enumerate(x_old):
+                    _close(out[i, 1], _pnorm(xo, norm), 1e-12, what=norm + " ||x||")
+                    length = _pnorm(xs[i].astype(np.float64) - xo, norm)
+                    _close(length, lr * k * _phi(_pnorm(xo, norm), gl, gu), 2e-5,
+                           what="%s %s step length" % (norm, algo))
+        x = [_f32(rng.standard_normal(30) * 0.3)]
+        g = [_f32(rng.standard_normal(30))]
+        m, v = _zeros_like(x), _zeros_like(x)
+        xo = x[0].astype(np.float64)
+        _lamb(o, x, g, m, v, [True], 1, lr=0.1, beta1=0.0, beta2=0.0, norm=norm)
+        div = 30.0 if norm == "l1" else 1.0
+        expect = xo - 0.1 * _phi(_pnorm(xo, norm), 0.0, 10.0) * np.sign(g[0]) / div
+        _close(x[0], expect, 2e-7, atol=1e-9, what=norm + " sign-SGD")
+
+
+def pin_skip_nonfinite(o):
+    """A step with any NaN or infinite scaled gradient, in any tensor, changes
+    nothing when skipping is asked for; finiteness is decided on the fp32
+    product (3e38 * 10 overflows fp32 though not double)."""
+    rng = np.random.default_rng(53)
+    base_x = [_f32(rng.standard_normal(n)) for n in (20, 9)]
+    for bad, scale in ((np.inf, 1.0), (np.nan, 1.0), (3e38, 10.0)):
+        gs = [_f32(rng.standard_normal(20) * 1e-3), _f32(rng.standard_normal(9) * 1e-3)]
+        gs[1][4] = bad
+        for algo in ("lamb", "nlamb", "lars"):
+            xs = [x.copy() for x in base_x]
+            ms = [np.full(x.size, 0.5, np.float32) for x in xs]
+            vs = [np.full(x.size, 0.25, np.float32) for x in xs]
+            kw = dict(grad_scale=scale, skip_nonfinite=True)
+            if algo == "lamb":
+                out = _lamb(o, xs, gs, ms, vs, [True, True], 3, **kw)
+            elif algo == "nlamb":
+                out = _nlamb(o, xs, gs, ms, vs, [True, True], 3, False, **kw)
+            else:
+                out = _lars(o, xs, gs, ms, [True, True], **kw)
+            assert np.all(np.isnan(out))
+            for a, b in zip(xs, base_x):
+                assert np.array_equal(a, b)
+            assert all(np.all(m == 0.5) for m in ms) and all(np.all(v == 0.25) for v in vs)
+        assert not o.gradients_finite(gs, scale)
+    gs = [_f32(rng.standard_normal(20) * 1e-3), _f32([3e38] * 9)]
+    assert o.gradients_finite(gs, 1.0)
+    xs = [x.copy() for x in base_x]
+    out = _lamb(o, xs, gs, _zeros_like(xs), _zeros_like(xs), [True, True], 1, skip_nonfinite=True)
+    assert np.all(np.isfinite(out)) and not np.array_equal(xs[0], base_x[0])
+
+
 NLAMB_PINS = [pin_nlamb_constant_gradient, pin_nnlamb_lookahead]
+EXTENSION_PINS = [pin_grad_scale, pin_other_norms, pin_skip_nonfinite]
 LARS_PINS = [pin_lars_normalized_sgd, pin_lars_constant_gradient, pin_lars_weight_decay,
              pin_lars_step_length]
-ALL_PINS = LAMB_PINS + NLAMB_PINS + LARS_PINS
+ALL_PINS = LAMB_PINS + NLAMB_PINS + EXTENSION_PINS + LARS_PINS

@@ -34,7 +34,8 @@ MUTANTS = [
     ("lamb_lambda_sign", "u[j] = r + lam * xj;", "u[j] = r - lam * xj;", 0),
     ("lamb_mask_ignored", "double lam = wd ? weight_decay : 0.0;",
      "double lam = weight_decay;", 0),
-    ("lamb_norm_of_r", "sum_uu += u[j] * u[j];", "sum_uu += r * r;", 0),
+    ("lamb_norm_of_r", "sum_uu = norm_add(norm, sum_uu, u[j]);",
+     "sum_uu = norm_add(norm, sum_uu, r);", 0),
     ("lamb_phi_of_norm_u", "phi(norm_x, gamma_l, gamma_u) / norm_u;",
      "phi(norm_u, gamma_l, gamma_u) / norm_u;", 0),
     ("lamb_not_normalised", "phi(norm_x, gamma_l, gamma_u) / norm_u;",
@@ -56,7 +57,8 @@ MUTANTS = [
      "double lam = weight_decay;", 1),
     ("lars_no_trust_coef", "trust_coef * phi(norm_x, gamma_l, gamma_u) / norm_m",
      "phi(norm_x, gamma_l, gamma_u) / norm_m", 0),
-    ("lars_norm_of_g", "sum_mm += mt[j] * mt[j];", "sum_mm += gj * gj;", 0),
+    ("lars_norm_of_g", "sum_mm = norm_add(norm, sum_mm, mt[j]);",
+     "sum_mm = norm_add(norm, sum_mm, gj);", 0),
     ("lars_phi_of_norm_m", "phi(norm_x, gamma_l, gamma_u) / norm_m",
      "phi(norm_m, gamma_l, gamma_u) / norm_m", 0),
     ("lars_update_sign", "(double)x[j] - lr * ratio * mt[j]", "(double)x[j] + lr * ratio * mt[j]", 0),
@@ -82,6 +84,19 @@ MUTANTS = [
     ("nlamb_mask_ignored", "double lam = wd ? weight_decay : 0.0;", "double lam = weight_decay;", 2),
     ("nlamb_eps_inside_sqrt", "double r = m_hat / (sqrt(v_hat) + eps);",
      "double r = m_hat / sqrt(v_hat + eps);", 1),
+    ("lamb_grad_scale_dropped", "double gj = grad_scale * gradient_at(g, g_is_bf16, j);",
+     "double gj = gradient_at(g, g_is_bf16, j);", 0),
+    ("lars_grad_scale_dropped", "double gj = grad_scale * gradient_at(g, g_is_bf16, j);",
+     "double gj = gradient_at(g, g_is_bf16, j);", 1),
+    ("nlamb_grad_scale_dropped", "double gj = grad_scale * gradient_at(g, g_is_bf16, j);",
+     "double gj = gradient_at(g, g_is_bf16, j);", 2),
+    ("l1_squares", "return acc + fabs(a);", "return acc + a * a;", 0),
+    ("linf_no_abs", "double b = fabs(a);", "double b = a;", 0),
+    ("linf_sums", "return (isnan(b) || b > acc) ? b : acc;", "return acc + b;", 0),
+    ("norm_finish_sqrt_always", "return norm == ORACLE_NORM_L2 ? sqrt(acc) : acc;",
+     "return sqrt(acc);", 0),
+    ("finite_check_in_double", "float p = gj * s;", "double p = (double)gj * 10.0 * (double)s / 10.0;", 0),
+    ("finite_check_ignores_nan", "if (!isfinite(p))", "if (isinf(p))", 0),
     ("lars_zero_norm_not_guarded", "(norm_m == 0.0)\n                       ? 0.0\n                       :", "", 0),
 ]
 
