@@ -35,18 +35,26 @@ def eprint(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def bytes_per_param(algo: str, g_bytes: int):
+def bytes_per_param(algo: str, g_bytes: int, deferred: bool = False):
     """Algorithmic HBM bytes per parameter of (moment pass, apply pass).
 
-    LAMB moment pass reads x, g, m, v and writes m, v; apply reads x, m, v and
-    writes x (N-LAMB and NN-LAMB also read g there). LARS moment pass reads x,
-    g, m and writes m; apply reads x, m and writes x.
+    Direct mode: the LAMB moment pass reads x, g, m, v and writes m, v; the
+    apply pass reads x, m, v and writes x (N-LAMB and NN-LAMB also read g
+    there). LARS reads x, g, m and writes m, then reads x, m and writes x.
+    Deferred mode (skip on a non-finite gradient): the moment pass only
+    reads; the apply pass reads x, g and the old moments and writes x and the
+    new moments.
     """
-    if algo == "lamb":
-        return 4 + g_bytes + 4 + 4 + 4 + 4, 4 + 4 + 4 + 4
-    if algo in ("nlamb", "nnlamb"):  # the Nesterov update also needs g in the apply pass
-        return 4 + g_bytes + 4 + 4 + 4 + 4, 4 + g_bytes + 4 + 4 + 4
-    return 4 + g_bytes + 4 + 4, 4 + 4 + 4
+    state = 8 if algo != "lars" else 4          # m, v  /  m
+    moment_reads = 4 + g_bytes + state
+    if deferred:
+        return moment_reads, moment_reads + 4 + state
+    needs_g = algo in ("nlamb", "nnlamb")
+    return moment_reads + state, 4 + state + 4 + (g_bytes if needs_g else 0)
+
+
+def algo_label(algo: str) -> str:
+    return {"lamb": "LAMB", "lars": "LARS", "nlamb": "N-LAMB", "nnlamb": "NN-LAMB"}[algo]
 
 
 def kernel_source_hash() -> str:
@@ -158,6 +166,11 @@ def main() -> int:
     ap.add_argument("--config", type=int, default=2)
     ap.add_argument("--algo", choices=("lamb", "lars", "nlamb", "nnlamb"), default="lamb")
     ap.add_argument("--chunk", type=int, default=0, help="elements per chunk (0 = default)")
+    ap.add_argument("--norm", choices=("l2", "l1", "linf"), default="l2",
+                    help="layer norm (Appendix F)")
+    ap.add_argument("--grad-scale", type=float, default=1.0)
+    ap.add_argument("--skip-nonfinite", action="store_true",
+                    help="deferred-write mode that skips steps with NaN/Inf gradients")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", action="store_true")
@@ -186,19 +199,19 @@ def main() -> int:
                                                           ps.g_dtype))
     xs = paramsets.draw_params(ps, device="cuda")
     grads = paramsets.draw_grads(ps, 1, device="cuda")
+    extra = dict(norm=args.norm, grad_scale=args.grad_scale, skip_nonfinite=args.skip_nonfinite,
+                 wd_mask=ps.wd_mask(), chunk_elems=args.chunk)
     if args.algo == "lamb":
         opt = LAMB(xs, grads, lr=ps.lr, betas=(ps.beta1, ps.beta2), eps=ps.eps,
-                   weight_decay=ps.weight_decay, clamp=(ps.gamma_l, ps.gamma_u),
-                   wd_mask=ps.wd_mask(), chunk_elems=args.chunk)
+                   weight_decay=ps.weight_decay, clamp=(ps.gamma_l, ps.gamma_u), **extra)
     elif args.algo in ("nlamb", "nnlamb"):
         opt = LAMB(xs, grads, lr=ps.lr, betas=(NLAMB_BETA1, ps.beta2), eps=NLAMB_EPS,
                    weight_decay=ps.weight_decay, clamp=(ps.gamma_l, ps.gamma_u),
-                   wd_mask=ps.wd_mask(), chunk_elems=args.chunk,
-                   variant="n-lamb" if args.algo == "nlamb" else "nn-lamb")
+                   variant="n-lamb" if args.algo == "nlamb" else "nn-lamb", **extra)
     else:
         opt = LARS(xs, grads, lr=ps.lars_lr, momentum=ps.lars_momentum,
                    weight_decay=ps.weight_decay, clamp=(ps.gamma_l, ps.gamma_u),
-                   trust_coef=ps.lars_trust_coef, wd_mask=ps.wd_mask(), chunk_elems=args.chunk)
+                   trust_coef=ps.lars_trust_coef, **extra)
     n_tensors, n_chunks, chunk = _lib.lamb_plan_info(opt.plan)
 
     # The oracle's sample is copied out before the GPU steps move x; the
@@ -233,7 +246,7 @@ def main() -> int:
     ms_step = total_ms / args.steps
     P = ps.numel
     g_bytes = 2 if ps.g_dtype == "bf16" else 4
-    b_mom, b_app = bytes_per_param(args.algo, g_bytes)
+    b_mom, b_app = bytes_per_param(args.algo, g_bytes, args.skip_nonfinite)
     avg_mom = k_mom / recorded
     avg_app = k_app / recorded
     avg_fin = k_fin / recorded
@@ -242,10 +255,11 @@ def main() -> int:
     step_gbps = (b_mom + b_app) * P / ms_step / 1e6
     workload = ps.name
     src_hash = kernel_source_hash()
-    traffic = counter_traffic(workload, src_hash) if args.algo == "lamb" else None
-    algo_name = {"lamb": "LAMB", "lars": "LARS", "nlamb": "N-LAMB", "nnlamb": "NN-LAMB"}[args.algo]
-    kernel = "%s_moments_kernel<%s>" % ("lars" if args.algo == "lars" else "lamb",
-                                        "bf16" if g_bytes == 2 else "f32")
+    default_mode = (args.algo == "lamb" and args.norm == "l2" and not args.skip_nonfinite)
+    traffic = counter_traffic(workload, src_hash) if default_mode else None
+    algo_name = algo_label(args.algo)
+    kernel = "moments_kernel<%s, %s, %s%s>" % (algo_label(args.algo), "bf16" if g_bytes == 2 else "f32",
+                                              args.norm, ", deferred" if args.skip_nonfinite else "")
     eprint("step %.4f ms | moments %.4f ms (%.0f GB/s) | finalize %.4f ms | apply %.4f ms "
            "(%.0f GB/s) | whole step %.0f GB/s" % (ms_step, avg_mom, mom_gbps, avg_fin, avg_app,
                                                    app_gbps, step_gbps))
@@ -266,7 +280,9 @@ def main() -> int:
             "workload": "%s %s step: %d tensors, %d fp32 params, %s gradients"
                         % (workload, algo_name, n_tensors, P, ps.g_dtype),
             "algo": args.algo, "tensors": n_tensors, "params": P, "grad_dtype": ps.g_dtype,
-            "chunk_elems": chunk, "chunks": n_chunks, "seed_x": 1000 * ps.cfg,
+            "chunk_elems": chunk, "chunks": n_chunks, "norm": args.norm,
+            "grad_scale": args.grad_scale, "skip_nonfinite": args.skip_nonfinite,
+            "seed_x": 1000 * ps.cfg,
             "seed_g": 1000 * ps.cfg + 1,
         },
         "hbm_GBps": step_gbps,

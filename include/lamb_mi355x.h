@@ -84,6 +84,67 @@ typedef struct lamb_tensor {
 
 typedef struct lamb_plan lamb_plan; /* opaque */
 
+/* Which algorithm a step runs (lamb_step_ex). */
+typedef enum lamb_variant {
+    LAMB_VARIANT_LAMB = 0,   /* Algorithm 2 (Section 3.2)                      */
+    LAMB_VARIANT_NLAMB = 1,  /* Algorithm 3, N-LAMB (Appendix D)               */
+    LAMB_VARIANT_NNLAMB = 2, /* Algorithm 4, NN-LAMB (Appendix D)              */
+    LAMB_VARIANT_LARS = 3    /* Algorithm 1 (Section 3.1); needs a LARS plan   */
+} lamb_variant;
+
+/* Layer norm used for ||x_i|| and for the update's ||u_i|| (Appendix F: L2
+ * is the paper's default; it does not name the others it tried). */
+typedef enum lamb_norm {
+    LAMB_NORM_L2 = 0,   /* sqrt(sum a^2)                                      */
+    LAMB_NORM_L1 = 1,   /* sum |a|                                            */
+    LAMB_NORM_LINF = 2  /* max |a| (a NaN element makes it NaN)               */
+} lamb_norm;
+
+/*
+ * Hyperparameters of one step (lamb_step_ex). lamb_hparams_init fills the
+ * paper's defaults for a variant; change fields afterwards.
+ *   variant          lamb_variant
+ *   norm             lamb_norm
+ *   step             t >= 1 (LAMB family; ignored by LARS)
+ *   lr               eta_t, finite
+ *   beta1            LAMB family beta1, LARS momentum; in [0, 1)
+ *   beta2, eps       LAMB family: beta2 in [0, 1), eps finite >= 0
+ *   weight_decay     lambda, finite; applied where the tensor's wd mask is 1
+ *   gamma_l, gamma_u phi's clamp, 0 <= gamma_l <= gamma_u (gamma_u may be inf)
+ *   trust_coef       LARS only: ratio = trust_coef * phi / ||m||, finite
+ *   grad_scale       every gradient element is multiplied by it first, so the
+ *                    caller can hand over a sum of per-sample gradients (the
+ *                    1/|S_t| of Algorithms 1-2) or a loss-scaled gradient;
+ *                    finite
+ *   bias_correction  LAMB only: 1 (Algorithm 2) or 0 (Appendix E); must be 1
+ *                    for N-LAMB and NN-LAMB
+ *   skip_nonfinite   1: if any scaled gradient element (computed in fp32) of
+ *                    any tensor is NaN or infinite, the step leaves every x,
+ *                    m, v unchanged. The moment pass then writes nothing and
+ *                    the apply pass recomputes and writes x, m, v together,
+ *                    which costs 2 more bytes per parameter (bf16 g) or 4
+ *                    (fp32 g). 0: no check, moments are written in the first
+ *                    pass. The ratio and norm outputs of a skipped step are
+ *                    unspecified.
+ */
+typedef struct lamb_hparams {
+    int32_t variant;
+    int32_t norm;
+    int64_t step;
+    float lr;
+    float beta1;
+    float beta2;
+    float eps;
+    float weight_decay;
+    float gamma_l;
+    float gamma_u;
+    float trust_coef;
+    float grad_scale;
+    int32_t bias_correction;
+    int32_t skip_nonfinite;
+    int32_t reserved; /* set to 0 (lamb_hparams_init does) */
+} lamb_hparams;
+
 /*
  * Build a plan for a fixed table of blocks (Section 2's decomposition of x).
  * The table is copied; the tensor pointers must stay valid and unchanged for
@@ -110,6 +171,30 @@ LAMB_API lamb_status lamb_plan_destroy(lamb_plan *plan);
 /* Sizes of a plan (host outputs; any may be NULL). */
 LAMB_API lamb_status lamb_plan_info(const lamb_plan *plan, int32_t *n_tensors,
                            int32_t *n_chunks, int32_t *chunk_elems);
+
+/*
+ * Fill `hp` with the paper's defaults for `variant` (Section 4, Appendix H:
+ * beta1 0.9, beta2 0.999, eps 1e-6, lambda 0.01; Appendix D for N-LAMB and
+ * NN-LAMB: beta1 0.975, eps 1e-8; LARS: momentum 0.9, trust_coef 1), with
+ * step 1, lr 1e-3, phi clamp [0, 10], L2 norms, grad_scale 1, bias
+ * correction on and no non-finite skip. Errors: LAMB_ENULL, LAMB_EINVAL.
+ */
+LAMB_API lamb_status lamb_hparams_init(lamb_hparams *hp, int32_t variant);
+
+/*
+ * One step of any algorithm over every block of the plan: moment pass,
+ * per-tensor finalize (norms, phi, trust ratio), apply pass.
+ *   hp             host, validated before any HIP call
+ *   stream         hipStream_t (NULL = null stream)
+ *   ratio_out      device, n_tensors doubles, or NULL
+ *   norms_out      device, 2*n_tensors doubles {||x_i||, ||u_i||}, or NULL
+ *   nonfinite_out  device int32, or NULL; needs skip_nonfinite = 1; receives 1
+ *                  when the step was skipped, else 0
+ * Errors: LAMB_ENULL, LAMB_EPLAN (variant and plan disagree), LAMB_EINVAL,
+ * LAMB_EHIP.
+ */
+LAMB_API lamb_status lamb_step_ex(lamb_plan *plan, const lamb_hparams *hp, void *stream,
+                         double *ratio_out, double *norms_out, int32_t *nonfinite_out);
 
 /*
  * One LAMB step (Algorithm 2) over every block of the plan, at step t = step:

@@ -33,9 +33,21 @@ LAMB_GRAD_BF16 = 1
 LAMB_ALGO_LAMB = 0
 LAMB_ALGO_LARS = 1
 
+LAMB_VARIANT_LAMB = 0
+LAMB_VARIANT_NLAMB = 1
+LAMB_VARIANT_NNLAMB = 2
+LAMB_VARIANT_LARS = 3
+VARIANTS = {"lamb": LAMB_VARIANT_LAMB, "n-lamb": LAMB_VARIANT_NLAMB,
+            "nn-lamb": LAMB_VARIANT_NNLAMB, "lars": LAMB_VARIANT_LARS}
+
+LAMB_NORM_L2 = 0
+LAMB_NORM_L1 = 1
+LAMB_NORM_LINF = 2
+NORMS = {"l2": LAMB_NORM_L2, "l1": LAMB_NORM_L1, "linf": LAMB_NORM_LINF}
+
 # Every symbol the header declares (checked by the test suite).
-EXPORTS = ("lamb_plan_create", "lamb_plan_destroy", "lamb_plan_info", "lamb_step",
-           "nlamb_step", "lars_step", "lamb_chunk_table", "lamb_plan_set_timing", "lamb_plan_timing",
+EXPORTS = ("lamb_plan_create", "lamb_plan_destroy", "lamb_plan_info", "lamb_hparams_init",
+           "lamb_step_ex", "lamb_step", "nlamb_step", "lars_step", "lamb_chunk_table", "lamb_plan_set_timing", "lamb_plan_timing",
            "lamb_status_str", "lamb_last_error")
 
 
@@ -49,6 +61,16 @@ class LambError(RuntimeError):
 class lamb_tensor(ctypes.Structure):
     _fields_ = [("x", ctypes.c_void_p), ("g", ctypes.c_void_p), ("m", ctypes.c_void_p),
                 ("v", ctypes.c_void_p), ("numel", ctypes.c_int64), ("wd", ctypes.c_int32),
+                ("reserved", ctypes.c_int32)]
+
+
+class lamb_hparams(ctypes.Structure):
+    _fields_ = [("variant", ctypes.c_int32), ("norm", ctypes.c_int32), ("step", ctypes.c_int64),
+                ("lr", ctypes.c_float), ("beta1", ctypes.c_float), ("beta2", ctypes.c_float),
+                ("eps", ctypes.c_float), ("weight_decay", ctypes.c_float),
+                ("gamma_l", ctypes.c_float), ("gamma_u", ctypes.c_float),
+                ("trust_coef", ctypes.c_float), ("grad_scale", ctypes.c_float),
+                ("bias_correction", ctypes.c_int32), ("skip_nonfinite", ctypes.c_int32),
                 ("reserved", ctypes.c_int32)]
 
 
@@ -76,6 +98,8 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
     lib.lamb_plan_info.argtypes = [vp, P(i32), P(i32), P(i32)]
     lib.lamb_step.argtypes = [vp, f32, f32, f32, f32, f32, f32, f32, i64, i32, vp, vp, vp]
     lib.nlamb_step.argtypes = [vp, f32, f32, f32, f32, f32, f32, f32, i64, i32, vp, vp, vp]
+    lib.lamb_hparams_init.argtypes = [P(lamb_hparams), i32]
+    lib.lamb_step_ex.argtypes = [vp, P(lamb_hparams), vp, vp, vp, vp]
     lib.lars_step.argtypes = [vp, f32, f32, f32, f32, f32, f32, vp, vp, vp]
     lib.lamb_chunk_table.argtypes = [P(i64), i32, i32, i32, P(i32), P(i64), P(i32), P(i32)]
     lib.lamb_plan_set_timing.argtypes = [vp, i32]
@@ -156,6 +180,27 @@ def lamb_plan_info(plan: Plan) -> Tuple[int, int, int]:
     _check(load().lamb_plan_info(_vp(plan.handle), ctypes.byref(a), ctypes.byref(b),
                                  ctypes.byref(c)), "lamb_plan_info")
     return a.value, b.value, c.value
+
+
+def lamb_hparams_init(variant="lamb", **fields) -> lamb_hparams:
+    """The paper's defaults for ``variant`` (a name or LAMB_VARIANT_*), then
+    ``fields`` set by name (``norm`` may be "l2", "l1" or "linf")."""
+    hp = lamb_hparams()
+    v = VARIANTS[variant] if isinstance(variant, str) else int(variant)
+    _check(load().lamb_hparams_init(ctypes.byref(hp), v), "lamb_hparams_init")
+    for k, val in fields.items():
+        if k == "norm" and isinstance(val, str):
+            val = NORMS[val]
+        if not hasattr(hp, k):
+            raise AttributeError("lamb_hparams has no field %r" % k)
+        setattr(hp, k, val)
+    return hp
+
+
+def lamb_step_ex(plan: Plan, hp: lamb_hparams, stream: int = 0, ratio_out: int = 0,
+                 norms_out: int = 0, nonfinite_out: int = 0) -> None:
+    _check(load().lamb_step_ex(_vp(plan.handle), ctypes.byref(hp), _vp(stream), _vp(ratio_out),
+                               _vp(norms_out), _vp(nonfinite_out)), "lamb_step_ex")
 
 
 def lamb_step(plan: Plan, lr: float, beta1: float, beta2: float, eps: float,

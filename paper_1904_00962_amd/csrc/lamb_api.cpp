@@ -26,10 +26,14 @@ struct lamb_plan {
     int32_t n_chunks = 0;
     int32_t chunk_elems = 0;
     void *device_block = nullptr;  // one allocation holding the four buffers below
+    int32_t n_coarse = 0;       // coarse chunks (kCoarseFactor * chunk_elems each)
     TensorDesc *tensors = nullptr;
     ChunkDesc *chunks = nullptr;
+    ChunkDesc *coarse_chunks = nullptr;
     Partial *partials = nullptr;
     float *scale = nullptr;
+    uint32_t *flags = nullptr;     // two non-finite flags, alternating per deferred step
+    uint32_t deferred_steps = 0;   // deferred steps enqueued so far (selects the flag)
     // timing hooks: 4 events per recorded step
     std::vector<hipEvent_t> events;
     int32_t timing_capacity = 0;
@@ -107,16 +111,14 @@ lamb_status check_phi_bounds(float gamma_l, float gamma_u) {
     return LAMB_OK;
 }
 
-lamb_status check_beta(float beta, const char *name) {
-    if (!(beta >= 0.0f && beta < 1.0f))
-        return fail(LAMB_EINVAL, "%s = %g outside [0, 1)", name, double(beta));
-    return LAMB_OK;
-}
-
 void record(lamb_plan *plan, int slot, hipStream_t stream) {
     if (plan->timing_used < plan->timing_capacity)
         (void)hipEventRecord(plan->events[size_t(plan->timing_used) * 4 + slot], stream);
 }
+
+// The chunk table of `numel` at `chunk` elements per chunk (lamb_chunk_table).
+lamb_status build_chunks(const std::vector<int64_t> &numel, int32_t chunk, int32_t n_chunks,
+                         std::vector<ChunkDesc> *out);
 
 void release_events(lamb_plan *plan) {
     for (hipEvent_t e : plan->events)
@@ -184,6 +186,29 @@ lamb_status lamb_chunk_table(const int64_t *numel, int32_t n_tensors, int32_t ch
     return LAMB_OK;
 }
 
+}  // extern "C"
+
+namespace {
+
+lamb_status build_chunks(const std::vector<int64_t> &numel, int32_t chunk, int32_t n_chunks,
+                         std::vector<ChunkDesc> *out) {
+    std::vector<int32_t> ct(static_cast<size_t>(n_chunks)), cl(static_cast<size_t>(n_chunks));
+    std::vector<int64_t> cs(static_cast<size_t>(n_chunks));
+    int32_t count = 0;
+    lamb_status st = lamb_chunk_table(numel.data(), int32_t(numel.size()), chunk, n_chunks,
+                                      ct.data(), cs.data(), cl.data(), &count);
+    if (st != LAMB_OK)
+        return st;
+    out->resize(static_cast<size_t>(n_chunks));
+    for (int32_t k = 0; k < n_chunks; ++k)
+        (*out)[size_t(k)] = ChunkDesc{ct[size_t(k)], cl[size_t(k)], cs[size_t(k)]};
+    return LAMB_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
 lamb_status lamb_plan_create(const lamb_tensor *tensors, int32_t n_tensors,
                              lamb_grad_dtype g_dtype, lamb_algo algo, int32_t chunk_elems,
                              lamb_plan **out) {
@@ -250,27 +275,30 @@ lamb_status lamb_plan_create(const lamb_tensor *tensors, int32_t n_tensors,
     if (total < 0)
         return fail(LAMB_EINVAL, "more than 2^31-1 chunks; raise chunk_elems");
     const int32_t n_chunks = int32_t(total);
+    const int32_t coarse = int32_t(std::min<int64_t>(int64_t(chunk) * kCoarseFactor,
+                                                     kMaxChunkElems));
+    const int32_t n_coarse = int32_t(count_chunks(numel.data(), n_tensors, coarse));
 
-    // Host images of the tables.
+    // Host images of the tables: the fine and the coarse chunk table, and the
+    // tensor table with each tensor's range in both.
     std::vector<TensorDesc> host_tensors(static_cast<size_t>(n_tensors));
-    std::vector<ChunkDesc> host_chunks(static_cast<size_t>(n_chunks));
+    std::vector<ChunkDesc> host_chunks;
+    std::vector<ChunkDesc> host_coarse;
+    st = build_chunks(numel, chunk, n_chunks, &host_chunks);
+    if (st == LAMB_OK)
+        st = build_chunks(numel, coarse, n_coarse, &host_coarse);
+    if (st != LAMB_OK)
+        return st;
     {
-        std::vector<int32_t> ct(static_cast<size_t>(n_chunks)), cl(static_cast<size_t>(n_chunks));
-        std::vector<int64_t> cs(static_cast<size_t>(n_chunks));
-        int32_t count = 0;
-        st = lamb_chunk_table(numel.data(), n_tensors, chunk, n_chunks, ct.data(), cs.data(),
-                              cl.data(), &count);
-        if (st != LAMB_OK)
-            return st;
-        for (int32_t k = 0; k < n_chunks; ++k)
-            host_chunks[size_t(k)] = ChunkDesc{ct[size_t(k)], cl[size_t(k)], cs[size_t(k)]};
-        int32_t first = 0;
+        int32_t first = 0, first_coarse = 0;
         for (int32_t i = 0; i < n_tensors; ++i) {
             const lamb_tensor &t = tensors[i];
             const int32_t nc = int32_t((t.numel + chunk - 1) / chunk);
+            const int32_t ncc = int32_t((t.numel + coarse - 1) / coarse);
             host_tensors[size_t(i)] = TensorDesc{t.x, t.g, t.m, needs_v ? t.v : nullptr, t.numel,
-                                                 t.wd, first, nc, 0, 0};
+                                                 t.wd, first, nc, first_coarse, ncc, 0};
             first += nc;
+            first_coarse += ncc;
         }
     }
 
@@ -285,9 +313,12 @@ lamb_status lamb_plan_create(const lamb_tensor *tensors, int32_t n_tensors,
     auto round256 = [](size_t b) { return (b + 255) & ~size_t(255); };
     const size_t tensors_bytes = round256(sizeof(TensorDesc) * size_t(n_tensors));
     const size_t chunks_bytes = round256(sizeof(ChunkDesc) * size_t(n_chunks));
+    const size_t coarse_bytes = round256(sizeof(ChunkDesc) * size_t(n_coarse));
     const size_t partial_bytes = round256(sizeof(Partial) * size_t(n_chunks));
     const size_t scale_bytes = round256(sizeof(float) * size_t(n_tensors));
-    err = hipMalloc(&plan->device_block, tensors_bytes + chunks_bytes + partial_bytes + scale_bytes);
+    const size_t flag_bytes = 256;
+    err = hipMalloc(&plan->device_block, tensors_bytes + chunks_bytes + coarse_bytes +
+                                             partial_bytes + scale_bytes + flag_bytes);
     if (err != hipSuccess) {
         delete plan;
         if (err == hipErrorOutOfMemory)
@@ -296,14 +327,26 @@ lamb_status lamb_plan_create(const lamb_tensor *tensors, int32_t n_tensors,
     }
     char *base = static_cast<char *>(plan->device_block);
     plan->tensors = reinterpret_cast<TensorDesc *>(base);
-    plan->chunks = reinterpret_cast<ChunkDesc *>(base + tensors_bytes);
-    plan->partials = reinterpret_cast<Partial *>(base + tensors_bytes + chunks_bytes);
-    plan->scale = reinterpret_cast<float *>(base + tensors_bytes + chunks_bytes + partial_bytes);
+    base += tensors_bytes;
+    plan->chunks = reinterpret_cast<ChunkDesc *>(base);
+    base += chunks_bytes;
+    plan->coarse_chunks = reinterpret_cast<ChunkDesc *>(base);
+    base += coarse_bytes;
+    plan->partials = reinterpret_cast<Partial *>(base);  // sized for the fine table
+    base += partial_bytes;
+    plan->scale = reinterpret_cast<float *>(base);
+    base += scale_bytes;
+    plan->flags = reinterpret_cast<uint32_t *>(base);
     err = hipMemcpy(plan->tensors, host_tensors.data(), sizeof(TensorDesc) * size_t(n_tensors),
                     hipMemcpyHostToDevice);
     if (err == hipSuccess)
         err = hipMemcpy(plan->chunks, host_chunks.data(), sizeof(ChunkDesc) * size_t(n_chunks),
                         hipMemcpyHostToDevice);
+    if (err == hipSuccess)
+        err = hipMemcpy(plan->coarse_chunks, host_coarse.data(),
+                        sizeof(ChunkDesc) * size_t(n_coarse), hipMemcpyHostToDevice);
+    if (err == hipSuccess)
+        err = hipMemset(plan->flags, 0, flag_bytes);
     if (err != hipSuccess) {
         (void)hipFree(plan->device_block);
         delete plan;
@@ -313,6 +356,7 @@ lamb_status lamb_plan_create(const lamb_tensor *tensors, int32_t n_tensors,
     plan->g_dtype = g_dtype;
     plan->n_tensors = n_tensors;
     plan->n_chunks = n_chunks;
+    plan->n_coarse = n_coarse;
     plan->chunk_elems = chunk;
     *out = plan;
     return LAMB_OK;
@@ -347,172 +391,233 @@ lamb_status lamb_plan_info(const lamb_plan *plan, int32_t *n_tensors, int32_t *n
 
 namespace {
 
-// Scalar checks shared by the LAMB family (Algorithms 2, 3 and 4).
-lamb_status check_lamb_scalars(const lamb_plan *plan, float lr, float beta1, float beta2,
-                               float eps, float weight_decay, float gamma_l, float gamma_u,
-                               int64_t step) {
-    if (!plan)
-        return fail(LAMB_ENULL, "plan must not be NULL");
-    if (plan->algo != LAMB_ALGO_LAMB)
-        return fail(LAMB_EPLAN, "the LAMB family needs a plan created for LAMB");
-    if (step < 1)
-        return fail(LAMB_EINVAL, "step = %lld, need >= 1", static_cast<long long>(step));
-    lamb_status st = check_beta(beta1, "beta1");
-    if (st == LAMB_OK)
-        st = check_beta(beta2, "beta2");
+bool valid_beta(float beta) { return beta >= 0.0f && beta < 1.0f; }
+
+// Host-side validation of one step's hyperparameters (all before any HIP call).
+lamb_status check_hparams(const lamb_plan *plan, const lamb_hparams *hp,
+                          const int32_t *nonfinite_out) {
+    if (!plan || !hp)
+        return fail(LAMB_ENULL, "plan and hparams must not be NULL");
+    if (hp->reserved != 0)
+        return fail(LAMB_EINVAL, "hparams.reserved must be 0");
+    const int32_t variant = hp->variant;
+    if (variant < LAMB_VARIANT_LAMB || variant > LAMB_VARIANT_LARS)
+        return fail(LAMB_EINVAL, "unknown variant %d", variant);
+    const bool lars = variant == LAMB_VARIANT_LARS;
+    if (lars != (plan->algo == LAMB_ALGO_LARS))
+        return fail(LAMB_EPLAN, "%s needs a plan created for %s", lars ? "LARS" : "the LAMB family",
+                    lars ? "LARS" : "LAMB");
+    if (hp->norm < LAMB_NORM_L2 || hp->norm > LAMB_NORM_LINF)
+        return fail(LAMB_EINVAL, "unknown norm %d", hp->norm);
+    if (!valid_beta(hp->beta1))
+        return fail(LAMB_EINVAL, "%s = %g outside [0, 1)", lars ? "momentum" : "beta1",
+                    double(hp->beta1));
+    if (!finite(hp->lr) || !finite(hp->weight_decay) || !finite(hp->grad_scale))
+        return fail(LAMB_EINVAL, "lr, weight_decay and grad_scale must be finite");
+    lamb_status st = check_phi_bounds(hp->gamma_l, hp->gamma_u);
     if (st != LAMB_OK)
         return st;
-    if (!(eps >= 0.0f) || !finite(eps))
-        return fail(LAMB_EINVAL, "eps = %g, need finite and >= 0", double(eps));
-    if (!finite(lr) || !finite(weight_decay))
-        return fail(LAMB_EINVAL, "lr and weight_decay must be finite");
-    return check_phi_bounds(gamma_l, gamma_u);
+    if (hp->skip_nonfinite != 0 && hp->skip_nonfinite != 1)
+        return fail(LAMB_EINVAL, "skip_nonfinite must be 0 or 1");
+    if (nonfinite_out && !hp->skip_nonfinite)
+        return fail(LAMB_EINVAL, "nonfinite_out needs skip_nonfinite = 1");
+    if (lars) {
+        if (!finite(hp->trust_coef))
+            return fail(LAMB_EINVAL, "trust_coef must be finite");
+        return LAMB_OK;
+    }
+    if (hp->step < 1)
+        return fail(LAMB_EINVAL, "step = %lld, need >= 1", static_cast<long long>(hp->step));
+    if (!valid_beta(hp->beta2))
+        return fail(LAMB_EINVAL, "beta2 = %g outside [0, 1)", double(hp->beta2));
+    if (!(hp->eps >= 0.0f) || !finite(hp->eps))
+        return fail(LAMB_EINVAL, "eps = %g, need finite and >= 0", double(hp->eps));
+    if (hp->bias_correction != 0 && hp->bias_correction != 1)
+        return fail(LAMB_EINVAL, "bias_correction must be 0 or 1");
+    if (variant != LAMB_VARIANT_LAMB && !hp->bias_correction)
+        return fail(LAMB_EINVAL, "N-LAMB and NN-LAMB carry their own bias correction");
+    return LAMB_OK;
 }
 
-LambArgs lamb_args(float beta1, float beta2, float eps, float weight_decay) {
-    LambArgs a;
-    a.beta1 = beta1;
-    a.one_minus_beta1 = float(1.0 - double(beta1));
-    a.beta2 = beta2;
-    a.one_minus_beta2 = float(1.0 - double(beta2));
+// fp32 kernel scalars of a validated step. The LAMB family's correction
+// coefficients are computed in double and rounded once.
+StepArgs step_args(const lamb_hparams &hp) {
+    StepArgs a;
+    a.beta1 = hp.beta1;
+    a.one_minus_beta1 = float(1.0 - double(hp.beta1));
+    a.beta2 = hp.beta2;
+    a.one_minus_beta2 = float(1.0 - double(hp.beta2));
     a.m_scale = a.v_scale = 1.0f;
     a.m_grad = a.v_grad = 0.0f;
-    a.eps = eps;
-    a.weight_decay = weight_decay;
+    a.eps = hp.eps;
+    a.weight_decay = hp.weight_decay;
+    a.grad_scale = hp.grad_scale;
+    a.flag_slot = 0;
+    const double b1 = hp.beta1, b2 = hp.beta2, t = double(hp.step);
+    switch (hp.variant) {
+    case LAMB_VARIANT_LAMB:
+        // Algorithm 2: m_hat = m_t / (1 - beta1^t), v_hat = v_t / (1 - beta2^t)
+        if (hp.bias_correction) {
+            a.m_scale = float(1.0 / (1.0 - std::pow(b1, t)));
+            a.v_scale = float(1.0 / (1.0 - std::pow(b2, t)));
+        }
+        break;
+    case LAMB_VARIANT_NLAMB:
+    case LAMB_VARIANT_NNLAMB:
+        // Algorithms 3 and 4 with the constant sequence beta1^t = beta1,
+        // whose running products are powers.
+        a.m_scale = float(b1 / (1.0 - std::pow(b1, t + 1.0)));
+        a.m_grad = float((1.0 - b1) / (1.0 - std::pow(b1, t)));
+        if (hp.variant == LAMB_VARIANT_NNLAMB) {
+            a.v_scale = float(b2 / (1.0 - std::pow(b2, t + 1.0)));
+            a.v_grad = float((1.0 - b2) / (1.0 - std::pow(b2, t)));
+        } else {
+            a.v_scale = float(b2 / (1.0 - std::pow(b2, t)));
+        }
+        break;
+    default:
+        break;
+    }
     return a;
-}
-
-// Enqueue moment pass, finalize and apply pass of the LAMB family.
-lamb_status launch_lamb_family(lamb_plan *plan, LambVariant variant, const LambArgs &a,
-                               const FinalizeArgs &f, void *stream, double *ratio_out,
-                               double *norms_out) {
-    DeviceGuard guard(plan->device);
-    if (guard.status != hipSuccess)
-        return fail_hip(guard.status, "selecting the plan's device");
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    const bool bf16 = plan->g_dtype == LAMB_GRAD_BF16;
-    record(plan, 0, s);
-    hipError_t err = launch_lamb_moments(plan->tensors, plan->chunks, plan->partials,
-                                         plan->n_chunks, bf16, variant, a, s);
-    if (err != hipSuccess)
-        return fail_hip(err, "launching the LAMB moment kernel");
-    record(plan, 1, s);
-    err = launch_finalize(plan->tensors, plan->n_tensors, plan->partials, f, plan->scale,
-                          ratio_out, norms_out, s);
-    if (err != hipSuccess)
-        return fail_hip(err, "launching the finalize kernel");
-    record(plan, 2, s);
-    err = launch_lamb_apply(plan->tensors, plan->chunks, plan->scale, plan->n_chunks, bf16,
-                            variant, a, s);
-    if (err != hipSuccess)
-        return fail_hip(err, "launching the LAMB apply kernel");
-    record(plan, 3, s);
-    if (plan->timing_used < plan->timing_capacity)
-        ++plan->timing_used;
-    return LAMB_OK;
 }
 
 }  // namespace
 
 extern "C" {
 
+lamb_status lamb_hparams_init(lamb_hparams *hp, int32_t variant) {
+    if (!hp)
+        return fail(LAMB_ENULL, "hparams must not be NULL");
+    if (variant < LAMB_VARIANT_LAMB || variant > LAMB_VARIANT_LARS)
+        return fail(LAMB_EINVAL, "unknown variant %d", variant);
+    *hp = lamb_hparams{};
+    hp->variant = variant;
+    hp->norm = LAMB_NORM_L2;
+    hp->step = 1;
+    hp->lr = 1e-3f;
+    hp->weight_decay = 0.01f;
+    hp->gamma_l = 0.0f;
+    hp->gamma_u = 10.0f;
+    hp->trust_coef = 1.0f;
+    hp->grad_scale = 1.0f;
+    hp->bias_correction = 1;
+    hp->skip_nonfinite = 0;
+    switch (variant) {
+    case LAMB_VARIANT_LAMB:  // Section 4 and Appendix H
+        hp->beta1 = 0.9f;
+        hp->beta2 = 0.999f;
+        hp->eps = 1e-6f;
+        break;
+    case LAMB_VARIANT_NLAMB:  // Appendix D, after Nadam
+    case LAMB_VARIANT_NNLAMB:
+        hp->beta1 = 0.975f;
+        hp->beta2 = 0.999f;
+        hp->eps = 1e-8f;
+        break;
+    default:  // LARS: heavy-ball momentum
+        hp->beta1 = 0.9f;
+        hp->beta2 = 0.0f;
+        hp->eps = 0.0f;
+        break;
+    }
+    return LAMB_OK;
+}
+
+lamb_status lamb_step_ex(lamb_plan *plan, const lamb_hparams *hp, void *stream,
+                         double *ratio_out, double *norms_out, int32_t *nonfinite_out) {
+    lamb_status st = check_hparams(plan, hp, nonfinite_out);
+    if (st != LAMB_OK)
+        return st;
+    StepKind kind;
+    kind.algo = static_cast<Algo>(hp->variant);
+    kind.norm = static_cast<NormKind>(hp->norm);
+    kind.bf16_grad = plan->g_dtype == LAMB_GRAD_BF16;
+    kind.deferred = hp->skip_nonfinite != 0;
+    StepArgs a = step_args(*hp);
+    a.flag_slot = plan->deferred_steps & 1u;
+    const bool lars = hp->variant == LAMB_VARIANT_LARS;
+    const FinalizeArgs f{double(hp->lr), double(hp->gamma_l), double(hp->gamma_u),
+                         lars ? double(hp->trust_coef) : 1.0};
+
+    DeviceGuard guard(plan->device);
+    if (guard.status != hipSuccess)
+        return fail_hip(guard.status, "selecting the plan's device");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    record(plan, 0, s);
+    // Deferred moment passes only read, and use the coarse chunk table.
+    const ChunkDesc *moment_chunks = kind.deferred ? plan->coarse_chunks : plan->chunks;
+    const int32_t n_moment_chunks = kind.deferred ? plan->n_coarse : plan->n_chunks;
+    hipError_t err = launch_moments(kind, plan->tensors, moment_chunks, plan->partials,
+                                    n_moment_chunks, plan->flags, a, s);
+    if (err != hipSuccess)
+        return fail_hip(err, "launching the moment kernel");
+    record(plan, 1, s);
+    err = launch_finalize(kind.norm, kind.deferred, plan->tensors, plan->n_tensors,
+                          plan->partials, f, plan->scale, ratio_out, norms_out, s);
+    if (err != hipSuccess)
+        return fail_hip(err, "launching the finalize kernel");
+    record(plan, 2, s);
+    err = launch_apply(kind, plan->tensors, plan->chunks, plan->scale, plan->n_chunks,
+                       plan->flags, nonfinite_out, a, s);
+    if (err != hipSuccess)
+        return fail_hip(err, "launching the apply kernel");
+    record(plan, 3, s);
+    if (plan->timing_used < plan->timing_capacity)
+        ++plan->timing_used;
+    if (kind.deferred)
+        ++plan->deferred_steps;
+    return LAMB_OK;
+}
+
 lamb_status lamb_step(lamb_plan *plan, float lr, float beta1, float beta2, float eps,
                       float weight_decay, float gamma_l, float gamma_u, int64_t step,
                       int32_t bias_correction, void *stream, double *ratio_out,
                       double *norms_out) {
-    lamb_status st = check_lamb_scalars(plan, lr, beta1, beta2, eps, weight_decay, gamma_l,
-                                        gamma_u, step);
-    if (st != LAMB_OK)
-        return st;
-    if (bias_correction != 0 && bias_correction != 1)
-        return fail(LAMB_EINVAL, "bias_correction must be 0 or 1");
-    // Bias-correction denominators 1 - beta^t in double (Algorithm 2).
-    double c1 = 1.0, c2 = 1.0;
-    if (bias_correction) {
-        c1 = 1.0 - std::pow(double(beta1), double(step));
-        c2 = 1.0 - std::pow(double(beta2), double(step));
-    }
-    LambArgs a = lamb_args(beta1, beta2, eps, weight_decay);
-    a.m_scale = float(1.0 / c1);
-    a.v_scale = float(1.0 / c2);
-    const FinalizeArgs f{double(lr), double(gamma_l), double(gamma_u), 1.0};
-    return launch_lamb_family(plan, kLamb, a, f, stream, ratio_out, norms_out);
+    lamb_hparams hp;
+    lamb_hparams_init(&hp, LAMB_VARIANT_LAMB);
+    hp.lr = lr;
+    hp.beta1 = beta1;
+    hp.beta2 = beta2;
+    hp.eps = eps;
+    hp.weight_decay = weight_decay;
+    hp.gamma_l = gamma_l;
+    hp.gamma_u = gamma_u;
+    hp.step = step;
+    hp.bias_correction = bias_correction;
+    return lamb_step_ex(plan, &hp, stream, ratio_out, norms_out, nullptr);
 }
 
 lamb_status nlamb_step(lamb_plan *plan, float lr, float beta1, float beta2, float eps,
                        float weight_decay, float gamma_l, float gamma_u, int64_t step,
                        int32_t nesterov_v, void *stream, double *ratio_out,
                        double *norms_out) {
-    lamb_status st = check_lamb_scalars(plan, lr, beta1, beta2, eps, weight_decay, gamma_l,
-                                        gamma_u, step);
-    if (st != LAMB_OK)
-        return st;
     if (nesterov_v != 0 && nesterov_v != 1)
         return fail(LAMB_EINVAL, "nesterov_v must be 0 or 1");
-    // Algorithms 3 and 4 with the constant sequence beta1^t = beta1, whose
-    // products are powers: coefficients in double, rounded once to fp32.
-    const double b1 = beta1, b2 = beta2, t = double(step);
-    const double b1_t = std::pow(b1, t), b1_next = std::pow(b1, t + 1.0);
-    const double b2_t = std::pow(b2, t), b2_next = std::pow(b2, t + 1.0);
-    LambArgs a = lamb_args(beta1, beta2, eps, weight_decay);
-    a.m_scale = float(b1 / (1.0 - b1_next));
-    a.m_grad = float((1.0 - b1) / (1.0 - b1_t));
-    if (nesterov_v) {
-        a.v_scale = float(b2 / (1.0 - b2_next));
-        a.v_grad = float((1.0 - b2) / (1.0 - b2_t));
-    } else {
-        a.v_scale = float(b2 / (1.0 - b2_t));
-    }
-    const FinalizeArgs f{double(lr), double(gamma_l), double(gamma_u), 1.0};
-    return launch_lamb_family(plan, nesterov_v ? kNNLamb : kNLamb, a, f, stream, ratio_out,
-                              norms_out);
+    lamb_hparams hp;
+    lamb_hparams_init(&hp, nesterov_v ? LAMB_VARIANT_NNLAMB : LAMB_VARIANT_NLAMB);
+    hp.lr = lr;
+    hp.beta1 = beta1;
+    hp.beta2 = beta2;
+    hp.eps = eps;
+    hp.weight_decay = weight_decay;
+    hp.gamma_l = gamma_l;
+    hp.gamma_u = gamma_u;
+    hp.step = step;
+    return lamb_step_ex(plan, &hp, stream, ratio_out, norms_out, nullptr);
 }
 
 lamb_status lars_step(lamb_plan *plan, float lr, float momentum, float weight_decay,
                       float gamma_l, float gamma_u, float trust_coef, void *stream,
                       double *ratio_out, double *norms_out) {
-    if (!plan)
-        return fail(LAMB_ENULL, "plan must not be NULL");
-    if (plan->algo != LAMB_ALGO_LARS)
-        return fail(LAMB_EPLAN, "lars_step needs a plan created for LARS");
-    lamb_status st = check_beta(momentum, "momentum");
-    if (st != LAMB_OK)
-        return st;
-    if (!finite(lr) || !finite(weight_decay) || !finite(trust_coef))
-        return fail(LAMB_EINVAL, "lr, weight_decay and trust_coef must be finite");
-    st = check_phi_bounds(gamma_l, gamma_u);
-    if (st != LAMB_OK)
-        return st;
-
-    LarsArgs a;
-    a.beta1 = momentum;
-    a.one_minus_beta1 = float(1.0 - double(momentum));
-    a.weight_decay = weight_decay;
-    FinalizeArgs f{double(lr), double(gamma_l), double(gamma_u), double(trust_coef)};
-
-    DeviceGuard guard(plan->device);
-    if (guard.status != hipSuccess)
-        return fail_hip(guard.status, "selecting the plan's device");
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    const bool bf16 = plan->g_dtype == LAMB_GRAD_BF16;
-    record(plan, 0, s);
-    hipError_t err = launch_lars_moments(plan->tensors, plan->chunks, plan->partials,
-                                         plan->n_chunks, bf16, a, s);
-    if (err != hipSuccess)
-        return fail_hip(err, "launching the LARS momentum kernel");
-    record(plan, 1, s);
-    err = launch_finalize(plan->tensors, plan->n_tensors, plan->partials, f, plan->scale,
-                          ratio_out, norms_out, s);
-    if (err != hipSuccess)
-        return fail_hip(err, "launching the finalize kernel");
-    record(plan, 2, s);
-    err = launch_lars_apply(plan->tensors, plan->chunks, plan->scale, plan->n_chunks, s);
-    if (err != hipSuccess)
-        return fail_hip(err, "launching the LARS apply kernel");
-    record(plan, 3, s);
-    if (plan->timing_used < plan->timing_capacity)
-        ++plan->timing_used;
-    return LAMB_OK;
+    lamb_hparams hp;
+    lamb_hparams_init(&hp, LAMB_VARIANT_LARS);
+    hp.lr = lr;
+    hp.beta1 = momentum;
+    hp.weight_decay = weight_decay;
+    hp.gamma_l = gamma_l;
+    hp.gamma_u = gamma_u;
+    hp.trust_coef = trust_coef;
+    return lamb_step_ex(plan, &hp, stream, ratio_out, norms_out, nullptr);
 }
 
 lamb_status lamb_plan_set_timing(lamb_plan *plan, int32_t max_steps) {

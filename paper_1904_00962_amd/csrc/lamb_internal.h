@@ -9,7 +9,7 @@
 namespace lamb_mi355x {
 
 // Work is cut into chunks of at most `chunk_elems` elements of one tensor;
-// one workgroup of kBlock threads handles one chunk. kBlock = 4 wave64s.
+// one workgroup of kBlock threads handles one chunk.
 #ifndef LAMB_BLOCK
 #define LAMB_BLOCK 256
 #endif
@@ -20,18 +20,25 @@ constexpr int kBlock = LAMB_BLOCK;
 constexpr int kWaves = kBlock / 64;
 constexpr int32_t kDefaultChunkElems = LAMB_DEFAULT_CHUNK;
 
+// A plan cuts every tensor twice: into fine chunks of chunk_elems elements
+// (direct-mode moment passes and every apply pass) and into coarse chunks of
+// kCoarseFactor times as many (deferred-mode moment passes, which only read
+// and run faster with more work per workgroup).
+constexpr int32_t kCoarseFactor = 4;
+
 // One layer block x^(i) (Section 2) as the kernels see it. 64 bytes.
 struct TensorDesc {
     float *x;
     const void *g;
     float *m;
-    float *v;
+    float *v;              // null for LARS plans
     int64_t numel;
-    int32_t wd;           // 1: lambda applies, 0: lambda = 0
-    int32_t first_chunk;  // this tensor's chunks are [first_chunk, first_chunk + n_chunks)
+    int32_t wd;            // 1: lambda applies, 0: lambda = 0
+    int32_t first_chunk;   // fine chunks [first_chunk, first_chunk + n_chunks)
     int32_t n_chunks;
-    int32_t pad0;
-    int64_t pad1;
+    int32_t first_coarse;  // coarse chunks [first_coarse, first_coarse + n_coarse)
+    int32_t n_coarse;
+    int32_t pad;
 };
 static_assert(sizeof(TensorDesc) == 64, "TensorDesc layout");
 
@@ -43,58 +50,70 @@ struct ChunkDesc {
 };
 static_assert(sizeof(ChunkDesc) == 16, "ChunkDesc layout");
 
-// Per-chunk partial sums of squares, written once per step at a fixed slot.
+// Per-chunk partial norms of x and of the update direction u (LAMB family)
+// or m_t (LARS), written once per step at a fixed slot: sums of squares (L2),
+// sums of magnitudes (L1) or maxima of magnitudes (L-infinity).
 struct Partial {
-    double sum_xx;  // sum of x^2 over the chunk
-    double sum_uu;  // sum of u^2 (LAMB) or m_t^2 (LARS) over the chunk
+    double sum_xx;
+    double sum_uu;
 };
 
-// Which corrected moments the update uses.
-enum LambVariant : int {
+// Algorithms (the kernels' template argument).
+enum Algo : int {
     kLamb = 0,    // Algorithm 2: m_hat = m_t / c1, v_hat = v_t / c2
     kNLamb = 1,   // Algorithm 3: Nesterov m_hat, v_hat = beta2 v_t / c2
     kNNLamb = 2,  // Algorithm 4: Nesterov m_hat and v_hat
+    kLars = 3,    // Algorithm 1: momentum with weight decay
 };
 
-// fp32 scalars of the elementwise LAMB-family passes. The corrected moments
-// are m_hat = m_scale * m_t + m_grad * g_t and v_hat = v_scale * v_t +
-// v_grad * g_t^2; Algorithm 2 has m_grad = v_grad = 0.
-struct LambArgs {
+// Layer norms (Appendix F).
+enum NormKind : int { kL2 = 0, kL1 = 1, kLinf = 2 };
+
+// fp32 scalars of the elementwise passes. For the LAMB family the corrected
+// moments are m_hat = m_scale * m_t + m_grad * g_t and v_hat = v_scale * v_t +
+// v_grad * g_t^2 (Algorithm 2 has m_grad = v_grad = 0). LARS uses beta1 as its
+// momentum. Every gradient element is multiplied by grad_scale first.
+struct StepArgs {
     float beta1, one_minus_beta1;
     float beta2, one_minus_beta2;
     float m_scale, m_grad;
     float v_scale, v_grad;
     float eps;
     float weight_decay;
-};
-
-// fp32 scalars of the elementwise LARS passes (Algorithm 1).
-struct LarsArgs {
-    float beta1, one_minus_beta1;
-    float weight_decay;
+    float grad_scale;
+    uint32_t flag_slot;  // deferred mode: which of the plan's two flags this step uses
 };
 
 // Scalars of the per-tensor finalize (trust ratio and step scale).
 struct FinalizeArgs {
     double lr;
     double gamma_l, gamma_u;
-    double trust_coef;  // 1 for LAMB
+    double trust_coef;  // 1 for the LAMB family
+};
+
+// What one step launches.
+struct StepKind {
+    Algo algo;
+    NormKind norm;
+    bool bf16_grad;
+    bool deferred;  // moment pass writes nothing; apply pass recomputes and
+                    // writes x, m, v unless a scaled gradient was non-finite
 };
 
 // Kernel launchers (lamb_kernels.hip). Each returns the launch status.
-hipError_t launch_lamb_moments(const TensorDesc *tensors, const ChunkDesc *chunks,
-                               Partial *partials, int32_t n_chunks, bool bf16_grad,
-                               LambVariant variant, const LambArgs &args, hipStream_t stream);
-hipError_t launch_lamb_apply(const TensorDesc *tensors, const ChunkDesc *chunks,
-                             const float *scale, int32_t n_chunks, bool bf16_grad,
-                             LambVariant variant, const LambArgs &args, hipStream_t stream);
-hipError_t launch_lars_moments(const TensorDesc *tensors, const ChunkDesc *chunks,
-                               Partial *partials, int32_t n_chunks, bool bf16_grad,
-                               const LarsArgs &args, hipStream_t stream);
-hipError_t launch_lars_apply(const TensorDesc *tensors, const ChunkDesc *chunks,
-                             const float *scale, int32_t n_chunks, hipStream_t stream);
-hipError_t launch_finalize(const TensorDesc *tensors, int32_t n_tensors,
-                           const Partial *partials, const FinalizeArgs &args, float *scale,
-                           double *ratio_out, double *norms_out, hipStream_t stream);
+// `flags` points at the plan's two non-finite flags (deferred mode only);
+// `nonfinite_out` may be null.
+hipError_t launch_moments(const StepKind &kind, const TensorDesc *tensors,
+                          const ChunkDesc *chunks, Partial *partials, int32_t n_chunks,
+                          uint32_t *flags, const StepArgs &args, hipStream_t stream);
+// `coarse`: the partials were written per coarse chunk (deferred mode).
+hipError_t launch_finalize(NormKind norm, bool coarse, const TensorDesc *tensors,
+                           int32_t n_tensors, const Partial *partials, const FinalizeArgs &args,
+                           float *scale, double *ratio_out, double *norms_out,
+                           hipStream_t stream);
+hipError_t launch_apply(const StepKind &kind, const TensorDesc *tensors,
+                        const ChunkDesc *chunks, const float *scale, int32_t n_chunks,
+                        uint32_t *flags, int32_t *nonfinite_out, const StepArgs &args,
+                        hipStream_t stream);
 
 }  // namespace lamb_mi355x

@@ -1,27 +1,34 @@
-// HIP kernels of the multi-tensor LAMB / LARS step for gfx950 (MI355X).
+// HIP kernels of the multi-tensor LAMB-family and LARS step for gfx950
+// (MI355X).
 //
 // You et al., "Large Batch Optimization for Deep Learning" (arXiv:1904.00962):
-// LAMB is Algorithm 2, LARS is Algorithm 1, phi is defined in Section 3.
+// LARS is Algorithm 1, LAMB Algorithm 2, N-LAMB and NN-LAMB Algorithms 3 and 4
+// (Appendix D); phi is defined in Section 3, the other layer norms in
+// Appendix F.
 //
 // The step needs every per-layer norm ||u_i|| before any x_i may move, so it
 // is two streaming passes over HBM with a tiny reduction between them:
 //
-//   moments  (one workgroup per chunk): read x, g, m, v; write the new m, v;
-//            write the chunk's sums of x^2 and u^2 to a fixed slot.
-//   finalize (one wave64 per tensor):  sum the tensor's chunk slots in a
-//            fixed order, form ||x_i||, ||u_i||, phi, the trust ratio and the
+//   moments  (one workgroup per chunk): read x, g, m (and v); form the new
+//            moments and the update direction u (m_t for LARS); write the
+//            chunk's partial norms of x and u to a fixed slot; store the new
+//            moments (direct mode) or nothing (deferred mode).
+//   finalize (one workgroup per tensor): combine the tensor's chunk slots in
+//            a fixed order into ||x_i||, ||u_i||, phi, the trust ratio and the
 //            step scale lr * ratio.
-//   apply    (one workgroup per chunk): read x and the new m, v; recompute u
-//            with the same inline function the moment pass used (so it is
-//            bit-identical) and write x - scale_i * u.
+//   apply    (one workgroup per chunk): read x and the moments; recompute u
+//            with the same inline functions the moment pass used (so it is
+//            bit-identical) and write x - scale_i * u. In deferred mode it
+//            recomputes the new moments from the old ones and writes them
+//            too, unless the moment pass found a non-finite scaled gradient,
+//            in which case nothing changes.
 //
 // Recomputing u instead of storing it saves 4 bytes per parameter of HBM
-// traffic. There are no float atomics: every sum has a fixed order, so a step
-// is bitwise reproducible for a given chunk size. Every global access of the
-// vector loops is a 16-byte (fp32) or 8-byte (bf16) load or store, and the
-// lanes of a wave touch consecutive addresses, so one instruction moves 1 KiB
-// (fp32) or 512 B (bf16) of contiguous memory. This path has no dense
-// contraction, so it uses no MFMA; it is bound by HBM bandwidth.
+// traffic. There are no float atomics: every reduction has a fixed order, so
+// a step is bitwise reproducible for a given chunk size. The vector loops
+// move 16 bytes per lane (8 for bf16 gradients) with nontemporal loads and
+// stores, and the lanes of a wave touch consecutive addresses. This path has
+// no dense contraction, so it uses no MFMA; it is bound by HBM bandwidth.
 
 #include <hip/hip_runtime.h>
 
@@ -49,7 +56,9 @@ __device__ __forceinline__ gcfloat *global_view(const float *p) { return (gcfloa
 // LAMB_NONTEMPORAL: stream x, g, m, v with nontemporal loads and stores; the
 //   data is touched once per pass, so it should not displace cache lines.
 // LAMB_APPLY_REVERSE: the apply pass walks chunks last-to-first, so its first
-//   reads are the lines the moment pass touched last (still in the caches).
+//   reads are the lines the moment pass touched last.
+// LAMB_XCD_CONTIGUOUS: each of the 8 XCDs takes one contiguous eighth of the
+//   chunk list instead of every eighth chunk.
 #ifndef LAMB_UNROLL
 #define LAMB_UNROLL 2
 #endif
@@ -91,102 +100,148 @@ __device__ __forceinline__ void store4(gfloat *p, f32x4 v) {
 }
 
 // The gradient of one chunk: fp32, or bf16 bit patterns that widen exactly
-// (a bf16 is the top half of an fp32).
+// (a bf16 is the top half of an fp32), multiplied by the step's grad_scale.
 template <bool kBf16>
 struct GradView {
     const void *base;
-    __device__ __forceinline__ GradView(const void *g, int64_t start)
+    float scale;
+    __device__ __forceinline__ GradView(const void *g, int64_t start, float s)
         : base(kBf16 ? static_cast<const void *>(static_cast<const uint16_t *>(g) + start)
-                     : static_cast<const void *>(static_cast<const float *>(g) + start)) {}
+                     : static_cast<const void *>(static_cast<const float *>(g) + start)),
+          scale(s) {}
 
     __device__ __forceinline__ float at(int i) const {
+        float r;
         if constexpr (kBf16)
-            return __uint_as_float(uint32_t(((gcbf16 *)base)[i]) << 16);
+            r = __uint_as_float(uint32_t(((gcbf16 *)base)[i]) << 16);
         else
-            return ((gcfloat *)base)[i];
+            r = ((gcfloat *)base)[i];
+        return r * scale;
     }
 
     // elements i..i+3, i a multiple of 4
     __device__ __forceinline__ f32x4 at4(int i) const {
+        f32x4 r;
         if constexpr (kBf16) {
             const u32x2 w = stream_load((LAMB_GLOBAL const u32x2 *)((gcbf16 *)base + i));
-            f32x4 r;
             r.x = __uint_as_float(w.x << 16);
             r.y = __uint_as_float(w.x & 0xffff0000u);
             r.z = __uint_as_float(w.y << 16);
             r.w = __uint_as_float(w.y & 0xffff0000u);
-            return r;
         } else {
-            return load4((gcfloat *)base + i);
+            r = load4((gcfloat *)base + i);
         }
+        return r * scale;
     }
 };
 
 // ---------------------------------------------------------------------------
-// Elementwise arithmetic of Algorithm 2 (LAMB) and Algorithm 1 (LARS).
+// Elementwise arithmetic of Algorithms 1-4.
 // ---------------------------------------------------------------------------
 
-// m_t = beta1 m_{t-1} + (1 - beta1) g_t
-__device__ __forceinline__ float lamb_first_moment(float m, float g, const LambArgs &a) {
-    return fmaf(a.beta1, m, a.one_minus_beta1 * g);
-}
+template <int kAlgo>
+constexpr bool kHasSecondMoment = kAlgo != kLars;
 
-// v_t = beta2 v_{t-1} + (1 - beta2) g_t^2
-__device__ __forceinline__ float lamb_second_moment(float v, float g, const LambArgs &a) {
-    return fmaf(a.beta2, v, a.one_minus_beta2 * (g * g));
-}
+// Nesterov variants need g_t to form the corrected moments, so their apply
+// pass reads the gradient again.
+template <int kAlgo>
+constexpr bool kDirectionNeedsGrad = kAlgo == kNLamb || kAlgo == kNNLamb;
 
-// u = r + lambda x with r = m_hat / (sqrt(v_hat) + eps), from the NEW moments
-// m = m_t, v = v_t. Algorithm 2 corrects by 1 / (1 - beta^t); Algorithms 3
-// and 4 add the Nesterov gradient terms, which is why their apply pass also
-// reads g. The moment and apply passes both call this, so their u agree bit
-// for bit; division and square root are the correctly rounded IEEE
-// operations.
-template <int kVariant>
-__device__ __forceinline__ float lamb_update(float x, float g, float m, float v, float lam,
-                                             const LambArgs &a) {
-    float m_hat, v_hat;
-    if constexpr (kVariant == kLamb) {
-        m_hat = m * a.m_scale;
-        v_hat = v * a.v_scale;
+// New moments from the old ones, in place:
+//   LAMB family: m_t = beta1 m + (1 - beta1) g,  v_t = beta2 v + (1 - beta2) g^2
+//   LARS:        m_t = beta1 m + (1 - beta1) (g + lambda x)
+template <int kAlgo>
+__device__ __forceinline__ void new_moments(float x, float g, float lam, float &m, float &v,
+                                            const StepArgs &a) {
+    if constexpr (kAlgo == kLars) {
+        m = fmaf(a.beta1, m, a.one_minus_beta1 * fmaf(lam, x, g));
     } else {
-        m_hat = fmaf(a.m_scale, m, a.m_grad * g);
-        if constexpr (kVariant == kNNLamb)
-            v_hat = fmaf(a.v_scale, v, a.v_grad * (g * g));
-        else
-            v_hat = v * a.v_scale;
+        m = fmaf(a.beta1, m, a.one_minus_beta1 * g);
+        v = fmaf(a.beta2, v, a.one_minus_beta2 * (g * g));
     }
-    const float r = __fdiv_rn(m_hat, __fadd_rn(__fsqrt_rn(v_hat), a.eps));
-    return fmaf(lam, x, r);
 }
 
-// m_t = beta1 m_{t-1} + (1 - beta1) (g_t + lambda x_t)
-__device__ __forceinline__ float lars_momentum(float m, float g, float x, float lam,
-                                               const LarsArgs &a) {
-    return fmaf(a.beta1, m, a.one_minus_beta1 * fmaf(lam, x, g));
+// The update direction from the NEW moments m = m_t, v = v_t: for the LAMB
+// family u = r + lambda x with r = m_hat / (sqrt(v_hat) + eps); for LARS it is
+// m_t itself. The moment and apply passes both call this, so their u agree
+// bit for bit; division and square root are the correctly rounded IEEE
+// operations.
+template <int kAlgo>
+__device__ __forceinline__ float direction(float x, float g, float m, float v, float lam,
+                                           const StepArgs &a) {
+    if constexpr (kAlgo == kLars) {
+        return m;
+    } else {
+        float m_hat, v_hat;
+        if constexpr (kAlgo == kLamb) {
+            m_hat = m * a.m_scale;
+            v_hat = v * a.v_scale;
+        } else {
+            m_hat = fmaf(a.m_scale, m, a.m_grad * g);
+            if constexpr (kAlgo == kNNLamb)
+                v_hat = fmaf(a.v_scale, v, a.v_grad * (g * g));
+            else
+                v_hat = v * a.v_scale;
+        }
+        const float r = __fdiv_rn(m_hat, __fadd_rn(__fsqrt_rn(v_hat), a.eps));
+        return fmaf(lam, x, r);
+    }
 }
 
 // ---------------------------------------------------------------------------
-// Deterministic reductions.
+// Layer norms (Appendix F) and their deterministic reductions, in fp64.
 // ---------------------------------------------------------------------------
 
-__device__ __forceinline__ double wave_sum(double v) {
+// Maximum that keeps NaN: once a NaN is seen the result is NaN.
+__device__ __forceinline__ double max_keep_nan(double a, double b) {
+    return (isnan(a) || a > b) ? a : b;
+}
+
+template <int kNorm>
+__device__ __forceinline__ double norm_add(double acc, float value) {
+    const double d = value;
+    if constexpr (kNorm == kL1)
+        return acc + fabs(d);
+    else if constexpr (kNorm == kLinf)
+        return max_keep_nan(fabs(d), acc);
+    else
+        return fma(d, d, acc);
+}
+
+template <int kNorm>
+__device__ __forceinline__ double norm_combine(double a, double b) {
+    if constexpr (kNorm == kLinf)
+        return max_keep_nan(a, b);
+    else
+        return a + b;
+}
+
+template <int kNorm>
+__device__ __forceinline__ double norm_finish(double acc) {
+    if constexpr (kNorm == kL2)
+        return sqrt(acc);
+    else
+        return acc;
+}
+
+template <int kNorm>
+__device__ __forceinline__ double wave_combine(double v) {
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1)
-        v += __shfl_xor(v, off, 64);
+        v = norm_combine<kNorm>(v, __shfl_xor(v, off, 64));
     return v;
 }
 
-// Sum (a, b) over a workgroup of kNumWaves wave64s in a fixed tree and store
-// it at `out` (thread 0 writes).
-template <int kNumWaves>
-__device__ __forceinline__ void block_sums(double a, double b, Partial *out) {
+// Combine (a, b) over a workgroup of kNumWaves wave64s in a fixed tree and
+// store it at `out` (thread 0 writes).
+template <int kNorm, int kNumWaves>
+__device__ __forceinline__ void block_combine(double a, double b, Partial *out) {
     __shared__ double red_a[kNumWaves];
     __shared__ double red_b[kNumWaves];
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
-    a = wave_sum(a);
-    b = wave_sum(b);
+    a = wave_combine<kNorm>(a);
+    b = wave_combine<kNorm>(b);
     if (lane == 0) {
         red_a[wave] = a;
         red_b[wave] = b;
@@ -196,17 +251,15 @@ __device__ __forceinline__ void block_sums(double a, double b, Partial *out) {
         double sa = red_a[0], sb = red_b[0];
 #pragma unroll
         for (int w = 1; w < kNumWaves; ++w) {
-            sa += red_a[w];
-            sb += red_b[w];
+            sa = norm_combine<kNorm>(sa, red_a[w]);
+            sb = norm_combine<kNorm>(sb, red_b[w]);
         }
         out->sum_xx = sa;
         out->sum_uu = sb;
     }
 }
 
-// Workgroups are dispatched round-robin over the 8 XCDs. With
-// LAMB_XCD_CONTIGUOUS each XCD takes one contiguous eighth of the chunk list
-// instead of every eighth chunk.
+// Workgroups are dispatched round-robin over the 8 XCDs.
 __device__ __forceinline__ uint32_t dispatch_rank() {
 #if LAMB_XCD_CONTIGUOUS
     const uint32_t n = gridDim.x, b = blockIdx.x;
@@ -232,22 +285,24 @@ __device__ __forceinline__ uint32_t apply_chunk_index() {
 }
 
 // ---------------------------------------------------------------------------
-// LAMB passes.
+// Moment pass.
 // ---------------------------------------------------------------------------
 
-template <bool kBf16, int kVariant>
-__global__ __launch_bounds__(kBlock) void lamb_moments_kernel(
+template <int kAlgo, bool kBf16, int kNorm, bool kDeferred>
+__global__ __launch_bounds__(kBlock) void moments_kernel(
     const TensorDesc *__restrict__ tensors, const ChunkDesc *__restrict__ chunks,
-    Partial *__restrict__ partials, LambArgs a) {
+    Partial *__restrict__ partials, uint32_t *__restrict__ flags, StepArgs a) {
+    constexpr bool kV = kHasSecondMoment<kAlgo>;
     const ChunkDesc c = chunks[chunk_index()];
     const TensorDesc &t = tensors[c.tensor];
-    gcfloat *x = global_view(t.x + c.start);
+    gcfloat *x = global_view(static_cast<const float *>(t.x) + c.start);
     gfloat *m = global_view(t.m + c.start);
-    gfloat *v = global_view(t.v + c.start);
-    const GradView<kBf16> g(t.g, c.start);
+    gfloat *v = kV ? global_view(t.v + c.start) : nullptr;
+    const GradView<kBf16> g(t.g, c.start, a.grad_scale);
     const float lam = t.wd ? a.weight_decay : 0.0f;
 
     double sum_xx = 0.0, sum_uu = 0.0;
+    bool nonfinite = false;
     const int n4 = c.len >> 2;
     for (int base = threadIdx.x; base < n4; base += kBlock * kUnroll) {
         f32x4 xr[kUnroll], gr[kUnroll], mr[kUnroll], vr[kUnroll];
@@ -258,25 +313,33 @@ __global__ __launch_bounds__(kBlock) void lamb_moments_kernel(
                 xr[k] = load4(x + 4 * q);
                 gr[k] = g.at4(4 * q);
                 mr[k] = load4(m + 4 * q);
-                vr[k] = load4(v + 4 * q);
+                if constexpr (kV)
+                    vr[k] = load4(v + 4 * q);
+                else
+                    vr[k] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
             }
         }
 #pragma unroll
         for (int k = 0; k < kUnroll; ++k) {
             const int q = base + k * kBlock;
             if (q < n4) {
-                f32x4 mn, vn;
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    mn[e] = lamb_first_moment(mr[k][e], gr[k][e], a);
-                    vn[e] = lamb_second_moment(vr[k][e], gr[k][e], a);
-                    const float u = lamb_update<kVariant>(xr[k][e], gr[k][e], mn[e], vn[e], lam, a);
-                    const double xd = xr[k][e], ud = u;
-                    sum_xx = fma(xd, xd, sum_xx);
-                    sum_uu = fma(ud, ud, sum_uu);
+                    float me = mr[k][e], ve = vr[k][e];
+                    new_moments<kAlgo>(xr[k][e], gr[k][e], lam, me, ve, a);
+                    const float u = direction<kAlgo>(xr[k][e], gr[k][e], me, ve, lam, a);
+                    sum_xx = norm_add<kNorm>(sum_xx, xr[k][e]);
+                    sum_uu = norm_add<kNorm>(sum_uu, u);
+                    mr[k][e] = me;
+                    vr[k][e] = ve;
+                    if constexpr (kDeferred)
+                        nonfinite |= !isfinite(gr[k][e]);
                 }
-                store4(m + 4 * q, mn);
-                store4(v + 4 * q, vn);
+                if constexpr (!kDeferred) {
+                    store4(m + 4 * q, mr[k]);
+                    if constexpr (kV)
+                        store4(v + 4 * q, vr[k]);
+                }
             }
         }
     }
@@ -284,30 +347,57 @@ __global__ __launch_bounds__(kBlock) void lamb_moments_kernel(
     if (tail < c.len) {
         const float xj = x[tail];
         const float gj = g.at(tail);
-        const float mj = lamb_first_moment(m[tail], gj, a);
-        const float vj = lamb_second_moment(v[tail], gj, a);
-        const float u = lamb_update<kVariant>(xj, gj, mj, vj, lam, a);
-        m[tail] = mj;
-        v[tail] = vj;
-        const double xd = xj, ud = u;
-        sum_xx = fma(xd, xd, sum_xx);
-        sum_uu = fma(ud, ud, sum_uu);
+        float mj = m[tail];
+        float vj = kV ? v[tail] : 0.0f;
+        new_moments<kAlgo>(xj, gj, lam, mj, vj, a);
+        const float u = direction<kAlgo>(xj, gj, mj, vj, lam, a);
+        sum_xx = norm_add<kNorm>(sum_xx, xj);
+        sum_uu = norm_add<kNorm>(sum_uu, u);
+        if constexpr (kDeferred) {
+            nonfinite |= !isfinite(gj);
+        } else {
+            m[tail] = mj;
+            if constexpr (kV)
+                v[tail] = vj;
+        }
     }
-    block_sums<kWaves>(sum_xx, sum_uu, partials + chunk_index());
+    if constexpr (kDeferred) {
+        // Rare event: one integer atomic per chunk that saw a bad gradient.
+        if (__syncthreads_or(nonfinite) && threadIdx.x == 0)
+            atomicOr(flags + a.flag_slot, 1u);
+    }
+    block_combine<kNorm, kWaves>(sum_xx, sum_uu, partials + chunk_index());
 }
 
-// kVariant = kLamb never reads g (the template flag kBf16 is then unused).
-template <bool kBf16, int kVariant>
-__global__ __launch_bounds__(kBlock) void lamb_apply_kernel(
+// ---------------------------------------------------------------------------
+// Apply pass.
+// ---------------------------------------------------------------------------
+
+template <int kAlgo, bool kBf16, bool kDeferred>
+__global__ __launch_bounds__(kBlock) void apply_kernel(
     const TensorDesc *__restrict__ tensors, const ChunkDesc *__restrict__ chunks,
-    const float *__restrict__ scale, LambArgs a) {
-    constexpr bool kReadsGrad = kVariant != kLamb;
+    const float *__restrict__ scale, uint32_t *__restrict__ flags,
+    int32_t *__restrict__ nonfinite_out, StepArgs a) {
+    constexpr bool kV = kHasSecondMoment<kAlgo>;
+    constexpr bool kReadsGrad = kDeferred || kDirectionNeedsGrad<kAlgo>;
+    if constexpr (kDeferred) {
+        // The moment pass raised this step's flag if any scaled gradient was
+        // NaN or infinite; clear the other flag for the next deferred step.
+        const uint32_t bad = flags[a.flag_slot];
+        if (blockIdx.x == 0 && threadIdx.x == 0) {
+            flags[a.flag_slot ^ 1u] = 0u;
+            if (nonfinite_out)
+                *nonfinite_out = bad ? 1 : 0;
+        }
+        if (bad)
+            return;
+    }
     const ChunkDesc c = chunks[apply_chunk_index()];
     const TensorDesc &t = tensors[c.tensor];
     gfloat *x = global_view(t.x + c.start);
-    gcfloat *m = global_view(static_cast<const float *>(t.m) + c.start);
-    gcfloat *v = global_view(static_cast<const float *>(t.v) + c.start);
-    const GradView<kBf16> g(t.g, c.start);
+    gfloat *m = global_view(t.m + c.start);
+    gfloat *v = kV ? global_view(t.v + c.start) : nullptr;
+    const GradView<kBf16> g(t.g, c.start, a.grad_scale);
     const float lam = t.wd ? a.weight_decay : 0.0f;
     const float s = scale[c.tensor];
 
@@ -324,7 +414,10 @@ __global__ __launch_bounds__(kBlock) void lamb_apply_kernel(
                 else
                     gr[k] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
                 mr[k] = load4(m + 4 * q);
-                vr[k] = load4(v + 4 * q);
+                if constexpr (kV)
+                    vr[k] = load4(v + 4 * q);
+                else
+                    vr[k] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
             }
         }
 #pragma unroll
@@ -333,162 +426,90 @@ __global__ __launch_bounds__(kBlock) void lamb_apply_kernel(
             if (q < n4) {
                 f32x4 xn;
 #pragma unroll
-                for (int e = 0; e < 4; ++e)
-                    xn[e] = fmaf(-s, lamb_update<kVariant>(xr[k][e], gr[k][e], mr[k][e],
-                                                           vr[k][e], lam, a),
-                                 xr[k][e]);
-                store4(x + 4 * q, xn);
-            }
-        }
-    }
-    const int tail = 4 * n4 + threadIdx.x;
-    if (tail < c.len) {
-        const float gj = kReadsGrad ? g.at(tail) : 0.0f;
-        x[tail] = fmaf(-s, lamb_update<kVariant>(x[tail], gj, m[tail], v[tail], lam, a), x[tail]);
-    }
-}
-
-// ---------------------------------------------------------------------------
-// LARS passes.
-// ---------------------------------------------------------------------------
-
-template <bool kBf16>
-__global__ __launch_bounds__(kBlock) void lars_moments_kernel(
-    const TensorDesc *__restrict__ tensors, const ChunkDesc *__restrict__ chunks,
-    Partial *__restrict__ partials, LarsArgs a) {
-    const ChunkDesc c = chunks[chunk_index()];
-    const TensorDesc &t = tensors[c.tensor];
-    gcfloat *x = global_view(static_cast<const float *>(t.x) + c.start);
-    gfloat *m = global_view(t.m + c.start);
-    const GradView<kBf16> g(t.g, c.start);
-    const float lam = t.wd ? a.weight_decay : 0.0f;
-
-    double sum_xx = 0.0, sum_mm = 0.0;
-    const int n4 = c.len >> 2;
-    for (int base = threadIdx.x; base < n4; base += kBlock * kUnroll) {
-        f32x4 xr[kUnroll], gr[kUnroll], mr[kUnroll];
-#pragma unroll
-        for (int k = 0; k < kUnroll; ++k) {
-            const int q = base + k * kBlock;
-            if (q < n4) {
-                xr[k] = load4(x + 4 * q);
-                gr[k] = g.at4(4 * q);
-                mr[k] = load4(m + 4 * q);
-            }
-        }
-#pragma unroll
-        for (int k = 0; k < kUnroll; ++k) {
-            const int q = base + k * kBlock;
-            if (q < n4) {
-                f32x4 mn;
-#pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    mn[e] = lars_momentum(mr[k][e], gr[k][e], xr[k][e], lam, a);
-                    const double xd = xr[k][e], md = mn[e];
-                    sum_xx = fma(xd, xd, sum_xx);
-                    sum_mm = fma(md, md, sum_mm);
+                    float me = mr[k][e], ve = vr[k][e];
+                    if constexpr (kDeferred)
+                        new_moments<kAlgo>(xr[k][e], gr[k][e], lam, me, ve, a);
+                    const float u = direction<kAlgo>(xr[k][e], gr[k][e], me, ve, lam, a);
+                    xn[e] = fmaf(-s, u, xr[k][e]);
+                    mr[k][e] = me;
+                    vr[k][e] = ve;
                 }
-                store4(m + 4 * q, mn);
+                store4(x + 4 * q, xn);
+                if constexpr (kDeferred) {
+                    store4(m + 4 * q, mr[k]);
+                    if constexpr (kV)
+                        store4(v + 4 * q, vr[k]);
+                }
             }
         }
     }
     const int tail = 4 * n4 + threadIdx.x;
     if (tail < c.len) {
         const float xj = x[tail];
-        const float mj = lars_momentum(m[tail], g.at(tail), xj, lam, a);
-        m[tail] = mj;
-        const double xd = xj, md = mj;
-        sum_xx = fma(xd, xd, sum_xx);
-        sum_mm = fma(md, md, sum_mm);
-    }
-    block_sums<kWaves>(sum_xx, sum_mm, partials + chunk_index());
-}
-
-__global__ __launch_bounds__(kBlock) void lars_apply_kernel(
-    const TensorDesc *__restrict__ tensors, const ChunkDesc *__restrict__ chunks,
-    const float *__restrict__ scale) {
-    const ChunkDesc c = chunks[apply_chunk_index()];
-    const TensorDesc &t = tensors[c.tensor];
-    gfloat *x = global_view(t.x + c.start);
-    gcfloat *m = global_view(static_cast<const float *>(t.m) + c.start);
-    const float s = scale[c.tensor];
-
-    const int n4 = c.len >> 2;
-    for (int base = threadIdx.x; base < n4; base += kBlock * kUnroll) {
-        f32x4 xr[kUnroll], mr[kUnroll];
-#pragma unroll
-        for (int k = 0; k < kUnroll; ++k) {
-            const int q = base + k * kBlock;
-            if (q < n4) {
-                xr[k] = load4(x + 4 * q);
-                mr[k] = load4(m + 4 * q);
-            }
-        }
-#pragma unroll
-        for (int k = 0; k < kUnroll; ++k) {
-            const int q = base + k * kBlock;
-            if (q < n4) {
-                f32x4 xn;
-#pragma unroll
-                for (int e = 0; e < 4; ++e)
-                    xn[e] = fmaf(-s, mr[k][e], xr[k][e]);
-                store4(x + 4 * q, xn);
-            }
+        const float gj = kReadsGrad ? g.at(tail) : 0.0f;
+        float mj = m[tail];
+        float vj = kV ? v[tail] : 0.0f;
+        if constexpr (kDeferred)
+            new_moments<kAlgo>(xj, gj, lam, mj, vj, a);
+        x[tail] = fmaf(-s, direction<kAlgo>(xj, gj, mj, vj, lam, a), xj);
+        if constexpr (kDeferred) {
+            m[tail] = mj;
+            if constexpr (kV)
+                v[tail] = vj;
         }
     }
-    const int tail = 4 * n4 + threadIdx.x;
-    if (tail < c.len)
-        x[tail] = fmaf(-s, m[tail], x[tail]);
 }
 
 // ---------------------------------------------------------------------------
 // Per-tensor finalize: norms, phi, trust ratio, step scale. One workgroup of
 // kFinalizeBlock threads per tensor. Thread k owns slots k + j*kFinalizeBlock
-// and sums them into kFinalizeLanes independent accumulators (so several
-// loads are in flight), which it then adds in a fixed order; the fixed
+// and combines them into kFinalizeLanes independent accumulators (so several
+// loads are in flight), which it then combines in a fixed order; the fixed
 // wave/LDS tree combines the threads. The order never depends on timing.
 // ---------------------------------------------------------------------------
 
 constexpr int kFinalizeBlock = 1024;
 constexpr int kFinalizeLanes = 16;
 
+template <int kNorm>
 __global__ __launch_bounds__(kFinalizeBlock) void finalize_kernel(
-    const TensorDesc *__restrict__ tensors, const Partial *__restrict__ partials,
+    const TensorDesc *__restrict__ tensors, const Partial *__restrict__ partials, int coarse,
     FinalizeArgs a, float *__restrict__ scale, double *__restrict__ ratio_out,
     double *__restrict__ norms_out) {
     const int i = blockIdx.x;
     const TensorDesc &t = tensors[i];
-    const Partial *p = partials + t.first_chunk;
-    const int n = t.n_chunks;
+    const Partial *p = partials + (coarse ? t.first_coarse : t.first_chunk);
+    const int n = coarse ? t.n_coarse : t.n_chunks;
     double sx[kFinalizeLanes] = {}, su[kFinalizeLanes] = {};
     int k = threadIdx.x;
     for (; k + (kFinalizeLanes - 1) * kFinalizeBlock < n; k += kFinalizeLanes * kFinalizeBlock) {
 #pragma unroll
         for (int j = 0; j < kFinalizeLanes; ++j) {
             const Partial q = p[k + j * kFinalizeBlock];
-            sx[j] += q.sum_xx;
-            su[j] += q.sum_uu;
+            sx[j] = norm_combine<kNorm>(sx[j], q.sum_xx);
+            su[j] = norm_combine<kNorm>(su[j], q.sum_uu);
         }
     }
 #pragma unroll
     for (int j = 0; j < kFinalizeLanes - 1; ++j) {
         if (k + j * kFinalizeBlock < n) {
             const Partial q = p[k + j * kFinalizeBlock];
-            sx[j] += q.sum_xx;
-            su[j] += q.sum_uu;
+            sx[j] = norm_combine<kNorm>(sx[j], q.sum_xx);
+            su[j] = norm_combine<kNorm>(su[j], q.sum_uu);
         }
     }
 #pragma unroll
     for (int j = 1; j < kFinalizeLanes; ++j) {
-        sx[0] += sx[j];
-        su[0] += su[j];
+        sx[0] = norm_combine<kNorm>(sx[0], sx[j]);
+        su[0] = norm_combine<kNorm>(su[0], su[j]);
     }
     __shared__ Partial total;
-    block_sums<kFinalizeBlock / 64>(sx[0], su[0], &total);
+    block_combine<kNorm, kFinalizeBlock / 64>(sx[0], su[0], &total);
     __syncthreads();
     if (threadIdx.x == 0) {
-        const double norm_x = sqrt(total.sum_xx);
-        const double norm_u = sqrt(total.sum_uu);
+        const double norm_x = norm_finish<kNorm>(total.sum_xx);
+        const double norm_u = norm_finish<kNorm>(total.sum_uu);
         // phi(z) = min(max(z, gamma_l), gamma_u), Section 3; comparisons keep NaN.
         double phi = norm_x;
         if (phi < a.gamma_l)
@@ -507,70 +528,89 @@ __global__ __launch_bounds__(kFinalizeBlock) void finalize_kernel(
     }
 }
 
+// ---------------------------------------------------------------------------
+// Kernel selection: the template arguments are spelled out so every
+// combination the launchers may pick is instantiated.
+// ---------------------------------------------------------------------------
+
+template <int kAlgo, bool kBf16, int kNorm>
+const void *moments_fn(bool deferred) {
+    return deferred ? reinterpret_cast<const void *>(&moments_kernel<kAlgo, kBf16, kNorm, true>)
+                    : reinterpret_cast<const void *>(&moments_kernel<kAlgo, kBf16, kNorm, false>);
+}
+
+template <int kAlgo, bool kBf16>
+const void *moments_fn(int norm, bool deferred) {
+    switch (norm) {
+    case kL1: return moments_fn<kAlgo, kBf16, kL1>(deferred);
+    case kLinf: return moments_fn<kAlgo, kBf16, kLinf>(deferred);
+    default: return moments_fn<kAlgo, kBf16, kL2>(deferred);
+    }
+}
+
+template <int kAlgo>
+const void *moments_fn(const StepKind &k) {
+    return k.bf16_grad ? moments_fn<kAlgo, true>(k.norm, k.deferred)
+                       : moments_fn<kAlgo, false>(k.norm, k.deferred);
+}
+
+template <int kAlgo>
+const void *apply_fn(const StepKind &k) {
+    if (k.bf16_grad)
+        return k.deferred ? reinterpret_cast<const void *>(&apply_kernel<kAlgo, true, true>)
+                          : reinterpret_cast<const void *>(&apply_kernel<kAlgo, true, false>);
+    return k.deferred ? reinterpret_cast<const void *>(&apply_kernel<kAlgo, false, true>)
+                      : reinterpret_cast<const void *>(&apply_kernel<kAlgo, false, false>);
+}
+
 }  // namespace
 
 // ---------------------------------------------------------------------------
 // Launchers.
 // ---------------------------------------------------------------------------
 
-template <int kVariant>
-const void *moments_fn(bool bf16) {
-    return bf16 ? reinterpret_cast<const void *>(&lamb_moments_kernel<true, kVariant>)
-                : reinterpret_cast<const void *>(&lamb_moments_kernel<false, kVariant>);
-}
-
-hipError_t launch_lamb_moments(const TensorDesc *tensors, const ChunkDesc *chunks,
-                               Partial *partials, int32_t n_chunks, bool bf16_grad,
-                               LambVariant variant, const LambArgs &args, hipStream_t stream) {
-    LambArgs a = args;
-    void *params[] = {&tensors, &chunks, &partials, &a};
-    const void *fn = variant == kNLamb    ? moments_fn<kNLamb>(bf16_grad)
-                     : variant == kNNLamb ? moments_fn<kNNLamb>(bf16_grad)
-                                          : moments_fn<kLamb>(bf16_grad);
-    return hipLaunchKernel(fn, dim3(n_chunks), dim3(kBlock), params, 0, stream);
-}
-
-hipError_t launch_lamb_apply(const TensorDesc *tensors, const ChunkDesc *chunks,
-                             const float *scale, int32_t n_chunks, bool bf16_grad,
-                             LambVariant variant, const LambArgs &args, hipStream_t stream) {
-    LambArgs a = args;
-    void *params[] = {&tensors, &chunks, &scale, &a};
+hipError_t launch_moments(const StepKind &kind, const TensorDesc *tensors,
+                          const ChunkDesc *chunks, Partial *partials, int32_t n_chunks,
+                          uint32_t *flags, const StepArgs &args, hipStream_t stream) {
+    StepArgs a = args;
+    void *params[] = {&tensors, &chunks, &partials, &flags, &a};
     const void *fn;
-    if (variant == kNLamb)
-        fn = bf16_grad ? reinterpret_cast<const void *>(&lamb_apply_kernel<true, kNLamb>)
-                       : reinterpret_cast<const void *>(&lamb_apply_kernel<false, kNLamb>);
-    else if (variant == kNNLamb)
-        fn = bf16_grad ? reinterpret_cast<const void *>(&lamb_apply_kernel<true, kNNLamb>)
-                       : reinterpret_cast<const void *>(&lamb_apply_kernel<false, kNNLamb>);
-    else
-        fn = reinterpret_cast<const void *>(&lamb_apply_kernel<false, kLamb>);
+    switch (kind.algo) {
+    case kNLamb: fn = moments_fn<kNLamb>(kind); break;
+    case kNNLamb: fn = moments_fn<kNNLamb>(kind); break;
+    case kLars: fn = moments_fn<kLars>(kind); break;
+    default: fn = moments_fn<kLamb>(kind); break;
+    }
     return hipLaunchKernel(fn, dim3(n_chunks), dim3(kBlock), params, 0, stream);
 }
 
-hipError_t launch_lars_moments(const TensorDesc *tensors, const ChunkDesc *chunks,
-                               Partial *partials, int32_t n_chunks, bool bf16_grad,
-                               const LarsArgs &args, hipStream_t stream) {
-    LarsArgs a = args;
-    void *params[] = {&tensors, &chunks, &partials, &a};
-    const void *fn = bf16_grad ? reinterpret_cast<const void *>(&lars_moments_kernel<true>)
-                               : reinterpret_cast<const void *>(&lars_moments_kernel<false>);
+hipError_t launch_apply(const StepKind &kind, const TensorDesc *tensors,
+                        const ChunkDesc *chunks, const float *scale, int32_t n_chunks,
+                        uint32_t *flags, int32_t *nonfinite_out, const StepArgs &args,
+                        hipStream_t stream) {
+    StepArgs a = args;
+    void *params[] = {&tensors, &chunks, &scale, &flags, &nonfinite_out, &a};
+    const void *fn;
+    switch (kind.algo) {
+    case kNLamb: fn = apply_fn<kNLamb>(kind); break;
+    case kNNLamb: fn = apply_fn<kNNLamb>(kind); break;
+    case kLars: fn = apply_fn<kLars>(kind); break;
+    default: fn = apply_fn<kLamb>(kind); break;
+    }
     return hipLaunchKernel(fn, dim3(n_chunks), dim3(kBlock), params, 0, stream);
 }
 
-hipError_t launch_lars_apply(const TensorDesc *tensors, const ChunkDesc *chunks,
-                             const float *scale, int32_t n_chunks, hipStream_t stream) {
-    void *params[] = {&tensors, &chunks, &scale};
-    return hipLaunchKernel(reinterpret_cast<const void *>(&lars_apply_kernel), dim3(n_chunks),
-                           dim3(kBlock), params, 0, stream);
-}
-
-hipError_t launch_finalize(const TensorDesc *tensors, int32_t n_tensors,
-                           const Partial *partials, const FinalizeArgs &args, float *scale,
-                           double *ratio_out, double *norms_out, hipStream_t stream) {
+hipError_t launch_finalize(NormKind norm, bool coarse, const TensorDesc *tensors,
+                           int32_t n_tensors, const Partial *partials, const FinalizeArgs &args,
+                           float *scale, double *ratio_out, double *norms_out,
+                           hipStream_t stream) {
     FinalizeArgs a = args;
-    void *params[] = {&tensors, &partials, &a, &scale, &ratio_out, &norms_out};
-    return hipLaunchKernel(reinterpret_cast<const void *>(&finalize_kernel), dim3(n_tensors),
-                           dim3(kFinalizeBlock), params, 0, stream);
+    int coarse_flag = coarse ? 1 : 0;
+    void *params[] = {&tensors, &partials, &coarse_flag, &a, &scale, &ratio_out, &norms_out};
+    const void *fn = norm == kL1     ? reinterpret_cast<const void *>(&finalize_kernel<kL1>)
+                     : norm == kLinf ? reinterpret_cast<const void *>(&finalize_kernel<kLinf>)
+                                     : reinterpret_cast<const void *>(&finalize_kernel<kL2>);
+    return hipLaunchKernel(fn, dim3(n_tensors), dim3(kFinalizeBlock), params, 0, stream);
 }
 
 }  // namespace lamb_mi355x

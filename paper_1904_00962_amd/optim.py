@@ -51,7 +51,8 @@ class _LayerwiseOptimizer:
 
     def __init__(self, params: Sequence, grads: Sequence, lr: float, weight_decay: float,
                  clamp: Tuple[float, float], wd_mask: Optional[Sequence[bool]],
-                 chunk_elems: int, with_v: bool):
+                 chunk_elems: int, with_v: bool, norm: str = "l2", grad_scale: float = 1.0,
+                 skip_nonfinite: bool = False):
         torch = _torch()
         self.params = list(params)
         self.grads = list(grads)
@@ -69,6 +70,13 @@ class _LayerwiseOptimizer:
         n = len(self.params)
         self.ratios = torch.zeros(n, dtype=torch.float64, device=self.device)
         self.norms = torch.zeros(2 * n, dtype=torch.float64, device=self.device)
+        if norm not in _lib.NORMS:
+            raise ValueError("norm must be one of %s" % (tuple(_lib.NORMS),))
+        self.norm = norm
+        self.grad_scale = float(grad_scale)
+        self.skip_nonfinite = bool(skip_nonfinite)
+        # 1 after a step skipped for a non-finite gradient (device int32)
+        self.found_nonfinite = torch.zeros(1, dtype=torch.int32, device=self.device)
         rows = []
         for i, (p, g) in enumerate(zip(self.params, self.grads)):
             v = self.v[i].data_ptr() if with_v else 0
@@ -81,6 +89,13 @@ class _LayerwiseOptimizer:
 
     def _stream(self) -> int:
         return _torch().cuda.current_stream(self.device).cuda_stream
+
+    def _run(self, hp) -> None:
+        hp.norm = _lib.NORMS[self.norm]
+        hp.skip_nonfinite = int(self.skip_nonfinite)
+        _lib.lamb_step_ex(self.plan, hp, self._stream(), self.ratios.data_ptr(),
+                          self.norms.data_ptr(),
+                          self.found_nonfinite.data_ptr() if self.skip_nonfinite else 0)
 
     def close(self) -> None:
         self.plan.close()
@@ -95,14 +110,20 @@ class LAMB(_LayerwiseOptimizer):
 
     def __init__(self, params, grads, lr: float = 1e-3, betas=(0.9, 0.999), eps: float = 1e-6,
                  weight_decay: float = 0.01, clamp=(0.0, 10.0), wd_mask=None,
-                 bias_correction: bool = True, chunk_elems: int = 0, variant: str = "lamb"):
+                 bias_correction: bool = True, chunk_elems: int = 0, variant: str = "lamb",
+                 norm: str = "l2", grad_scale: float = 1.0, skip_nonfinite: bool = False):
         """``variant``: "lamb" (Algorithm 2), "n-lamb" (Algorithm 3) or "nn-lamb"
-        (Algorithm 4; the paper pairs both with betas=(0.975, 0.999), eps=1e-8)."""
+        (Algorithm 4; the paper pairs both with betas=(0.975, 0.999), eps=1e-8).
+        ``norm``: "l2" (default), "l1" or "linf" (Appendix F). ``grad_scale``
+        multiplies every gradient element (e.g. 1/N for a summed gradient, or a
+        loss-scale inverse). ``skip_nonfinite``: a step whose scaled gradient
+        holds a NaN or infinity changes nothing and sets ``found_nonfinite``."""
         if variant not in self.VARIANTS:
             raise ValueError("variant must be one of %s" % (self.VARIANTS,))
         if variant != "lamb" and not bias_correction:
             raise ValueError("N-LAMB and NN-LAMB carry their own bias correction")
-        super().__init__(params, grads, lr, weight_decay, clamp, wd_mask, chunk_elems, True)
+        super().__init__(params, grads, lr, weight_decay, clamp, wd_mask, chunk_elems, True,
+                         norm, grad_scale, skip_nonfinite)
         self.beta1, self.beta2 = float(betas[0]), float(betas[1])
         self.eps = float(eps)
         self.bias_correction = bool(bias_correction)
@@ -112,15 +133,11 @@ class LAMB(_LayerwiseOptimizer):
         """Advance t and apply one step; per-tensor ratios and norms land in
         ``self.ratios`` and ``self.norms`` (device, float64)."""
         self.t += 1
-        lr = self.lr if lr is None else float(lr)
-        if self.variant == "lamb":
-            _lib.lamb_step(self.plan, lr, self.beta1, self.beta2, self.eps, self.weight_decay,
-                           self.gamma_l, self.gamma_u, self.t, self.bias_correction,
-                           self._stream(), self.ratios.data_ptr(), self.norms.data_ptr())
-        else:
-            _lib.nlamb_step(self.plan, lr, self.beta1, self.beta2, self.eps, self.weight_decay,
-                            self.gamma_l, self.gamma_u, self.t, self.variant == "nn-lamb",
-                            self._stream(), self.ratios.data_ptr(), self.norms.data_ptr())
+        self._run(_lib.lamb_hparams_init(
+            self.variant, step=self.t, lr=self.lr if lr is None else float(lr),
+            beta1=self.beta1, beta2=self.beta2, eps=self.eps, weight_decay=self.weight_decay,
+            gamma_l=self.gamma_l, gamma_u=self.gamma_u, grad_scale=self.grad_scale,
+            bias_correction=int(self.bias_correction)))
 
     def state_dict(self):
         return {"step": self.t, "m": [m.clone() for m in self.m], "v": [v.clone() for v in self.v]}
@@ -140,16 +157,19 @@ class LARS(_LayerwiseOptimizer):
 
     def __init__(self, params, grads, lr: float = 1e-3, momentum: float = 0.9,
                  weight_decay: float = 0.01, clamp=(0.0, 10.0), trust_coef: float = 1e-3,
-                 wd_mask=None, chunk_elems: int = 0):
-        super().__init__(params, grads, lr, weight_decay, clamp, wd_mask, chunk_elems, False)
+                 wd_mask=None, chunk_elems: int = 0, norm: str = "l2", grad_scale: float = 1.0,
+                 skip_nonfinite: bool = False):
+        super().__init__(params, grads, lr, weight_decay, clamp, wd_mask, chunk_elems, False,
+                         norm, grad_scale, skip_nonfinite)
         self.momentum = float(momentum)
         self.trust_coef = float(trust_coef)
 
     def step(self, lr: Optional[float] = None) -> None:
         self.t += 1
-        _lib.lars_step(self.plan, self.lr if lr is None else float(lr), self.momentum,
-                       self.weight_decay, self.gamma_l, self.gamma_u, self.trust_coef,
-                       self._stream(), self.ratios.data_ptr(), self.norms.data_ptr())
+        self._run(_lib.lamb_hparams_init(
+            "lars", lr=self.lr if lr is None else float(lr), beta1=self.momentum,
+            weight_decay=self.weight_decay, gamma_l=self.gamma_l, gamma_u=self.gamma_u,
+            trust_coef=self.trust_coef, grad_scale=self.grad_scale))
 
     def state_dict(self):
         return {"step": self.t, "m": [m.clone() for m in self.m]}

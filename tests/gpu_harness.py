@@ -171,7 +171,8 @@ class Pair:
                                      **f32_scalars(hp))
 
     def compare(self, ref: np.ndarray, label: str) -> Report:
-        """Element-wise state and per-tensor ratio/norm comparison for the subset."""
+        """Element-wise state and per-tensor ratio/norm comparison for the subset
+        (ratios and norms only when the oracle did not skip the step)."""
         self.torch.cuda.synchronize()
         rep = Report()
         ratio = self.ratio.cpu().numpy()
@@ -185,6 +186,8 @@ class Pair:
                 rep.merge(compare_state(paramsets.host_array(self.V[i]), self.hv[k],
                                         "%s v[%d]" % (label, i)))
         idx = np.asarray(self.subset)
+        if np.all(np.isnan(ref)):
+            return rep
         compare_ratios(ratio[idx], ref[:, 0], label + " trust ratio")
         compare_ratios(norms[idx, 0], ref[:, 1], label + " ||x||")
         compare_ratios(norms[idx, 1], ref[:, 2], label + " ||u||")
@@ -219,6 +222,33 @@ def nlamb_hp(ps: paramsets.ParamSet) -> dict:
 def lars_hp(ps: paramsets.ParamSet) -> dict:
     return dict(lr=ps.lars_lr, momentum=ps.lars_momentum, weight_decay=ps.weight_decay,
                 gamma_l=ps.gamma_l, gamma_u=ps.gamma_u, trust_coef=ps.lars_trust_coef)
+
+
+NORM_NAMES = {0: "l2", 1: "l1", 2: "linf"}
+
+
+def step_ex_both(pair: Pair, hp, hg, nonfinite=None):
+    """One ``lamb_step_ex`` with hyperparameters ``hp`` (an ``_lib.lamb_hparams``,
+    fp32 fields) on the GPU and the matching oracle step; returns the oracle's
+    per-tensor [ratio, ||x||, ||u||] (NaN rows when it skipped the step)."""
+    _lib.lamb_step_ex(pair.plan, hp, pair.torch.cuda.current_stream().cuda_stream,
+                      pair.ratio.data_ptr(), pair.norms.data_ptr(),
+                      nonfinite.data_ptr() if nonfinite is not None else 0)
+    wd = [pair.wd[i] for i in pair.subset]
+    common = dict(lr=hp.lr, weight_decay=hp.weight_decay, gamma_l=hp.gamma_l,
+                  gamma_u=hp.gamma_u, grad_scale=hp.grad_scale, norm=NORM_NAMES[hp.norm],
+                  skip_nonfinite=bool(hp.skip_nonfinite))
+    o = pair.oracle
+    if hp.variant == _lib.LAMB_VARIANT_LAMB:
+        return o.lamb_step(pair.hx, hg, pair.hm, pair.hv, wd, beta1=hp.beta1, beta2=hp.beta2,
+                           eps=hp.eps, step=hp.step, bias_correction=bool(hp.bias_correction),
+                           **common)
+    if hp.variant in (_lib.LAMB_VARIANT_NLAMB, _lib.LAMB_VARIANT_NNLAMB):
+        return o.nlamb_step(pair.hx, hg, pair.hm, pair.hv, wd, beta1=hp.beta1, beta2=hp.beta2,
+                            eps=hp.eps, step=hp.step,
+                            nesterov_v=hp.variant == _lib.LAMB_VARIANT_NNLAMB, **common)
+    return o.lars_step(pair.hx, hg, pair.hm, wd, momentum=hp.beta1, trust_coef=hp.trust_coef,
+                       **common)
 
 
 def step_both(pair: Pair, algo: str, hg, hp: dict, t: int, bias_correction: bool = True):

@@ -126,6 +126,22 @@ def test_bf16_overlap_uses_two_byte_elements(lib):
     assert e.value.status == _lib.LAMB_EALIGN
 
 
+def test_hparams_defaults(lib):
+    hp = _lib.lamb_hparams_init("lamb")
+    assert (hp.beta1, hp.beta2, hp.weight_decay, hp.step, hp.norm) == (
+        pytest.approx(0.9), pytest.approx(0.999), pytest.approx(0.01), 1, _lib.LAMB_NORM_L2)
+    assert hp.eps == pytest.approx(1e-6) and hp.grad_scale == 1.0 and hp.bias_correction == 1
+    hp = _lib.lamb_hparams_init("n-lamb", norm="linf", lr=0.5)
+    assert hp.beta1 == pytest.approx(0.975) and hp.eps == pytest.approx(1e-8)
+    assert hp.norm == _lib.LAMB_NORM_LINF and hp.lr == 0.5
+    hp = _lib.lamb_hparams_init("lars")
+    assert hp.variant == _lib.LAMB_VARIANT_LARS and hp.trust_coef == 1.0
+    with pytest.raises(_lib.LambError):
+        _lib.lamb_hparams_init(9)
+    assert lib.lamb_hparams_init(None, 0) == _lib.LAMB_ENULL
+    assert lib.lamb_step_ex(None, ctypes.byref(hp), None, None, None, None) == _lib.LAMB_ENULL
+
+
 def test_null_plan_and_outputs(lib):
     assert lib.lamb_step(None, 1e-3, 0.9, 0.999, 1e-6, 0.01, 0.0, 10.0, 1, 1, None, None,
                          None) == _lib.LAMB_ENULL
