@@ -171,6 +171,8 @@ def main() -> int:
     ap.add_argument("--grad-scale", type=float, default=1.0)
     ap.add_argument("--skip-nonfinite", action="store_true",
                     help="deferred-write mode that skips steps with NaN/Inf gradients")
+    ap.add_argument("--bf16-copy", action="store_true",
+                    help="the apply pass also writes a bf16 copy of x")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", action="store_true")
@@ -212,6 +214,8 @@ def main() -> int:
         opt = LARS(xs, grads, lr=ps.lars_lr, momentum=ps.lars_momentum,
                    weight_decay=ps.weight_decay, clamp=(ps.gamma_l, ps.gamma_u),
                    trust_coef=ps.lars_trust_coef, **extra)
+    if args.bf16_copy:
+        opt.attach_bf16_copies("allocate")
     n_tensors, n_chunks, chunk = _lib.lamb_plan_info(opt.plan)
 
     # The oracle's sample is copied out before the GPU steps move x; the
@@ -247,6 +251,7 @@ def main() -> int:
     P = ps.numel
     g_bytes = 2 if ps.g_dtype == "bf16" else 4
     b_mom, b_app = bytes_per_param(args.algo, g_bytes, args.skip_nonfinite)
+    b_app += 2 if args.bf16_copy else 0  # the bf16 working copy of x
     avg_mom = k_mom / recorded
     avg_app = k_app / recorded
     avg_fin = k_fin / recorded
@@ -255,7 +260,8 @@ def main() -> int:
     step_gbps = (b_mom + b_app) * P / ms_step / 1e6
     workload = ps.name
     src_hash = kernel_source_hash()
-    default_mode = (args.algo == "lamb" and args.norm == "l2" and not args.skip_nonfinite)
+    default_mode = (args.algo == "lamb" and args.norm == "l2" and not args.skip_nonfinite
+                    and not args.bf16_copy)
     traffic = counter_traffic(workload, src_hash) if default_mode else None
     algo_name = algo_label(args.algo)
     kernel = "moments_kernel<%s, %s, %s%s>" % (algo_label(args.algo), "bf16" if g_bytes == 2 else "f32",
@@ -282,6 +288,7 @@ def main() -> int:
             "algo": args.algo, "tensors": n_tensors, "params": P, "grad_dtype": ps.g_dtype,
             "chunk_elems": chunk, "chunks": n_chunks, "norm": args.norm,
             "grad_scale": args.grad_scale, "skip_nonfinite": args.skip_nonfinite,
+            "bf16_copy": args.bf16_copy,
             "seed_x": 1000 * ps.cfg,
             "seed_g": 1000 * ps.cfg + 1,
         },

@@ -168,6 +168,21 @@ LAMB_API lamb_status lamb_plan_create(const lamb_tensor *tensors, int32_t n_tens
  * caller must not destroy a plan whose step is still running. */
 LAMB_API lamb_status lamb_plan_destroy(lamb_plan *plan);
 
+/*
+ * Attach bf16 working copies of the parameters (for the next forward pass of
+ * mixed-precision training): every later step's apply pass also writes
+ * copy_i[j] = bf16(x_i[j]) after the update, rounded to nearest with ties to
+ * even (NaN becomes 0x7fc0), at 2 more bytes per parameter instead of a
+ * separate cast pass.
+ *   copies  host array of n_tensors device pointers to numel bf16 each,
+ *           16-byte aligned, overlapping no buffer of the plan or each other;
+ *           an entry may be NULL (no copy for that tensor); copies = NULL
+ *           detaches all.
+ * Copies a table to the device synchronously; do not call while a step runs.
+ * Errors: LAMB_ENULL (plan), LAMB_EALIGN, LAMB_EOVERLAP, LAMB_EHIP.
+ */
+LAMB_API lamb_status lamb_plan_set_bf16_copies(lamb_plan *plan, void *const *copies);
+
 /* Sizes of a plan (host outputs; any may be NULL). */
 LAMB_API lamb_status lamb_plan_info(const lamb_plan *plan, int32_t *n_tensors,
                            int32_t *n_chunks, int32_t *chunk_elems);
@@ -283,6 +298,42 @@ LAMB_API lamb_status lamb_plan_set_timing(lamb_plan *plan, int32_t max_steps);
  * start a new recording window.
  */
 LAMB_API lamb_status lamb_plan_timing(lamb_plan *plan, double *kernel_ms, int64_t *steps);
+
+/*
+ * Host-side learning-rate schedule (Section 4): a polynomially decaying rate
+ * eta = eta_0 (1 - tau/T)^power after a linear warmup, in stages that run
+ * back to back, so that the second stage of mixed-batch training (Section
+ * 4.1) warms up again.
+ *   steps         T, iterations in the stage (>= 1)
+ *   warmup_steps  W, 0 <= W <= T
+ *   peak_lr       eta_0, finite and >= 0
+ *   power         decay exponent (1 in the paper), finite and >= 0
+ */
+typedef struct lamb_lr_stage {
+    int64_t steps;
+    int64_t warmup_steps;
+    double peak_lr;
+    double power;
+} lamb_lr_stage;
+
+/*
+ * Learning rate for step t >= 1 (the t passed to lamb_step). With tau = the
+ * number of steps already taken inside the stage holding t:
+ *   tau <  W:  eta_0 (tau + 1) / W          (reaches eta_0 on the last warmup step)
+ *   tau >= W:  eta_0 (1 - tau / T)^power
+ * and 0 after the last stage. Errors: LAMB_ENULL, LAMB_EINVAL (t < 1 or a
+ * stage out of range); *lr_out is untouched on error.
+ */
+LAMB_API lamb_status lamb_lr_at(const lamb_lr_stage *stages, int32_t n_stages, int64_t step,
+                       double *lr_out);
+
+/*
+ * Square-root learning-rate scaling (Section 4; Tables 4 and 5):
+ * lr = base_lr * sqrt(batch / base_batch). Errors: LAMB_ENULL, LAMB_EINVAL
+ * (non-positive batch sizes, negative or non-finite base_lr).
+ */
+LAMB_API lamb_status lamb_sqrt_scaled_lr(double base_lr, int64_t base_batch, int64_t batch,
+                                double *lr_out);
 
 /* Static description of a status code. */
 LAMB_API const char *lamb_status_str(lamb_status status);

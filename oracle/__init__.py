@@ -89,6 +89,8 @@ class Oracle:
             ctypes.c_void_p, ctypes.c_double, ctypes.c_double, ctypes.c_double,
             ctypes.c_int, ctypes.c_double, ctypes.c_double, ctypes.c_double,
             ctypes.c_double, ctypes.c_int, _DP]
+        lib.oracle_round_bf16.restype = None
+        lib.oracle_round_bf16.argtypes = [ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p]
         lib.oracle_gradient_finite.restype = ctypes.c_int
         lib.oracle_gradient_finite.argtypes = [ctypes.c_int64, ctypes.c_void_p, ctypes.c_int,
                                                ctypes.c_double]
@@ -101,6 +103,13 @@ class Oracle:
             if not self._lib.oracle_gradient_finite(g.size, _ptr(g), kind, grad_scale):
                 return False
         return True
+
+    def round_bf16(self, x: np.ndarray) -> np.ndarray:
+        """bf16 bit patterns (uint16) of fp32 ``x``, round to nearest even."""
+        x = np.ascontiguousarray(x, dtype=np.float32)
+        out = np.empty(x.size, dtype=np.uint16)
+        self._lib.oracle_round_bf16(x.size, _ptr(x), _ptr(out))
+        return out
 
     def _skipped(self, gs, grad_scale, skip_nonfinite):
         if skip_nonfinite and not self.gradients_finite(gs, grad_scale):

@@ -310,3 +310,24 @@ int oracle_nlamb_layer(int64_t d, float *x, const void *g, int g_is_bf16,
     free(u);
     return ORACLE_OK;
 }
+
+/*
+ * The bf16 working copy of updated parameters: each fp32 x_j rounded to the
+ * nearest bf16, ties to even; every NaN becomes the quiet NaN 0x7fc0.
+ */
+void oracle_round_bf16(int64_t d, const float *x, uint16_t *out)
+{
+    for (int64_t j = 0; j < d; ++j) {
+        if (isnan(x[j])) {
+            out[j] = 0x7fc0;
+            continue;
+        }
+        uint32_t bits;
+        memcpy(&bits, &x[j], sizeof bits);
+        uint32_t low = bits & 0xffffu;            /* the 16 bits dropped */
+        uint32_t high = bits >> 16;
+        if (low > 0x8000u || (low == 0x8000u && (high & 1u)))
+            high += 1u;                           /* carries into the exponent as needed */
+        out[j] = (uint16_t)high;
+    }
+}

@@ -46,8 +46,10 @@ LAMB_NORM_LINF = 2
 NORMS = {"l2": LAMB_NORM_L2, "l1": LAMB_NORM_L1, "linf": LAMB_NORM_LINF}
 
 # Every symbol the header declares (checked by the test suite).
-EXPORTS = ("lamb_plan_create", "lamb_plan_destroy", "lamb_plan_info", "lamb_hparams_init",
-           "lamb_step_ex", "lamb_step", "nlamb_step", "lars_step", "lamb_chunk_table", "lamb_plan_set_timing", "lamb_plan_timing",
+EXPORTS = ("lamb_plan_create", "lamb_plan_destroy", "lamb_plan_info",
+           "lamb_plan_set_bf16_copies", "lamb_hparams_init",
+           "lamb_step_ex", "lamb_step", "nlamb_step", "lars_step", "lamb_lr_at",
+           "lamb_sqrt_scaled_lr", "lamb_chunk_table", "lamb_plan_set_timing", "lamb_plan_timing",
            "lamb_status_str", "lamb_last_error")
 
 
@@ -74,6 +76,11 @@ class lamb_hparams(ctypes.Structure):
                 ("reserved", ctypes.c_int32)]
 
 
+class lamb_lr_stage(ctypes.Structure):
+    _fields_ = [("steps", ctypes.c_int64), ("warmup_steps", ctypes.c_int64),
+                ("peak_lr", ctypes.c_double), ("power", ctypes.c_double)]
+
+
 _lib: Optional[ctypes.CDLL] = None
 
 
@@ -96,9 +103,12 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
     lib.lamb_plan_create.argtypes = [P(lamb_tensor), i32, i32, i32, i32, P(vp)]
     lib.lamb_plan_destroy.argtypes = [vp]
     lib.lamb_plan_info.argtypes = [vp, P(i32), P(i32), P(i32)]
+    lib.lamb_plan_set_bf16_copies.argtypes = [vp, P(vp)]
     lib.lamb_step.argtypes = [vp, f32, f32, f32, f32, f32, f32, f32, i64, i32, vp, vp, vp]
     lib.nlamb_step.argtypes = [vp, f32, f32, f32, f32, f32, f32, f32, i64, i32, vp, vp, vp]
     lib.lamb_hparams_init.argtypes = [P(lamb_hparams), i32]
+    lib.lamb_lr_at.argtypes = [P(lamb_lr_stage), i32, i64, P(ctypes.c_double)]
+    lib.lamb_sqrt_scaled_lr.argtypes = [ctypes.c_double, i64, i64, P(ctypes.c_double)]
     lib.lamb_step_ex.argtypes = [vp, P(lamb_hparams), vp, vp, vp, vp]
     lib.lars_step.argtypes = [vp, f32, f32, f32, f32, f32, f32, vp, vp, vp]
     lib.lamb_chunk_table.argtypes = [P(i64), i32, i32, i32, P(i32), P(i64), P(i32), P(i32)]
@@ -175,6 +185,16 @@ def lamb_plan_destroy(plan: Plan) -> None:
     plan.close()
 
 
+def lamb_plan_set_bf16_copies(plan: Plan, copies: Optional[Sequence[int]]) -> None:
+    """Attach bf16 copies (device pointers, one per tensor, 0 for none) or
+    detach all (None)."""
+    if copies is None:
+        arr = None
+    else:
+        arr = (ctypes.c_void_p * max(len(copies), 1))(*[int(c) or None for c in copies])
+    _check(load().lamb_plan_set_bf16_copies(_vp(plan.handle), arr), "lamb_plan_set_bf16_copies")
+
+
 def lamb_plan_info(plan: Plan) -> Tuple[int, int, int]:
     a, b, c = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
     _check(load().lamb_plan_info(_vp(plan.handle), ctypes.byref(a), ctypes.byref(b),
@@ -248,6 +268,23 @@ def lamb_chunk_table(numel: Sequence[int], chunk_elems: int = 0):
                                 cl.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
                                 ctypes.byref(count)), "lamb_chunk_table")
     return ct, cs, cl
+
+
+def lamb_lr_at(stages: Sequence[Tuple[int, int, float, float]], step: int) -> float:
+    """Learning rate at step ``step`` (>= 1) of back-to-back stages given as
+    (steps, warmup_steps, peak_lr, power)."""
+    arr = (lamb_lr_stage * max(len(stages), 1))(*[lamb_lr_stage(int(a), int(b), float(c), float(d))
+                                                  for a, b, c, d in stages])
+    out = ctypes.c_double()
+    _check(load().lamb_lr_at(arr, len(stages), int(step), ctypes.byref(out)), "lamb_lr_at")
+    return out.value
+
+
+def lamb_sqrt_scaled_lr(base_lr: float, base_batch: int, batch: int) -> float:
+    out = ctypes.c_double()
+    _check(load().lamb_sqrt_scaled_lr(float(base_lr), int(base_batch), int(batch),
+                                      ctypes.byref(out)), "lamb_sqrt_scaled_lr")
+    return out.value
 
 
 def lamb_plan_set_timing(plan: Plan, max_steps: int) -> None:

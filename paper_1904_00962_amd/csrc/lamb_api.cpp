@@ -12,6 +12,7 @@
 #include <cstdio>
 #include <cstring>
 #include <new>
+#include <utility>
 #include <vector>
 
 #include "lamb_internal.h"
@@ -34,6 +35,8 @@ struct lamb_plan {
     float *scale = nullptr;
     uint32_t *flags = nullptr;     // two non-finite flags, alternating per deferred step
     uint32_t deferred_steps = 0;   // deferred steps enqueued so far (selects the flag)
+    std::vector<TensorDesc> host_tensors;  // host image of the tensor table
+    std::vector<std::pair<uintptr_t, uintptr_t>> ranges;  // sorted buffer ranges of the table
     // timing hooks: 4 events per recorded step
     std::vector<hipEvent_t> events;
     int32_t timing_capacity = 0;
@@ -295,8 +298,9 @@ lamb_status lamb_plan_create(const lamb_tensor *tensors, int32_t n_tensors,
             const lamb_tensor &t = tensors[i];
             const int32_t nc = int32_t((t.numel + chunk - 1) / chunk);
             const int32_t ncc = int32_t((t.numel + coarse - 1) / coarse);
-            host_tensors[size_t(i)] = TensorDesc{t.x, t.g, t.m, needs_v ? t.v : nullptr, t.numel,
-                                                 t.wd, first, nc, first_coarse, ncc, 0};
+            host_tensors[size_t(i)] = TensorDesc{t.x, t.g, t.m, needs_v ? t.v : nullptr, nullptr,
+                                                 t.numel, t.wd, first, nc, first_coarse, ncc, 0,
+                                                 0};
             first += nc;
             first_coarse += ncc;
         }
@@ -357,6 +361,9 @@ lamb_status lamb_plan_create(const lamb_tensor *tensors, int32_t n_tensors,
     plan->n_tensors = n_tensors;
     plan->n_chunks = n_chunks;
     plan->n_coarse = n_coarse;
+    plan->host_tensors = std::move(host_tensors);
+    for (const Range &r : ranges)
+        plan->ranges.emplace_back(r.lo, r.hi);
     plan->chunk_elems = chunk;
     *out = plan;
     return LAMB_OK;
@@ -618,6 +625,78 @@ lamb_status lars_step(lamb_plan *plan, float lr, float momentum, float weight_de
     hp.gamma_u = gamma_u;
     hp.trust_coef = trust_coef;
     return lamb_step_ex(plan, &hp, stream, ratio_out, norms_out, nullptr);
+}
+
+lamb_status lamb_plan_set_bf16_copies(lamb_plan *plan, void *const *copies) {
+    if (!plan)
+        return fail(LAMB_ENULL, "plan must not be NULL");
+    std::vector<TensorDesc> next = plan->host_tensors;
+    std::vector<std::pair<uintptr_t, uintptr_t>> mine;
+    for (int32_t i = 0; i < plan->n_tensors; ++i) {
+        uint16_t *c = copies ? static_cast<uint16_t *>(copies[i]) : nullptr;
+        next[size_t(i)].x_copy = c;
+        if (!c)
+            continue;
+        if (!aligned16(c))
+            return fail(LAMB_EALIGN, "copy %d must be 16-byte aligned", i);
+        const uintptr_t lo = reinterpret_cast<uintptr_t>(c);
+        mine.emplace_back(lo, lo + uintptr_t(next[size_t(i)].numel) * 2u);
+    }
+    // Copies may overlap neither each other nor any buffer of the table.
+    std::vector<std::pair<uintptr_t, uintptr_t>> all = plan->ranges;
+    all.insert(all.end(), mine.begin(), mine.end());
+    std::sort(all.begin(), all.end());
+    for (size_t k = 1; k < all.size(); ++k)
+        if (all[k].first < all[k - 1].second)
+            return fail(LAMB_EOVERLAP, "a bf16 copy overlaps another buffer of the plan");
+    DeviceGuard guard(plan->device);
+    if (guard.status != hipSuccess)
+        return fail_hip(guard.status, "selecting the plan's device");
+    hipError_t err = hipMemcpy(plan->tensors, next.data(),
+                               sizeof(TensorDesc) * size_t(plan->n_tensors), hipMemcpyHostToDevice);
+    if (err != hipSuccess)
+        return fail_hip(err, "hipMemcpy of the tensor table");
+    plan->host_tensors = std::move(next);
+    return LAMB_OK;
+}
+
+lamb_status lamb_lr_at(const lamb_lr_stage *stages, int32_t n_stages, int64_t step,
+                       double *lr_out) {
+    if (!stages || !lr_out)
+        return fail(LAMB_ENULL, "stages and lr_out must not be NULL");
+    if (n_stages < 1 || step < 1)
+        return fail(LAMB_EINVAL, "need n_stages >= 1 and step >= 1");
+    for (int32_t k = 0; k < n_stages; ++k) {
+        const lamb_lr_stage &s = stages[k];
+        if (s.steps < 1 || s.warmup_steps < 0 || s.warmup_steps > s.steps ||
+            !(s.peak_lr >= 0.0) || !std::isfinite(s.peak_lr) || !(s.power >= 0.0) ||
+            !std::isfinite(s.power))
+            return fail(LAMB_EINVAL, "stage %d out of range", k);
+    }
+    int64_t tau = step - 1;  // steps already taken, counted from the first stage
+    for (int32_t k = 0; k < n_stages; ++k) {
+        const lamb_lr_stage &s = stages[k];
+        if (tau < s.steps) {
+            if (tau < s.warmup_steps)
+                *lr_out = s.peak_lr * double(tau + 1) / double(s.warmup_steps);
+            else
+                *lr_out = s.peak_lr * std::pow(1.0 - double(tau) / double(s.steps), s.power);
+            return LAMB_OK;
+        }
+        tau -= s.steps;
+    }
+    *lr_out = 0.0;
+    return LAMB_OK;
+}
+
+lamb_status lamb_sqrt_scaled_lr(double base_lr, int64_t base_batch, int64_t batch,
+                                double *lr_out) {
+    if (!lr_out)
+        return fail(LAMB_ENULL, "lr_out must not be NULL");
+    if (base_batch < 1 || batch < 1 || !(base_lr >= 0.0) || !std::isfinite(base_lr))
+        return fail(LAMB_EINVAL, "need positive batch sizes and a finite base_lr >= 0");
+    *lr_out = base_lr * std::sqrt(double(batch) / double(base_batch));
+    return LAMB_OK;
 }
 
 lamb_status lamb_plan_set_timing(lamb_plan *plan, int32_t max_steps) {

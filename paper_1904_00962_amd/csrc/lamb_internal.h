@@ -26,21 +26,23 @@ constexpr int32_t kDefaultChunkElems = LAMB_DEFAULT_CHUNK;
 // and run faster with more work per workgroup).
 constexpr int32_t kCoarseFactor = 4;
 
-// One layer block x^(i) (Section 2) as the kernels see it. 64 bytes.
+// One layer block x^(i) (Section 2) as the kernels see it. 80 bytes.
 struct TensorDesc {
     float *x;
     const void *g;
     float *m;
     float *v;              // null for LARS plans
+    uint16_t *x_copy;      // bf16 working copy written by the apply pass, or null
     int64_t numel;
     int32_t wd;            // 1: lambda applies, 0: lambda = 0
     int32_t first_chunk;   // fine chunks [first_chunk, first_chunk + n_chunks)
     int32_t n_chunks;
     int32_t first_coarse;  // coarse chunks [first_coarse, first_coarse + n_coarse)
     int32_t n_coarse;
-    int32_t pad;
+    int32_t pad0;
+    int64_t pad1;
 };
-static_assert(sizeof(TensorDesc) == 64, "TensorDesc layout");
+static_assert(sizeof(TensorDesc) == 80, "TensorDesc layout");
 
 // One chunk: `len` elements of tensor `tensor` starting at element `start`.
 struct ChunkDesc {

@@ -135,6 +135,19 @@ struct GradView {
     }
 };
 
+// bf16 bit pattern of an fp32 value, rounded to nearest with ties to even
+// (NaN becomes the quiet NaN 0x7fc0). Adding 0x7fff plus the lowest kept bit
+// and truncating rounds the dropped half correctly; a carry moves into the
+// exponent, so the largest finite values round to infinity.
+__device__ __forceinline__ uint32_t bf16_bits(float f) {
+    const uint32_t b = __float_as_uint(f);
+    if ((b & 0x7fffffffu) > 0x7f800000u)
+        return 0x7fc0u;
+    return (b + 0x7fffu + ((b >> 16) & 1u)) >> 16;
+}
+
+typedef LAMB_GLOBAL uint16_t gbf16;
+
 // ---------------------------------------------------------------------------
 // Elementwise arithmetic of Algorithms 1-4.
 // ---------------------------------------------------------------------------
@@ -398,6 +411,7 @@ __global__ __launch_bounds__(kBlock) void apply_kernel(
     gfloat *m = global_view(t.m + c.start);
     gfloat *v = kV ? global_view(t.v + c.start) : nullptr;
     const GradView<kBf16> g(t.g, c.start, a.grad_scale);
+    gbf16 *copy = t.x_copy ? (gbf16 *)(t.x_copy + c.start) : nullptr;
     const float lam = t.wd ? a.weight_decay : 0.0f;
     const float s = scale[c.tensor];
 
@@ -436,6 +450,11 @@ __global__ __launch_bounds__(kBlock) void apply_kernel(
                     vr[k][e] = ve;
                 }
                 store4(x + 4 * q, xn);
+                if (copy) {
+                    const u32x2 packed = {bf16_bits(xn[0]) | (bf16_bits(xn[1]) << 16),
+                                          bf16_bits(xn[2]) | (bf16_bits(xn[3]) << 16)};
+                    stream_store((LAMB_GLOBAL u32x2 *)(copy + 4 * q), packed);
+                }
                 if constexpr (kDeferred) {
                     store4(m + 4 * q, mr[k]);
                     if constexpr (kV)
@@ -452,7 +471,10 @@ __global__ __launch_bounds__(kBlock) void apply_kernel(
         float vj = kV ? v[tail] : 0.0f;
         if constexpr (kDeferred)
             new_moments<kAlgo>(xj, gj, lam, mj, vj, a);
-        x[tail] = fmaf(-s, direction<kAlgo>(xj, gj, mj, vj, lam, a), xj);
+        const float xn = fmaf(-s, direction<kAlgo>(xj, gj, mj, vj, lam, a), xj);
+        x[tail] = xn;
+        if (copy)
+            copy[tail] = uint16_t(bf16_bits(xn));
         if constexpr (kDeferred) {
             m[tail] = mj;
             if constexpr (kV)

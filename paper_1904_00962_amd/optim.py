@@ -52,7 +52,7 @@ class _LayerwiseOptimizer:
     def __init__(self, params: Sequence, grads: Sequence, lr: float, weight_decay: float,
                  clamp: Tuple[float, float], wd_mask: Optional[Sequence[bool]],
                  chunk_elems: int, with_v: bool, norm: str = "l2", grad_scale: float = 1.0,
-                 skip_nonfinite: bool = False):
+                 skip_nonfinite: bool = False, schedule=None):
         torch = _torch()
         self.params = list(params)
         self.grads = list(grads)
@@ -77,6 +77,10 @@ class _LayerwiseOptimizer:
         self.skip_nonfinite = bool(skip_nonfinite)
         # 1 after a step skipped for a non-finite gradient (device int32)
         self.found_nonfinite = torch.zeros(1, dtype=torch.int32, device=self.device)
+        self.bf16_copies = None
+        # (steps, warmup_steps, peak_lr, power) stages: the lr of step t comes
+        # from lamb_lr_at (Section 4) unless step() is given one
+        self.schedule = [tuple(s) for s in schedule] if schedule else None
         rows = []
         for i, (p, g) in enumerate(zip(self.params, self.grads)):
             v = self.v[i].data_ptr() if with_v else 0
@@ -90,12 +94,47 @@ class _LayerwiseOptimizer:
     def _stream(self) -> int:
         return _torch().cuda.current_stream(self.device).cuda_stream
 
+    def _lr(self, lr: Optional[float]) -> float:
+        if lr is not None:
+            return float(lr)
+        if self.schedule:
+            return _lib.lamb_lr_at(self.schedule, self.t)
+        return self.lr
+
     def _run(self, hp) -> None:
         hp.norm = _lib.NORMS[self.norm]
         hp.skip_nonfinite = int(self.skip_nonfinite)
         _lib.lamb_step_ex(self.plan, hp, self._stream(), self.ratios.data_ptr(),
                           self.norms.data_ptr(),
                           self.found_nonfinite.data_ptr() if self.skip_nonfinite else 0)
+
+    def attach_bf16_copies(self, copies="allocate"):
+        """Have every later step also write bf16(x) (round to nearest even) into
+        ``copies``: one contiguous bf16 tensor per parameter with the same
+        numel, or "allocate" to create them, or None to detach. Returns the
+        attached list (``self.bf16_copies``)."""
+        torch = _torch()
+        if copies is None:
+            _lib.lamb_plan_set_bf16_copies(self.plan, None)
+            self.bf16_copies = None
+            return None
+        if isinstance(copies, str) and copies == "allocate":
+            copies = [torch.empty(p.numel(), dtype=torch.bfloat16, device=self.device)
+                      for p in self.params]
+        copies = list(copies)
+        if len(copies) != len(self.params):
+            raise ValueError("need one copy per parameter tensor")
+        for i, (c, p) in enumerate(zip(copies, self.params)):
+            if c is None:
+                continue
+            if c.dtype != torch.bfloat16 or c.device != self.device or not c.is_contiguous():
+                raise TypeError("copy %d must be a contiguous bf16 tensor on %s" % (i, self.device))
+            if c.numel() != p.numel():
+                raise ValueError("copy %d has %d elements, parameter %d" % (i, c.numel(), p.numel()))
+        _lib.lamb_plan_set_bf16_copies(self.plan, [c.data_ptr() if c is not None else 0
+                                                   for c in copies])
+        self.bf16_copies = copies
+        return copies
 
     def close(self) -> None:
         self.plan.close()
@@ -111,19 +150,22 @@ class LAMB(_LayerwiseOptimizer):
     def __init__(self, params, grads, lr: float = 1e-3, betas=(0.9, 0.999), eps: float = 1e-6,
                  weight_decay: float = 0.01, clamp=(0.0, 10.0), wd_mask=None,
                  bias_correction: bool = True, chunk_elems: int = 0, variant: str = "lamb",
-                 norm: str = "l2", grad_scale: float = 1.0, skip_nonfinite: bool = False):
+                 norm: str = "l2", grad_scale: float = 1.0, skip_nonfinite: bool = False,
+                 schedule=None):
         """``variant``: "lamb" (Algorithm 2), "n-lamb" (Algorithm 3) or "nn-lamb"
         (Algorithm 4; the paper pairs both with betas=(0.975, 0.999), eps=1e-8).
         ``norm``: "l2" (default), "l1" or "linf" (Appendix F). ``grad_scale``
         multiplies every gradient element (e.g. 1/N for a summed gradient, or a
         loss-scale inverse). ``skip_nonfinite``: a step whose scaled gradient
-        holds a NaN or infinity changes nothing and sets ``found_nonfinite``."""
+        holds a NaN or infinity changes nothing and sets ``found_nonfinite``.
+        ``schedule``: stages (steps, warmup_steps, peak_lr, power) that set the
+        learning rate of each step (warmup, then polynomial decay, Section 4)."""
         if variant not in self.VARIANTS:
             raise ValueError("variant must be one of %s" % (self.VARIANTS,))
         if variant != "lamb" and not bias_correction:
             raise ValueError("N-LAMB and NN-LAMB carry their own bias correction")
         super().__init__(params, grads, lr, weight_decay, clamp, wd_mask, chunk_elems, True,
-                         norm, grad_scale, skip_nonfinite)
+                         norm, grad_scale, skip_nonfinite, schedule)
         self.beta1, self.beta2 = float(betas[0]), float(betas[1])
         self.eps = float(eps)
         self.bias_correction = bool(bias_correction)
@@ -134,7 +176,7 @@ class LAMB(_LayerwiseOptimizer):
         ``self.ratios`` and ``self.norms`` (device, float64)."""
         self.t += 1
         self._run(_lib.lamb_hparams_init(
-            self.variant, step=self.t, lr=self.lr if lr is None else float(lr),
+            self.variant, step=self.t, lr=self._lr(lr),
             beta1=self.beta1, beta2=self.beta2, eps=self.eps, weight_decay=self.weight_decay,
             gamma_l=self.gamma_l, gamma_u=self.gamma_u, grad_scale=self.grad_scale,
             bias_correction=int(self.bias_correction)))
@@ -158,16 +200,16 @@ class LARS(_LayerwiseOptimizer):
     def __init__(self, params, grads, lr: float = 1e-3, momentum: float = 0.9,
                  weight_decay: float = 0.01, clamp=(0.0, 10.0), trust_coef: float = 1e-3,
                  wd_mask=None, chunk_elems: int = 0, norm: str = "l2", grad_scale: float = 1.0,
-                 skip_nonfinite: bool = False):
+                 skip_nonfinite: bool = False, schedule=None):
         super().__init__(params, grads, lr, weight_decay, clamp, wd_mask, chunk_elems, False,
-                         norm, grad_scale, skip_nonfinite)
+                         norm, grad_scale, skip_nonfinite, schedule)
         self.momentum = float(momentum)
         self.trust_coef = float(trust_coef)
 
     def step(self, lr: Optional[float] = None) -> None:
         self.t += 1
         self._run(_lib.lamb_hparams_init(
-            "lars", lr=self.lr if lr is None else float(lr), beta1=self.momentum,
+            "lars", lr=self._lr(lr), beta1=self.momentum,
             weight_decay=self.weight_decay, gamma_l=self.gamma_l, gamma_u=self.gamma_u,
             trust_coef=self.trust_coef, grad_scale=self.grad_scale))
 

@@ -631,8 +631,29 @@ def pin_skip_nonfinite(o):
     assert np.all(np.isfinite(out)) and not np.array_equal(xs[0], base_x[0])
 
 
+def pin_bf16_copy_rounding(o):
+    """The bf16 working copy is round-to-nearest-even of fp32 x, bit for bit
+    torch's own conversion: random values, exact ties (both parities),
+    subnormals, +-inf, the largest finite fp32 (rounds to inf), NaN."""
+    import torch
+    rng = np.random.default_rng(54)
+    vals = [rng.standard_normal(4000).astype(np.float32) * 10.0 ** rng.uniform(-30, 30, 4000)]
+    base = rng.integers(0, 1 << 15, size=200).astype(np.uint32) << 16
+    ties = (base | 0x8000).view(np.float32)                     # halfway: round to even
+    near = (base | 0x7FFF).view(np.float32)
+    above = (base | 0x8001).view(np.float32)
+    special = np.array([0.0, -0.0, 1e-45, -1e-40, np.inf, -np.inf, 3.4028235e38, -3.4028235e38,
+                        1.0, 1.00390625, 1.01171875], dtype=np.float32)
+    x = np.concatenate(vals + [ties, near, above, special]).astype(np.float32)
+    ours = o.round_bf16(x)
+    ref = torch.from_numpy(x).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(ours, ref)
+    nan = o.round_bf16(np.array([np.nan, -np.nan], dtype=np.float32))
+    assert np.all(nan == 0x7FC0)
+
+
 NLAMB_PINS = [pin_nlamb_constant_gradient, pin_nnlamb_lookahead]
-EXTENSION_PINS = [pin_grad_scale, pin_other_norms, pin_skip_nonfinite]
+EXTENSION_PINS = [pin_grad_scale, pin_other_norms, pin_skip_nonfinite, pin_bf16_copy_rounding]
 LARS_PINS = [pin_lars_normalized_sgd, pin_lars_constant_gradient, pin_lars_weight_decay,
              pin_lars_step_length]
 ALL_PINS = LAMB_PINS + NLAMB_PINS + EXTENSION_PINS + LARS_PINS

@@ -182,3 +182,82 @@ def test_step_ex_validation():
     finally:
         lamb.close()
         lars.close()
+
+
+def _bf16_bits(t):
+    import torch
+    return t.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+
+
+@pytest.mark.parametrize("algo,skip,g_dtype", [("lamb", 0, "bf16"), ("nn-lamb", 0, "f32"),
+                                               ("lars", 1, "bf16"), ("lamb", 1, "f32")])
+def test_bf16_copies(algo, skip, g_dtype):
+    """The apply pass writes bf16(x_{t+1}): bit for bit torch's cast of the
+    GPU's own x, within one bf16 ulp of the oracle's rounding of the oracle's
+    x; a tensor without a copy is unaffected; x, m, v still match the oracle."""
+    torch = H.torch_cuda()
+    rng = np.random.default_rng(11)
+    sizes = [1, 3, 8, 255, 513, 1029, 4097, 70000]
+    xs = [(rng.standard_normal(n) * 0.5).astype(np.float32) for n in sizes]
+    pair = _pair(xs, [i % 2 == 0 for i in range(len(sizes))], g_dtype, algo, 256)
+    copies = [torch.full((n,), 12345, dtype=torch.int16, device="cuda").view(torch.bfloat16)
+              for n in sizes]
+    copies[2] = None
+    _lib.lamb_plan_set_bf16_copies(pair.plan, [c.data_ptr() if c is not None else 0
+                                               for c in copies])
+    try:
+        for t in range(1, 4):
+            hg = pair.set_grads(_grads(rng, pair.X, g_dtype))
+            ref = H.step_ex_both(pair, _hp(algo, step=t, skip_nonfinite=skip), hg)
+            pair.compare(ref, "bf16 copy %s step %d" % (algo, t))
+            for i, c in enumerate(copies):
+                if c is None:
+                    continue
+                got = _bf16_bits(c)
+                assert np.array_equal(got, _bf16_bits(pair.X[i].to(torch.bfloat16)))
+                want = pair.oracle.round_bf16(pair.hx[i])
+                assert np.all(np.abs(got.astype(np.int32) - want.astype(np.int32)) <= 1)
+    finally:
+        pair.close()
+
+
+def test_bf16_copy_guard_bands_and_detach():
+    torch = H.torch_cuda()
+    rng = np.random.default_rng(12)
+    sizes = [5, 1000, 33]
+    xs = [(rng.standard_normal(n)).astype(np.float32) for n in sizes]
+    pair = _pair(xs, [True] * 3, "f32", "lamb", 64)
+    gap = 64
+    buf = torch.full((sum(sizes) + gap * 4,), -3, dtype=torch.int16, device="cuda")
+    views, off = [], gap
+    for n in sizes:
+        views.append(buf[off:off + n].view(torch.bfloat16))
+        off = (off + n + gap + 7) // 8 * 8
+    mask = torch.ones(buf.numel(), dtype=torch.bool, device="cuda")
+    for v in views:
+        k = (v.data_ptr() - buf.data_ptr()) // 2
+        mask[k:k + v.numel()] = False
+    before = buf.clone()
+    try:
+        _lib.lamb_plan_set_bf16_copies(pair.plan, [v.data_ptr() for v in views])
+        pair.set_grads(_grads(rng, pair.X, "f32"))
+        H.step_ex_both(pair, _hp("lamb", step=1), [paramsets.host_array(g) for g in pair.G])
+        torch.cuda.synchronize()
+        assert torch.equal(buf[mask], before[mask])
+        assert not torch.equal(buf[~mask], before[~mask])
+        _lib.lamb_plan_set_bf16_copies(pair.plan, None)
+        snap = buf.clone()
+        H.step_ex_both(pair, _hp("lamb", step=2), [paramsets.host_array(g) for g in pair.G])
+        torch.cuda.synchronize()
+        assert torch.equal(buf, snap)
+        with pytest.raises(_lib.LambError) as e:  # misaligned
+            _lib.lamb_plan_set_bf16_copies(pair.plan, [views[0].data_ptr() + 2, 0, 0])
+        assert e.value.status == _lib.LAMB_EALIGN
+        with pytest.raises(_lib.LambError) as e:  # copy over x
+            _lib.lamb_plan_set_bf16_copies(pair.plan, [pair.X[1].data_ptr(), 0, 0])
+        assert e.value.status == _lib.LAMB_EOVERLAP
+        with pytest.raises(_lib.LambError) as e:  # two copies share memory
+            _lib.lamb_plan_set_bf16_copies(pair.plan, [views[1].data_ptr(), views[1].data_ptr(), 0])
+        assert e.value.status == _lib.LAMB_EOVERLAP
+    finally:
+        pair.close()

@@ -157,3 +157,24 @@ def test_facade_matches_oracle():
                 H.compare_state(paramsets.host_array(xs[i]), hx[i], "facade x")
             H.compare_ratios(opt.ratios.cpu().numpy(), ref[:, 0], "facade ratio")
         opt.close()
+
+
+def test_facade_schedule_sets_each_steps_lr():
+    """A facade step with a schedule equals a plain step given that lr."""
+    torch = H.torch_cuda()
+    from paper_1904_00962_amd.optim import LAMB
+    ps = paramsets.get(0)
+    stages = [(5, 2, 1e-2, 1.0), (4, 1, 5e-3, 1.0)]
+    xs = paramsets.draw_params(ps, device="cuda")
+    grads = [torch.zeros(x.numel(), device="cuda") for x in xs]
+    a = LAMB([x.clone() for x in xs], grads, wd_mask=ps.wd_mask(), schedule=stages)
+    b = LAMB([x.clone() for x in xs], grads, wd_mask=ps.wd_mask())
+    for t in range(1, 10):
+        for g, d in zip(grads, paramsets.draw_grads(ps, t, device="cuda")):
+            g.copy_(d)
+        a.step()
+        b.step(lr=_lib.lamb_lr_at(stages, t))
+    torch.cuda.synchronize()
+    assert all(torch.equal(p, q) for p, q in zip(a.params, b.params))
+    a.close()
+    b.close()

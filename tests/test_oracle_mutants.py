@@ -97,6 +97,10 @@ MUTANTS = [
      "return sqrt(acc);", 0),
     ("finite_check_in_double", "float p = gj * s;", "double p = (double)gj * 10.0 * (double)s / 10.0;", 0),
     ("finite_check_ignores_nan", "if (!isfinite(p))", "if (isinf(p))", 0),
+    ("bf16_round_half_up", "if (low > 0x8000u || (low == 0x8000u && (high & 1u)))",
+     "if (low >= 0x8000u)", 0),
+    ("bf16_truncate", "            high += 1u;", "            high += 0u;", 0),
+    ("bf16_nan_payload", "            out[j] = 0x7fc0;", "            out[j] = 0x7f80;", 0),
     ("lars_zero_norm_not_guarded", "(norm_m == 0.0)\n                       ? 0.0\n                       :", "", 0),
 ]
 
