@@ -29,6 +29,7 @@ METRIC = "LAMB step: params updated/sec + achieved HBM GB/s (% peak), BERT-Large
 HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, published
 PROFILES = os.path.join(ROOT, "profiles")
 NLAMB_BETA1, NLAMB_EPS = 0.975, 1e-8  # N-LAMB / NN-LAMB settings (Appendix D)
+TIMING_EVERY = 4  # kernel-level events on one timed step in four
 
 
 def eprint(*a):
@@ -58,9 +59,11 @@ def algo_label(algo: str) -> str:
 
 
 def kernel_source_hash() -> str:
+    """Hash of what the kernels' machine code depends on: the kernel source,
+    the layout header it shares with the host side, and the compile flags."""
     from paper_1904_00962_amd import build as hb
     h = hashlib.sha256()
-    for p in hb.SOURCES + hb.HEADERS:
+    for p in (os.path.join(hb.CSRC, "lamb_kernels.hip"), os.path.join(hb.CSRC, "lamb_internal.h")):
         with open(p, "rb") as f:
             h.update(f.read())
     h.update(" ".join(hb.HIPCC_FLAGS).encode())
@@ -226,7 +229,8 @@ def main() -> int:
     for _ in range(args.warmup):
         opt.step()
     torch.cuda.synchronize()
-    _lib.lamb_plan_set_timing(opt.plan, args.steps)
+    # HIP events around the three kernels of every TIMING_EVERY-th timed step
+    _lib.lamb_plan_set_timing(opt.plan, args.steps, TIMING_EVERY)
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     start.record()
@@ -295,7 +299,8 @@ def main() -> int:
         "hbm_GBps": step_gbps,
         "hbm_frac_of_peak": step_gbps / HBM_PEAK_GBPS,
         "bytes_per_param": b_mom + b_app,
-        "kernels_ms": {"moments": avg_mom, "finalize": avg_fin, "apply": avg_app},
+        "kernels_ms": {"moments": avg_mom, "finalize": avg_fin, "apply": avg_app,
+                       "steps_sampled": recorded},
         "roofline": {
             "bound": "hbm", "kernel": kernel, "achieved": mom_gbps, "peak": HBM_PEAK_GBPS,
             "unit": "GB/s", "frac": mom_gbps / HBM_PEAK_GBPS, "traffic": traffic,

@@ -285,11 +285,14 @@ LAMB_API lamb_status lamb_chunk_table(const int64_t *numel, int32_t n_tensors,
 
 /*
  * Per-kernel timing with HIP events, for measurement. max_steps > 0 creates
- * event pairs for that many steps and makes each later step record them
- * around its three kernels on the step's stream; 0 turns timing off and
- * frees the events. A step beyond max_steps records nothing.
+ * events for that many recorded steps; from then on one step in `every`
+ * (the first, then every `every`-th) records events around its three
+ * kernels on the step's stream, until max_steps steps are recorded. Each
+ * recorded step costs a few microseconds of event processing, which
+ * sampling (every > 1) spreads thin. max_steps = 0 turns timing off and
+ * frees the events. Errors: LAMB_ENULL, LAMB_EINVAL, LAMB_EHIP.
  */
-LAMB_API lamb_status lamb_plan_set_timing(lamb_plan *plan, int32_t max_steps);
+LAMB_API lamb_status lamb_plan_set_timing(lamb_plan *plan, int32_t max_steps, int32_t every);
 
 /*
  * Synchronise on the recorded events and return the summed durations in

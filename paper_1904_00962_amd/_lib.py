@@ -112,7 +112,7 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
     lib.lamb_step_ex.argtypes = [vp, P(lamb_hparams), vp, vp, vp, vp]
     lib.lars_step.argtypes = [vp, f32, f32, f32, f32, f32, f32, vp, vp, vp]
     lib.lamb_chunk_table.argtypes = [P(i64), i32, i32, i32, P(i32), P(i64), P(i32), P(i32)]
-    lib.lamb_plan_set_timing.argtypes = [vp, i32]
+    lib.lamb_plan_set_timing.argtypes = [vp, i32, i32]
     lib.lamb_plan_timing.argtypes = [vp, P(ctypes.c_double), P(i64)]
     lib.lamb_status_str.argtypes = [i32]
     lib.lamb_status_str.restype = ctypes.c_char_p
@@ -287,8 +287,9 @@ def lamb_sqrt_scaled_lr(base_lr: float, base_batch: int, batch: int) -> float:
     return out.value
 
 
-def lamb_plan_set_timing(plan: Plan, max_steps: int) -> None:
-    _check(load().lamb_plan_set_timing(_vp(plan.handle), int(max_steps)), "lamb_plan_set_timing")
+def lamb_plan_set_timing(plan: Plan, max_steps: int, every: int = 1) -> None:
+    _check(load().lamb_plan_set_timing(_vp(plan.handle), int(max_steps), int(every)),
+           "lamb_plan_set_timing")
 
 
 def lamb_plan_timing(plan: Plan) -> Tuple[Tuple[float, float, float], int]:

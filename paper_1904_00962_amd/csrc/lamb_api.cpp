@@ -41,6 +41,9 @@ struct lamb_plan {
     std::vector<hipEvent_t> events;
     int32_t timing_capacity = 0;
     int32_t timing_used = 0;
+    int32_t timing_every = 1;      // record one step in timing_every
+    int64_t timing_seen = 0;       // steps enqueued since timing was enabled
+    bool timing_this_step = false;
 };
 
 namespace {
@@ -114,9 +117,22 @@ lamb_status check_phi_bounds(float gamma_l, float gamma_u) {
     return LAMB_OK;
 }
 
+// Timing hooks: begin_timing decides whether this step is recorded.
+void begin_timing(lamb_plan *plan) {
+    plan->timing_this_step = plan->timing_used < plan->timing_capacity &&
+                             plan->timing_seen % plan->timing_every == 0;
+    ++plan->timing_seen;
+}
+
 void record(lamb_plan *plan, int slot, hipStream_t stream) {
-    if (plan->timing_used < plan->timing_capacity)
+    if (plan->timing_this_step)
         (void)hipEventRecord(plan->events[size_t(plan->timing_used) * 4 + slot], stream);
+}
+
+void end_timing(lamb_plan *plan) {
+    if (plan->timing_this_step)
+        ++plan->timing_used;
+    plan->timing_this_step = false;
 }
 
 // The chunk table of `numel` at `chunk` elements per chunk (lamb_chunk_table).
@@ -129,6 +145,8 @@ void release_events(lamb_plan *plan) {
     plan->events.clear();
     plan->timing_capacity = 0;
     plan->timing_used = 0;
+    plan->timing_every = 1;
+    plan->timing_seen = 0;
 }
 
 }  // namespace
@@ -550,6 +568,7 @@ lamb_status lamb_step_ex(lamb_plan *plan, const lamb_hparams *hp, void *stream,
     if (guard.status != hipSuccess)
         return fail_hip(guard.status, "selecting the plan's device");
     hipStream_t s = static_cast<hipStream_t>(stream);
+    begin_timing(plan);
     record(plan, 0, s);
     // Deferred moment passes only read, and use the coarse chunk table.
     const ChunkDesc *moment_chunks = kind.deferred ? plan->coarse_chunks : plan->chunks;
@@ -569,8 +588,7 @@ lamb_status lamb_step_ex(lamb_plan *plan, const lamb_hparams *hp, void *stream,
     if (err != hipSuccess)
         return fail_hip(err, "launching the apply kernel");
     record(plan, 3, s);
-    if (plan->timing_used < plan->timing_capacity)
-        ++plan->timing_used;
+    end_timing(plan);
     if (kind.deferred)
         ++plan->deferred_steps;
     return LAMB_OK;
@@ -699,11 +717,13 @@ lamb_status lamb_sqrt_scaled_lr(double base_lr, int64_t base_batch, int64_t batc
     return LAMB_OK;
 }
 
-lamb_status lamb_plan_set_timing(lamb_plan *plan, int32_t max_steps) {
+lamb_status lamb_plan_set_timing(lamb_plan *plan, int32_t max_steps, int32_t every) {
     if (!plan)
         return fail(LAMB_ENULL, "plan must not be NULL");
     if (max_steps < 0 || max_steps > (1 << 20))
         return fail(LAMB_EINVAL, "max_steps = %d outside [0, 2^20]", max_steps);
+    if (every < 1)
+        return fail(LAMB_EINVAL, "every = %d, need >= 1", every);
     DeviceGuard guard(plan->device);
     if (guard.status != hipSuccess)
         return fail_hip(guard.status, "selecting the plan's device");
@@ -721,6 +741,8 @@ lamb_status lamb_plan_set_timing(lamb_plan *plan, int32_t max_steps) {
     }
     plan->timing_capacity = max_steps;
     plan->timing_used = 0;
+    plan->timing_every = every;
+    plan->timing_seen = 0;
     return LAMB_OK;
 }
 

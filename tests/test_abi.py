@@ -150,6 +150,6 @@ def test_null_plan_and_outputs(lib):
                           None) == _lib.LAMB_ENULL
     assert lib.lamb_plan_destroy(None) == _lib.LAMB_OK
     assert lib.lamb_plan_info(None, None, None, None) == _lib.LAMB_ENULL
-    assert lib.lamb_plan_set_timing(None, 4) == _lib.LAMB_ENULL
+    assert lib.lamb_plan_set_timing(None, 4, 1) == _lib.LAMB_ENULL
     assert lib.lamb_plan_set_bf16_copies(None, None) == _lib.LAMB_ENULL
     assert lib.lamb_plan_create(None, 1, 0, 0, 0, None) == _lib.LAMB_ENULL

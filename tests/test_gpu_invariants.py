@@ -119,6 +119,13 @@ def test_timing_hooks_record_each_kernel():
     assert steps == 5 and all(v > 0 for v in ms)
     ms2, steps2 = _lib.lamb_plan_timing(pair.plan)
     assert steps2 == 0
+    _lib.lamb_plan_set_timing(pair.plan, 3, 4)  # steps 1, 5, 9 of the next 12
+    for t in range(6, 18):
+        pair.gpu_lamb(H.lamb_hp(ps), t)
+    ms, steps = _lib.lamb_plan_timing(pair.plan)
+    assert steps == 3 and all(v > 0 for v in ms)
+    with pytest.raises(_lib.LambError):
+        _lib.lamb_plan_set_timing(pair.plan, 3, 0)
     _lib.lamb_plan_set_timing(pair.plan, 0)
     pair.close()
 
