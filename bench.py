@@ -176,6 +176,9 @@ def main() -> int:
                     help="deferred-write mode that skips steps with NaN/Inf gradients")
     ap.add_argument("--bf16-copy", action="store_true",
                     help="the apply pass also writes a bf16 copy of x")
+    ap.add_argument("--shard", type=int, default=1,
+                    help="time one rank's share of a step sharded N ways: the first 1/N slice "
+                         "of every tensor (the kernels at that rank's real shape)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", action="store_true")
@@ -204,6 +207,15 @@ def main() -> int:
                                                           ps.g_dtype))
     xs = paramsets.draw_params(ps, device="cuda")
     grads = paramsets.draw_grads(ps, 1, device="cuda")
+    if args.shard > 1:
+        # rank 0's slice of each tensor's flat range: ceil(n / N) rounded up
+        # to a multiple of 4 elements, so every rank's slice starts 16-byte aligned
+        def share(n):
+            per_rank = -(-n // args.shard)          # ceil(n / N)
+            return min(n, (per_rank + 3) // 4 * 4)
+        lens = [share(x.numel()) for x in xs]
+        xs = [x[:k] for x, k in zip(xs, lens)]
+        grads = [g[:k] for g, k in zip(grads, lens)]
     extra = dict(norm=args.norm, grad_scale=args.grad_scale, skip_nonfinite=args.skip_nonfinite,
                  wd_mask=ps.wd_mask(), chunk_elems=args.chunk)
     if args.algo == "lamb":
@@ -252,7 +264,7 @@ def main() -> int:
         eprint("cpu baseline: %.3e params/s (%s)" % (cpu["value"], cpu["sample"]))
 
     ms_step = total_ms / args.steps
-    P = ps.numel
+    P = sum(x.numel() for x in xs)
     g_bytes = 2 if ps.g_dtype == "bf16" else 4
     b_mom, b_app = bytes_per_param(args.algo, g_bytes, args.skip_nonfinite)
     b_app += 2 if args.bf16_copy else 0  # the bf16 working copy of x
@@ -262,7 +274,7 @@ def main() -> int:
     mom_gbps = b_mom * P / avg_mom / 1e6
     app_gbps = b_app * P / avg_app / 1e6
     step_gbps = (b_mom + b_app) * P / ms_step / 1e6
-    workload = ps.name
+    workload = ps.name if args.shard == 1 else "%s-shard-1of%d" % (ps.name, args.shard)
     src_hash = kernel_source_hash()
     default_mode = (args.algo == "lamb" and args.norm == "l2" and not args.skip_nonfinite
                     and not args.bf16_copy)
@@ -293,7 +305,7 @@ def main() -> int:
             "chunk_elems": chunk, "chunks": n_chunks, "norm": args.norm,
             "grad_scale": args.grad_scale, "skip_nonfinite": args.skip_nonfinite,
             "bf16_copy": args.bf16_copy,
-            "seed_x": 1000 * ps.cfg,
+            "shard": args.shard, "seed_x": 1000 * ps.cfg,
             "seed_g": 1000 * ps.cfg + 1,
         },
         "hbm_GBps": step_gbps,

@@ -224,3 +224,43 @@ def test_validation_leaves_state_untouched():
     finally:
         pair.close()
         lars.close()
+
+
+def test_tensor_beyond_int32_elements():
+    """One tensor of 2^31 + 1029 elements (8 GiB per fp32 array), so chunk
+    starts pass 2^31. With constant x = c and g = a, every u_j equals the
+    same value, so ||x|| = |c| sqrt(d), ||u|| = |u| sqrt(d) and the step is
+    x - lr * phi / sqrt(d) * sign(u) for every element; each element of x,
+    m, v is checked against that closed form (Algorithm 2), which also
+    shows every element was updated exactly once."""
+    torch = H.torch_cuda()
+    d = (1 << 31) + 1029
+    c, a = 0.02, 1e-3
+    lr, b1, b2, eps, lam = 6e-3, 0.9, 0.999, 1e-6, 0.01
+    H.log("int64 tensor: %d elements" % d)
+    x = torch.full((d,), c, dtype=torch.float32, device="cuda")
+    g = torch.full((d,), a, dtype=torch.bfloat16, device="cuda")
+    m = torch.zeros_like(x)
+    v = torch.zeros_like(x)
+    ratio = torch.zeros(1, dtype=torch.float64, device="cuda")
+    norms = torch.zeros(2, dtype=torch.float64, device="cuda")
+    rows = [(x.data_ptr(), g.data_ptr(), m.data_ptr(), v.data_ptr(), d, 1)]
+    with _lib.lamb_plan_create(rows, _lib.LAMB_GRAD_BF16, _lib.LAMB_ALGO_LAMB, 0) as plan:
+        _lib.lamb_step(plan, lr, b1, b2, eps, lam, 0.0, 10.0, 1, True,
+                       torch.cuda.current_stream().cuda_stream, ratio.data_ptr(), norms.data_ptr())
+        torch.cuda.synchronize()
+    f = lambda z: float(np.float32(z))  # noqa: E731  (scalars as the ABI receives them)
+    X, G = f(c), float(torch.tensor(a, dtype=torch.bfloat16).float())
+    M, V = (1 - f(b1)) * G, (1 - f(b2)) * G * G          # step 1 from zero moments
+    u = (M / (1 - f(b1))) / (np.sqrt(V / (1 - f(b2))) + f(eps)) + f(lam) * X
+    phi = min(abs(X) * np.sqrt(d), 10.0)
+    want_ratio = phi / (abs(u) * np.sqrt(d))
+    assert abs(float(ratio) - want_ratio) <= 1e-6 * want_ratio
+    assert abs(float(norms[0]) - abs(X) * np.sqrt(d)) <= 1e-9 * abs(X) * np.sqrt(d)
+    want_x = X - f(lr) * want_ratio * u
+    for name, t, want in (("x", x, want_x), ("m", m, M), ("v", v, V)):
+        lo, hi = float(t.min()), float(t.max())
+        assert abs(lo - want) <= 1e-6 * abs(want) and abs(hi - want) <= 1e-6 * abs(want), \
+            (name, lo, hi, want)
+    del x, g, m, v
+    torch.cuda.empty_cache()
