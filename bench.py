@@ -7,7 +7,8 @@ in HBM before timing starts. Prints ONE JSON line on stdout; diagnostics go
 to stderr.
 
   python bench.py [--steps K] [--warmup W] [--config 2] [--algo lamb|lars]
-                  [--chunk ELEMS] [--cpu-seconds S | --no-cpu-baseline]
+                  [--path auto|two-pass] [--chunk ELEMS]
+                  [--cpu-seconds S | --no-cpu-baseline]
   python bench.py --copy-probe      # plain copy of known size (counter scale)
 """
 
@@ -54,6 +55,13 @@ def bytes_per_param(algo: str, g_bytes: int, deferred: bool = False):
     return moment_reads + state, 4 + state + 4 + (g_bytes if needs_g else 0)
 
 
+def single_pass_bytes(algo: str, g_bytes: int) -> int:
+    """Algorithmic HBM bytes per parameter of the single-pass kernel: x, g and
+    the moments read once, the moments and x written once."""
+    state = 8 if algo != "lars" else 4
+    return 4 + g_bytes + state + state + 4
+
+
 def algo_label(algo: str) -> str:
     return {"lamb": "LAMB", "lars": "LARS", "nlamb": "N-LAMB", "nnlamb": "NN-LAMB"}[algo]
 
@@ -70,10 +78,11 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def counter_traffic(workload: str, src_hash: str):
-    """HBM bytes per launch of the moment kernel from the committed rocprofv3
-    counter summary for this workload, or None if absent or stale."""
-    path = os.path.join(PROFILES, "lamb_moments_%s_traffic.md" % workload)
+def counter_traffic(kernel: str, workload: str, src_hash: str):
+    """HBM bytes per launch of `kernel` ("moments" or "single_pass") from the
+    committed rocprofv3 counter summary for this workload, or None if absent
+    or stale."""
+    path = os.path.join(PROFILES, "lamb_%s_%s_traffic.md" % (kernel, workload))
     if not os.path.exists(path):
         return None
     text = open(path).read()
@@ -169,6 +178,8 @@ def main() -> int:
     ap.add_argument("--config", type=int, default=2)
     ap.add_argument("--algo", choices=("lamb", "lars", "nlamb", "nnlamb"), default="lamb")
     ap.add_argument("--chunk", type=int, default=0, help="elements per chunk (0 = default)")
+    ap.add_argument("--path", choices=("auto", "two-pass"), default="auto",
+                    help="auto: layers of up to 8M elements take the single-pass kernel")
     ap.add_argument("--norm", choices=("l2", "l1", "linf"), default="l2",
                     help="layer norm (Appendix F)")
     ap.add_argument("--grad-scale", type=float, default=1.0)
@@ -217,7 +228,7 @@ def main() -> int:
         xs = [x[:k] for x, k in zip(xs, lens)]
         grads = [g[:k] for g, k in zip(grads, lens)]
     extra = dict(norm=args.norm, grad_scale=args.grad_scale, skip_nonfinite=args.skip_nonfinite,
-                 wd_mask=ps.wd_mask(), chunk_elems=args.chunk)
+                 wd_mask=ps.wd_mask(), chunk_elems=args.chunk, path=args.path)
     if args.algo == "lamb":
         opt = LAMB(xs, grads, lr=ps.lr, betas=(ps.beta1, ps.beta2), eps=ps.eps,
                    weight_decay=ps.weight_decay, clamp=(ps.gamma_l, ps.gamma_u), **extra)
@@ -232,6 +243,9 @@ def main() -> int:
     if args.bf16_copy:
         opt.attach_bf16_copies("allocate")
     n_tensors, n_chunks, chunk = _lib.lamb_plan_info(opt.plan)
+    tiles_per_tensor, n_tiles = _lib.lamb_plan_tiles(opt.plan)
+    single = args.path == "auto" and not args.skip_nonfinite
+    P_single = sum(x.numel() for x, k in zip(xs, tiles_per_tensor) if k) if single else 0
 
     # The oracle's sample is copied out before the GPU steps move x; the
     # oracle itself runs after the GPU timing, so the GPU is not left idle
@@ -241,7 +255,7 @@ def main() -> int:
     for _ in range(args.warmup):
         opt.step()
     torch.cuda.synchronize()
-    # HIP events around the three kernels of every TIMING_EVERY-th timed step
+    # HIP events around the kernels of every TIMING_EVERY-th timed step
     _lib.lamb_plan_set_timing(opt.plan, args.steps, TIMING_EVERY)
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -251,8 +265,9 @@ def main() -> int:
     end.record()
     torch.cuda.synchronize()
     total_ms = start.elapsed_time(end)
-    (k_mom, k_fin, k_app), recorded = _lib.lamb_plan_timing(opt.plan)
+    (k_mom, k_fin, k_app, k_one), recorded = _lib.lamb_plan_timing(opt.plan)
     _lib.lamb_plan_set_timing(opt.plan, 0)
+    opt.check()
     ratios = opt.ratios.cpu()
     if not torch.isfinite(ratios).all():
         eprint("non-finite trust ratio after the timed steps")
@@ -265,26 +280,41 @@ def main() -> int:
 
     ms_step = total_ms / args.steps
     P = sum(x.numel() for x in xs)
+    P_rest = P - P_single
     g_bytes = 2 if ps.g_dtype == "bf16" else 4
+    copy_bytes = 2 if args.bf16_copy else 0  # the bf16 working copy of x
     b_mom, b_app = bytes_per_param(args.algo, g_bytes, args.skip_nonfinite)
-    b_app += 2 if args.bf16_copy else 0  # the bf16 working copy of x
-    avg_mom = k_mom / recorded
-    avg_app = k_app / recorded
-    avg_fin = k_fin / recorded
-    mom_gbps = b_mom * P / avg_mom / 1e6
-    app_gbps = b_app * P / avg_app / 1e6
-    step_gbps = (b_mom + b_app) * P / ms_step / 1e6
+    b_app += copy_bytes
+    b_one = single_pass_bytes(args.algo, g_bytes) + copy_bytes
+    avg_mom, avg_fin, avg_app, avg_one = (k / recorded for k in (k_mom, k_fin, k_app, k_one))
+    gbps = lambda b, n, ms: b * n / ms / 1e6 if ms > 0 and n else 0.0  # noqa: E731
+    mom_gbps = gbps(b_mom, P_rest, avg_mom)
+    app_gbps = gbps(b_app, P_rest, avg_app)
+    one_gbps = gbps(b_one, P_single, avg_one)
+    step_bytes = b_one * P_single + (b_mom + b_app) * P_rest
+    step_gbps = step_bytes / ms_step / 1e6
     workload = ps.name if args.shard == 1 else "%s-shard-1of%d" % (ps.name, args.shard)
     src_hash = kernel_source_hash()
     default_mode = (args.algo == "lamb" and args.norm == "l2" and not args.skip_nonfinite
                     and not args.bf16_copy)
-    traffic = counter_traffic(workload, src_hash) if default_mode else None
     algo_name = algo_label(args.algo)
-    kernel = "moments_kernel<%s, %s, %s%s>" % (algo_label(args.algo), "bf16" if g_bytes == 2 else "f32",
-                                              args.norm, ", deferred" if args.skip_nonfinite else "")
-    eprint("step %.4f ms | moments %.4f ms (%.0f GB/s) | finalize %.4f ms | apply %.4f ms "
-           "(%.0f GB/s) | whole step %.0f GB/s" % (ms_step, avg_mom, mom_gbps, avg_fin, avg_app,
-                                                   app_gbps, step_gbps))
+    g_name = "bf16" if g_bytes == 2 else "f32"
+    # the roofline entry covers the kernel that takes the most time
+    if avg_one >= avg_mom:
+        dom = dict(kernel="fused_kernel<%s, %s, %s>" % (algo_name, g_name, args.norm),
+                   achieved=one_gbps, bytes_per_launch=b_one * P_single,
+                   traffic=counter_traffic("single_pass", workload, src_hash)
+                   if default_mode else None)
+    else:
+        dom = dict(kernel="moments_kernel<%s, %s, %s%s>" % (
+                       algo_name, g_name, args.norm, ", deferred" if args.skip_nonfinite else ""),
+                   achieved=mom_gbps, bytes_per_launch=b_mom * P_rest,
+                   traffic=counter_traffic("moments", workload, src_hash)
+                   if default_mode else None)
+    eprint("step %.4f ms | single pass %.4f ms (%.0f GB/s, %d params) | moments %.4f ms "
+           "(%.0f GB/s) | finalize %.4f ms | apply %.4f ms (%.0f GB/s, %d params) | whole step "
+           "%.0f GB/s" % (ms_step, avg_one, one_gbps, P_single, avg_mom, mom_gbps, avg_fin,
+                          avg_app, app_gbps, P_rest, step_gbps))
     line = {
         "metric": METRIC,
         "value": P / (ms_step / 1e3),
@@ -302,6 +332,7 @@ def main() -> int:
             "workload": "%s %s step: %d tensors, %d fp32 params, %s gradients"
                         % (workload, algo_name, n_tensors, P, ps.g_dtype),
             "algo": args.algo, "tensors": n_tensors, "params": P, "grad_dtype": ps.g_dtype,
+            "path": args.path, "single_pass_params": P_single, "single_pass_tiles": n_tiles,
             "chunk_elems": chunk, "chunks": n_chunks, "norm": args.norm,
             "grad_scale": args.grad_scale, "skip_nonfinite": args.skip_nonfinite,
             "bf16_copy": args.bf16_copy,
@@ -310,13 +341,14 @@ def main() -> int:
         },
         "hbm_GBps": step_gbps,
         "hbm_frac_of_peak": step_gbps / HBM_PEAK_GBPS,
-        "bytes_per_param": b_mom + b_app,
-        "kernels_ms": {"moments": avg_mom, "finalize": avg_fin, "apply": avg_app,
-                       "steps_sampled": recorded},
+        "bytes_per_param": step_bytes / P,
+        "kernels_ms": {"single_pass": avg_one, "moments": avg_mom, "finalize": avg_fin,
+                       "apply": avg_app, "steps_sampled": recorded},
         "roofline": {
-            "bound": "hbm", "kernel": kernel, "achieved": mom_gbps, "peak": HBM_PEAK_GBPS,
-            "unit": "GB/s", "frac": mom_gbps / HBM_PEAK_GBPS, "traffic": traffic,
-            "bytes_per_launch": b_mom * P, "kernel_source_hash": src_hash,
+            "bound": "hbm", "kernel": dom["kernel"], "achieved": dom["achieved"],
+            "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": dom["achieved"] / HBM_PEAK_GBPS,
+            "traffic": dom["traffic"], "bytes_per_launch": dom["bytes_per_launch"],
+            "kernel_source_hash": src_hash,
         },
         "cpu_baseline": cpu,
     }

@@ -20,8 +20,9 @@
  *    fails validation returns a negative lamb_status, launches nothing and
  *    changes no state. lamb_last_error() then describes the failure.
  *  - Step calls enqueue work on `stream` (a hipStream_t; NULL = the null
- *    stream) and return without synchronising, allocating or copying to the
- *    host. Device faults surface at the caller's next synchronisation.
+ *    stream) and return without synchronising, allocating (beyond one HIP
+ *    event per device, created by the first single-pass step) or copying to
+ *    the host. Device faults surface at the caller's next synchronisation.
  *  - One step may be in flight per plan (its partials buffer is reused);
  *    a plan is not thread-safe. Distinct plans are independent.
  *  - NaN and Inf in the inputs propagate by IEEE rules; nothing is masked.
@@ -50,7 +51,8 @@ typedef enum lamb_status {
     LAMB_EOVERLAP = -4, /* two tensor buffers of the table overlap            */
     LAMB_EHIP = -5,     /* a HIP runtime call failed                          */
     LAMB_ENOMEM = -6,   /* a host or device allocation failed                 */
-    LAMB_EPLAN = -7     /* the plan was built for the other algorithm         */
+    LAMB_EPLAN = -7,    /* the plan was built for the other algorithm         */
+    LAMB_ESYNC = -8     /* a single-pass step abandoned a wait (lamb_plan_check) */
 } lamb_status;
 
 typedef enum lamb_grad_dtype {
@@ -99,6 +101,35 @@ typedef enum lamb_norm {
     LAMB_NORM_L1 = 1,   /* sum |a|                                            */
     LAMB_NORM_LINF = 2  /* max |a| (a NaN element makes it NaN)               */
 } lamb_norm;
+
+/*
+ * How a plan's direct-mode steps (skip_nonfinite = 0) run.
+ *  LAMB_PATH_AUTO      (default) every layer of at most 4 * (compute units)
+ *                      tiles of 8192 elements (8M elements on MI355X) takes
+ *                      one single-pass kernel that reads x, g, m, v and
+ *                      writes x, m, v once: a persistent grid keeps each
+ *                      tile's x and update direction in registers while the
+ *                      layer's norms are combined. Larger layers take the
+ *                      two-pass kernels. Needs the device's full occupancy
+ *                      for the length of that kernel: the library runs the
+ *                      single-pass kernels of one process one at a time
+ *                      (a step on another stream than the previous one
+ *                      waits for it); steps of other processes on the same
+ *                      device, or replays of captured graphs that overlap
+ *                      another single-pass kernel, may stall until a wait
+ *                      gives up (lamb_plan_check).
+ *  LAMB_PATH_TWO_PASS  every layer takes the two-pass kernels: a moment pass
+ *                      that reads x, g, m, v and writes m, v; a per-layer
+ *                      finalize; an apply pass that reads x, m, v (and g for
+ *                      N-LAMB / NN-LAMB) and writes x.
+ * Deferred-mode steps (skip_nonfinite = 1) always take the two-pass kernels.
+ * Both paths give the same m and v bit for bit; the layer norms are summed
+ * in a different order, so ratios and x agree to rounding.
+ */
+typedef enum lamb_path {
+    LAMB_PATH_AUTO = 0,
+    LAMB_PATH_TWO_PASS = 1
+} lamb_path;
 
 /*
  * Hyperparameters of one step (lamb_step_ex). lamb_hparams_init fills the
@@ -187,6 +218,29 @@ LAMB_API lamb_status lamb_plan_set_bf16_copies(lamb_plan *plan, void *const *cop
 LAMB_API lamb_status lamb_plan_info(const lamb_plan *plan, int32_t *n_tensors,
                            int32_t *n_chunks, int32_t *chunk_elems);
 
+/* Select the plan's path (lamb_path) for later steps. Errors: LAMB_ENULL,
+ * LAMB_EINVAL. */
+LAMB_API lamb_status lamb_plan_set_path(lamb_plan *plan, int32_t path);
+
+/*
+ * The single-pass layout (host outputs; either may be NULL):
+ *   tiles_per_tensor  n_tensors entries: the layer's tile count, or 0 when
+ *                     the layer takes the two-pass kernels
+ *   n_tiles           total tiles of the single pass
+ * Errors: LAMB_ENULL (plan).
+ */
+LAMB_API lamb_status lamb_plan_tiles(const lamb_plan *plan, int32_t *tiles_per_tensor,
+                            int32_t *n_tiles);
+
+/*
+ * Wait for `stream` and report whether a single-pass step of the plan gave
+ * up a wait (a layer's tiles were not all resident within about a second).
+ * That step's state is then undefined and the plan's single pass does no
+ * further work: restore the state and build a new plan. Synchronises the
+ * stream. Errors: LAMB_ENULL, LAMB_EHIP, LAMB_ESYNC.
+ */
+LAMB_API lamb_status lamb_plan_check(lamb_plan *plan, void *stream);
+
 /*
  * Fill `hp` with the paper's defaults for `variant` (Section 4, Appendix H:
  * beta1 0.9, beta2 0.999, eps 1e-6, lambda 0.01; Appendix D for N-LAMB and
@@ -197,8 +251,10 @@ LAMB_API lamb_status lamb_plan_info(const lamb_plan *plan, int32_t *n_tensors,
 LAMB_API lamb_status lamb_hparams_init(lamb_hparams *hp, int32_t variant);
 
 /*
- * One step of any algorithm over every block of the plan: moment pass,
- * per-tensor finalize (norms, phi, trust ratio), apply pass.
+ * One step of any algorithm over every block of the plan: the single-pass
+ * kernel for the layers that take it (lamb_path), then for the other layers
+ * a moment pass, a per-tensor finalize (norms, phi, trust ratio) and an
+ * apply pass.
  *   hp             host, validated before any HIP call
  *   stream         hipStream_t (NULL = null stream)
  *   ratio_out      device, n_tensors doubles, or NULL
@@ -284,10 +340,38 @@ LAMB_API lamb_status lamb_chunk_table(const int64_t *numel, int32_t n_tensors,
                              int32_t *chunk_len, int32_t *n_chunks);
 
 /*
+ * The single-pass schedule a plan would use (host only, no HIP call). The
+ * single-pass kernel runs a persistent grid of `round` workgroups (4 per
+ * compute unit); workgroup w takes entries w, w + round, ..., so the entry
+ * list falls into rounds of `round` entries. A layer of at most `round`
+ * tiles of 8192 elements takes the single pass: its tiles are consecutive
+ * entries inside one round, tile j starting at element 8192 j. Layers are
+ * packed first-fit by decreasing tile count (ties in table order); the gap
+ * a full round leaves is filled with empty entries (tensor -1, length 0).
+ *   numel         host, n_tensors sizes (>= 1 each)
+ *   round         entries per round, >= 1
+ *   capacity      length of the three entry arrays (0 with NULL arrays to
+ *                 query the count)
+ *   entry_tensor  host, layer of each entry or -1
+ *   entry_start   host, first element of each entry
+ *   entry_len     host, elements of each entry (0 for an empty entry)
+ *   first_tile    host, n_tensors: the layer's first entry (0 if none)
+ *   tiles         host, n_tensors: the layer's tile count, 0 when it takes
+ *                 the two-pass kernels (more than `round` tiles)
+ *   n_entries     receives the length of the list
+ * Errors: LAMB_ENULL, LAMB_EINVAL (including capacity too small, in which
+ * case *n_entries, first_tile and tiles are still filled).
+ */
+LAMB_API lamb_status lamb_tile_schedule(const int64_t *numel, int32_t n_tensors, int32_t round,
+                               int32_t capacity, int32_t *entry_tensor, int64_t *entry_start,
+                               int32_t *entry_len, int32_t *first_tile, int32_t *tiles,
+                               int32_t *n_entries);
+
+/*
  * Per-kernel timing with HIP events, for measurement. max_steps > 0 creates
  * events for that many recorded steps; from then on one step in `every`
- * (the first, then every `every`-th) records events around its three
- * kernels on the step's stream, until max_steps steps are recorded. Each
+ * (the first, then every `every`-th) records events around its kernels on
+ * the step's stream, until max_steps steps are recorded. Each
  * recorded step costs a few microseconds of event processing, which
  * sampling (every > 1) spreads thin. max_steps = 0 turns timing off and
  * frees the events. Errors: LAMB_ENULL, LAMB_EINVAL, LAMB_EHIP.
@@ -296,9 +380,10 @@ LAMB_API lamb_status lamb_plan_set_timing(lamb_plan *plan, int32_t max_steps, in
 
 /*
  * Synchronise on the recorded events and return the summed durations in
- * milliseconds of the moment kernel, the finalize kernel and the apply
- * kernel (kernel_ms[0..2], host) over `steps` recorded steps (host); then
- * start a new recording window.
+ * milliseconds of the moment kernel, the finalize kernel, the apply kernel
+ * and the single-pass kernel (kernel_ms[0..3], host; 0 for a kernel the
+ * steps did not launch) over `steps` recorded steps (host); then start a
+ * new recording window.
  */
 LAMB_API lamb_status lamb_plan_timing(lamb_plan *plan, double *kernel_ms, int64_t *steps);
 

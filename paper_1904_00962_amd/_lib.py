@@ -27,6 +27,7 @@ LAMB_EOVERLAP = -4
 LAMB_EHIP = -5
 LAMB_ENOMEM = -6
 LAMB_EPLAN = -7
+LAMB_ESYNC = -8
 
 LAMB_GRAD_F32 = 0
 LAMB_GRAD_BF16 = 1
@@ -45,11 +46,16 @@ LAMB_NORM_L1 = 1
 LAMB_NORM_LINF = 2
 NORMS = {"l2": LAMB_NORM_L2, "l1": LAMB_NORM_L1, "linf": LAMB_NORM_LINF}
 
+LAMB_PATH_AUTO = 0
+LAMB_PATH_TWO_PASS = 1
+PATHS = {"auto": LAMB_PATH_AUTO, "two-pass": LAMB_PATH_TWO_PASS}
+
 # Every symbol the header declares (checked by the test suite).
 EXPORTS = ("lamb_plan_create", "lamb_plan_destroy", "lamb_plan_info",
            "lamb_plan_set_bf16_copies", "lamb_hparams_init",
            "lamb_step_ex", "lamb_step", "nlamb_step", "lars_step", "lamb_lr_at",
            "lamb_sqrt_scaled_lr", "lamb_chunk_table", "lamb_plan_set_timing", "lamb_plan_timing",
+           "lamb_plan_set_path", "lamb_plan_tiles", "lamb_plan_check", "lamb_tile_schedule",
            "lamb_status_str", "lamb_last_error")
 
 
@@ -114,6 +120,11 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
     lib.lamb_chunk_table.argtypes = [P(i64), i32, i32, i32, P(i32), P(i64), P(i32), P(i32)]
     lib.lamb_plan_set_timing.argtypes = [vp, i32, i32]
     lib.lamb_plan_timing.argtypes = [vp, P(ctypes.c_double), P(i64)]
+    lib.lamb_plan_set_path.argtypes = [vp, i32]
+    lib.lamb_plan_tiles.argtypes = [vp, P(i32), P(i32)]
+    lib.lamb_plan_check.argtypes = [vp, vp]
+    lib.lamb_tile_schedule.argtypes = [P(i64), i32, i32, i32, P(i32), P(i64), P(i32), P(i32),
+                                       P(i32), P(i32)]
     lib.lamb_status_str.argtypes = [i32]
     lib.lamb_status_str.restype = ctypes.c_char_p
     lib.lamb_last_error.argtypes = []
@@ -292,10 +303,51 @@ def lamb_plan_set_timing(plan: Plan, max_steps: int, every: int = 1) -> None:
            "lamb_plan_set_timing")
 
 
-def lamb_plan_timing(plan: Plan) -> Tuple[Tuple[float, float, float], int]:
-    """Summed (moments, finalize, apply) kernel milliseconds and the step count."""
-    ms = (ctypes.c_double * 3)()
+def lamb_plan_timing(plan: Plan) -> Tuple[Tuple[float, float, float, float], int]:
+    """Summed (moments, finalize, apply, single-pass) kernel milliseconds and
+    the step count."""
+    ms = (ctypes.c_double * 4)()
     steps = ctypes.c_int64()
     _check(load().lamb_plan_timing(_vp(plan.handle), ms, ctypes.byref(steps)),
            "lamb_plan_timing")
-    return (ms[0], ms[1], ms[2]), steps.value
+    return (ms[0], ms[1], ms[2], ms[3]), steps.value
+
+
+def lamb_plan_set_path(plan: Plan, path="auto") -> None:
+    """``path``: "auto" (single pass where a layer fits) or "two-pass"."""
+    code = PATHS[path] if isinstance(path, str) else int(path)
+    _check(load().lamb_plan_set_path(_vp(plan.handle), code), "lamb_plan_set_path")
+
+
+def lamb_plan_tiles(plan: Plan) -> Tuple[list, int]:
+    """(tiles per tensor, 0 for a two-pass layer; total single-pass tiles)."""
+    n = lamb_plan_info(plan)[0]
+    per = (ctypes.c_int32 * n)()
+    total = ctypes.c_int32()
+    _check(load().lamb_plan_tiles(_vp(plan.handle), per, ctypes.byref(total)), "lamb_plan_tiles")
+    return list(per), total.value
+
+
+def lamb_tile_schedule(numel: Sequence[int], round: int):
+    """The single-pass schedule (host only): (entry_tensor, entry_start,
+    entry_len, first_tile, tiles) as lists; entry_tensor -1 marks an empty
+    entry."""
+    n = len(numel)
+    arr = (ctypes.c_int64 * n)(*[int(v) for v in numel])
+    first = (ctypes.c_int32 * n)()
+    tiles = (ctypes.c_int32 * n)()
+    count = ctypes.c_int32()
+    lib = load()
+    _check(lib.lamb_tile_schedule(arr, n, int(round), 0, None, None, None, first, tiles,
+                                  ctypes.byref(count)), "lamb_tile_schedule")
+    k = count.value
+    et, es, el = (ctypes.c_int32 * k)(), (ctypes.c_int64 * k)(), (ctypes.c_int32 * k)()
+    _check(lib.lamb_tile_schedule(arr, n, int(round), k, et, es, el, first, tiles,
+                                  ctypes.byref(count)), "lamb_tile_schedule")
+    return list(et), list(es), list(el), list(first), list(tiles)
+
+
+def lamb_plan_check(plan: Plan, stream: int = 0) -> None:
+    """Synchronise `stream`; raise LambError (LAMB_ESYNC) if a single-pass step
+    of the plan abandoned a wait."""
+    _check(load().lamb_plan_check(_vp(plan.handle), _vp(stream)), "lamb_plan_check")

@@ -11,6 +11,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <utility>
 #include <vector>
@@ -33,11 +34,25 @@ struct lamb_plan {
     ChunkDesc *coarse_chunks = nullptr;
     Partial *partials = nullptr;
     float *scale = nullptr;
-    uint32_t *flags = nullptr;     // two non-finite flags, alternating per deferred step
-    uint32_t deferred_steps = 0;   // deferred steps enqueued so far (selects the flag)
+    uint32_t *flags = nullptr;     // deferred mode: raised by the moment pass, verdict
+    // Single-pass path: the tiles of the layers that fit, and a second tensor
+    // and chunk table holding only the other layers (their two-pass work).
+    lamb_path path = LAMB_PATH_AUTO;
+    int32_t cu_count = 0;
+    int32_t round = 0;             // single-pass grid: workgroups per round of the tile list
+    int32_t n_tiles = 0;
+    int32_t n_rest = 0;            // layers outside the single pass
+    int32_t n_rest_chunks = 0;
+    ChunkDesc *tiles = nullptr;
+    uint64_t *slots = nullptr;     // 2 x 3 x n_tiles slot words
+    uint32_t *ctl = nullptr;       // FusedCtl words
+    TensorDesc *rest_tensors = nullptr;
+    ChunkDesc *rest_chunks = nullptr;
+    int fused_per_cu[4][2][3] = {};  // single-pass workgroups per CU by algo, bf16, norm
     std::vector<TensorDesc> host_tensors;  // host image of the tensor table
+    std::vector<TensorDesc> host_rest;     // host image of the other-layers table
     std::vector<std::pair<uintptr_t, uintptr_t>> ranges;  // sorted buffer ranges of the table
-    // timing hooks: 4 events per recorded step
+    // timing hooks: kEvents events per recorded step
     std::vector<hipEvent_t> events;
     int32_t timing_capacity = 0;
     int32_t timing_used = 0;
@@ -47,6 +62,8 @@ struct lamb_plan {
 };
 
 namespace {
+
+constexpr int kEvents = 5;  // before single pass, moments, finalize, apply, after
 
 thread_local char g_last_error[512] = "";
 
@@ -126,7 +143,57 @@ void begin_timing(lamb_plan *plan) {
 
 void record(lamb_plan *plan, int slot, hipStream_t stream) {
     if (plan->timing_this_step)
-        (void)hipEventRecord(plan->events[size_t(plan->timing_used) * 4 + slot], stream);
+        (void)hipEventRecord(plan->events[size_t(plan->timing_used) * kEvents + slot], stream);
+}
+
+// Single-pass launches of one process on one device run one at a time: each
+// persistent grid needs the whole device resident, and two such grids on
+// different streams could each hold part of it and wait on each other. A
+// launch on another stream than the previous one first waits for the
+// previous launch. Graph capture skips the gate (the replay order is the
+// caller's).
+struct FusedGate {
+    hipEvent_t done = nullptr;
+    hipStream_t stream = nullptr;
+    bool used = false;
+};
+std::mutex g_gate_mutex;
+std::vector<FusedGate> g_gates;  // by device; events live until the process ends
+
+hipError_t gated_fused_launch(int device, hipStream_t stream, const StepKind &kind,
+                              const lamb_plan *plan, int32_t grid, const StepArgs &a,
+                              const FinalizeArgs &f, double *ratio_out, double *norms_out) {
+    hipStreamCaptureStatus capture = hipStreamCaptureStatusNone;
+    hipError_t err = hipStreamIsCapturing(stream, &capture);
+    if (err != hipSuccess)
+        return err;
+    if (capture != hipStreamCaptureStatusNone)
+        return launch_fused(kind, plan->tensors, plan->tiles, plan->n_tiles, grid, plan->slots,
+                            plan->ctl, a, f, ratio_out, norms_out, stream);
+    std::lock_guard<std::mutex> lock(g_gate_mutex);
+    if (g_gates.size() <= size_t(device))
+        g_gates.resize(size_t(device) + 1);
+    FusedGate &gate = g_gates[size_t(device)];
+    if (!gate.done) {
+        err = hipEventCreateWithFlags(&gate.done, hipEventDisableTiming);
+        if (err != hipSuccess)
+            return err;
+    }
+    if (gate.used && gate.stream != stream) {
+        err = hipStreamWaitEvent(stream, gate.done, 0);
+        if (err != hipSuccess)
+            return err;
+    }
+    err = launch_fused(kind, plan->tensors, plan->tiles, plan->n_tiles, grid, plan->slots,
+                       plan->ctl, a, f, ratio_out, norms_out, stream);
+    if (err != hipSuccess)
+        return err;
+    err = hipEventRecord(gate.done, stream);
+    if (err != hipSuccess)
+        return err;
+    gate.stream = stream;
+    gate.used = true;
+    return hipSuccess;
 }
 
 void end_timing(lamb_plan *plan) {
@@ -163,6 +230,7 @@ const char *lamb_status_str(lamb_status status) {
     case LAMB_EHIP: return "HIP runtime error";
     case LAMB_ENOMEM: return "out of memory";
     case LAMB_EPLAN: return "plan built for the other algorithm";
+    case LAMB_ESYNC: return "a single-pass step abandoned a wait";
     }
     return "unknown status";
 }
@@ -202,6 +270,85 @@ lamb_status lamb_chunk_table(const int64_t *numel, int32_t n_tensors, int32_t ch
             chunk_start[k] = s;
             chunk_len[k] = int32_t(std::min<int64_t>(chunk, numel[i] - s));
             ++k;
+        }
+    }
+    return LAMB_OK;
+}
+
+lamb_status lamb_tile_schedule(const int64_t *numel, int32_t n_tensors, int32_t round,
+                               int32_t capacity, int32_t *entry_tensor, int64_t *entry_start,
+                               int32_t *entry_len, int32_t *first_tile, int32_t *tiles,
+                               int32_t *n_entries) {
+    if (!numel || !n_entries || !first_tile || !tiles)
+        return fail(LAMB_ENULL, "numel, first_tile, tiles and n_entries must not be NULL");
+    if (n_tensors < 1)
+        return fail(LAMB_EINVAL, "n_tensors = %d, need >= 1", n_tensors);
+    if (round < 1)
+        return fail(LAMB_EINVAL, "round = %d, need >= 1", round);
+    for (int32_t i = 0; i < n_tensors; ++i)
+        if (numel[i] < 1)
+            return fail(LAMB_EINVAL, "tensor %d has numel %lld, need >= 1", i,
+                        static_cast<long long>(numel[i]));
+    // Layers of at most `round` tiles, packed first-fit by decreasing tile
+    // count (ties in table order) into rounds of `round` entries.
+    std::vector<std::pair<int64_t, int32_t>> teams;
+    for (int32_t i = 0; i < n_tensors; ++i) {
+        const int64_t nt = (numel[i] + kTileElems - 1) / kTileElems;
+        first_tile[i] = 0;
+        tiles[i] = 0;
+        if (nt <= round)
+            teams.emplace_back(nt, i);
+    }
+    std::stable_sort(teams.begin(), teams.end(),
+                     [](const std::pair<int64_t, int32_t> &a, const std::pair<int64_t, int32_t> &b) {
+                         return a.first > b.first;
+                     });
+    std::vector<int64_t> fill;
+    std::vector<std::vector<int32_t>> members;
+    for (const auto &team : teams) {
+        size_t r = 0;
+        while (r < fill.size() && fill[r] + team.first > round)
+            ++r;
+        if (r == fill.size()) {
+            fill.push_back(0);
+            members.emplace_back();
+        }
+        fill[r] += team.first;
+        members[r].push_back(team.second);
+    }
+    const int64_t total =
+        fill.empty() ? 0 : int64_t(round) * int64_t(fill.size() - 1) + fill.back();
+    if (total > INT32_MAX / 8)
+        return fail(LAMB_EINVAL, "too many single-pass tiles");
+    *n_entries = int32_t(total);
+    const bool write = capacity != 0 || entry_tensor || entry_start || entry_len;
+    if (write && capacity < total)
+        return fail(LAMB_EINVAL, "capacity %d < %lld entries", capacity,
+                    static_cast<long long>(total));
+    if (write && (!entry_tensor || !entry_start || !entry_len))
+        return fail(LAMB_ENULL, "entry output arrays must not be NULL");
+    int32_t k = 0;
+    for (size_t r = 0; r < fill.size(); ++r) {
+        for (int32_t i : members[r]) {
+            const int64_t nt = (numel[i] + kTileElems - 1) / kTileElems;
+            first_tile[i] = k;
+            tiles[i] = int32_t(nt);
+            for (int64_t j = 0; j < nt; ++j, ++k) {
+                if (!write)
+                    continue;
+                entry_tensor[k] = i;
+                entry_start[k] = j * kTileElems;
+                entry_len[k] = int32_t(std::min<int64_t>(kTileElems, numel[i] - j * kTileElems));
+            }
+        }
+        if (r + 1 < fill.size()) {
+            for (int64_t j = fill[r]; j < round; ++j, ++k) {
+                if (!write)
+                    continue;
+                entry_tensor[k] = -1;
+                entry_start[k] = 0;
+                entry_len[k] = 0;
+            }
         }
     }
     return LAMB_OK;
@@ -310,28 +457,73 @@ lamb_status lamb_plan_create(const lamb_tensor *tensors, int32_t n_tensors,
         st = build_chunks(numel, coarse, n_coarse, &host_coarse);
     if (st != LAMB_OK)
         return st;
+    int device = 0, cu_count = 0;
+    hipError_t err = hipGetDevice(&device);
+    if (err == hipSuccess)
+        err = hipDeviceGetAttribute(&cu_count, hipDeviceAttributeMultiprocessorCount, device);
+    if (err != hipSuccess)
+        return fail_hip(err, "querying the current device");
+    // Single-pass schedule (lamb_tile_schedule): rounds of one tile per
+    // workgroup of the persistent grid, which keeps kFusedBlocksPerCu
+    // workgroups on every CU.
+    const int32_t round = int32_t(std::max<int64_t>(1, int64_t(kFusedBlocksPerCu) * cu_count));
+    std::vector<int32_t> first_tile(static_cast<size_t>(n_tensors)),
+        tile_count(static_cast<size_t>(n_tensors));
+    int32_t n_entries = 0;
+    st = lamb_tile_schedule(numel.data(), n_tensors, round, 0, nullptr, nullptr, nullptr,
+                            first_tile.data(), tile_count.data(), &n_entries);
+    std::vector<int32_t> entry_tensor(static_cast<size_t>(n_entries)),
+        entry_len(static_cast<size_t>(n_entries));
+    std::vector<int64_t> entry_start(static_cast<size_t>(n_entries));
+    if (st == LAMB_OK)
+        st = lamb_tile_schedule(numel.data(), n_tensors, round, n_entries, entry_tensor.data(),
+                                entry_start.data(), entry_len.data(), first_tile.data(),
+                                tile_count.data(), &n_entries);
+    if (st != LAMB_OK)
+        return st;
+    std::vector<ChunkDesc> host_tiles(static_cast<size_t>(n_entries));
+    for (int32_t k = 0; k < n_entries; ++k)
+        host_tiles[size_t(k)] =
+            ChunkDesc{entry_tensor[size_t(k)], entry_len[size_t(k)], entry_start[size_t(k)]};
+    std::vector<TensorDesc> host_rest;
+    std::vector<ChunkDesc> host_rest_chunks;
     {
         int32_t first = 0, first_coarse = 0;
         for (int32_t i = 0; i < n_tensors; ++i) {
             const lamb_tensor &t = tensors[i];
             const int32_t nc = int32_t((t.numel + chunk - 1) / chunk);
             const int32_t ncc = int32_t((t.numel + coarse - 1) / coarse);
-            host_tensors[size_t(i)] = TensorDesc{t.x, t.g, t.m, needs_v ? t.v : nullptr, nullptr,
-                                                 t.numel, t.wd, first, nc, first_coarse, ncc, 0,
-                                                 0};
+            TensorDesc d{t.x,          t.g,          t.m,   needs_v ? t.v : nullptr,
+                         nullptr,      t.numel,      t.wd,  first,
+                         nc,           first_coarse, ncc,   first_tile[size_t(i)],
+                         tile_count[size_t(i)], i};
+            if (d.n_tiles == 0) {
+                TensorDesc r = d;
+                r.first_chunk = int32_t(host_rest_chunks.size());
+                r.first_coarse = r.n_coarse = 0;
+                const int32_t ri = int32_t(host_rest.size());
+                for (int32_t k = 0; k < nc; ++k) {
+                    ChunkDesc c = host_chunks[size_t(first + k)];
+                    c.tensor = ri;
+                    host_rest_chunks.push_back(c);
+                }
+                host_rest.push_back(r);
+            }
+            host_tensors[size_t(i)] = d;
             first += nc;
             first_coarse += ncc;
         }
     }
+    const int32_t n_tiles = int32_t(host_tiles.size());
+    const int32_t n_rest = int32_t(host_rest.size());
+    const int32_t n_rest_chunks = int32_t(host_rest_chunks.size());
 
     lamb_plan *plan = new (std::nothrow) lamb_plan();
     if (!plan)
         return fail(LAMB_ENOMEM, "host allocation of the plan failed");
-    hipError_t err = hipGetDevice(&plan->device);
-    if (err != hipSuccess) {
-        delete plan;
-        return fail_hip(err, "hipGetDevice");
-    }
+    plan->device = device;
+    plan->cu_count = cu_count;
+    plan->round = round;
     auto round256 = [](size_t b) { return (b + 255) & ~size_t(255); };
     const size_t tensors_bytes = round256(sizeof(TensorDesc) * size_t(n_tensors));
     const size_t chunks_bytes = round256(sizeof(ChunkDesc) * size_t(n_chunks));
@@ -339,8 +531,15 @@ lamb_status lamb_plan_create(const lamb_tensor *tensors, int32_t n_tensors,
     const size_t partial_bytes = round256(sizeof(Partial) * size_t(n_chunks));
     const size_t scale_bytes = round256(sizeof(float) * size_t(n_tensors));
     const size_t flag_bytes = 256;
+    const size_t tiles_bytes = round256(sizeof(ChunkDesc) * size_t(n_tiles));
+    const size_t slot_bytes = round256(sizeof(uint64_t) * 6 * size_t(n_tiles));
+    const size_t ctl_bytes = 256;
+    const size_t rest_bytes = round256(sizeof(TensorDesc) * size_t(n_rest));
+    const size_t rest_chunk_bytes = round256(sizeof(ChunkDesc) * size_t(n_rest_chunks));
     err = hipMalloc(&plan->device_block, tensors_bytes + chunks_bytes + coarse_bytes +
-                                             partial_bytes + scale_bytes + flag_bytes);
+                                             partial_bytes + scale_bytes + flag_bytes +
+                                             tiles_bytes + slot_bytes + ctl_bytes + rest_bytes +
+                                             rest_chunk_bytes);
     if (err != hipSuccess) {
         delete plan;
         if (err == hipErrorOutOfMemory)
@@ -359,6 +558,16 @@ lamb_status lamb_plan_create(const lamb_tensor *tensors, int32_t n_tensors,
     plan->scale = reinterpret_cast<float *>(base);
     base += scale_bytes;
     plan->flags = reinterpret_cast<uint32_t *>(base);
+    base += flag_bytes;
+    plan->tiles = reinterpret_cast<ChunkDesc *>(base);
+    base += tiles_bytes;
+    plan->slots = reinterpret_cast<uint64_t *>(base);
+    base += slot_bytes;
+    plan->ctl = reinterpret_cast<uint32_t *>(base);
+    base += ctl_bytes;
+    plan->rest_tensors = reinterpret_cast<TensorDesc *>(base);
+    base += rest_bytes;
+    plan->rest_chunks = reinterpret_cast<ChunkDesc *>(base);
     err = hipMemcpy(plan->tensors, host_tensors.data(), sizeof(TensorDesc) * size_t(n_tensors),
                     hipMemcpyHostToDevice);
     if (err == hipSuccess)
@@ -367,19 +576,61 @@ lamb_status lamb_plan_create(const lamb_tensor *tensors, int32_t n_tensors,
     if (err == hipSuccess)
         err = hipMemcpy(plan->coarse_chunks, host_coarse.data(),
                         sizeof(ChunkDesc) * size_t(n_coarse), hipMemcpyHostToDevice);
+    if (err == hipSuccess && n_tiles > 0)
+        err = hipMemcpy(plan->tiles, host_tiles.data(), sizeof(ChunkDesc) * size_t(n_tiles),
+                        hipMemcpyHostToDevice);
+    if (err == hipSuccess && n_rest > 0)
+        err = hipMemcpy(plan->rest_tensors, host_rest.data(), sizeof(TensorDesc) * size_t(n_rest),
+                        hipMemcpyHostToDevice);
+    if (err == hipSuccess && n_rest > 0)
+        err = hipMemcpy(plan->rest_chunks, host_rest_chunks.data(),
+                        sizeof(ChunkDesc) * size_t(n_rest_chunks), hipMemcpyHostToDevice);
     if (err == hipSuccess)
         err = hipMemset(plan->flags, 0, flag_bytes);
+    if (err == hipSuccess && slot_bytes > 0)
+        err = hipMemset(plan->slots, 0xff, slot_bytes);  // every slot kEmptySlot
+    if (err == hipSuccess)
+        err = hipMemset(plan->ctl, 0, ctl_bytes);
+    if (err == hipSuccess)
+        err = hipDeviceSynchronize();
     if (err != hipSuccess) {
         (void)hipFree(plan->device_block);
         delete plan;
         return fail_hip(err, "hipMemcpy of plan tables");
+    }
+    // Occupancy of every single-pass kernel a step of this plan may pick, so
+    // that a step makes no HIP query (it may be under graph capture).
+    if (n_tiles > 0) {
+        const Algo algos[3] = {kLamb, kNLamb, kNNLamb};
+        const int n_algos = algo == LAMB_ALGO_LARS ? 1 : 3;
+        for (int ai = 0; ai < n_algos && err == hipSuccess; ++ai) {
+            for (int nk = 0; nk < 3 && err == hipSuccess; ++nk) {
+                StepKind kind;
+                kind.algo = algo == LAMB_ALGO_LARS ? kLars : algos[ai];
+                kind.norm = static_cast<NormKind>(nk);
+                kind.bf16_grad = g_dtype == LAMB_GRAD_BF16;
+                kind.deferred = false;
+                int per_cu = 0;
+                err = fused_blocks_per_cu(kind, &per_cu);
+                plan->fused_per_cu[int(kind.algo)][kind.bf16_grad ? 1 : 0][nk] = per_cu;
+            }
+        }
+        if (err != hipSuccess) {
+            (void)hipFree(plan->device_block);
+            delete plan;
+            return fail_hip(err, "occupancy of the single-pass kernel");
+        }
     }
     plan->algo = algo;
     plan->g_dtype = g_dtype;
     plan->n_tensors = n_tensors;
     plan->n_chunks = n_chunks;
     plan->n_coarse = n_coarse;
+    plan->n_tiles = n_tiles;
+    plan->n_rest = n_rest;
+    plan->n_rest_chunks = n_rest_chunks;
     plan->host_tensors = std::move(host_tensors);
+    plan->host_rest = std::move(host_rest);
     for (const Range &r : ranges)
         plan->ranges.emplace_back(r.lo, r.hi);
     plan->chunk_elems = chunk;
@@ -477,7 +728,6 @@ StepArgs step_args(const lamb_hparams &hp) {
     a.eps = hp.eps;
     a.weight_decay = hp.weight_decay;
     a.grad_scale = hp.grad_scale;
-    a.flag_slot = 0;
     const double b1 = hp.beta1, b2 = hp.beta2, t = double(hp.step);
     switch (hp.variant) {
     case LAMB_VARIANT_LAMB:
@@ -558,39 +808,68 @@ lamb_status lamb_step_ex(lamb_plan *plan, const lamb_hparams *hp, void *stream,
     kind.norm = static_cast<NormKind>(hp->norm);
     kind.bf16_grad = plan->g_dtype == LAMB_GRAD_BF16;
     kind.deferred = hp->skip_nonfinite != 0;
-    StepArgs a = step_args(*hp);
-    a.flag_slot = plan->deferred_steps & 1u;
+    const StepArgs a = step_args(*hp);
     const bool lars = hp->variant == LAMB_VARIANT_LARS;
     const FinalizeArgs f{double(hp->lr), double(hp->gamma_l), double(hp->gamma_u),
                          lars ? double(hp->trust_coef) : 1.0};
+    // The single pass serves direct-mode steps of the layers that fit; the
+    // two-pass kernels take the rest (or everything).
+    const bool single = plan->path == LAMB_PATH_AUTO && !kind.deferred && plan->n_tiles > 0;
 
     DeviceGuard guard(plan->device);
     if (guard.status != hipSuccess)
         return fail_hip(guard.status, "selecting the plan's device");
+    int32_t grid = 0;
+    if (single) {
+        const int per_cu =
+            plan->fused_per_cu[int(kind.algo)][kind.bf16_grad ? 1 : 0][int(kind.norm)];
+        // The tile list was packed in rounds of kFusedBlocksPerCu * CUs
+        // entries; the grid is one round, so it must all be resident at once.
+        if (per_cu < kFusedBlocksPerCu)
+            return fail(LAMB_EHIP, "single-pass kernel keeps %d workgroups per CU resident, needs %d",
+                        per_cu, kFusedBlocksPerCu);
+        grid = std::min(plan->n_tiles, plan->round);
+    }
     hipStream_t s = static_cast<hipStream_t>(stream);
     begin_timing(plan);
     record(plan, 0, s);
-    // Deferred moment passes only read, and use the coarse chunk table.
-    const ChunkDesc *moment_chunks = kind.deferred ? plan->coarse_chunks : plan->chunks;
-    const int32_t n_moment_chunks = kind.deferred ? plan->n_coarse : plan->n_chunks;
-    hipError_t err = launch_moments(kind, plan->tensors, moment_chunks, plan->partials,
-                                    n_moment_chunks, plan->flags, a, s);
-    if (err != hipSuccess)
-        return fail_hip(err, "launching the moment kernel");
+    if (single) {
+        hipError_t err = gated_fused_launch(plan->device, s, kind, plan, grid, a, f, ratio_out,
+                                            norms_out);
+        if (err != hipSuccess)
+            return fail_hip(err, "launching the single-pass kernel");
+    }
     record(plan, 1, s);
-    err = launch_finalize(kind.norm, kind.deferred, plan->tensors, plan->n_tensors,
-                          plan->partials, f, plan->scale, ratio_out, norms_out, s);
-    if (err != hipSuccess)
-        return fail_hip(err, "launching the finalize kernel");
-    record(plan, 2, s);
-    err = launch_apply(kind, plan->tensors, plan->chunks, plan->scale, plan->n_chunks,
-                       plan->flags, nonfinite_out, a, s);
-    if (err != hipSuccess)
-        return fail_hip(err, "launching the apply kernel");
-    record(plan, 3, s);
+    const bool two_pass = !single || plan->n_rest > 0;
+    const TensorDesc *tensors = single ? plan->rest_tensors : plan->tensors;
+    const int32_t n_tensors = single ? plan->n_rest : plan->n_tensors;
+    const ChunkDesc *chunks = single ? plan->rest_chunks : plan->chunks;
+    const int32_t n_chunks = single ? plan->n_rest_chunks : plan->n_chunks;
+    if (two_pass) {
+        // Deferred moment passes only read, and use the coarse chunk table.
+        const ChunkDesc *moment_chunks = kind.deferred ? plan->coarse_chunks : chunks;
+        const int32_t n_moment_chunks = kind.deferred ? plan->n_coarse : n_chunks;
+        hipError_t err = launch_moments(kind, tensors, moment_chunks, plan->partials,
+                                        n_moment_chunks, plan->flags, a, s);
+        if (err != hipSuccess)
+            return fail_hip(err, "launching the moment kernel");
+        record(plan, 2, s);
+        err = launch_finalize(kind.norm, kind.deferred, tensors, n_tensors, plan->partials, f,
+                              plan->scale, ratio_out, norms_out,
+                              kind.deferred ? plan->flags : nullptr, s);
+        if (err != hipSuccess)
+            return fail_hip(err, "launching the finalize kernel");
+        record(plan, 3, s);
+        err = launch_apply(kind, tensors, chunks, plan->scale, n_chunks, plan->flags,
+                           nonfinite_out, a, s);
+        if (err != hipSuccess)
+            return fail_hip(err, "launching the apply kernel");
+    } else {
+        record(plan, 2, s);
+        record(plan, 3, s);
+    }
+    record(plan, 4, s);
     end_timing(plan);
-    if (kind.deferred)
-        ++plan->deferred_steps;
     return LAMB_OK;
 }
 
@@ -667,14 +946,67 @@ lamb_status lamb_plan_set_bf16_copies(lamb_plan *plan, void *const *copies) {
     for (size_t k = 1; k < all.size(); ++k)
         if (all[k].first < all[k - 1].second)
             return fail(LAMB_EOVERLAP, "a bf16 copy overlaps another buffer of the plan");
+    std::vector<TensorDesc> next_rest = plan->host_rest;
+    for (TensorDesc &r : next_rest)
+        r.x_copy = next[size_t(r.out_index)].x_copy;
     DeviceGuard guard(plan->device);
     if (guard.status != hipSuccess)
         return fail_hip(guard.status, "selecting the plan's device");
     hipError_t err = hipMemcpy(plan->tensors, next.data(),
                                sizeof(TensorDesc) * size_t(plan->n_tensors), hipMemcpyHostToDevice);
+    if (err == hipSuccess && plan->n_rest > 0)
+        err = hipMemcpy(plan->rest_tensors, next_rest.data(),
+                        sizeof(TensorDesc) * size_t(plan->n_rest), hipMemcpyHostToDevice);
+    if (err == hipSuccess)
+        err = hipDeviceSynchronize();
     if (err != hipSuccess)
         return fail_hip(err, "hipMemcpy of the tensor table");
     plan->host_tensors = std::move(next);
+    plan->host_rest = std::move(next_rest);
+    return LAMB_OK;
+}
+
+lamb_status lamb_plan_set_path(lamb_plan *plan, int32_t path) {
+    if (!plan)
+        return fail(LAMB_ENULL, "plan must not be NULL");
+    if (path != LAMB_PATH_AUTO && path != LAMB_PATH_TWO_PASS)
+        return fail(LAMB_EINVAL, "unknown path %d", path);
+    plan->path = static_cast<lamb_path>(path);
+    return LAMB_OK;
+}
+
+lamb_status lamb_plan_tiles(const lamb_plan *plan, int32_t *tiles_per_tensor, int32_t *n_tiles) {
+    if (!plan)
+        return fail(LAMB_ENULL, "plan must not be NULL");
+    if (tiles_per_tensor)
+        for (int32_t i = 0; i < plan->n_tensors; ++i)
+            tiles_per_tensor[i] = plan->host_tensors[size_t(i)].n_tiles;
+    if (n_tiles)
+        *n_tiles = plan->n_tiles;
+    return LAMB_OK;
+}
+
+lamb_status lamb_plan_check(lamb_plan *plan, void *stream) {
+    if (!plan)
+        return fail(LAMB_ENULL, "plan must not be NULL");
+    DeviceGuard guard(plan->device);
+    if (guard.status != hipSuccess)
+        return fail_hip(guard.status, "selecting the plan's device");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    uint32_t *host = nullptr;
+    hipError_t err = hipHostMalloc(reinterpret_cast<void **>(&host), 4 * sizeof(uint32_t), 0);
+    if (err != hipSuccess)
+        return fail_hip(err, "hipHostMalloc");
+    err = hipMemcpyAsync(host, plan->ctl, 4 * sizeof(uint32_t), hipMemcpyDeviceToHost, s);
+    if (err == hipSuccess)
+        err = hipStreamSynchronize(s);
+    const uint32_t fault = host[kCtlFault];
+    (void)hipHostFree(host);
+    if (err != hipSuccess)
+        return fail_hip(err, "reading the plan's synchronisation words");
+    if (fault)
+        return fail(LAMB_ESYNC, "a single-pass step of this plan abandoned a wait; the plan's "
+                                "single pass is disabled and the state of that step is undefined");
     return LAMB_OK;
 }
 
@@ -730,7 +1062,7 @@ lamb_status lamb_plan_set_timing(lamb_plan *plan, int32_t max_steps, int32_t eve
     release_events(plan);
     if (max_steps == 0)
         return LAMB_OK;
-    plan->events.assign(size_t(max_steps) * 4, nullptr);
+    plan->events.assign(size_t(max_steps) * kEvents, nullptr);
     for (size_t k = 0; k < plan->events.size(); ++k) {
         hipError_t err = hipEventCreate(&plan->events[k]);
         if (err != hipSuccess) {
@@ -752,15 +1084,17 @@ lamb_status lamb_plan_timing(lamb_plan *plan, double *kernel_ms, int64_t *steps)
     DeviceGuard guard(plan->device);
     if (guard.status != hipSuccess)
         return fail_hip(guard.status, "selecting the plan's device");
-    kernel_ms[0] = kernel_ms[1] = kernel_ms[2] = 0.0;
+    kernel_ms[0] = kernel_ms[1] = kernel_ms[2] = kernel_ms[3] = 0.0;
+    // events: before the single pass, after it, after moments, finalize, apply
+    static const int kFrom[4] = {1, 2, 3, 0};
     for (int32_t k = 0; k < plan->timing_used; ++k) {
-        hipEvent_t *e = &plan->events[size_t(k) * 4];
-        hipError_t err = hipEventSynchronize(e[3]);
+        hipEvent_t *e = &plan->events[size_t(k) * kEvents];
+        hipError_t err = hipEventSynchronize(e[kEvents - 1]);
         if (err != hipSuccess)
             return fail_hip(err, "hipEventSynchronize");
-        for (int j = 0; j < 3; ++j) {
+        for (int j = 0; j < 4; ++j) {
             float ms = 0.0f;
-            err = hipEventElapsedTime(&ms, e[j], e[j + 1]);
+            err = hipEventElapsedTime(&ms, e[kFrom[j]], e[kFrom[j] + 1]);
             if (err != hipSuccess)
                 return fail_hip(err, "hipEventElapsedTime");
             kernel_ms[j] += ms;

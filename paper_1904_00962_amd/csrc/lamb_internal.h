@@ -26,6 +26,30 @@ constexpr int32_t kDefaultChunkElems = LAMB_DEFAULT_CHUNK;
 // and run faster with more work per workgroup).
 constexpr int32_t kCoarseFactor = 4;
 
+// Single-pass path: a layer is cut into tiles of kTileElems elements; one
+// workgroup keeps a tile's x (in LDS) and update direction (in registers,
+// kTileGroups float4 groups per thread) until the layer's step scale is
+// known. The persistent grid keeps kFusedBlocksPerCu workgroups on every CU,
+// so a layer of up to kFusedBlocksPerCu * (compute units) tiles can have
+// every tile resident at once.
+#ifndef LAMB_TILE_GROUPS
+#define LAMB_TILE_GROUPS 8
+#endif
+#ifndef LAMB_FUSED_WAVES
+#define LAMB_FUSED_WAVES 4
+#endif
+constexpr int kTileGroups = LAMB_TILE_GROUPS;
+constexpr int32_t kTileElems = kBlock * 4 * kTileGroups;
+constexpr int kFusedWaves = LAMB_FUSED_WAVES;
+constexpr int kFusedBlocksPerCu = kFusedWaves * 4 / kWaves;  // 4 SIMDs per CU
+
+// Synchronisation words of the single-pass path (per plan).
+enum FusedCtl : int {
+    kCtlEpoch = 0,  // single-pass steps completed; its low bit selects the slot buffer
+    kCtlDone = 1,   // workgroups of the running step that have finished
+    kCtlFault = 2,  // sticky: a wait ran out of time and the step was abandoned
+};
+
 // One layer block x^(i) (Section 2) as the kernels see it. 80 bytes.
 struct TensorDesc {
     float *x;
@@ -39,8 +63,9 @@ struct TensorDesc {
     int32_t n_chunks;
     int32_t first_coarse;  // coarse chunks [first_coarse, first_coarse + n_coarse)
     int32_t n_coarse;
-    int32_t pad0;
-    int64_t pad1;
+    int32_t first_tile;    // single-pass tiles [first_tile, first_tile + n_tiles);
+    int32_t n_tiles;       //   n_tiles = 0: the layer takes the two-pass path
+    int32_t out_index;     // the layer's index in ratio_out / norms_out
 };
 static_assert(sizeof(TensorDesc) == 80, "TensorDesc layout");
 
@@ -83,7 +108,6 @@ struct StepArgs {
     float eps;
     float weight_decay;
     float grad_scale;
-    uint32_t flag_slot;  // deferred mode: which of the plan's two flags this step uses
 };
 
 // Scalars of the per-tensor finalize (trust ratio and step scale).
@@ -103,19 +127,34 @@ struct StepKind {
 };
 
 // Kernel launchers (lamb_kernels.hip). Each returns the launch status.
-// `flags` points at the plan's two non-finite flags (deferred mode only);
-// `nonfinite_out` may be null.
+// `flags` points at the plan's two non-finite words (deferred mode only): the
+// moment pass raises flags[0], the finalize moves it to flags[1] and clears
+// flags[0], the apply pass reads flags[1]. Nothing depends on a host counter,
+// so a captured graph replays correctly. `nonfinite_out` may be null.
 hipError_t launch_moments(const StepKind &kind, const TensorDesc *tensors,
                           const ChunkDesc *chunks, Partial *partials, int32_t n_chunks,
                           uint32_t *flags, const StepArgs &args, hipStream_t stream);
 // `coarse`: the partials were written per coarse chunk (deferred mode).
 hipError_t launch_finalize(NormKind norm, bool coarse, const TensorDesc *tensors,
                            int32_t n_tensors, const Partial *partials, const FinalizeArgs &args,
-                           float *scale, double *ratio_out, double *norms_out,
+                           float *scale, double *ratio_out, double *norms_out, uint32_t *flags,
                            hipStream_t stream);
 hipError_t launch_apply(const StepKind &kind, const TensorDesc *tensors,
                         const ChunkDesc *chunks, const float *scale, int32_t n_chunks,
                         uint32_t *flags, int32_t *nonfinite_out, const StepArgs &args,
                         hipStream_t stream);
+
+// Single-pass kernel over the `n_tiles` tiles of the layers with n_tiles > 0,
+// on a persistent grid of `grid` workgroups. `slots` holds 2 x 3 x n_tiles
+// words (two buffers of partial norms and broadcast scales, alternating per
+// step by the epoch in `ctl`), all initialised to kEmptySlot; `ctl` holds the
+// FusedCtl words, initialised to 0.
+constexpr uint64_t kEmptySlot = ~uint64_t(0);
+hipError_t launch_fused(const StepKind &kind, const TensorDesc *tensors, const ChunkDesc *tiles,
+                        int32_t n_tiles, int32_t grid, uint64_t *slots, uint32_t *ctl,
+                        const StepArgs &args, const FinalizeArgs &fargs, double *ratio_out,
+                        double *norms_out, hipStream_t stream);
+// Workgroups of the single-pass kernel for `kind` that fit on one CU at once.
+hipError_t fused_blocks_per_cu(const StepKind &kind, int *blocks);
 
 }  // namespace lamb_mi355x

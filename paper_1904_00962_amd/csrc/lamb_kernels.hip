@@ -23,6 +23,11 @@
 //            too, unless the moment pass found a non-finite scaled gradient,
 //            in which case nothing changes.
 //
+// A layer small enough to sit in the registers of the resident workgroups
+// takes a single pass instead (fused_kernel below): each tile's x and u stay
+// in registers while the layer's partial norms meet, so x, g, m, v are read
+// and x, m, v written exactly once.
+//
 // Recomputing u instead of storing it saves 4 bytes per parameter of HBM
 // traffic. There are no float atomics: every reduction has a fixed order, so
 // a step is bitwise reproducible for a given chunk size. The vector loops
@@ -377,7 +382,7 @@ __global__ __launch_bounds__(kBlock) void moments_kernel(
     if constexpr (kDeferred) {
         // Rare event: one integer atomic per chunk that saw a bad gradient.
         if (__syncthreads_or(nonfinite) && threadIdx.x == 0)
-            atomicOr(flags + a.flag_slot, 1u);
+            atomicOr(flags, 1u);
     }
     block_combine<kNorm, kWaves>(sum_xx, sum_uu, partials + chunk_index());
 }
@@ -394,14 +399,11 @@ __global__ __launch_bounds__(kBlock) void apply_kernel(
     constexpr bool kV = kHasSecondMoment<kAlgo>;
     constexpr bool kReadsGrad = kDeferred || kDirectionNeedsGrad<kAlgo>;
     if constexpr (kDeferred) {
-        // The moment pass raised this step's flag if any scaled gradient was
-        // NaN or infinite; clear the other flag for the next deferred step.
-        const uint32_t bad = flags[a.flag_slot];
-        if (blockIdx.x == 0 && threadIdx.x == 0) {
-            flags[a.flag_slot ^ 1u] = 0u;
-            if (nonfinite_out)
-                *nonfinite_out = bad ? 1 : 0;
-        }
+        // The finalize moved the moment pass's verdict (raised if any scaled
+        // gradient was NaN or infinite) into flags[1].
+        const uint32_t bad = flags[1];
+        if (blockIdx.x == 0 && threadIdx.x == 0 && nonfinite_out)
+            *nonfinite_out = bad ? 1 : 0;
         if (bad)
             return;
     }
@@ -483,6 +485,30 @@ __global__ __launch_bounds__(kBlock) void apply_kernel(
     }
 }
 
+// One layer's norms, phi, trust ratio and step scale lr * ratio from its
+// combined partial norms; reports ratio and norms at index `out`.
+template <int kNorm>
+__device__ float finish_layer(const Partial &total, const FinalizeArgs &a, int32_t out,
+                              double *ratio_out, double *norms_out) {
+    const double norm_x = norm_finish<kNorm>(total.sum_xx);
+    const double norm_u = norm_finish<kNorm>(total.sum_uu);
+    // phi(z) = min(max(z, gamma_l), gamma_u), Section 3; comparisons keep NaN.
+    double phi = norm_x;
+    if (phi < a.gamma_l)
+        phi = a.gamma_l;
+    if (phi > a.gamma_u)
+        phi = a.gamma_u;
+    // A zero update norm means a zero update: report ratio 0, move nothing.
+    const double ratio = (norm_u == 0.0) ? 0.0 : a.trust_coef * phi / norm_u;
+    if (ratio_out)
+        ratio_out[out] = ratio;
+    if (norms_out) {
+        norms_out[2 * out] = norm_x;
+        norms_out[2 * out + 1] = norm_u;
+    }
+    return static_cast<float>(a.lr * ratio);
+}
+
 // ---------------------------------------------------------------------------
 // Per-tensor finalize: norms, phi, trust ratio, step scale. One workgroup of
 // kFinalizeBlock threads per tensor. Thread k owns slots k + j*kFinalizeBlock
@@ -498,7 +524,7 @@ template <int kNorm>
 __global__ __launch_bounds__(kFinalizeBlock) void finalize_kernel(
     const TensorDesc *__restrict__ tensors, const Partial *__restrict__ partials, int coarse,
     FinalizeArgs a, float *__restrict__ scale, double *__restrict__ ratio_out,
-    double *__restrict__ norms_out) {
+    double *__restrict__ norms_out, uint32_t *__restrict__ flags) {
     const int i = blockIdx.x;
     const TensorDesc &t = tensors[i];
     const Partial *p = partials + (coarse ? t.first_coarse : t.first_chunk);
@@ -530,22 +556,267 @@ __global__ __launch_bounds__(kFinalizeBlock) void finalize_kernel(
     block_combine<kNorm, kFinalizeBlock / 64>(sx[0], su[0], &total);
     __syncthreads();
     if (threadIdx.x == 0) {
-        const double norm_x = norm_finish<kNorm>(total.sum_xx);
-        const double norm_u = norm_finish<kNorm>(total.sum_uu);
-        // phi(z) = min(max(z, gamma_l), gamma_u), Section 3; comparisons keep NaN.
-        double phi = norm_x;
-        if (phi < a.gamma_l)
-            phi = a.gamma_l;
-        if (phi > a.gamma_u)
-            phi = a.gamma_u;
-        // A zero update norm means a zero update: report ratio 0, move nothing.
-        const double ratio = (norm_u == 0.0) ? 0.0 : a.trust_coef * phi / norm_u;
-        scale[i] = static_cast<float>(a.lr * ratio);
-        if (ratio_out)
-            ratio_out[i] = ratio;
-        if (norms_out) {
-            norms_out[2 * i] = norm_x;
-            norms_out[2 * i + 1] = norm_u;
+        scale[i] = finish_layer<kNorm>(total, a, t.out_index, ratio_out, norms_out);
+        // Deferred mode: hand the moment pass's non-finite verdict to the apply
+        // pass and clear the word the next moment pass raises.
+        if (flags && i == 0) {
+            flags[1] = flags[0];
+            flags[0] = 0u;
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Single-pass path.
+//
+// A persistent grid of `grid` workgroups, all resident at once, walks the
+// tile list: workgroup w takes entries w, w + grid, w + 2 grid, ..., so the
+// list falls into rounds of `grid` entries. The host packs every layer's
+// tiles consecutively inside one round (empty entries pad a round's gap). For
+// each tile a workgroup reads x, g, m, v once, writes the new moments at
+// once, and keeps x in LDS and u in registers. The tile's partial norms go
+// to a slot; the layer's first tile (its leader) waits for every slot of the
+// layer, combines them in tile order, forms the step scale exactly as the
+// finalize kernel does and writes it to each member's broadcast slot; every
+// member then writes x - scale * u. A workgroup only waits after publishing
+// its own slot, and a layer's members sit in one round on distinct
+// workgroups that reach it once their earlier rounds are done, so by
+// induction over rounds every wait ends.
+//
+// Slots are 64-bit words read and written with agent-scope atomics, which
+// are coherent across the XCDs' separate L2 caches. An empty slot holds
+// kEmptySlot, which no published value equals. Two slot buffers alternate by
+// the epoch word: a step fills buffer (epoch & 1) and empties the other for
+// the next step; the last workgroup to finish advances the epoch. Nothing
+// depends on a host counter, so a captured graph replays correctly.
+// Every wait is bounded: after kSpinLimit polls, or once another workgroup
+// has given up, a workgroup raises the sticky fault word and abandons the
+// step, and every later step of the plan does nothing.
+// ---------------------------------------------------------------------------
+
+constexpr uint32_t kSpinLimit = 1u << 22;
+static_assert(kTileGroups % kUnroll == 0, "tile groups must be a multiple of the unroll");
+
+__device__ __forceinline__ uint64_t slot_load(const uint64_t *p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ void slot_store(uint64_t *p, uint64_t w) {
+    __hip_atomic_store(p, w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ uint32_t ctl_load(const uint32_t *p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// A partial norm as a slot word. Partial norms are >= 0, +inf or NaN; every
+// NaN is stored as the positive quiet NaN, so no value is kEmptySlot.
+__device__ __forceinline__ uint64_t slot_word(double d) {
+    return isnan(d) ? 0x7ff8000000000000ull : static_cast<uint64_t>(__double_as_longlong(d));
+}
+
+// Polls *p until it holds a value; kEmptySlot if the wait was abandoned.
+__device__ uint64_t slot_wait(const uint64_t *p, uint32_t *ctl) {
+    for (uint32_t k = 1;; ++k) {
+        const uint64_t w = slot_load(p);
+        if (w != kEmptySlot)
+            return w;
+        if ((k & 255u) == 0) {
+            if (ctl_load(ctl + kCtlFault) != 0)
+                return kEmptySlot;
+            if (k >= kSpinLimit) {
+                __hip_atomic_fetch_or(ctl + kCtlFault, 1u, __ATOMIC_RELAXED,
+                                      __HIP_MEMORY_SCOPE_AGENT);
+                return kEmptySlot;
+            }
+        }
+        __builtin_amdgcn_s_sleep(2);
+    }
+}
+
+template <int kAlgo, bool kBf16, int kNorm>
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(kFusedWaves)))
+void fused_kernel(const TensorDesc *__restrict__ tensors, const ChunkDesc *__restrict__ tiles,
+                  int32_t n_tiles, uint64_t *__restrict__ slots, uint32_t *__restrict__ ctl,
+                  StepArgs a, FinalizeArgs f, double *__restrict__ ratio_out,
+                  double *__restrict__ norms_out) {
+    constexpr bool kV = kHasSecondMoment<kAlgo>;
+    __shared__ uint32_t sh_epoch, sh_fault;
+    __shared__ float sh_scale;
+    __shared__ Partial sh_tile, sh_layer;
+    // The tile's x waits in LDS (32 KB), its update direction in registers.
+    __shared__ f32x4 sh_x[kTileGroups][kBlock];
+    if (threadIdx.x == 0) {
+        sh_epoch = ctl_load(ctl + kCtlEpoch);
+        sh_fault = ctl_load(ctl + kCtlFault);
+    }
+    __syncthreads();
+    const uint32_t epoch = sh_epoch;
+    const size_t n = static_cast<size_t>(n_tiles);
+    // per buffer: partial ||x|| words, partial ||u|| words, broadcast scales
+    uint64_t *cur = slots + size_t(epoch & 1u) * 3 * n;
+    uint64_t *next = slots + size_t((epoch & 1u) ^ 1u) * 3 * n;
+    bool stop = sh_fault != 0;
+
+    for (int32_t j = blockIdx.x; !stop && j < n_tiles; j += gridDim.x) {
+        const ChunkDesc c = tiles[j];
+        if (c.len == 0)
+            continue;  // an empty entry that pads a round
+        const TensorDesc &t = tensors[c.tensor];
+        gfloat *x = global_view(t.x + c.start);
+        gfloat *m = global_view(t.m + c.start);
+        gfloat *v = kV ? global_view(t.v + c.start) : nullptr;
+        const GradView<kBf16> g(t.g, c.start, a.grad_scale);
+        const float lam = t.wd ? a.weight_decay : 0.0f;
+        const int n4 = c.len >> 2;
+
+        // Read once, write the new moments, keep x and u.
+        f32x4 us[kTileGroups];
+        double sum_xx = 0.0, sum_uu = 0.0;
+#pragma unroll
+        for (int k0 = 0; k0 < kTileGroups; k0 += kUnroll) {
+            f32x4 xr[kUnroll], gr[kUnroll], mr[kUnroll], vr[kUnroll];
+#pragma unroll
+            for (int k = 0; k < kUnroll; ++k) {
+                const int q = (k0 + k) * kBlock + threadIdx.x;
+                xr[k] = gr[k] = mr[k] = vr[k] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+                if (q < n4) {
+                    xr[k] = load4(x + 4 * q);
+                    gr[k] = g.at4(4 * q);
+                    mr[k] = load4(m + 4 * q);
+                    if constexpr (kV)
+                        vr[k] = load4(v + 4 * q);
+                }
+            }
+#pragma unroll
+            for (int k = 0; k < kUnroll; ++k) {
+                const int q = (k0 + k) * kBlock + threadIdx.x;
+                f32x4 ur = {0.0f, 0.0f, 0.0f, 0.0f};
+                if (q < n4) {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        float me = mr[k][e], ve = vr[k][e];
+                        new_moments<kAlgo>(xr[k][e], gr[k][e], lam, me, ve, a);
+                        ur[e] = direction<kAlgo>(xr[k][e], gr[k][e], me, ve, lam, a);
+                        sum_xx = norm_add<kNorm>(sum_xx, xr[k][e]);
+                        sum_uu = norm_add<kNorm>(sum_uu, ur[e]);
+                        mr[k][e] = me;
+                        vr[k][e] = ve;
+                    }
+                    store4(m + 4 * q, mr[k]);
+                    if constexpr (kV)
+                        store4(v + 4 * q, vr[k]);
+                }
+                sh_x[k0 + k][threadIdx.x] = xr[k];
+                us[k0 + k] = ur;
+            }
+        }
+        const int tail = 4 * n4 + threadIdx.x;
+        float x_tail = 0.0f, u_tail = 0.0f;
+        if (tail < c.len) {
+            x_tail = x[tail];
+            const float gj = g.at(tail);
+            float mj = m[tail];
+            float vj = kV ? v[tail] : 0.0f;
+            new_moments<kAlgo>(x_tail, gj, lam, mj, vj, a);
+            u_tail = direction<kAlgo>(x_tail, gj, mj, vj, lam, a);
+            sum_xx = norm_add<kNorm>(sum_xx, x_tail);
+            sum_uu = norm_add<kNorm>(sum_uu, u_tail);
+            m[tail] = mj;
+            if constexpr (kV)
+                v[tail] = vj;
+        }
+        block_combine<kNorm, kWaves>(sum_xx, sum_uu, &sh_tile);
+        __syncthreads();
+
+        // The layer's step scale.
+        const int32_t first = t.first_tile, team = t.n_tiles;
+        int give_up = 0;
+        if (team == 1) {
+            if (threadIdx.x == 0)
+                sh_scale = finish_layer<kNorm>(sh_tile, f, t.out_index, ratio_out, norms_out);
+        } else {
+            if (threadIdx.x == 0) {
+                slot_store(cur + j, slot_word(sh_tile.sum_xx));
+                slot_store(cur + n + j, slot_word(sh_tile.sum_uu));
+                slot_store(next + j, kEmptySlot);
+                slot_store(next + n + j, kEmptySlot);
+                slot_store(next + 2 * n + j, kEmptySlot);
+            }
+            if (j == first) {
+                double ax = 0.0, au = 0.0;
+                for (int k = threadIdx.x; k < team; k += kBlock) {
+                    const uint64_t wx = slot_wait(cur + first + k, ctl);
+                    const uint64_t wu =
+                        wx == kEmptySlot ? kEmptySlot : slot_wait(cur + n + first + k, ctl);
+                    if (wu == kEmptySlot) {
+                        give_up = 1;
+                        break;
+                    }
+                    ax = norm_combine<kNorm>(ax, __longlong_as_double(static_cast<long long>(wx)));
+                    au = norm_combine<kNorm>(au, __longlong_as_double(static_cast<long long>(wu)));
+                }
+                block_combine<kNorm, kWaves>(ax, au, &sh_layer);
+                give_up = __syncthreads_or(give_up);
+                if (!give_up) {
+                    if (threadIdx.x == 0)
+                        sh_scale = finish_layer<kNorm>(sh_layer, f, t.out_index, ratio_out,
+                                                       norms_out);
+                    __syncthreads();
+                    const uint64_t w = __float_as_uint(sh_scale);
+                    for (int k = threadIdx.x + 1; k < team; k += kBlock)
+                        slot_store(cur + 2 * n + first + k, w);
+                }
+            } else if (threadIdx.x == 0) {
+                const uint64_t w = slot_wait(cur + 2 * n + j, ctl);
+                if (w == kEmptySlot)
+                    give_up = 1;
+                else
+                    sh_scale = __uint_as_float(static_cast<uint32_t>(w));
+            }
+        }
+        stop = __syncthreads_or(give_up) != 0;
+        if (stop)
+            break;
+
+        // x - scale * u from the registers.
+        const float s = sh_scale;
+        gbf16 *copy = t.x_copy ? (gbf16 *)(t.x_copy + c.start) : nullptr;
+#pragma unroll
+        for (int k = 0; k < kTileGroups; ++k) {
+            const int q = k * kBlock + threadIdx.x;
+            if (q < n4) {
+                const f32x4 xo = sh_x[k][threadIdx.x];
+                f32x4 xn;
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    xn[e] = fmaf(-s, us[k][e], xo[e]);
+                store4(x + 4 * q, xn);
+                if (copy) {
+                    const u32x2 packed = {bf16_bits(xn[0]) | (bf16_bits(xn[1]) << 16),
+                                          bf16_bits(xn[2]) | (bf16_bits(xn[3]) << 16)};
+                    stream_store((LAMB_GLOBAL u32x2 *)(copy + 4 * q), packed);
+                }
+            }
+        }
+        if (tail < c.len) {
+            const float xn = fmaf(-s, u_tail, x_tail);
+            x[tail] = xn;
+            if (copy)
+                copy[tail] = uint16_t(bf16_bits(xn));
+        }
+    }
+
+    // The last workgroup to finish advances the epoch. Every workgroup read
+    // the epoch before any of its work, so none can still be reading it.
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        const uint32_t done =
+            __hip_atomic_fetch_add(ctl + kCtlDone, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (done == gridDim.x - 1) {
+            __hip_atomic_store(ctl + kCtlDone, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(ctl + kCtlEpoch, epoch + 1u, __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
         }
     }
 }
@@ -583,6 +854,29 @@ const void *apply_fn(const StepKind &k) {
                           : reinterpret_cast<const void *>(&apply_kernel<kAlgo, true, false>);
     return k.deferred ? reinterpret_cast<const void *>(&apply_kernel<kAlgo, false, true>)
                       : reinterpret_cast<const void *>(&apply_kernel<kAlgo, false, false>);
+}
+
+template <int kAlgo, bool kBf16>
+const void *fused_fn(int norm) {
+    switch (norm) {
+    case kL1: return reinterpret_cast<const void *>(&fused_kernel<kAlgo, kBf16, kL1>);
+    case kLinf: return reinterpret_cast<const void *>(&fused_kernel<kAlgo, kBf16, kLinf>);
+    default: return reinterpret_cast<const void *>(&fused_kernel<kAlgo, kBf16, kL2>);
+    }
+}
+
+template <int kAlgo>
+const void *fused_fn(const StepKind &k) {
+    return k.bf16_grad ? fused_fn<kAlgo, true>(k.norm) : fused_fn<kAlgo, false>(k.norm);
+}
+
+const void *fused_fn(const StepKind &k) {
+    switch (k.algo) {
+    case kNLamb: return fused_fn<kNLamb>(k);
+    case kNNLamb: return fused_fn<kNNLamb>(k);
+    case kLars: return fused_fn<kLars>(k);
+    default: return fused_fn<kLamb>(k);
+    }
 }
 
 }  // namespace
@@ -624,15 +918,30 @@ hipError_t launch_apply(const StepKind &kind, const TensorDesc *tensors,
 
 hipError_t launch_finalize(NormKind norm, bool coarse, const TensorDesc *tensors,
                            int32_t n_tensors, const Partial *partials, const FinalizeArgs &args,
-                           float *scale, double *ratio_out, double *norms_out,
+                           float *scale, double *ratio_out, double *norms_out, uint32_t *flags,
                            hipStream_t stream) {
     FinalizeArgs a = args;
     int coarse_flag = coarse ? 1 : 0;
-    void *params[] = {&tensors, &partials, &coarse_flag, &a, &scale, &ratio_out, &norms_out};
+    void *params[] = {&tensors, &partials, &coarse_flag, &a,
+                      &scale,   &ratio_out, &norms_out,  &flags};
     const void *fn = norm == kL1     ? reinterpret_cast<const void *>(&finalize_kernel<kL1>)
                      : norm == kLinf ? reinterpret_cast<const void *>(&finalize_kernel<kLinf>)
                                      : reinterpret_cast<const void *>(&finalize_kernel<kL2>);
     return hipLaunchKernel(fn, dim3(n_tensors), dim3(kFinalizeBlock), params, 0, stream);
+}
+
+hipError_t launch_fused(const StepKind &kind, const TensorDesc *tensors, const ChunkDesc *tiles,
+                        int32_t n_tiles, int32_t grid, uint64_t *slots, uint32_t *ctl,
+                        const StepArgs &args, const FinalizeArgs &fargs, double *ratio_out,
+                        double *norms_out, hipStream_t stream) {
+    StepArgs a = args;
+    FinalizeArgs f = fargs;
+    void *params[] = {&tensors, &tiles, &n_tiles, &slots, &ctl, &a, &f, &ratio_out, &norms_out};
+    return hipLaunchKernel(fused_fn(kind), dim3(grid), dim3(kBlock), params, 0, stream);
+}
+
+hipError_t fused_blocks_per_cu(const StepKind &kind, int *blocks) {
+    return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, fused_fn(kind), kBlock, 0);
 }
 
 }  // namespace lamb_mi355x

@@ -52,8 +52,10 @@ class _LayerwiseOptimizer:
     def __init__(self, params: Sequence, grads: Sequence, lr: float, weight_decay: float,
                  clamp: Tuple[float, float], wd_mask: Optional[Sequence[bool]],
                  chunk_elems: int, with_v: bool, norm: str = "l2", grad_scale: float = 1.0,
-                 skip_nonfinite: bool = False, schedule=None):
+                 skip_nonfinite: bool = False, schedule=None, path: str = "auto"):
         torch = _torch()
+        if path not in _lib.PATHS:
+            raise ValueError("path must be one of %s" % (tuple(_lib.PATHS),))
         self.params = list(params)
         self.grads = list(grads)
         g_dtype, self.device = _check_tensors(self.params, self.grads)
@@ -89,6 +91,8 @@ class _LayerwiseOptimizer:
         kind = _lib.LAMB_GRAD_BF16 if g_dtype == torch.bfloat16 else _lib.LAMB_GRAD_F32
         with torch.cuda.device(self.device):
             self.plan = _lib.lamb_plan_create(rows, kind, self.algo, chunk_elems)
+        _lib.lamb_plan_set_path(self.plan, path)
+        self.path = path
         self.t = 0
 
     def _stream(self) -> int:
@@ -136,6 +140,11 @@ class _LayerwiseOptimizer:
         self.bf16_copies = copies
         return copies
 
+    def check(self) -> None:
+        """Wait for the current stream and raise if a single-pass step gave up
+        a wait (the plan is then unusable; see ``lamb_plan_check``)."""
+        _lib.lamb_plan_check(self.plan, self._stream())
+
     def close(self) -> None:
         self.plan.close()
 
@@ -151,7 +160,7 @@ class LAMB(_LayerwiseOptimizer):
                  weight_decay: float = 0.01, clamp=(0.0, 10.0), wd_mask=None,
                  bias_correction: bool = True, chunk_elems: int = 0, variant: str = "lamb",
                  norm: str = "l2", grad_scale: float = 1.0, skip_nonfinite: bool = False,
-                 schedule=None):
+                 schedule=None, path: str = "auto"):
         """``variant``: "lamb" (Algorithm 2), "n-lamb" (Algorithm 3) or "nn-lamb"
         (Algorithm 4; the paper pairs both with betas=(0.975, 0.999), eps=1e-8).
         ``norm``: "l2" (default), "l1" or "linf" (Appendix F). ``grad_scale``
@@ -159,13 +168,15 @@ class LAMB(_LayerwiseOptimizer):
         loss-scale inverse). ``skip_nonfinite``: a step whose scaled gradient
         holds a NaN or infinity changes nothing and sets ``found_nonfinite``.
         ``schedule``: stages (steps, warmup_steps, peak_lr, power) that set the
-        learning rate of each step (warmup, then polynomial decay, Section 4)."""
+        learning rate of each step (warmup, then polynomial decay, Section 4).
+        ``path``: "auto" (layers of up to 8M elements take the single-pass
+        kernel) or "two-pass"."""
         if variant not in self.VARIANTS:
             raise ValueError("variant must be one of %s" % (self.VARIANTS,))
         if variant != "lamb" and not bias_correction:
             raise ValueError("N-LAMB and NN-LAMB carry their own bias correction")
         super().__init__(params, grads, lr, weight_decay, clamp, wd_mask, chunk_elems, True,
-                         norm, grad_scale, skip_nonfinite, schedule)
+                         norm, grad_scale, skip_nonfinite, schedule, path)
         self.beta1, self.beta2 = float(betas[0]), float(betas[1])
         self.eps = float(eps)
         self.bias_correction = bool(bias_correction)
@@ -200,9 +211,9 @@ class LARS(_LayerwiseOptimizer):
     def __init__(self, params, grads, lr: float = 1e-3, momentum: float = 0.9,
                  weight_decay: float = 0.01, clamp=(0.0, 10.0), trust_coef: float = 1e-3,
                  wd_mask=None, chunk_elems: int = 0, norm: str = "l2", grad_scale: float = 1.0,
-                 skip_nonfinite: bool = False, schedule=None):
+                 skip_nonfinite: bool = False, schedule=None, path: str = "auto"):
         super().__init__(params, grads, lr, weight_decay, clamp, wd_mask, chunk_elems, False,
-                         norm, grad_scale, skip_nonfinite, schedule)
+                         norm, grad_scale, skip_nonfinite, schedule, path)
         self.momentum = float(momentum)
         self.trust_coef = float(trust_coef)
 

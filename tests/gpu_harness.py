@@ -107,7 +107,8 @@ class Pair:
     """Device state + plan for the HIP path, and host state for the oracle."""
 
     def __init__(self, xs: Sequence, wd: Sequence[bool], g_dtype: str, algo: str,
-                 chunk_elems: int = 0, oracle_subset: Optional[Sequence[int]] = None):
+                 chunk_elems: int = 0, oracle_subset: Optional[Sequence[int]] = None,
+                 path: str = "auto"):
         torch = torch_cuda()
         self.torch = torch
         self.algo = algo
@@ -131,6 +132,8 @@ class Pair:
         kind = _lib.LAMB_GRAD_BF16 if g_dtype == "bf16" else _lib.LAMB_GRAD_F32
         algo_id = _lib.LAMB_ALGO_LARS if algo == "lars" else _lib.LAMB_ALGO_LAMB
         self.plan = _lib.lamb_plan_create(rows, kind, algo_id, chunk_elems)
+        _lib.lamb_plan_set_path(self.plan, path)
+        self.path = path
         self.oracle = oracle.load()
 
     def set_grads(self, grads: Sequence) -> List[np.ndarray]:
@@ -170,9 +173,11 @@ class Pair:
         return self.oracle.lars_step(self.hx, hg, self.hm, [self.wd[i] for i in self.subset],
                                      **f32_scalars(hp))
 
-    def compare(self, ref: np.ndarray, label: str) -> Report:
+    def compare(self, ref: np.ndarray, label: str, ratio_tol: float = RATIO_TOL) -> Report:
         """Element-wise state and per-tensor ratio/norm comparison for the subset
-        (ratios and norms only when the oracle did not skip the step)."""
+        (ratios and norms only when the oracle did not skip the step). First
+        checks that no single-pass wait of the plan was abandoned."""
+        _lib.lamb_plan_check(self.plan, self.torch.cuda.current_stream().cuda_stream)
         self.torch.cuda.synchronize()
         rep = Report()
         ratio = self.ratio.cpu().numpy()
@@ -188,9 +193,9 @@ class Pair:
         idx = np.asarray(self.subset)
         if np.all(np.isnan(ref)):
             return rep
-        compare_ratios(ratio[idx], ref[:, 0], label + " trust ratio")
-        compare_ratios(norms[idx, 0], ref[:, 1], label + " ||x||")
-        compare_ratios(norms[idx, 1], ref[:, 2], label + " ||u||")
+        compare_ratios(ratio[idx], ref[:, 0], label + " trust ratio", ratio_tol)
+        compare_ratios(norms[idx, 0], ref[:, 1], label + " ||x||", ratio_tol)
+        compare_ratios(norms[idx, 1], ref[:, 2], label + " ||u||", ratio_tol)
         return rep
 
     def close(self) -> None:
@@ -265,12 +270,17 @@ def step_both(pair: Pair, algo: str, hg, hp: dict, t: int, bias_correction: bool
 
 
 def run_config(cfg: int, steps: int, algo: str = "lamb", chunk_elems: int = 0,
-               device: str = "cuda", oracle_subset: Optional[Sequence[int]] = None) -> Report:
+               device: str = "cuda", oracle_subset: Optional[Sequence[int]] = None,
+               path: str = "auto") -> Report:
     """Parity over ``steps`` steps of a named parameter set, compared every step."""
     ps = paramsets.get(cfg)
-    log("parity cfg=%d (%s) algo=%s steps=%d chunk=%d" % (cfg, ps.name, algo, steps, chunk_elems))
+    log("parity cfg=%d (%s) algo=%s steps=%d chunk=%d path=%s"
+        % (cfg, ps.name, algo, steps, chunk_elems, path))
     pair = Pair(paramsets.draw_params(ps, device=device), ps.wd_mask(), ps.g_dtype, algo,
-                chunk_elems, oracle_subset)
+                chunk_elems, oracle_subset, path)
+    per, total = _lib.lamb_plan_tiles(pair.plan)
+    log("  single-pass layers %d of %d, %d tiles"
+        % (sum(1 for k in per if k), len(per), total))
     rep = Report()
     hp = {"lamb": lamb_hp, "lars": lars_hp, "nlamb": nlamb_hp, "nnlamb": nlamb_hp}[algo](ps)
     try:

@@ -29,14 +29,19 @@ def _gs(rng, sizes, g_dtype="f32", scale=1e-3):
     return out
 
 
-def _run(xs, wd, g_dtype, algo, chunk, steps, hp, rng, grads=None, bias_correction=True):
-    pair = H.Pair(xs, wd, g_dtype, algo, chunk)
+PATHS = ["auto", "two-pass"]
+
+
+def _run(xs, wd, g_dtype, algo, chunk, steps, hp, rng, grads=None, bias_correction=True,
+         ratio_tol=H.RATIO_TOL, path="auto"):
+    pair = H.Pair(xs, wd, g_dtype, algo, chunk, path=path)
     try:
         for t in range(1, steps + 1):
             gs = grads(t) if grads else _gs(rng, [x.size for x in xs], g_dtype)
             hg = pair.set_grads(gs)
             ref = H.step_both(pair, algo, hg, hp, t, bias_correction)
-            pair.compare(ref, "%s %s chunk=%d step %d" % (algo, g_dtype, chunk, t))
+            pair.compare(ref, "%s %s chunk=%d %s step %d" % (algo, g_dtype, chunk, path, t),
+                         ratio_tol)
         return pair
     finally:
         pair.close()
@@ -52,29 +57,35 @@ NLAMB = dict(DEFAULT, beta1=0.975, eps=1e-8)
 @pytest.mark.parametrize("algo,g_dtype", [("lamb", "f32"), ("lamb", "bf16"), ("lars", "f32"),
                                           ("lars", "bf16"), ("nlamb", "bf16"),
                                           ("nnlamb", "f32")])
-@pytest.mark.parametrize("chunk", [8, 64, 1024, 0])
-def test_ragged_sizes(algo, g_dtype, chunk):
+@pytest.mark.parametrize("chunk,path", [(8, "two-pass"), (64, "two-pass"), (1024, "two-pass"),
+                                        (0, "two-pass"), (0, "auto")])
+def test_ragged_sizes(algo, g_dtype, chunk, path):
     """Every tensor length around the 4-element group, the 256-thread tile,
-    the unrolled loop trip and the chunk boundary."""
+    the unrolled loop trip and the chunk boundary; on the single pass, around
+    the 8192-element tile and its multiples (layers of several tiles)."""
     rng = np.random.default_rng(1000 + chunk)
     sizes = list(RAGGED)
     if chunk:
         sizes += [chunk - 1, chunk, chunk + 1, 4 * chunk + 5]
     else:
         sizes += [32767, 32768, 32769, 4 * 32768 + 5]
+    if path == "auto":
+        sizes += [8191, 8192, 8193, 2 * 8192 - 3, 3 * 8192, 5 * 8192 + 7]
     xs = _xs(rng, sizes)
     wd = [i % 3 != 0 for i in range(len(sizes))]
     hp = {"lamb": DEFAULT, "lars": LARS, "nlamb": NLAMB, "nnlamb": NLAMB}[algo]
-    H.log("ragged algo=%s g=%s chunk=%d tensors=%d" % (algo, g_dtype, chunk, len(sizes)))
-    _run(xs, wd, g_dtype, algo, chunk, 3, hp, rng)
+    H.log("ragged algo=%s g=%s chunk=%d path=%s tensors=%d"
+          % (algo, g_dtype, chunk, path, len(sizes)))
+    _run(xs, wd, g_dtype, algo, chunk, 3, hp, rng, path=path)
 
 
-def test_zero_gradient_block_does_not_move():
+@pytest.mark.parametrize("path", PATHS)
+def test_zero_gradient_block_does_not_move(path):
     """||u|| = 0: ratio exactly 0, x bit for bit unchanged, no NaN."""
     torch = H.torch_cuda()
     rng = np.random.default_rng(5)
     xs = _xs(rng, [100, 37])
-    pair = H.Pair(xs, [False, True], "f32", "lamb")
+    pair = H.Pair(xs, [False, True], "f32", "lamb", path=path)
     try:
         hg = pair.set_grads([torch.zeros(100), torch.from_numpy(rng.standard_normal(37).astype(np.float32) * 1e-3)])
         x0 = pair.X[0].clone()
@@ -87,30 +98,35 @@ def test_zero_gradient_block_does_not_move():
         pair.close()
 
 
+@pytest.mark.parametrize("path", PATHS)
 @pytest.mark.parametrize("gamma_l", [0.0, 0.25])
-def test_zero_parameter_block(gamma_l):
+def test_zero_parameter_block(gamma_l, path):
     """phi(0) = gamma_l: a zero block stays put at gamma_l = 0, else moves."""
     rng = np.random.default_rng(6)
     xs = [np.zeros(513, np.float32), _xs(rng, [300])[0]]
     hp = dict(DEFAULT, gamma_l=gamma_l)
-    _run(xs, [True, True], "f32", "lamb", 0, 2, hp, rng)
-    _run(xs, [True, True], "f32", "lars", 0, 2, dict(LARS, gamma_l=gamma_l), rng)
+    _run(xs, [True, True], "f32", "lamb", 0, 2, hp, rng, path=path)
+    _run(xs, [True, True], "f32", "lars", 0, 2, dict(LARS, gamma_l=gamma_l), rng, path=path)
 
 
-def test_nan_gradient_propagates_like_the_oracle():
+@pytest.mark.parametrize("path", PATHS)
+def test_nan_gradient_propagates_like_the_oracle(path):
     torch = H.torch_cuda()
     rng = np.random.default_rng(7)
-    xs = _xs(rng, [64, 65])
+    xs = _xs(rng, [64, 65, 3 * 8192 + 1])
     g0 = torch.from_numpy((rng.standard_normal(64) * 1e-3).astype(np.float32))
     g0[17] = float("nan")
     g1 = torch.from_numpy((rng.standard_normal(65) * 1e-3).astype(np.float32))
-    pair = H.Pair(xs, [True, True], "f32", "lamb")
+    g2 = torch.from_numpy((rng.standard_normal(3 * 8192 + 1) * 1e-3).astype(np.float32))
+    g2[2 * 8192 + 5] = float("inf")  # in the third tile of a three-tile layer
+    pair = H.Pair(xs, [True, True, False], "f32", "lamb", path=path)
     try:
-        hg = pair.set_grads([g0, g1])
+        hg = pair.set_grads([g0, g1, g2])
         pair.gpu_lamb(DEFAULT, 1)
         ref = pair.oracle_lamb(hg, DEFAULT, 1)
         pair.compare(ref, "nan grad")
         assert np.isnan(ref[0, 0]) and math.isnan(float(pair.ratio[0]))
+        assert np.isnan(ref[2, 0]) and math.isnan(float(pair.ratio[2]))
     finally:
         pair.close()
 
@@ -122,29 +138,35 @@ def test_nan_gradient_propagates_like_the_oracle():
     dict(DEFAULT, eps=0.0),
     dict(DEFAULT, weight_decay=0.5, lr=0.3),
 ], ids=["no-upper-clamp", "phi-const", "sign-sgd", "eps0", "big-lr-wd"])
-def test_scalar_settings(hp):
+@pytest.mark.parametrize("path", PATHS)
+def test_scalar_settings(hp, path):
     rng = np.random.default_rng(8)
-    xs = _xs(rng, [4096, 333, 9, 1], scale=2.0)
-    _run(xs, [True, False, True, True], "f32", "lamb", 1024, 4, hp, rng)
+    xs = _xs(rng, [4096, 333, 9, 1, 20000], scale=2.0)
+    _run(xs, [True, False, True, True, False], "f32", "lamb", 1024, 4, hp, rng, path=path)
 
 
-def test_without_bias_correction():
+@pytest.mark.parametrize("path", PATHS)
+def test_without_bias_correction(path):
     rng = np.random.default_rng(9)
-    xs = _xs(rng, [5000, 77])
-    _run(xs, [True, False], "bf16", "lamb", 2048, 4, DEFAULT, rng, bias_correction=False)
+    xs = _xs(rng, [5000, 77, 17000])
+    _run(xs, [True, False, True], "bf16", "lamb", 2048, 4, DEFAULT, rng, bias_correction=False,
+         path=path)
 
 
-def test_lars_trust_coefficient_one_and_no_momentum():
+@pytest.mark.parametrize("path", PATHS)
+def test_lars_trust_coefficient_one_and_no_momentum(path):
     rng = np.random.default_rng(10)
-    xs = _xs(rng, [3000, 5])
-    _run(xs, [True, False], "f32", "lars", 0, 3, dict(LARS, trust_coef=1.0, momentum=0.0), rng)
+    xs = _xs(rng, [3000, 5, 9000])
+    _run(xs, [True, False, True], "f32", "lars", 0, 3,
+         dict(LARS, trust_coef=1.0, momentum=0.0), rng, path=path)
 
 
-def test_guard_bands_untouched():
+@pytest.mark.parametrize("path", PATHS)
+def test_guard_bands_untouched(path):
     """Tensors carved out of one buffer with canary gaps between them: no
     kernel writes outside its tensors."""
     torch = H.torch_cuda()
-    sizes = [1, 7, 1000, 4097, 33]
+    sizes = [1, 7, 1000, 4097, 33, 20001]
     gap = 64
     total = sum(sizes) + gap * (len(sizes) + 1)
     bufs = {k: torch.full((total,), -7.25, device="cuda") for k in "xgmv"}
@@ -169,9 +191,11 @@ def test_guard_bands_untouched():
     rows = [(views["x"][i].data_ptr(), views["g"][i].data_ptr(), views["m"][i].data_ptr(),
              views["v"][i].data_ptr(), sizes[i], 1) for i in range(len(sizes))]
     with _lib.lamb_plan_create(rows, _lib.LAMB_GRAD_F32, _lib.LAMB_ALGO_LAMB, 8) as plan:
+        _lib.lamb_plan_set_path(plan, path)
         for t in range(1, 4):
             _lib.lamb_step(plan, 0.01, 0.9, 0.999, 1e-6, 0.01, 0.0, 10.0, t, True,
                            torch.cuda.current_stream().cuda_stream)
+        _lib.lamb_plan_check(plan)
         torch.cuda.synchronize()
     for k in "xgmv":
         assert torch.equal(bufs[k][mask], canary[k][mask]), "canary overwritten in " + k
@@ -264,3 +288,56 @@ def test_tensor_beyond_int32_elements():
             (name, lo, hi, want)
     del x, g, m, v
     torch.cuda.empty_cache()
+
+
+def test_subnormal_and_zero_gradients():
+    """bf16 and fp32 gradients that are subnormal or exactly zero (with the
+    paper's eps > 0): the step stays finite and matches the oracle.
+
+    The second tensor's first moment m_t = (1 - beta1) g ~ 3e-40 is an fp32
+    subnormal: the kernel derives u from the stored fp32 m_t, whose spacing
+    there is 2^-149, so the per-tensor ratio may move by half that spacing
+    relative to |m_t| on top of the usual bound."""
+    torch = H.torch_cuda()
+    rng = np.random.default_rng(13)
+    for g_dtype in ("f32", "bf16"):
+        xs = _xs(rng, [300, 64])
+        g0 = torch.from_numpy((rng.standard_normal(300) * 1e-3).astype(np.float32))
+        g0[::7] = 0.0
+        g0[1::7] = 1e-40          # fp32 subnormal (bf16 keeps its top half)
+        g1 = torch.full((64,), 3e-39)
+        gs = [g0, g1] if g_dtype == "f32" else [g0.to(torch.bfloat16), g1.to(torch.bfloat16)]
+        tol = H.RATIO_TOL + 2.0 ** -150 / (0.1 * float(gs[1][0].float()))
+        _run(xs, [True, False], g_dtype, "lamb", 64, 3, DEFAULT, rng, grads=lambda t: gs,
+             ratio_tol=tol)
+
+
+def test_single_pass_layout_and_rounds():
+    """The single pass runs in rounds of one workgroup per tile, four per CU.
+    A layer of exactly one round of 8192-element tiles takes it, a layer of
+    one element more takes the two-pass kernels; layers that leave a gap in
+    a round (padded with empty entries) and a layer that fills the last
+    round still match the oracle on every element."""
+    torch = H.torch_cuda()
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    R, T = 4 * cus, 8192
+    sizes = [R * T, R * T + 1, int(0.68 * R) * T - 3, int(0.39 * R) * T + 5, int(0.29 * R) * T,
+             30 * T - 1, 100, 7]
+    rng = np.random.default_rng(21)
+    xs = _xs(rng, sizes)
+    wd = [i % 2 == 0 for i in range(len(sizes))]
+    H.log("single-pass rounds: R=%d sizes=%s" % (R, sizes))
+    pair = H.Pair(xs, wd, "bf16", "lamb", path="auto")
+    try:
+        per, total = _lib.lamb_plan_tiles(pair.plan)
+        want = [(n + T - 1) // T for n in sizes]
+        want[1] = 0
+        assert per == want
+        assert total >= sum(want)
+        for t in range(1, 3):
+            gs = _gs(rng, sizes, "bf16")
+            hg = pair.set_grads(gs)
+            ref = H.step_both(pair, "lamb", hg, DEFAULT, t)
+            pair.compare(ref, "rounds step %d" % t)
+    finally:
+        pair.close()

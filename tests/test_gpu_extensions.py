@@ -21,8 +21,8 @@ def _hp(algo, **kw):
     return _lib.lamb_hparams_init(algo, **base)
 
 
-def _pair(xs, wd, g_dtype, algo, chunk=0):
-    return H.Pair(xs, wd, g_dtype, "lars" if algo == "lars" else "lamb", chunk)
+def _pair(xs, wd, g_dtype, algo, chunk=0, path="auto"):
+    return H.Pair(xs, wd, g_dtype, "lars" if algo == "lars" else "lamb", chunk, path=path)
 
 
 def _grads(rng, xs, g_dtype, scale=1e-3):
@@ -41,11 +41,13 @@ def test_other_norms(algo, norm):
     ps = paramsets.get(0)
     rng = np.random.default_rng(7)
     ragged = [(rng.standard_normal(n) * 0.3).astype(np.float32)
-              for n in (1, 3, 5, 64, 257, 1023, 2049, 4097)]
-    for xs, wd, g_dtype, chunk in ((paramsets.draw_params(ps), ps.wd_mask(), "f32", 0),
-                                   (ragged, [i % 2 == 0 for i in range(len(ragged))], "bf16", 64)):
-        H.log("norm=%s algo=%s tensors=%d chunk=%d" % (norm, algo, len(xs), chunk))
-        pair = _pair(xs, wd, g_dtype, algo, chunk)
+              for n in (1, 3, 5, 64, 257, 1023, 2049, 4097, 3 * 8192 + 3)]
+    rwd = [i % 2 == 0 for i in range(len(ragged))]
+    for xs, wd, g_dtype, chunk, path in ((paramsets.draw_params(ps), ps.wd_mask(), "f32", 0, "auto"),
+                                         (ragged, rwd, "bf16", 64, "two-pass"),
+                                         (ragged, rwd, "bf16", 0, "auto")):
+        H.log("norm=%s algo=%s tensors=%d chunk=%d path=%s" % (norm, algo, len(xs), chunk, path))
+        pair = _pair(xs, wd, g_dtype, algo, chunk, path)
         try:
             for t in range(1, 4):
                 hg = pair.set_grads(_grads(rng, pair.X, g_dtype))
@@ -85,7 +87,7 @@ def test_deferred_mode_equals_direct_mode(algo):
     xs = paramsets.draw_params(ps, device="cuda")
     runs = []
     for skip, chunk in ((0, 2048), (1, 512)):
-        pair = _pair([x.clone() for x in xs], ps.wd_mask(), "f32", algo, chunk)
+        pair = _pair([x.clone() for x in xs], ps.wd_mask(), "f32", algo, chunk, "two-pass")
         pair.subset = []
         flag = torch.zeros(1, dtype=torch.int32, device="cuda")
         for t in range(1, 4):
@@ -189,9 +191,10 @@ def _bf16_bits(t):
     return t.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
 
 
-@pytest.mark.parametrize("algo,skip,g_dtype", [("lamb", 0, "bf16"), ("nn-lamb", 0, "f32"),
-                                               ("lars", 1, "bf16"), ("lamb", 1, "f32")])
-def test_bf16_copies(algo, skip, g_dtype):
+@pytest.mark.parametrize("algo,skip,g_dtype,path", [
+    ("lamb", 0, "bf16", "auto"), ("lamb", 0, "bf16", "two-pass"), ("nn-lamb", 0, "f32", "auto"),
+    ("lars", 0, "f32", "auto"), ("lars", 1, "bf16", "auto"), ("lamb", 1, "f32", "auto")])
+def test_bf16_copies(algo, skip, g_dtype, path):
     """The apply pass writes bf16(x_{t+1}): bit for bit torch's cast of the
     GPU's own x, within one bf16 ulp of the oracle's rounding of the oracle's
     x; a tensor without a copy is unaffected; x, m, v still match the oracle."""
@@ -199,7 +202,7 @@ def test_bf16_copies(algo, skip, g_dtype):
     rng = np.random.default_rng(11)
     sizes = [1, 3, 8, 255, 513, 1029, 4097, 70000]
     xs = [(rng.standard_normal(n) * 0.5).astype(np.float32) for n in sizes]
-    pair = _pair(xs, [i % 2 == 0 for i in range(len(sizes))], g_dtype, algo, 256)
+    pair = _pair(xs, [i % 2 == 0 for i in range(len(sizes))], g_dtype, algo, 256, path)
     copies = [torch.full((n,), 12345, dtype=torch.int16, device="cuda").view(torch.bfloat16)
               for n in sizes]
     copies[2] = None
@@ -221,12 +224,13 @@ def test_bf16_copies(algo, skip, g_dtype):
         pair.close()
 
 
-def test_bf16_copy_guard_bands_and_detach():
+@pytest.mark.parametrize("path", ["auto", "two-pass"])
+def test_bf16_copy_guard_bands_and_detach(path):
     torch = H.torch_cuda()
     rng = np.random.default_rng(12)
     sizes = [5, 1000, 33]
     xs = [(rng.standard_normal(n)).astype(np.float32) for n in sizes]
-    pair = _pair(xs, [True] * 3, "f32", "lamb", 64)
+    pair = _pair(xs, [True] * 3, "f32", "lamb", 64, path)
     gap = 64
     buf = torch.full((sum(sizes) + gap * 4,), -3, dtype=torch.int16, device="cuda")
     views, off = [], gap

@@ -18,11 +18,11 @@ def _state(pair):
     return out + [pair.ratio.clone()]
 
 
-def _steps(cfg, algo, chunk, steps, device="cuda", subset=None):
+def _steps(cfg, algo, chunk, steps, device="cuda", subset=None, path="auto"):
     ps = paramsets.get(cfg)
     xs = paramsets.draw_params(ps, indices=subset, device=device)
     wd = ps.wd_mask() if subset is None else [ps.wd_mask()[i] for i in subset]
-    pair = H.Pair(xs, wd, ps.g_dtype, algo, chunk, oracle_subset=[])
+    pair = H.Pair(xs, wd, ps.g_dtype, algo, chunk, oracle_subset=[], path=path)
     hp = H.lamb_hp(ps) if algo == "lamb" else H.lars_hp(ps)
     for t in range(1, steps + 1):
         pair.set_grads(paramsets.draw_grads(ps, t, indices=subset, device=device))
@@ -33,12 +33,13 @@ def _steps(cfg, algo, chunk, steps, device="cuda", subset=None):
     return pair
 
 
+@pytest.mark.parametrize("path", ["auto", "two-pass"])
 @pytest.mark.parametrize("cfg,algo", [(2, "lamb"), (3, "lars")])
-def test_bitwise_deterministic(cfg, algo):
+def test_bitwise_deterministic(cfg, algo, path):
     torch = H.torch_cuda()
     runs = []
     for _ in range(2):
-        pair = _steps(cfg, algo, 0, 2)
+        pair = _steps(cfg, algo, 0, 2, path=path)
         runs.append(_state(pair))
         pair.close()
     for a, b in zip(*runs):
@@ -46,10 +47,12 @@ def test_bitwise_deterministic(cfg, algo):
 
 
 def test_chunk_size_invariance():
-    """m and v are elementwise, so they do not depend on the chunking at all;
-    x and the ratios agree to rounding of the reduction order."""
+    """m and v are elementwise, so they do not depend on the chunking or on
+    the path at all; x and the ratios agree to rounding of the reduction
+    order. The first run is the single pass."""
     torch = H.torch_cuda()
-    runs = [_state(_steps(1, "lamb", c, 2)) for c in (0, 4096, 65536)]
+    runs = [_state(_steps(1, "lamb", 0, 2))]
+    runs += [_state(_steps(1, "lamb", c, 2, path="two-pass")) for c in (0, 4096, 65536)]
     n = paramsets.get(1).n_tensors
     for other in runs[1:]:
         for k in range(n, 3 * n):
@@ -59,12 +62,14 @@ def test_chunk_size_invariance():
         H.compare_ratios(other[-1].cpu().numpy(), runs[0][-1].cpu().numpy(), "ratio")
 
 
-def test_layer_independence():
-    """A step on {A, B} equals a step on {A} and a step on {B}, bit for bit."""
+@pytest.mark.parametrize("path,chunk", [("two-pass", 1024), ("auto", 0)])
+def test_layer_independence(path, chunk):
+    """A step on {A, B} equals a step on {A} and a step on {B}, bit for bit
+    (on the single pass, wherever the packing puts each layer)."""
     torch = H.torch_cuda()
     ps = paramsets.get(0)
-    joint = _steps(0, "lamb", 1024, 3)
-    parts = [_steps(0, "lamb", 1024, 3, subset=[i]) for i in range(ps.n_tensors)]
+    joint = _steps(0, "lamb", chunk, 3, path=path)
+    parts = [_steps(0, "lamb", chunk, 3, subset=[i], path=path) for i in range(ps.n_tensors)]
     for i, p in enumerate(parts):
         assert torch.equal(joint.X[i], p.X[0])
         assert torch.equal(joint.M[i], p.M[0])
@@ -107,23 +112,25 @@ def test_resume_is_bitwise():
     c.close()
 
 
-def test_timing_hooks_record_each_kernel():
+@pytest.mark.parametrize("path", ["auto", "two-pass"])
+def test_timing_hooks_record_each_kernel(path):
     torch = H.torch_cuda()
-    pair = _steps(0, "lamb", 0, 0)
+    pair = _steps(0, "lamb", 0, 0, path=path)
     ps = paramsets.get(0)
+    launched = [3] if path == "auto" else [0, 1, 2]  # the tiny set fits the single pass
     _lib.lamb_plan_set_timing(pair.plan, 8)
     pair.set_grads(paramsets.draw_grads(ps, 1, device="cuda"))
     for t in range(1, 6):
         pair.gpu_lamb(H.lamb_hp(ps), t)
     ms, steps = _lib.lamb_plan_timing(pair.plan)
-    assert steps == 5 and all(v > 0 for v in ms)
+    assert steps == 5 and all(ms[k] > 0 for k in launched)
     ms2, steps2 = _lib.lamb_plan_timing(pair.plan)
     assert steps2 == 0
     _lib.lamb_plan_set_timing(pair.plan, 3, 4)  # steps 1, 5, 9 of the next 12
     for t in range(6, 18):
         pair.gpu_lamb(H.lamb_hp(ps), t)
     ms, steps = _lib.lamb_plan_timing(pair.plan)
-    assert steps == 3 and all(v > 0 for v in ms)
+    assert steps == 3 and all(ms[k] > 0 for k in launched)
     with pytest.raises(_lib.LambError):
         _lib.lamb_plan_set_timing(pair.plan, 3, 0)
     _lib.lamb_plan_set_timing(pair.plan, 0)
@@ -185,3 +192,102 @@ def test_facade_schedule_sets_each_steps_lr():
     assert all(torch.equal(p, q) for p, q in zip(a.params, b.params))
     a.close()
     b.close()
+
+
+def test_independent_plans_on_concurrent_streams():
+    """Two plans stepped on two streams at once give what each gives alone."""
+    torch = H.torch_cuda()
+    ps = paramsets.get(3)
+    results = []
+    for concurrent in (False, True):
+        pairs = [_steps(3, algo, 0, 0) for algo in ("lamb", "lars")]
+        streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+        for p in pairs:
+            p.set_grads(paramsets.draw_grads(ps, 1, device="cuda"))
+        torch.cuda.synchronize()
+        for t in range(1, 4):
+            for k, (p, s) in enumerate(zip(pairs, streams)):
+                with torch.cuda.stream(s):
+                    if k == 0:
+                        p.gpu_lamb(H.lamb_hp(ps), t)
+                    else:
+                        p.gpu_lars(H.lars_hp(ps))
+                if not concurrent:
+                    torch.cuda.synchronize()
+        torch.cuda.synchronize()
+        results.append([_state(p) for p in pairs])
+        for p in pairs:
+            p.close()
+    for a, b in zip(results[0], results[1]):
+        assert all(torch.equal(u, w) for u, w in zip(a, b))
+
+
+@pytest.mark.parametrize("path,skip", [("auto", 0), ("two-pass", 0), ("two-pass", 1)])
+def test_graph_capture_replays_match_eager(path, skip):
+    """A captured step (fixed scalars, gradients read from the same buffers)
+    replayed three times, with eager work between replays, equals three eager
+    steps. The single pass keeps its slot epoch on the device; in deferred
+    mode the second replay sees a NaN gradient and must skip, and the third
+    must not: the non-finite verdict is handed over on the device, not by a
+    host counter or a memset."""
+    torch = H.torch_cuda()
+    ps = paramsets.get(0)
+    hp = _lib.lamb_hparams_init("lamb", step=4, lr=ps.lr, skip_nonfinite=skip)
+    grads = [paramsets.draw_grads(ps, t, device="cuda") for t in (1, 2, 3)]
+    if skip:
+        grads[1][2][5] = float("nan")
+    runs = []
+    for graph in (False, True):
+        pair = _steps(0, "lamb", 1024, 0, path=path)
+        flag = torch.full((1,), 7, dtype=torch.int32, device="cuda")
+
+        def step():
+            _lib.lamb_step_ex(pair.plan, hp, torch.cuda.current_stream().cuda_stream,
+                              pair.ratio.data_ptr(), pair.norms.data_ptr(),
+                              flag.data_ptr() if skip else 0)
+
+        pair.set_grads(grads[0])
+        step()  # one eager step first in both runs
+        torch.cuda.synchronize()
+        states = []
+        if graph:
+            side = torch.cuda.Stream()
+            side.wait_stream(torch.cuda.current_stream())
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=side):
+                step()
+            torch.cuda.synchronize()
+            for r in range(3):
+                pair.set_grads(grads[r])
+                torch.cuda.synchronize()
+                g.replay()
+                torch.cuda.synchronize()
+                scratch = torch.randn(1 << 20, device="cuda").sum()  # eager work between replays
+                torch.cuda.synchronize()
+                states.append(_state(pair) + [flag.clone()])
+            del scratch
+        else:
+            for r in range(3):
+                pair.set_grads(grads[r])
+                step()
+                torch.cuda.synchronize()
+                states.append(_state(pair) + [flag.clone()])
+        _lib.lamb_plan_check(pair.plan)
+        runs.append(states)
+        pair.close()
+    if skip:
+        assert [int(s[-1]) for s in runs[0]] == [0, 1, 0]
+        for a, b in zip(runs[0][0][:-2], runs[0][1][:-2]):
+            assert torch.equal(a, b)  # the NaN step left x, m, v alone
+    for eager, replay in zip(runs[0], runs[1]):
+        assert all(_same_bits(a, b) for a, b in zip(eager, replay))
+
+
+def _same_bits(a, b):
+    """Bitwise equality that also holds for equal NaN patterns."""
+    torch = H.torch_cuda()
+    if a.dtype == torch.float64:
+        return torch.equal(a.view(torch.int64), b.view(torch.int64))
+    if a.dtype == torch.float32:
+        return torch.equal(a.view(torch.int32), b.view(torch.int32))
+    return torch.equal(a, b)
