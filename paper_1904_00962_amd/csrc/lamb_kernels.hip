@@ -594,6 +594,15 @@ __global__ __launch_bounds__(kFinalizeBlock) void finalize_kernel(
 // step, and every later step of the plan does nothing.
 // ---------------------------------------------------------------------------
 
+// s_sleep argument between polls (units of 64 clocks): LAMB_SPIN_SLEEP for
+// a layer's leader waiting for its tiles' partial norms, LAMB_MEMBER_SLEEP
+// for a tile waiting for the leader's scale.
+#ifndef LAMB_SPIN_SLEEP
+#define LAMB_SPIN_SLEEP 8
+#endif
+#ifndef LAMB_MEMBER_SLEEP
+#define LAMB_MEMBER_SLEEP LAMB_SPIN_SLEEP
+#endif
 constexpr uint32_t kSpinLimit = 1u << 22;
 static_assert(kTileGroups % kUnroll == 0, "tile groups must be a multiple of the unroll");
 
@@ -616,6 +625,7 @@ __device__ __forceinline__ uint64_t slot_word(double d) {
 }
 
 // Polls *p until it holds a value; kEmptySlot if the wait was abandoned.
+template <int kSleep>
 __device__ uint64_t slot_wait(const uint64_t *p, uint32_t *ctl) {
     for (uint32_t k = 1;; ++k) {
         const uint64_t w = slot_load(p);
@@ -630,7 +640,7 @@ __device__ uint64_t slot_wait(const uint64_t *p, uint32_t *ctl) {
                 return kEmptySlot;
             }
         }
-        __builtin_amdgcn_s_sleep(2);
+        __builtin_amdgcn_s_sleep(kSleep);
     }
 }
 
@@ -746,9 +756,10 @@ void fused_kernel(const TensorDesc *__restrict__ tensors, const ChunkDesc *__res
             if (j == first) {
                 double ax = 0.0, au = 0.0;
                 for (int k = threadIdx.x; k < team; k += kBlock) {
-                    const uint64_t wx = slot_wait(cur + first + k, ctl);
-                    const uint64_t wu =
-                        wx == kEmptySlot ? kEmptySlot : slot_wait(cur + n + first + k, ctl);
+                    const uint64_t wx = slot_wait<LAMB_SPIN_SLEEP>(cur + first + k, ctl);
+                    const uint64_t wu = wx == kEmptySlot
+                                            ? kEmptySlot
+                                            : slot_wait<LAMB_SPIN_SLEEP>(cur + n + first + k, ctl);
                     if (wu == kEmptySlot) {
                         give_up = 1;
                         break;
@@ -768,7 +779,7 @@ void fused_kernel(const TensorDesc *__restrict__ tensors, const ChunkDesc *__res
                         slot_store(cur + 2 * n + first + k, w);
                 }
             } else if (threadIdx.x == 0) {
-                const uint64_t w = slot_wait(cur + 2 * n + j, ctl);
+                const uint64_t w = slot_wait<LAMB_MEMBER_SLEEP>(cur + 2 * n + j, ctl);
                 if (w == kEmptySlot)
                     give_up = 1;
                 else
