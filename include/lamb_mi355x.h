@@ -234,7 +234,10 @@ LAMB_API lamb_status lamb_plan_tiles(const lamb_plan *plan, int32_t *tiles_per_t
 
 /*
  * Wait for `stream` and report whether a single-pass step of the plan gave
- * up a wait (a layer's tiles were not all resident within about a second).
+ * up a wait (a layer's tiles were not all resident within about a second:
+ * 2^22 polls, or the count in the environment variable
+ * LAMB_MI355X_SPIN_LIMIT when lamb_plan_create ran, which tests use to
+ * exercise this path).
  * That step's state is then undefined and the plan's single pass does no
  * further work: restore the state and build a new plan. Synchronises the
  * stream. Errors: LAMB_ENULL, LAMB_EHIP, LAMB_ESYNC.

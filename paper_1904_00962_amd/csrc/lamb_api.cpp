@@ -10,6 +10,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <mutex>
 #include <new>
@@ -40,6 +41,7 @@ struct lamb_plan {
     lamb_path path = LAMB_PATH_AUTO;
     int32_t cu_count = 0;
     int32_t round = 0;             // single-pass grid: workgroups per round of the tile list
+    uint32_t spin_limit = kDefaultSpinLimit;
     int32_t n_tiles = 0;
     int32_t n_rest = 0;            // layers outside the single pass
     int32_t n_rest_chunks = 0;
@@ -524,6 +526,10 @@ lamb_status lamb_plan_create(const lamb_tensor *tensors, int32_t n_tensors,
     plan->device = device;
     plan->cu_count = cu_count;
     plan->round = round;
+    if (const char *env = std::getenv("LAMB_MI355X_SPIN_LIMIT")) {
+        const long long v = std::atoll(env);
+        plan->spin_limit = uint32_t(std::min<long long>(std::max<long long>(v, 1), 1LL << 30));
+    }
     auto round256 = [](size_t b) { return (b + 255) & ~size_t(255); };
     const size_t tensors_bytes = round256(sizeof(TensorDesc) * size_t(n_tensors));
     const size_t chunks_bytes = round256(sizeof(ChunkDesc) * size_t(n_chunks));
@@ -728,6 +734,7 @@ StepArgs step_args(const lamb_hparams &hp) {
     a.eps = hp.eps;
     a.weight_decay = hp.weight_decay;
     a.grad_scale = hp.grad_scale;
+    a.spin_limit = kDefaultSpinLimit;
     const double b1 = hp.beta1, b2 = hp.beta2, t = double(hp.step);
     switch (hp.variant) {
     case LAMB_VARIANT_LAMB:
@@ -808,7 +815,8 @@ lamb_status lamb_step_ex(lamb_plan *plan, const lamb_hparams *hp, void *stream,
     kind.norm = static_cast<NormKind>(hp->norm);
     kind.bf16_grad = plan->g_dtype == LAMB_GRAD_BF16;
     kind.deferred = hp->skip_nonfinite != 0;
-    const StepArgs a = step_args(*hp);
+    StepArgs a = step_args(*hp);
+    a.spin_limit = plan->spin_limit;
     const bool lars = hp->variant == LAMB_VARIANT_LARS;
     const FinalizeArgs f{double(hp->lr), double(hp->gamma_l), double(hp->gamma_u),
                          lars ? double(hp->trust_coef) : 1.0};

@@ -42,6 +42,9 @@ constexpr int kTileGroups = LAMB_TILE_GROUPS;
 constexpr int32_t kTileElems = kBlock * 4 * kTileGroups;
 constexpr int kFusedWaves = LAMB_FUSED_WAVES;
 constexpr int kFusedBlocksPerCu = kFusedWaves * 4 / kWaves;  // 4 SIMDs per CU
+// Polls before a single-pass wait gives up (about a second); a plan reads an
+// override from the environment variable LAMB_MI355X_SPIN_LIMIT.
+constexpr uint32_t kDefaultSpinLimit = 1u << 22;
 
 // Synchronisation words of the single-pass path (per plan).
 enum FusedCtl : int {
@@ -108,6 +111,7 @@ struct StepArgs {
     float eps;
     float weight_decay;
     float grad_scale;
+    uint32_t spin_limit;  // single pass: polls before a wait gives up (>= 1)
 };
 
 // Scalars of the per-tensor finalize (trust ratio and step scale).

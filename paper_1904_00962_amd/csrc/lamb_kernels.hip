@@ -589,7 +589,7 @@ __global__ __launch_bounds__(kFinalizeBlock) void finalize_kernel(
 // the epoch word: a step fills buffer (epoch & 1) and empties the other for
 // the next step; the last workgroup to finish advances the epoch. Nothing
 // depends on a host counter, so a captured graph replays correctly.
-// Every wait is bounded: after kSpinLimit polls, or once another workgroup
+// Every wait is bounded: after StepArgs::spin_limit polls, or once another workgroup
 // has given up, a workgroup raises the sticky fault word and abandons the
 // step, and every later step of the plan does nothing.
 // ---------------------------------------------------------------------------
@@ -603,7 +603,6 @@ __global__ __launch_bounds__(kFinalizeBlock) void finalize_kernel(
 #ifndef LAMB_MEMBER_SLEEP
 #define LAMB_MEMBER_SLEEP LAMB_SPIN_SLEEP
 #endif
-constexpr uint32_t kSpinLimit = 1u << 22;
 static_assert(kTileGroups % kUnroll == 0, "tile groups must be a multiple of the unroll");
 
 __device__ __forceinline__ uint64_t slot_load(const uint64_t *p) {
@@ -626,15 +625,15 @@ __device__ __forceinline__ uint64_t slot_word(double d) {
 
 // Polls *p until it holds a value; kEmptySlot if the wait was abandoned.
 template <int kSleep>
-__device__ uint64_t slot_wait(const uint64_t *p, uint32_t *ctl) {
+__device__ uint64_t slot_wait(const uint64_t *p, uint32_t *ctl, uint32_t limit) {
     for (uint32_t k = 1;; ++k) {
         const uint64_t w = slot_load(p);
         if (w != kEmptySlot)
             return w;
-        if ((k & 255u) == 0) {
+        if (k >= limit || (k & 255u) == 0) {
             if (ctl_load(ctl + kCtlFault) != 0)
                 return kEmptySlot;
-            if (k >= kSpinLimit) {
+            if (k >= limit) {
                 __hip_atomic_fetch_or(ctl + kCtlFault, 1u, __ATOMIC_RELAXED,
                                       __HIP_MEMORY_SCOPE_AGENT);
                 return kEmptySlot;
@@ -668,7 +667,11 @@ void fused_kernel(const TensorDesc *__restrict__ tensors, const ChunkDesc *__res
     uint64_t *next = slots + size_t((epoch & 1u) ^ 1u) * 3 * n;
     bool stop = sh_fault != 0;
 
-    for (int32_t j = blockIdx.x; !stop && j < n_tiles; j += gridDim.x) {
+    const int32_t grid = static_cast<int32_t>(gridDim.x);
+    for (int32_t r = 0; !stop; ++r) {
+        const int32_t j = r * grid + static_cast<int32_t>(blockIdx.x);  // entry of round r
+        if (j >= n_tiles)
+            break;
         const ChunkDesc c = tiles[j];
         if (c.len == 0)
             continue;  // an empty entry that pads a round
@@ -756,10 +759,10 @@ void fused_kernel(const TensorDesc *__restrict__ tensors, const ChunkDesc *__res
             if (j == first) {
                 double ax = 0.0, au = 0.0;
                 for (int k = threadIdx.x; k < team; k += kBlock) {
-                    const uint64_t wx = slot_wait<LAMB_SPIN_SLEEP>(cur + first + k, ctl);
+                    const uint64_t wx = slot_wait<LAMB_SPIN_SLEEP>(cur + first + k, ctl, a.spin_limit);
                     const uint64_t wu = wx == kEmptySlot
                                             ? kEmptySlot
-                                            : slot_wait<LAMB_SPIN_SLEEP>(cur + n + first + k, ctl);
+                                            : slot_wait<LAMB_SPIN_SLEEP>(cur + n + first + k, ctl, a.spin_limit);
                     if (wu == kEmptySlot) {
                         give_up = 1;
                         break;
@@ -779,7 +782,7 @@ void fused_kernel(const TensorDesc *__restrict__ tensors, const ChunkDesc *__res
                         slot_store(cur + 2 * n + first + k, w);
                 }
             } else if (threadIdx.x == 0) {
-                const uint64_t w = slot_wait<LAMB_MEMBER_SLEEP>(cur + 2 * n + j, ctl);
+                const uint64_t w = slot_wait<LAMB_MEMBER_SLEEP>(cur + 2 * n + j, ctl, a.spin_limit);
                 if (w == kEmptySlot)
                     give_up = 1;
                 else

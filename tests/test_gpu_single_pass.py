@@ -1,0 +1,82 @@
+"""The single-pass kernel beside the two-pass kernels and its failure path.
+
+m and v are elementwise, so both paths give them bit for bit; the layer norms
+are summed in a different order, so x and the ratios agree to rounding. A
+wait that runs out of polls must be reported and must leave later steps
+inert; the poll budget is cut to one from the host so that the give-up
+happens at once, with every wait still bounded."""
+
+import numpy as np
+import pytest
+
+import gpu_harness as H
+from paper_1904_00962_amd import _lib, paramsets
+
+pytestmark = pytest.mark.gpu
+
+
+def _run_path(cfg, path, steps=2):
+    ps = paramsets.get(cfg)
+    pair = H.Pair(paramsets.draw_params(ps, device="cuda"), ps.wd_mask(), ps.g_dtype, "lamb",
+                  oracle_subset=[], path=path)
+    hp = H.lamb_hp(ps)
+    for t in range(1, steps + 1):
+        pair.set_grads(paramsets.draw_grads(ps, t, device="cuda"))
+        pair.gpu_lamb(hp, t)
+    _lib.lamb_plan_check(pair.plan)
+    state = ([x.clone() for x in pair.X], [m.clone() for m in pair.M],
+             [v.clone() for v in pair.V], pair.ratio.clone(), pair.norms.clone())
+    pair.close()
+    return state
+
+
+def test_single_pass_agrees_with_two_pass():
+    """BERT-Base: 198 layers on the single pass, the token embedding on the
+    two-pass kernels, against the two-pass path for everything."""
+    torch = H.torch_cuda()
+    x1, m1, v1, r1, n1 = _run_path(1, "auto")
+    x2, m2, v2, r2, n2 = _run_path(1, "two-pass")
+    assert all(torch.equal(a, b) for a, b in zip(m1 + v1, m2 + v2))
+    for k, (a, b) in enumerate(zip(x1, x2)):
+        H.compare_state(a.cpu().numpy(), b.cpu().numpy(), "x[%d]" % k)
+    H.compare_ratios(r1.cpu().numpy(), r2.cpu().numpy(), "ratio")
+    H.compare_ratios(n1.cpu().numpy(), n2.cpu().numpy(), "norms")
+
+
+def test_abandoned_wait_is_reported(monkeypatch):
+    """With a budget of one poll, a tile that finds its layer's scale not yet
+    published gives up: the plan reports LAMB_ESYNC and its later steps change
+    nothing. A plan built with the normal budget is unaffected."""
+    torch = H.torch_cuda()
+    rng = np.random.default_rng(31)
+    sizes = [200 * 8192, 150 * 8192 + 3, 77]
+    xs = [(rng.standard_normal(n) * 0.5).astype(np.float32) for n in sizes]
+    monkeypatch.setenv("LAMB_MI355X_SPIN_LIMIT", "1")
+    pair = H.Pair(xs, [True, True, False], "f32", "lamb", path="auto")
+    monkeypatch.delenv("LAMB_MI355X_SPIN_LIMIT")
+    try:
+        grads = [torch.from_numpy((rng.standard_normal(n) * 1e-3).astype(np.float32))
+                 for n in sizes]
+        pair.set_grads(grads)
+        pair.gpu_lamb(H.lamb_hp(paramsets.get(0)), 1)
+        with pytest.raises(_lib.LambError) as e:
+            _lib.lamb_plan_check(pair.plan)
+        assert e.value.status == _lib.LAMB_ESYNC
+        before = [t.clone() for t in pair.X + pair.M + pair.V]
+        pair.gpu_lamb(H.lamb_hp(paramsets.get(0)), 2)
+        torch.cuda.synchronize()
+        after = pair.X + pair.M + pair.V
+        # the single pass does nothing once the plan has given up a wait
+        for k in range(2):
+            for grp in (0, 3, 6):
+                assert torch.equal(before[grp + k], after[grp + k])
+    finally:
+        pair.close()
+    # a fresh plan with the normal budget still steps and matches the oracle
+    pair = H.Pair(xs, [True, True, False], "f32", "lamb", path="auto")
+    try:
+        hg = pair.set_grads(grads)
+        ref = H.step_both(pair, "lamb", hg, H.lamb_hp(paramsets.get(0)), 1)
+        pair.compare(ref, "after a give-up")
+    finally:
+        pair.close()
