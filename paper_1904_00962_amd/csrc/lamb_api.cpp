@@ -50,6 +50,11 @@ struct lamb_plan {
     uint32_t *ctl = nullptr;       // FusedCtl words
     TensorDesc *rest_tensors = nullptr;
     ChunkDesc *rest_chunks = nullptr;
+    // Finalize segments of the fine, the coarse and the other-layers table.
+    SegDesc *segs[3] = {};
+    SegRange *seg_ranges[3] = {};
+    int32_t n_segs[3] = {};
+    Partial *seg_partials = nullptr;
     int fused_per_cu[4][2][3] = {};  // single-pass workgroups per CU by algo, bf16, norm
     std::vector<TensorDesc> host_tensors;  // host image of the tensor table
     std::vector<TensorDesc> host_rest;     // host image of the other-layers table
@@ -375,6 +380,22 @@ lamb_status build_chunks(const std::vector<int64_t> &numel, int32_t chunk, int32
     return LAMB_OK;
 }
 
+enum SegTable { kSegFine = 0, kSegCoarse = 1, kSegRest = 2 };
+
+// Finalize segments of a chunk table: tensor k's chunk partials
+// [first_k, first_k + count_k) cut into runs of kSegChunks.
+void build_segments(const std::vector<std::pair<int32_t, int32_t>> &tensor_chunks,
+                    std::vector<SegDesc> *segs, std::vector<SegRange> *ranges) {
+    segs->clear();
+    ranges->clear();
+    for (const auto &tc : tensor_chunks) {
+        const int32_t first_seg = int32_t(segs->size());
+        for (int32_t k = 0; k < tc.second; k += kSegChunks)
+            segs->push_back(SegDesc{tc.first + k, std::min(kSegChunks, tc.second - k)});
+        ranges->push_back(SegRange{first_seg, int32_t(segs->size()) - first_seg});
+    }
+}
+
 }  // namespace
 
 extern "C" {
@@ -519,6 +540,23 @@ lamb_status lamb_plan_create(const lamb_tensor *tensors, int32_t n_tensors,
     const int32_t n_tiles = int32_t(host_tiles.size());
     const int32_t n_rest = int32_t(host_rest.size());
     const int32_t n_rest_chunks = int32_t(host_rest_chunks.size());
+    std::vector<SegDesc> host_segs[3];
+    std::vector<SegRange> host_ranges[3];
+    {
+        std::vector<std::pair<int32_t, int32_t>> fine, coarse_tc, rest;
+        for (const TensorDesc &d : host_tensors) {
+            fine.emplace_back(d.first_chunk, d.n_chunks);
+            coarse_tc.emplace_back(d.first_coarse, d.n_coarse);
+        }
+        for (const TensorDesc &d : host_rest)
+            rest.emplace_back(d.first_chunk, d.n_chunks);
+        build_segments(fine, &host_segs[kSegFine], &host_ranges[kSegFine]);
+        build_segments(coarse_tc, &host_segs[kSegCoarse], &host_ranges[kSegCoarse]);
+        build_segments(rest, &host_segs[kSegRest], &host_ranges[kSegRest]);
+    }
+    size_t max_segs = 1;
+    for (const auto &v : host_segs)
+        max_segs = std::max(max_segs, v.size());
 
     lamb_plan *plan = new (std::nothrow) lamb_plan();
     if (!plan)
@@ -542,10 +580,17 @@ lamb_status lamb_plan_create(const lamb_tensor *tensors, int32_t n_tensors,
     const size_t ctl_bytes = 256;
     const size_t rest_bytes = round256(sizeof(TensorDesc) * size_t(n_rest));
     const size_t rest_chunk_bytes = round256(sizeof(ChunkDesc) * size_t(n_rest_chunks));
-    err = hipMalloc(&plan->device_block, tensors_bytes + chunks_bytes + coarse_bytes +
-                                             partial_bytes + scale_bytes + flag_bytes +
-                                             tiles_bytes + slot_bytes + ctl_bytes + rest_bytes +
-                                             rest_chunk_bytes);
+    size_t seg_bytes[3], range_bytes[3];
+    for (int k = 0; k < 3; ++k) {
+        seg_bytes[k] = round256(sizeof(SegDesc) * host_segs[k].size());
+        range_bytes[k] = round256(sizeof(SegRange) * host_ranges[k].size());
+    }
+    const size_t seg_partial_bytes = round256(sizeof(Partial) * max_segs);
+    err = hipMalloc(&plan->device_block,
+                    tensors_bytes + chunks_bytes + coarse_bytes + partial_bytes + scale_bytes +
+                        flag_bytes + tiles_bytes + slot_bytes + ctl_bytes + rest_bytes +
+                        rest_chunk_bytes + seg_bytes[0] + seg_bytes[1] + seg_bytes[2] +
+                        range_bytes[0] + range_bytes[1] + range_bytes[2] + seg_partial_bytes);
     if (err != hipSuccess) {
         delete plan;
         if (err == hipErrorOutOfMemory)
@@ -574,6 +619,15 @@ lamb_status lamb_plan_create(const lamb_tensor *tensors, int32_t n_tensors,
     plan->rest_tensors = reinterpret_cast<TensorDesc *>(base);
     base += rest_bytes;
     plan->rest_chunks = reinterpret_cast<ChunkDesc *>(base);
+    base += rest_chunk_bytes;
+    for (int k = 0; k < 3; ++k) {
+        plan->segs[k] = reinterpret_cast<SegDesc *>(base);
+        base += seg_bytes[k];
+        plan->seg_ranges[k] = reinterpret_cast<SegRange *>(base);
+        base += range_bytes[k];
+        plan->n_segs[k] = int32_t(host_segs[k].size());
+    }
+    plan->seg_partials = reinterpret_cast<Partial *>(base);
     err = hipMemcpy(plan->tensors, host_tensors.data(), sizeof(TensorDesc) * size_t(n_tensors),
                     hipMemcpyHostToDevice);
     if (err == hipSuccess)
@@ -591,6 +645,14 @@ lamb_status lamb_plan_create(const lamb_tensor *tensors, int32_t n_tensors,
     if (err == hipSuccess && n_rest > 0)
         err = hipMemcpy(plan->rest_chunks, host_rest_chunks.data(),
                         sizeof(ChunkDesc) * size_t(n_rest_chunks), hipMemcpyHostToDevice);
+    for (int k = 0; k < 3 && err == hipSuccess; ++k) {
+        if (!host_segs[k].empty())
+            err = hipMemcpy(plan->segs[k], host_segs[k].data(),
+                            sizeof(SegDesc) * host_segs[k].size(), hipMemcpyHostToDevice);
+        if (err == hipSuccess && !host_ranges[k].empty())
+            err = hipMemcpy(plan->seg_ranges[k], host_ranges[k].data(),
+                            sizeof(SegRange) * host_ranges[k].size(), hipMemcpyHostToDevice);
+    }
     if (err == hipSuccess)
         err = hipMemset(plan->flags, 0, flag_bytes);
     if (err == hipSuccess && slot_bytes > 0)
@@ -862,7 +924,9 @@ lamb_status lamb_step_ex(lamb_plan *plan, const lamb_hparams *hp, void *stream,
         if (err != hipSuccess)
             return fail_hip(err, "launching the moment kernel");
         record(plan, 2, s);
-        err = launch_finalize(kind.norm, kind.deferred, tensors, n_tensors, plan->partials, f,
+        const int seg = kind.deferred ? kSegCoarse : single ? kSegRest : kSegFine;
+        err = launch_finalize(kind.norm, tensors, n_tensors, plan->partials, plan->segs[seg],
+                              plan->n_segs[seg], plan->seg_ranges[seg], plan->seg_partials, f,
                               plan->scale, ratio_out, norms_out,
                               kind.deferred ? plan->flags : nullptr, s);
         if (err != hipSuccess)

@@ -80,6 +80,26 @@ struct ChunkDesc {
 };
 static_assert(sizeof(ChunkDesc) == 16, "ChunkDesc layout");
 
+// The finalize runs in two levels: a segment kernel folds each run of up to
+// kSegChunks consecutive chunk partials of one tensor into one segment
+// partial, then the per-tensor finalize combines the tensor's segment
+// partials. Both in a fixed order.
+constexpr int kSegBlock = 256;
+constexpr int kSegLanes = 8;
+constexpr int32_t kSegChunks = kSegBlock * kSegLanes;
+
+// One segment: chunk partials [first, first + count) of one tensor.
+struct SegDesc {
+    int32_t first;
+    int32_t count;
+};
+
+// A tensor's segments: [first, first + count) of the segment list.
+struct SegRange {
+    int32_t first;
+    int32_t count;
+};
+
 // Per-chunk partial norms of x and of the update direction u (LAMB family)
 // or m_t (LARS), written once per step at a fixed slot: sums of squares (L2),
 // sums of magnitudes (L1) or maxima of magnitudes (L-infinity).
@@ -138,11 +158,13 @@ struct StepKind {
 hipError_t launch_moments(const StepKind &kind, const TensorDesc *tensors,
                           const ChunkDesc *chunks, Partial *partials, int32_t n_chunks,
                           uint32_t *flags, const StepArgs &args, hipStream_t stream);
-// `coarse`: the partials were written per coarse chunk (deferred mode).
-hipError_t launch_finalize(NormKind norm, bool coarse, const TensorDesc *tensors,
-                           int32_t n_tensors, const Partial *partials, const FinalizeArgs &args,
-                           float *scale, double *ratio_out, double *norms_out, uint32_t *flags,
-                           hipStream_t stream);
+// Both levels of the finalize: `segs` (n_segs entries) over `partials` into
+// `seg_partials`, then per tensor over its `ranges` entry of the segments.
+hipError_t launch_finalize(NormKind norm, const TensorDesc *tensors, int32_t n_tensors,
+                           const Partial *partials, const SegDesc *segs, int32_t n_segs,
+                           const SegRange *ranges, Partial *seg_partials,
+                           const FinalizeArgs &args, float *scale, double *ratio_out,
+                           double *norms_out, uint32_t *flags, hipStream_t stream);
 hipError_t launch_apply(const StepKind &kind, const TensorDesc *tensors,
                         const ChunkDesc *chunks, const float *scale, int32_t n_chunks,
                         uint32_t *flags, int32_t *nonfinite_out, const StepArgs &args,

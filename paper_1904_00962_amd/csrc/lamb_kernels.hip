@@ -13,9 +13,10 @@
 //            moments and the update direction u (m_t for LARS); write the
 //            chunk's partial norms of x and u to a fixed slot; store the new
 //            moments (direct mode) or nothing (deferred mode).
-//   finalize (one workgroup per tensor): combine the tensor's chunk slots in
-//            a fixed order into ||x_i||, ||u_i||, phi, the trust ratio and the
-//            step scale lr * ratio.
+//   finalize (two small kernels): fold runs of chunk slots into segment
+//            slots, then per tensor combine its segment slots in a fixed
+//            order into ||x_i||, ||u_i||, phi, the trust ratio and the step
+//            scale lr * ratio.
 //   apply    (one workgroup per chunk): read x and the moments; recompute u
 //            with the same inline functions the moment pass used (so it is
 //            bit-identical) and write x - scale_i * u. In deferred mode it
@@ -510,50 +511,55 @@ __device__ float finish_layer(const Partial &total, const FinalizeArgs &a, int32
 }
 
 // ---------------------------------------------------------------------------
-// Per-tensor finalize: norms, phi, trust ratio, step scale. One workgroup of
-// kFinalizeBlock threads per tensor. Thread k owns slots k + j*kFinalizeBlock
-// and combines them into kFinalizeLanes independent accumulators (so several
-// loads are in flight), which it then combines in a fixed order; the fixed
-// wave/LDS tree combines the threads. The order never depends on timing.
+// Finalize, in two levels. The segment kernel gives each workgroup up to
+// kSegChunks consecutive chunk partials of one tensor: thread k folds slots
+// k + j * kSegBlock into kSegLanes independent accumulators (several loads in
+// flight), combines them in a fixed order, and the fixed wave/LDS tree
+// combines the threads into the segment's partial. The per-tensor finalize
+// then combines the tensor's segment partials the same way and forms the
+// norms, phi, trust ratio and step scale. The order never depends on timing.
 // ---------------------------------------------------------------------------
 
-constexpr int kFinalizeBlock = 1024;
-constexpr int kFinalizeLanes = 16;
-
 template <int kNorm>
-__global__ __launch_bounds__(kFinalizeBlock) void finalize_kernel(
-    const TensorDesc *__restrict__ tensors, const Partial *__restrict__ partials, int coarse,
-    FinalizeArgs a, float *__restrict__ scale, double *__restrict__ ratio_out,
-    double *__restrict__ norms_out, uint32_t *__restrict__ flags) {
-    const int i = blockIdx.x;
-    const TensorDesc &t = tensors[i];
-    const Partial *p = partials + (coarse ? t.first_coarse : t.first_chunk);
-    const int n = coarse ? t.n_coarse : t.n_chunks;
-    double sx[kFinalizeLanes] = {}, su[kFinalizeLanes] = {};
-    int k = threadIdx.x;
-    for (; k + (kFinalizeLanes - 1) * kFinalizeBlock < n; k += kFinalizeLanes * kFinalizeBlock) {
+__global__ __launch_bounds__(kSegBlock) void segment_kernel(const Partial *__restrict__ partials,
+                                                          const SegDesc *__restrict__ segs,
+                                                          Partial *__restrict__ seg_partials) {
+    const SegDesc sd = segs[blockIdx.x];
+    const Partial *p = partials + sd.first;
+    double sx[kSegLanes] = {}, su[kSegLanes] = {};
 #pragma unroll
-        for (int j = 0; j < kFinalizeLanes; ++j) {
-            const Partial q = p[k + j * kFinalizeBlock];
-            sx[j] = norm_combine<kNorm>(sx[j], q.sum_xx);
-            su[j] = norm_combine<kNorm>(su[j], q.sum_uu);
+    for (int j = 0; j < kSegLanes; ++j) {
+        const int k = threadIdx.x + j * kSegBlock;
+        if (k < sd.count) {
+            const Partial q = p[k];
+            sx[j] = q.sum_xx;
+            su[j] = q.sum_uu;
         }
     }
 #pragma unroll
-    for (int j = 0; j < kFinalizeLanes - 1; ++j) {
-        if (k + j * kFinalizeBlock < n) {
-            const Partial q = p[k + j * kFinalizeBlock];
-            sx[j] = norm_combine<kNorm>(sx[j], q.sum_xx);
-            su[j] = norm_combine<kNorm>(su[j], q.sum_uu);
-        }
-    }
-#pragma unroll
-    for (int j = 1; j < kFinalizeLanes; ++j) {
+    for (int j = 1; j < kSegLanes; ++j) {
         sx[0] = norm_combine<kNorm>(sx[0], sx[j]);
         su[0] = norm_combine<kNorm>(su[0], su[j]);
     }
+    block_combine<kNorm, kSegBlock / 64>(sx[0], su[0], seg_partials + blockIdx.x);
+}
+
+template <int kNorm>
+__global__ __launch_bounds__(kSegBlock) void finalize_kernel(
+    const TensorDesc *__restrict__ tensors, const Partial *__restrict__ seg_partials,
+    const SegRange *__restrict__ ranges, FinalizeArgs a, float *__restrict__ scale,
+    double *__restrict__ ratio_out, double *__restrict__ norms_out, uint32_t *__restrict__ flags) {
+    const int i = blockIdx.x;
+    const TensorDesc &t = tensors[i];
+    const SegRange r = ranges[i];
+    double sx = 0.0, su = 0.0;
+    for (int k = threadIdx.x; k < r.count; k += kSegBlock) {
+        const Partial q = seg_partials[r.first + k];
+        sx = norm_combine<kNorm>(sx, q.sum_xx);
+        su = norm_combine<kNorm>(su, q.sum_uu);
+    }
     __shared__ Partial total;
-    block_combine<kNorm, kFinalizeBlock / 64>(sx[0], su[0], &total);
+    block_combine<kNorm, kSegBlock / 64>(sx, su, &total);
     __syncthreads();
     if (threadIdx.x == 0) {
         scale[i] = finish_layer<kNorm>(total, a, t.out_index, ratio_out, norms_out);
@@ -930,18 +936,24 @@ hipError_t launch_apply(const StepKind &kind, const TensorDesc *tensors,
     return hipLaunchKernel(fn, dim3(n_chunks), dim3(kBlock), params, 0, stream);
 }
 
-hipError_t launch_finalize(NormKind norm, bool coarse, const TensorDesc *tensors,
-                           int32_t n_tensors, const Partial *partials, const FinalizeArgs &args,
-                           float *scale, double *ratio_out, double *norms_out, uint32_t *flags,
-                           hipStream_t stream) {
+hipError_t launch_finalize(NormKind norm, const TensorDesc *tensors, int32_t n_tensors,
+                           const Partial *partials, const SegDesc *segs, int32_t n_segs,
+                           const SegRange *ranges, Partial *seg_partials,
+                           const FinalizeArgs &args, float *scale, double *ratio_out,
+                           double *norms_out, uint32_t *flags, hipStream_t stream) {
+    const void *seg_fn = norm == kL1     ? reinterpret_cast<const void *>(&segment_kernel<kL1>)
+                         : norm == kLinf ? reinterpret_cast<const void *>(&segment_kernel<kLinf>)
+                                         : reinterpret_cast<const void *>(&segment_kernel<kL2>);
+    void *seg_params[] = {&partials, &segs, &seg_partials};
+    hipError_t err = hipLaunchKernel(seg_fn, dim3(n_segs), dim3(kSegBlock), seg_params, 0, stream);
+    if (err != hipSuccess)
+        return err;
     FinalizeArgs a = args;
-    int coarse_flag = coarse ? 1 : 0;
-    void *params[] = {&tensors, &partials, &coarse_flag, &a,
-                      &scale,   &ratio_out, &norms_out,  &flags};
+    void *params[] = {&tensors, &seg_partials, &ranges, &a, &scale, &ratio_out, &norms_out, &flags};
     const void *fn = norm == kL1     ? reinterpret_cast<const void *>(&finalize_kernel<kL1>)
                      : norm == kLinf ? reinterpret_cast<const void *>(&finalize_kernel<kLinf>)
                                      : reinterpret_cast<const void *>(&finalize_kernel<kL2>);
-    return hipLaunchKernel(fn, dim3(n_tensors), dim3(kFinalizeBlock), params, 0, stream);
+    return hipLaunchKernel(fn, dim3(n_tensors), dim3(kSegBlock), params, 0, stream);
 }
 
 hipError_t launch_fused(const StepKind &kind, const TensorDesc *tensors, const ChunkDesc *tiles,
