@@ -344,15 +344,18 @@ LAMB_API lamb_status lamb_chunk_table(const int64_t *numel, int32_t n_tensors,
 
 /*
  * The single-pass schedule a plan would use (host only, no HIP call). The
- * single-pass kernel runs a persistent grid of `round` workgroups (4 per
- * compute unit); workgroup w takes entries w, w + round, ..., so the entry
- * list falls into rounds of `round` entries. A layer of at most `round`
- * tiles of 8192 elements takes the single pass: its tiles are consecutive
- * entries inside one round, tile j starting at element 8192 j. Layers are
- * packed first-fit by decreasing tile count (ties in table order); the gap
- * a full round leaves is filled with empty entries (tensor -1, length 0).
+ * single-pass kernel runs a persistent grid of `round` workgroups; workgroup
+ * w takes entries w, w + round, ..., so the entry list falls into rounds of
+ * `round` entries. A layer of at most `max_round` tiles of 8192 elements
+ * takes the single pass: its tiles are consecutive entries inside one round,
+ * tile j starting at element 8192 j. Layers are packed first-fit by
+ * decreasing tile count (ties in table order) into the fewest rounds of
+ * `max_round` entries; `round` is then the narrowest width that packs into
+ * as few rounds, so the rounds come out about equally full. The gap a
+ * round leaves is filled with empty entries (tensor -1, length 0). A plan
+ * uses max_round = 4 * (compute units).
  *   numel         host, n_tensors sizes (>= 1 each)
- *   round         entries per round, >= 1
+ *   max_round     widest round, >= 1
  *   capacity      length of the three entry arrays (0 with NULL arrays to
  *                 query the count)
  *   entry_tensor  host, layer of each entry or -1
@@ -360,15 +363,16 @@ LAMB_API lamb_status lamb_chunk_table(const int64_t *numel, int32_t n_tensors,
  *   entry_len     host, elements of each entry (0 for an empty entry)
  *   first_tile    host, n_tensors: the layer's first entry (0 if none)
  *   tiles         host, n_tensors: the layer's tile count, 0 when it takes
- *                 the two-pass kernels (more than `round` tiles)
+ *                 the two-pass kernels (more than `max_round` tiles)
  *   n_entries     receives the length of the list
+ *   round_out     receives the round width (the single-pass grid)
  * Errors: LAMB_ENULL, LAMB_EINVAL (including capacity too small, in which
- * case *n_entries, first_tile and tiles are still filled).
+ * case *n_entries, *round_out, first_tile and tiles are still filled).
  */
-LAMB_API lamb_status lamb_tile_schedule(const int64_t *numel, int32_t n_tensors, int32_t round,
-                               int32_t capacity, int32_t *entry_tensor, int64_t *entry_start,
-                               int32_t *entry_len, int32_t *first_tile, int32_t *tiles,
-                               int32_t *n_entries);
+LAMB_API lamb_status lamb_tile_schedule(const int64_t *numel, int32_t n_tensors,
+                               int32_t max_round, int32_t capacity, int32_t *entry_tensor,
+                               int64_t *entry_start, int32_t *entry_len, int32_t *first_tile,
+                               int32_t *tiles, int32_t *n_entries, int32_t *round_out);
 
 /*
  * Per-kernel timing with HIP events, for measurement. max_steps > 0 creates

@@ -124,7 +124,7 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
     lib.lamb_plan_tiles.argtypes = [vp, P(i32), P(i32)]
     lib.lamb_plan_check.argtypes = [vp, vp]
     lib.lamb_tile_schedule.argtypes = [P(i64), i32, i32, i32, P(i32), P(i64), P(i32), P(i32),
-                                       P(i32), P(i32)]
+                                       P(i32), P(i32), P(i32)]
     lib.lamb_status_str.argtypes = [i32]
     lib.lamb_status_str.restype = ctypes.c_char_p
     lib.lamb_last_error.argtypes = []
@@ -328,23 +328,23 @@ def lamb_plan_tiles(plan: Plan) -> Tuple[list, int]:
     return list(per), total.value
 
 
-def lamb_tile_schedule(numel: Sequence[int], round: int):
+def lamb_tile_schedule(numel: Sequence[int], max_round: int):
     """The single-pass schedule (host only): (entry_tensor, entry_start,
-    entry_len, first_tile, tiles) as lists; entry_tensor -1 marks an empty
-    entry."""
+    entry_len, first_tile, tiles, round) with lists for the first five;
+    entry_tensor -1 marks an empty entry, ``round`` is the grid width."""
     n = len(numel)
     arr = (ctypes.c_int64 * n)(*[int(v) for v in numel])
     first = (ctypes.c_int32 * n)()
     tiles = (ctypes.c_int32 * n)()
-    count = ctypes.c_int32()
+    count, width = ctypes.c_int32(), ctypes.c_int32()
     lib = load()
-    _check(lib.lamb_tile_schedule(arr, n, int(round), 0, None, None, None, first, tiles,
-                                  ctypes.byref(count)), "lamb_tile_schedule")
+    _check(lib.lamb_tile_schedule(arr, n, int(max_round), 0, None, None, None, first, tiles,
+                                  ctypes.byref(count), ctypes.byref(width)), "lamb_tile_schedule")
     k = count.value
     et, es, el = (ctypes.c_int32 * k)(), (ctypes.c_int64 * k)(), (ctypes.c_int32 * k)()
-    _check(lib.lamb_tile_schedule(arr, n, int(round), k, et, es, el, first, tiles,
-                                  ctypes.byref(count)), "lamb_tile_schedule")
-    return list(et), list(es), list(el), list(first), list(tiles)
+    _check(lib.lamb_tile_schedule(arr, n, int(max_round), k, et, es, el, first, tiles,
+                                  ctypes.byref(count), ctypes.byref(width)), "lamb_tile_schedule")
+    return list(et), list(es), list(el), list(first), list(tiles), width.value
 
 
 def lamb_plan_check(plan: Plan, stream: int = 0) -> None:

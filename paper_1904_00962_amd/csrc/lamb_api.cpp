@@ -282,47 +282,74 @@ lamb_status lamb_chunk_table(const int64_t *numel, int32_t n_tensors, int32_t ch
     return LAMB_OK;
 }
 
-lamb_status lamb_tile_schedule(const int64_t *numel, int32_t n_tensors, int32_t round,
+lamb_status lamb_tile_schedule(const int64_t *numel, int32_t n_tensors, int32_t max_round,
                                int32_t capacity, int32_t *entry_tensor, int64_t *entry_start,
                                int32_t *entry_len, int32_t *first_tile, int32_t *tiles,
-                               int32_t *n_entries) {
-    if (!numel || !n_entries || !first_tile || !tiles)
-        return fail(LAMB_ENULL, "numel, first_tile, tiles and n_entries must not be NULL");
+                               int32_t *n_entries, int32_t *round_out) {
+    if (!numel || !n_entries || !first_tile || !tiles || !round_out)
+        return fail(LAMB_ENULL, "numel, first_tile, tiles, n_entries and round_out must not be NULL");
     if (n_tensors < 1)
         return fail(LAMB_EINVAL, "n_tensors = %d, need >= 1", n_tensors);
-    if (round < 1)
-        return fail(LAMB_EINVAL, "round = %d, need >= 1", round);
+    if (max_round < 1)
+        return fail(LAMB_EINVAL, "max_round = %d, need >= 1", max_round);
     for (int32_t i = 0; i < n_tensors; ++i)
         if (numel[i] < 1)
             return fail(LAMB_EINVAL, "tensor %d has numel %lld, need >= 1", i,
                         static_cast<long long>(numel[i]));
-    // Layers of at most `round` tiles, packed first-fit by decreasing tile
-    // count (ties in table order) into rounds of `round` entries.
+    // Layers of at most `max_round` tiles, in decreasing tile count (ties in
+    // table order).
     std::vector<std::pair<int64_t, int32_t>> teams;
+    int64_t total_tiles = 0, largest = 0;
     for (int32_t i = 0; i < n_tensors; ++i) {
         const int64_t nt = (numel[i] + kTileElems - 1) / kTileElems;
         first_tile[i] = 0;
         tiles[i] = 0;
-        if (nt <= round)
+        if (nt <= max_round) {
             teams.emplace_back(nt, i);
+            total_tiles += nt;
+            largest = std::max(largest, nt);
+        }
     }
     std::stable_sort(teams.begin(), teams.end(),
                      [](const std::pair<int64_t, int32_t> &a, const std::pair<int64_t, int32_t> &b) {
                          return a.first > b.first;
                      });
+    // First-fit into rounds of `width` entries.
     std::vector<int64_t> fill;
     std::vector<std::vector<int32_t>> members;
-    for (const auto &team : teams) {
-        size_t r = 0;
-        while (r < fill.size() && fill[r] + team.first > round)
-            ++r;
-        if (r == fill.size()) {
-            fill.push_back(0);
-            members.emplace_back();
+    auto pack = [&](int64_t width) {
+        fill.clear();
+        members.clear();
+        for (const auto &team : teams) {
+            size_t r = 0;
+            while (r < fill.size() && fill[r] + team.first > width)
+                ++r;
+            if (r == fill.size()) {
+                fill.push_back(0);
+                members.emplace_back();
+            }
+            fill[r] += team.first;
+            members[r].push_back(team.second);
         }
-        fill[r] += team.first;
-        members[r].push_back(team.second);
+    };
+    // The fewest rounds, at the narrowest width that still needs no more:
+    // the rounds come out about equally full instead of full rounds and a
+    // short last one.
+    pack(max_round);
+    const size_t n_rounds = fill.size();
+    int64_t round = max_round;
+    if (n_rounds > 0) {
+        int64_t width = std::max(largest, (total_tiles + int64_t(n_rounds) - 1) / int64_t(n_rounds));
+        for (; width < max_round; ++width) {
+            pack(width);
+            if (fill.size() == n_rounds)
+                break;
+        }
+        if (width >= max_round)
+            pack(max_round);
+        round = std::min<int64_t>(width, max_round);
     }
+    *round_out = int32_t(round);
     const int64_t total =
         fill.empty() ? 0 : int64_t(round) * int64_t(fill.size() - 1) + fill.back();
     if (total > INT32_MAX / 8)
@@ -489,19 +516,19 @@ lamb_status lamb_plan_create(const lamb_tensor *tensors, int32_t n_tensors,
     // Single-pass schedule (lamb_tile_schedule): rounds of one tile per
     // workgroup of the persistent grid, which keeps kFusedBlocksPerCu
     // workgroups on every CU.
-    const int32_t round = int32_t(std::max<int64_t>(1, int64_t(kFusedBlocksPerCu) * cu_count));
+    const int32_t max_round = int32_t(std::max<int64_t>(1, int64_t(kFusedBlocksPerCu) * cu_count));
     std::vector<int32_t> first_tile(static_cast<size_t>(n_tensors)),
         tile_count(static_cast<size_t>(n_tensors));
-    int32_t n_entries = 0;
-    st = lamb_tile_schedule(numel.data(), n_tensors, round, 0, nullptr, nullptr, nullptr,
-                            first_tile.data(), tile_count.data(), &n_entries);
+    int32_t n_entries = 0, round = 0;
+    st = lamb_tile_schedule(numel.data(), n_tensors, max_round, 0, nullptr, nullptr, nullptr,
+                            first_tile.data(), tile_count.data(), &n_entries, &round);
     std::vector<int32_t> entry_tensor(static_cast<size_t>(n_entries)),
         entry_len(static_cast<size_t>(n_entries));
     std::vector<int64_t> entry_start(static_cast<size_t>(n_entries));
     if (st == LAMB_OK)
-        st = lamb_tile_schedule(numel.data(), n_tensors, round, n_entries, entry_tensor.data(),
-                                entry_start.data(), entry_len.data(), first_tile.data(),
-                                tile_count.data(), &n_entries);
+        st = lamb_tile_schedule(numel.data(), n_tensors, max_round, n_entries,
+                                entry_tensor.data(), entry_start.data(), entry_len.data(),
+                                first_tile.data(), tile_count.data(), &n_entries, &round);
     if (st != LAMB_OK)
         return st;
     std::vector<ChunkDesc> host_tiles(static_cast<size_t>(n_entries));
@@ -893,7 +920,7 @@ lamb_status lamb_step_ex(lamb_plan *plan, const lamb_hparams *hp, void *stream,
     if (single) {
         const int per_cu =
             plan->fused_per_cu[int(kind.algo)][kind.bf16_grad ? 1 : 0][int(kind.norm)];
-        // The tile list was packed in rounds of kFusedBlocksPerCu * CUs
+        // The tile list was packed in rounds of at most kFusedBlocksPerCu * CUs
         // entries; the grid is one round, so it must all be resident at once.
         if (per_cu < kFusedBlocksPerCu)
             return fail(LAMB_EHIP, "single-pass kernel keeps %d workgroups per CU resident, needs %d",

@@ -10,13 +10,20 @@ from paper_1904_00962_amd import _lib, paramsets
 TILE = 8192
 
 
-def _check_layout(numel, round_):
-    et, es, el, first, tiles = _lib.lamb_tile_schedule(numel, round_)
+def _check_layout(numel, max_round):
+    et, es, el, first, tiles, round_ = _lib.lamb_tile_schedule(numel, max_round)
     n = len(et)
+    assert 1 <= round_ <= max_round
+    n_rounds = -(-n // round_)
+    # the last round holds at least one entry; the rounds hold every tile
+    real = sum(tiles)
+    assert n == 0 or n > (n_rounds - 1) * round_
+    assert real <= n and n_rounds >= -(-real // max_round)
+    assert all(k <= round_ for k in tiles)
     seen = [False] * n
     for i, size in enumerate(numel):
         nt = -(-size // TILE)
-        if nt > round_:
+        if nt > max_round:
             assert tiles[i] == 0, "layer %d of %d tiles must take the two-pass path" % (i, nt)
             continue
         assert tiles[i] == nt
@@ -32,7 +39,7 @@ def _check_layout(numel, round_):
             assert et[j] == -1 and el[j] == 0
             assert j // round_ < (n - 1) // round_
             assert all(not seen[k] for k in range(j, (j // round_ + 1) * round_))
-    return et, first, tiles
+    return et, first, tiles, round_
 
 
 def _simulate(et, first, tiles, round_):
@@ -77,19 +84,29 @@ def _simulate(et, first, tiles, round_):
 def test_paramset_schedules(cfg):
     ps = paramsets.get(cfg)
     numel = [t.numel for t in ps.tensors]
-    et, first, tiles = _check_layout(numel, 1024)
-    _simulate(et, first, tiles, 1024)
+    et, first, tiles, round_ = _check_layout(numel, 1024)
+    _simulate(et, first, tiles, round_)
 
 
-def test_bert_large_packs_without_padding():
+def test_bert_large_layout():
     """BERT-Large on 256 CUs: every layer but the token embedding takes the
-    single pass, in 37 rounds with no empty entry."""
+    single pass, in 37 rounds with no empty entry. Two 512-tile FFN layers
+    fill a round, so no narrower round would do."""
     ps = paramsets.get(2)
     numel = [t.numel for t in ps.tensors]
-    et, first, tiles = _check_layout(numel, 1024)
+    et, first, tiles, round_ = _check_layout(numel, 1024)
     assert sum(1 for k in tiles if k == 0) == 1
-    assert -1 not in et
-    assert -(-len(et) // 1024) == 37
+    assert round_ == 1024 and -(-len(et) // round_) == 37 and -1 not in et
+
+
+def test_resnet50_rounds_are_balanced():
+    """ResNet-50's 3223 tiles need four rounds; they are packed four about
+    equal rounds instead of three full ones and a short one."""
+    ps = paramsets.get(3)
+    numel = [t.numel for t in ps.tensors]
+    et, first, tiles, round_ = _check_layout(numel, 1024)
+    assert -(-len(et) // round_) == 4 and sum(tiles) == 3223
+    assert round_ < 900
 
 
 @pytest.mark.parametrize("seed", range(12))
@@ -99,14 +116,19 @@ def test_random_layers_small_rounds(seed):
     n = int(rng.integers(1, 60))
     numel = [int(v) for v in rng.integers(1, TILE * (round_ + 3), size=n)]
     numel += [TILE * round_, TILE * round_ + 1, 1, TILE]
-    et, first, tiles = _check_layout(numel, round_)
+    et, first, tiles, width = _check_layout(numel, round_)
     if et:
-        _simulate(et, first, tiles, round_)
+        _simulate(et, first, tiles, width)
 
 
 def test_round_boundary_and_errors():
-    et, es, el, first, tiles = _lib.lamb_tile_schedule([TILE * 4, TILE * 4 + 1, 5], 4)
-    assert tiles == [4, 0, 1] and first == [0, 0, 4] and len(et) == 5
+    et, es, el, first, tiles, width = _lib.lamb_tile_schedule([TILE * 4, TILE * 4 + 1, 5], 4)
+    assert tiles == [4, 0, 1] and first == [0, 0, 4] and len(et) == 5 and width == 4
+    # three layers of 3, 3 and 2 tiles fill two rounds of 6 as {3, 3}, {2}; the
+    # narrowest width that still needs two rounds is 5: {3, 2}, {3}
+    et, es, el, first, tiles, width = _lib.lamb_tile_schedule([3 * TILE, 3 * TILE, 2 * TILE], 6)
+    assert width == 5 and tiles == [3, 3, 2] and len(et) == 8
+    assert et == [0, 0, 0, 2, 2, 1, 1, 1]
     with pytest.raises(_lib.LambError):
         _lib.lamb_tile_schedule([TILE], 0)
     with pytest.raises(_lib.LambError):
