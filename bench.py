@@ -244,8 +244,9 @@ def main() -> int:
         opt.attach_bf16_copies("allocate")
     n_tensors, n_chunks, chunk = _lib.lamb_plan_info(opt.plan)
     tiles_per_tensor, n_tiles = _lib.lamb_plan_tiles(opt.plan)
-    single = args.path == "auto" and not args.skip_nonfinite
+    single = args.path == "auto"
     P_single = sum(x.numel() for x, k in zip(xs, tiles_per_tensor) if k) if single else 0
+    checked = single and args.skip_nonfinite and P_single > 0
 
     # The oracle's sample is copied out before the GPU steps move x; the
     # oracle itself runs after the GPU timing, so the GPU is not left idle
@@ -265,7 +266,7 @@ def main() -> int:
     end.record()
     torch.cuda.synchronize()
     total_ms = start.elapsed_time(end)
-    (k_mom, k_fin, k_app, k_one), recorded = _lib.lamb_plan_timing(opt.plan)
+    (k_mom, k_fin, k_app, k_one, k_chk), recorded = _lib.lamb_plan_timing(opt.plan)
     _lib.lamb_plan_set_timing(opt.plan, 0)
     opt.check()
     ratios = opt.ratios.cpu()
@@ -283,15 +284,18 @@ def main() -> int:
     P_rest = P - P_single
     g_bytes = 2 if ps.g_dtype == "bf16" else 4
     copy_bytes = 2 if args.bf16_copy else 0  # the bf16 working copy of x
-    b_mom, b_app = bytes_per_param(args.algo, g_bytes, args.skip_nonfinite)
+    # a checked skip step runs the direct kernels after a read-only check of g
+    b_mom, b_app = bytes_per_param(args.algo, g_bytes, args.skip_nonfinite and not checked)
     b_app += copy_bytes
     b_one = single_pass_bytes(args.algo, g_bytes) + copy_bytes
-    avg_mom, avg_fin, avg_app, avg_one = (k / recorded for k in (k_mom, k_fin, k_app, k_one))
+    b_chk = g_bytes if checked else 0
+    avg_mom, avg_fin, avg_app, avg_one, avg_chk = (k / recorded for k in
+                                                   (k_mom, k_fin, k_app, k_one, k_chk))
     gbps = lambda b, n, ms: b * n / ms / 1e6 if ms > 0 and n else 0.0  # noqa: E731
     mom_gbps = gbps(b_mom, P_rest, avg_mom)
     app_gbps = gbps(b_app, P_rest, avg_app)
     one_gbps = gbps(b_one, P_single, avg_one)
-    step_bytes = b_one * P_single + (b_mom + b_app) * P_rest
+    step_bytes = b_one * P_single + (b_mom + b_app) * P_rest + b_chk * P
     step_gbps = step_bytes / ms_step / 1e6
     workload = ps.name if args.shard == 1 else "%s-shard-1of%d" % (ps.name, args.shard)
     src_hash = kernel_source_hash()
@@ -311,10 +315,10 @@ def main() -> int:
                    achieved=mom_gbps, bytes_per_launch=b_mom * P_rest,
                    traffic=counter_traffic("moments", workload, src_hash)
                    if default_mode else None)
-    eprint("step %.4f ms | single pass %.4f ms (%.0f GB/s, %d params) | moments %.4f ms "
-           "(%.0f GB/s) | finalize %.4f ms | apply %.4f ms (%.0f GB/s, %d params) | whole step "
-           "%.0f GB/s" % (ms_step, avg_one, one_gbps, P_single, avg_mom, mom_gbps, avg_fin,
-                          avg_app, app_gbps, P_rest, step_gbps))
+    eprint("step %.4f ms | check %.4f ms | single pass %.4f ms (%.0f GB/s, %d params) | moments "
+           "%.4f ms (%.0f GB/s) | finalize %.4f ms | apply %.4f ms (%.0f GB/s, %d params) | whole "
+           "step %.0f GB/s" % (ms_step, avg_chk, avg_one, one_gbps, P_single, avg_mom, mom_gbps,
+                               avg_fin, avg_app, app_gbps, P_rest, step_gbps))
     line = {
         "metric": METRIC,
         "value": P / (ms_step / 1e3),
@@ -343,7 +347,7 @@ def main() -> int:
         "hbm_frac_of_peak": step_gbps / HBM_PEAK_GBPS,
         "bytes_per_param": step_bytes / P,
         "kernels_ms": {"single_pass": avg_one, "moments": avg_mom, "finalize": avg_fin,
-                       "apply": avg_app, "steps_sampled": recorded},
+                       "apply": avg_app, "finite_check": avg_chk, "steps_sampled": recorded},
         "roofline": {
             "bound": "hbm", "kernel": dom["kernel"], "achieved": dom["achieved"],
             "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": dom["achieved"] / HBM_PEAK_GBPS,

@@ -122,7 +122,13 @@ typedef enum lamb_norm {
  *                      that reads x, g, m, v and writes m, v; a per-layer
  *                      finalize; an apply pass that reads x, m, v (and g for
  *                      N-LAMB / NN-LAMB) and writes x.
- * Deferred-mode steps (skip_nonfinite = 1) always take the two-pass kernels.
+ * skip_nonfinite = 1 on LAMB_PATH_AUTO (with any layer on the single pass)
+ * first reads every g once to take the step's verdict, then runs the same
+ * kernels as a direct step, which change nothing when the verdict is
+ * raised; the single pass runs last and reports the verdict. On
+ * LAMB_PATH_TWO_PASS it takes the deferred two-pass kernels: a read-only
+ * moment pass, then an apply pass that writes x, m, v unless the verdict
+ * is raised.
  * Both paths give the same m and v bit for bit; the layer norms are summed
  * in a different order, so ratios and x agree to rounding.
  */
@@ -387,10 +393,10 @@ LAMB_API lamb_status lamb_plan_set_timing(lamb_plan *plan, int32_t max_steps, in
 
 /*
  * Synchronise on the recorded events and return the summed durations in
- * milliseconds of the moment kernel, the finalize kernel, the apply kernel
- * and the single-pass kernel (kernel_ms[0..3], host; 0 for a kernel the
- * steps did not launch) over `steps` recorded steps (host); then start a
- * new recording window.
+ * milliseconds over `steps` recorded steps (host) of: kernel_ms[0] the
+ * moment kernel, [1] the finalize (both levels), [2] the apply kernel, [3]
+ * the single-pass kernel, [4] the finiteness check (host, 5 entries; 0 for
+ * a kernel the steps did not launch). Then start a new recording window.
  */
 LAMB_API lamb_status lamb_plan_timing(lamb_plan *plan, double *kernel_ms, int64_t *steps);
 

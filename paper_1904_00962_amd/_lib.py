@@ -303,14 +303,14 @@ def lamb_plan_set_timing(plan: Plan, max_steps: int, every: int = 1) -> None:
            "lamb_plan_set_timing")
 
 
-def lamb_plan_timing(plan: Plan) -> Tuple[Tuple[float, float, float, float], int]:
-    """Summed (moments, finalize, apply, single-pass) kernel milliseconds and
-    the step count."""
-    ms = (ctypes.c_double * 4)()
+def lamb_plan_timing(plan: Plan) -> Tuple[Tuple[float, float, float, float, float], int]:
+    """Summed (moments, finalize, apply, single-pass, finiteness-check) kernel
+    milliseconds and the step count."""
+    ms = (ctypes.c_double * 5)()
     steps = ctypes.c_int64()
     _check(load().lamb_plan_timing(_vp(plan.handle), ms, ctypes.byref(steps)),
            "lamb_plan_timing")
-    return (ms[0], ms[1], ms[2], ms[3]), steps.value
+    return tuple(ms[k] for k in range(5)), steps.value
 
 
 def lamb_plan_set_path(plan: Plan, path="auto") -> None:

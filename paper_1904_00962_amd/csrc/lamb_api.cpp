@@ -59,8 +59,15 @@ struct lamb_plan {
     std::vector<TensorDesc> host_tensors;  // host image of the tensor table
     std::vector<TensorDesc> host_rest;     // host image of the other-layers table
     std::vector<std::pair<uintptr_t, uintptr_t>> ranges;  // sorted buffer ranges of the table
-    // timing hooks: kEvents events per recorded step
+    // finiteness check of skip_nonfinite steps that take the single pass
+    ChunkDesc *check_chunks = nullptr;
+    int32_t n_check = 0;
+    // timing hooks: up to kEvents events per recorded step, in launch order,
+    // with the kernel kind of each interval
     std::vector<hipEvent_t> events;
+    std::vector<uint8_t> timing_kinds;
+    std::vector<uint8_t> timing_count;
+    int timing_next = 0;
     int32_t timing_capacity = 0;
     int32_t timing_used = 0;
     int32_t timing_every = 1;      // record one step in timing_every
@@ -70,7 +77,10 @@ struct lamb_plan {
 
 namespace {
 
-constexpr int kEvents = 5;  // before single pass, moments, finalize, apply, after
+// Kernel kinds of the timing hooks (the index in lamb_plan_timing's output).
+enum TimedKernel : uint8_t { kTimedMoments = 0, kTimedFinalize = 1, kTimedApply = 2,
+                             kTimedSingle = 3, kTimedCheck = 4, kTimedKinds = 5 };
+constexpr int kEvents = kTimedKinds + 1;  // at most one interval per kind
 
 thread_local char g_last_error[512] = "";
 
@@ -141,16 +151,24 @@ lamb_status check_phi_bounds(float gamma_l, float gamma_u) {
     return LAMB_OK;
 }
 
-// Timing hooks: begin_timing decides whether this step is recorded.
-void begin_timing(lamb_plan *plan) {
+// Timing hooks: begin_timing decides whether this step is recorded and
+// records its first event; mark() records the event after a kernel.
+void begin_timing(lamb_plan *plan, hipStream_t stream) {
     plan->timing_this_step = plan->timing_used < plan->timing_capacity &&
                              plan->timing_seen % plan->timing_every == 0;
     ++plan->timing_seen;
+    plan->timing_next = 0;
+    if (plan->timing_this_step)
+        (void)hipEventRecord(plan->events[size_t(plan->timing_used) * kEvents], stream);
 }
 
-void record(lamb_plan *plan, int slot, hipStream_t stream) {
-    if (plan->timing_this_step)
-        (void)hipEventRecord(plan->events[size_t(plan->timing_used) * kEvents + slot], stream);
+void mark(lamb_plan *plan, TimedKernel kind, hipStream_t stream) {
+    if (!plan->timing_this_step || plan->timing_next >= kEvents - 1)
+        return;
+    const size_t k = size_t(plan->timing_used);
+    plan->timing_kinds[k * (kEvents - 1) + size_t(plan->timing_next)] = kind;
+    ++plan->timing_next;
+    (void)hipEventRecord(plan->events[k * kEvents + size_t(plan->timing_next)], stream);
 }
 
 // Single-pass launches of one process on one device run one at a time: each
@@ -168,15 +186,17 @@ std::mutex g_gate_mutex;
 std::vector<FusedGate> g_gates;  // by device; events live until the process ends
 
 hipError_t gated_fused_launch(int device, hipStream_t stream, const StepKind &kind,
-                              const lamb_plan *plan, int32_t grid, const StepArgs &a,
-                              const FinalizeArgs &f, double *ratio_out, double *norms_out) {
+                              const lamb_plan *plan, int32_t grid, bool guarded,
+                              int32_t *nonfinite_out, const StepArgs &a, const FinalizeArgs &f,
+                              double *ratio_out, double *norms_out) {
     hipStreamCaptureStatus capture = hipStreamCaptureStatusNone;
     hipError_t err = hipStreamIsCapturing(stream, &capture);
     if (err != hipSuccess)
         return err;
     if (capture != hipStreamCaptureStatusNone)
         return launch_fused(kind, plan->tensors, plan->tiles, plan->n_tiles, grid, plan->slots,
-                            plan->ctl, a, f, ratio_out, norms_out, stream);
+                            plan->ctl, plan->flags, guarded, nonfinite_out, a, f, ratio_out,
+                            norms_out, stream);
     std::lock_guard<std::mutex> lock(g_gate_mutex);
     if (g_gates.size() <= size_t(device))
         g_gates.resize(size_t(device) + 1);
@@ -192,7 +212,8 @@ hipError_t gated_fused_launch(int device, hipStream_t stream, const StepKind &ki
             return err;
     }
     err = launch_fused(kind, plan->tensors, plan->tiles, plan->n_tiles, grid, plan->slots,
-                       plan->ctl, a, f, ratio_out, norms_out, stream);
+                       plan->ctl, plan->flags, guarded, nonfinite_out, a, f, ratio_out, norms_out,
+                       stream);
     if (err != hipSuccess)
         return err;
     err = hipEventRecord(gate.done, stream);
@@ -204,8 +225,10 @@ hipError_t gated_fused_launch(int device, hipStream_t stream, const StepKind &ki
 }
 
 void end_timing(lamb_plan *plan) {
-    if (plan->timing_this_step)
+    if (plan->timing_this_step) {
+        plan->timing_count[size_t(plan->timing_used)] = uint8_t(plan->timing_next);
         ++plan->timing_used;
+    }
     plan->timing_this_step = false;
 }
 
@@ -505,6 +528,12 @@ lamb_status lamb_plan_create(const lamb_tensor *tensors, int32_t n_tensors,
     st = build_chunks(numel, chunk, n_chunks, &host_chunks);
     if (st == LAMB_OK)
         st = build_chunks(numel, coarse, n_coarse, &host_coarse);
+    std::vector<ChunkDesc> host_check;
+    const int64_t n_check64 = count_chunks(numel.data(), n_tensors, kCheckElems);
+    if (st == LAMB_OK && n_check64 < 0)
+        st = fail(LAMB_EINVAL, "too many finiteness-check chunks");
+    if (st == LAMB_OK)
+        st = build_chunks(numel, kCheckElems, int32_t(n_check64), &host_check);
     if (st != LAMB_OK)
         return st;
     int device = 0, cu_count = 0;
@@ -613,11 +642,13 @@ lamb_status lamb_plan_create(const lamb_tensor *tensors, int32_t n_tensors,
         range_bytes[k] = round256(sizeof(SegRange) * host_ranges[k].size());
     }
     const size_t seg_partial_bytes = round256(sizeof(Partial) * max_segs);
+    const size_t check_bytes = round256(sizeof(ChunkDesc) * host_check.size());
     err = hipMalloc(&plan->device_block,
                     tensors_bytes + chunks_bytes + coarse_bytes + partial_bytes + scale_bytes +
                         flag_bytes + tiles_bytes + slot_bytes + ctl_bytes + rest_bytes +
                         rest_chunk_bytes + seg_bytes[0] + seg_bytes[1] + seg_bytes[2] +
-                        range_bytes[0] + range_bytes[1] + range_bytes[2] + seg_partial_bytes);
+                        range_bytes[0] + range_bytes[1] + range_bytes[2] + seg_partial_bytes +
+                        check_bytes);
     if (err != hipSuccess) {
         delete plan;
         if (err == hipErrorOutOfMemory)
@@ -655,6 +686,9 @@ lamb_status lamb_plan_create(const lamb_tensor *tensors, int32_t n_tensors,
         plan->n_segs[k] = int32_t(host_segs[k].size());
     }
     plan->seg_partials = reinterpret_cast<Partial *>(base);
+    base += seg_partial_bytes;
+    plan->check_chunks = reinterpret_cast<ChunkDesc *>(base);
+    plan->n_check = int32_t(host_check.size());
     err = hipMemcpy(plan->tensors, host_tensors.data(), sizeof(TensorDesc) * size_t(n_tensors),
                     hipMemcpyHostToDevice);
     if (err == hipSuccess)
@@ -680,6 +714,9 @@ lamb_status lamb_plan_create(const lamb_tensor *tensors, int32_t n_tensors,
             err = hipMemcpy(plan->seg_ranges[k], host_ranges[k].data(),
                             sizeof(SegRange) * host_ranges[k].size(), hipMemcpyHostToDevice);
     }
+    if (err == hipSuccess)
+        err = hipMemcpy(plan->check_chunks, host_check.data(),
+                        sizeof(ChunkDesc) * host_check.size(), hipMemcpyHostToDevice);
     if (err == hipSuccess)
         err = hipMemset(plan->flags, 0, flag_bytes);
     if (err == hipSuccess && slot_bytes > 0)
@@ -909,9 +946,15 @@ lamb_status lamb_step_ex(lamb_plan *plan, const lamb_hparams *hp, void *stream,
     const bool lars = hp->variant == LAMB_VARIANT_LARS;
     const FinalizeArgs f{double(hp->lr), double(hp->gamma_l), double(hp->gamma_u),
                          lars ? double(hp->trust_coef) : 1.0};
-    // The single pass serves direct-mode steps of the layers that fit; the
-    // two-pass kernels take the rest (or everything).
-    const bool single = plan->path == LAMB_PATH_AUTO && !kind.deferred && plan->n_tiles > 0;
+    // The single pass serves the layers that fit; the two-pass kernels take
+    // the rest (or everything on LAMB_PATH_TWO_PASS). A skip_nonfinite step
+    // on the single pass first takes its verdict with a read-only check of g,
+    // then runs the direct-mode kernels, which skip when it is raised; the
+    // single pass goes last and reports it.
+    const bool single = plan->path == LAMB_PATH_AUTO && plan->n_tiles > 0;
+    const bool checked = single && kind.deferred;
+    StepKind direct = kind;
+    direct.deferred = false;
 
     DeviceGuard guard(plan->device);
     if (guard.status != hipSuccess)
@@ -928,46 +971,57 @@ lamb_status lamb_step_ex(lamb_plan *plan, const lamb_hparams *hp, void *stream,
         grid = std::min(plan->n_tiles, plan->round);
     }
     hipStream_t s = static_cast<hipStream_t>(stream);
-    begin_timing(plan);
-    record(plan, 0, s);
-    if (single) {
-        hipError_t err = gated_fused_launch(plan->device, s, kind, plan, grid, a, f, ratio_out,
-                                            norms_out);
+    begin_timing(plan, s);
+    if (checked) {
+        hipError_t err = launch_finite(kind.bf16_grad, plan->tensors, plan->check_chunks,
+                                       plan->n_check, plan->flags, plan->ctl, a.grad_scale, s);
+        if (err != hipSuccess)
+            return fail_hip(err, "launching the finiteness check");
+        mark(plan, kTimedCheck, s);
+    }
+    if (single && !checked) {
+        hipError_t err = gated_fused_launch(plan->device, s, direct, plan, grid, false, nullptr, a,
+                                            f, ratio_out, norms_out);
         if (err != hipSuccess)
             return fail_hip(err, "launching the single-pass kernel");
+        mark(plan, kTimedSingle, s);
     }
-    record(plan, 1, s);
-    const bool two_pass = !single || plan->n_rest > 0;
-    const TensorDesc *tensors = single ? plan->rest_tensors : plan->tensors;
-    const int32_t n_tensors = single ? plan->n_rest : plan->n_tensors;
-    const ChunkDesc *chunks = single ? plan->rest_chunks : plan->chunks;
-    const int32_t n_chunks = single ? plan->n_rest_chunks : plan->n_chunks;
-    if (two_pass) {
+    if (!single || plan->n_rest > 0) {
+        const StepKind &k2 = single ? direct : kind;
+        const TensorDesc *tensors = single ? plan->rest_tensors : plan->tensors;
+        const int32_t n_tensors = single ? plan->n_rest : plan->n_tensors;
+        const ChunkDesc *chunks = single ? plan->rest_chunks : plan->chunks;
+        const int32_t n_chunks = single ? plan->n_rest_chunks : plan->n_chunks;
+        const uint32_t *guard_ctl = checked ? plan->ctl : nullptr;
         // Deferred moment passes only read, and use the coarse chunk table.
-        const ChunkDesc *moment_chunks = kind.deferred ? plan->coarse_chunks : chunks;
-        const int32_t n_moment_chunks = kind.deferred ? plan->n_coarse : n_chunks;
-        hipError_t err = launch_moments(kind, tensors, moment_chunks, plan->partials,
-                                        n_moment_chunks, plan->flags, a, s);
+        const ChunkDesc *moment_chunks = k2.deferred ? plan->coarse_chunks : chunks;
+        const int32_t n_moment_chunks = k2.deferred ? plan->n_coarse : n_chunks;
+        hipError_t err = launch_moments(k2, tensors, moment_chunks, plan->partials,
+                                        n_moment_chunks, plan->flags, guard_ctl, a, s);
         if (err != hipSuccess)
             return fail_hip(err, "launching the moment kernel");
-        record(plan, 2, s);
-        const int seg = kind.deferred ? kSegCoarse : single ? kSegRest : kSegFine;
-        err = launch_finalize(kind.norm, tensors, n_tensors, plan->partials, plan->segs[seg],
+        mark(plan, kTimedMoments, s);
+        const int seg = k2.deferred ? kSegCoarse : single ? kSegRest : kSegFine;
+        err = launch_finalize(k2.norm, tensors, n_tensors, plan->partials, plan->segs[seg],
                               plan->n_segs[seg], plan->seg_ranges[seg], plan->seg_partials, f,
                               plan->scale, ratio_out, norms_out,
-                              kind.deferred ? plan->flags : nullptr, s);
+                              k2.deferred ? plan->flags : nullptr, s);
         if (err != hipSuccess)
             return fail_hip(err, "launching the finalize kernel");
-        record(plan, 3, s);
-        err = launch_apply(kind, tensors, chunks, plan->scale, n_chunks, plan->flags,
-                           nonfinite_out, a, s);
+        mark(plan, kTimedFinalize, s);
+        err = launch_apply(k2, tensors, chunks, plan->scale, n_chunks, plan->flags, guard_ctl,
+                           k2.deferred ? nonfinite_out : nullptr, a, s);
         if (err != hipSuccess)
             return fail_hip(err, "launching the apply kernel");
-    } else {
-        record(plan, 2, s);
-        record(plan, 3, s);
+        mark(plan, kTimedApply, s);
     }
-    record(plan, 4, s);
+    if (checked) {
+        hipError_t err = gated_fused_launch(plan->device, s, direct, plan, grid, true,
+                                            nonfinite_out, a, f, ratio_out, norms_out);
+        if (err != hipSuccess)
+            return fail_hip(err, "launching the single-pass kernel");
+        mark(plan, kTimedSingle, s);
+    }
     end_timing(plan);
     return LAMB_OK;
 }
@@ -1162,6 +1216,8 @@ lamb_status lamb_plan_set_timing(lamb_plan *plan, int32_t max_steps, int32_t eve
     if (max_steps == 0)
         return LAMB_OK;
     plan->events.assign(size_t(max_steps) * kEvents, nullptr);
+    plan->timing_kinds.assign(size_t(max_steps) * (kEvents - 1), uint8_t(0));
+    plan->timing_count.assign(size_t(max_steps), uint8_t(0));
     for (size_t k = 0; k < plan->events.size(); ++k) {
         hipError_t err = hipEventCreate(&plan->events[k]);
         if (err != hipSuccess) {
@@ -1183,20 +1239,20 @@ lamb_status lamb_plan_timing(lamb_plan *plan, double *kernel_ms, int64_t *steps)
     DeviceGuard guard(plan->device);
     if (guard.status != hipSuccess)
         return fail_hip(guard.status, "selecting the plan's device");
-    kernel_ms[0] = kernel_ms[1] = kernel_ms[2] = kernel_ms[3] = 0.0;
-    // events: before the single pass, after it, after moments, finalize, apply
-    static const int kFrom[4] = {1, 2, 3, 0};
+    for (int j = 0; j < kTimedKinds; ++j)
+        kernel_ms[j] = 0.0;
     for (int32_t k = 0; k < plan->timing_used; ++k) {
         hipEvent_t *e = &plan->events[size_t(k) * kEvents];
-        hipError_t err = hipEventSynchronize(e[kEvents - 1]);
+        const int n = plan->timing_count[size_t(k)];
+        hipError_t err = hipEventSynchronize(e[n]);
         if (err != hipSuccess)
             return fail_hip(err, "hipEventSynchronize");
-        for (int j = 0; j < 4; ++j) {
+        for (int j = 0; j < n; ++j) {
             float ms = 0.0f;
-            err = hipEventElapsedTime(&ms, e[kFrom[j]], e[kFrom[j] + 1]);
+            err = hipEventElapsedTime(&ms, e[j], e[j + 1]);
             if (err != hipSuccess)
                 return fail_hip(err, "hipEventElapsedTime");
-            kernel_ms[j] += ms;
+            kernel_ms[plan->timing_kinds[size_t(k) * (kEvents - 1) + size_t(j)]] += ms;
         }
     }
     *steps = plan->timing_used;

@@ -150,14 +150,25 @@ struct StepKind {
                     // writes x, m, v unless a scaled gradient was non-finite
 };
 
+// The plan's flag words: [0] raised by a deferred-mode moment pass, [1] the
+// verdict the finalize hands to the deferred apply pass; [2] and [3] the
+// verdict of a skip_nonfinite step that checks the gradient first, selected
+// by the single pass's epoch (kVerdictWord + (epoch & 1)).
+constexpr int kVerdictWord = 2;
+// Elements per chunk of the finiteness check.
+constexpr int32_t kCheckElems = 16384;
+
 // Kernel launchers (lamb_kernels.hip). Each returns the launch status.
 // `flags` points at the plan's two non-finite words (deferred mode only): the
 // moment pass raises flags[0], the finalize moves it to flags[1] and clears
 // flags[0], the apply pass reads flags[1]. Nothing depends on a host counter,
 // so a captured graph replays correctly. `nonfinite_out` may be null.
+// `guard_ctl` non-null (direct mode only): return at once when the verdict
+// word of the epoch in guard_ctl is raised.
 hipError_t launch_moments(const StepKind &kind, const TensorDesc *tensors,
                           const ChunkDesc *chunks, Partial *partials, int32_t n_chunks,
-                          uint32_t *flags, const StepArgs &args, hipStream_t stream);
+                          uint32_t *flags, const uint32_t *guard_ctl, const StepArgs &args,
+                          hipStream_t stream);
 // Both levels of the finalize: `segs` (n_segs entries) over `partials` into
 // `seg_partials`, then per tensor over its `ranges` entry of the segments.
 hipError_t launch_finalize(NormKind norm, const TensorDesc *tensors, int32_t n_tensors,
@@ -167,8 +178,12 @@ hipError_t launch_finalize(NormKind norm, const TensorDesc *tensors, int32_t n_t
                            double *norms_out, uint32_t *flags, hipStream_t stream);
 hipError_t launch_apply(const StepKind &kind, const TensorDesc *tensors,
                         const ChunkDesc *chunks, const float *scale, int32_t n_chunks,
-                        uint32_t *flags, int32_t *nonfinite_out, const StepArgs &args,
-                        hipStream_t stream);
+                        uint32_t *flags, const uint32_t *guard_ctl, int32_t *nonfinite_out,
+                        const StepArgs &args, hipStream_t stream);
+// The finiteness check over `chunks` (all tensors, kCheckElems each).
+hipError_t launch_finite(bool bf16_grad, const TensorDesc *tensors, const ChunkDesc *chunks,
+                         int32_t n_chunks, uint32_t *flags, const uint32_t *ctl, float grad_scale,
+                         hipStream_t stream);
 
 // Single-pass kernel over the `n_tiles` tiles of the layers with n_tiles > 0,
 // on a persistent grid of `grid` workgroups. `slots` holds 2 x 3 x n_tiles
@@ -176,8 +191,13 @@ hipError_t launch_apply(const StepKind &kind, const TensorDesc *tensors,
 // step by the epoch in `ctl`), all initialised to kEmptySlot; `ctl` holds the
 // FusedCtl words, initialised to 0.
 constexpr uint64_t kEmptySlot = ~uint64_t(0);
+// `guarded`: a skip_nonfinite step, whose verdict word the finiteness check
+// raised or not; the last workgroup writes it to `nonfinite_out` (may be
+// null). Every step's last workgroup clears the verdict word of the next
+// epoch.
 hipError_t launch_fused(const StepKind &kind, const TensorDesc *tensors, const ChunkDesc *tiles,
                         int32_t n_tiles, int32_t grid, uint64_t *slots, uint32_t *ctl,
+                        uint32_t *flags, bool guarded, int32_t *nonfinite_out,
                         const StepArgs &args, const FinalizeArgs &fargs, double *ratio_out,
                         double *norms_out, hipStream_t stream);
 // Workgroups of the single-pass kernel for `kind` that fit on one CU at once.

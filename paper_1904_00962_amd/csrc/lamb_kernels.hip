@@ -307,11 +307,20 @@ __device__ __forceinline__ uint32_t apply_chunk_index() {
 // Moment pass.
 // ---------------------------------------------------------------------------
 
+// A direct-mode pass of a step whose verdict the finiteness check already
+// took (`ctl` non-null) returns at once when that verdict is raised.
+__device__ __forceinline__ bool verdict_raised(const uint32_t *flags, const uint32_t *ctl) {
+    return ctl && flags[kVerdictWord + (ctl[kCtlEpoch] & 1u)] != 0;
+}
+
 template <int kAlgo, bool kBf16, int kNorm, bool kDeferred>
 __global__ __launch_bounds__(kBlock) void moments_kernel(
     const TensorDesc *__restrict__ tensors, const ChunkDesc *__restrict__ chunks,
-    Partial *__restrict__ partials, uint32_t *__restrict__ flags, StepArgs a) {
+    Partial *__restrict__ partials, uint32_t *__restrict__ flags, const uint32_t *__restrict__ ctl,
+    StepArgs a) {
     constexpr bool kV = kHasSecondMoment<kAlgo>;
+    if (!kDeferred && verdict_raised(flags, ctl))
+        return;
     const ChunkDesc c = chunks[chunk_index()];
     const TensorDesc &t = tensors[c.tensor];
     gcfloat *x = global_view(static_cast<const float *>(t.x) + c.start);
@@ -395,10 +404,12 @@ __global__ __launch_bounds__(kBlock) void moments_kernel(
 template <int kAlgo, bool kBf16, bool kDeferred>
 __global__ __launch_bounds__(kBlock) void apply_kernel(
     const TensorDesc *__restrict__ tensors, const ChunkDesc *__restrict__ chunks,
-    const float *__restrict__ scale, uint32_t *__restrict__ flags,
+    const float *__restrict__ scale, uint32_t *__restrict__ flags, const uint32_t *__restrict__ ctl,
     int32_t *__restrict__ nonfinite_out, StepArgs a) {
     constexpr bool kV = kHasSecondMoment<kAlgo>;
     constexpr bool kReadsGrad = kDeferred || kDirectionNeedsGrad<kAlgo>;
+    if (!kDeferred && verdict_raised(flags, ctl))
+        return;
     if constexpr (kDeferred) {
         // The finalize moved the moment pass's verdict (raised if any scaled
         // gradient was NaN or infinite) into flags[1].
@@ -511,6 +522,37 @@ __device__ float finish_layer(const Partial &total, const FinalizeArgs &a, int32
 }
 
 // ---------------------------------------------------------------------------
+// Finiteness check: the verdict of a skip_nonfinite step taken before
+// anything is written (the step then runs the direct-mode kernels, which
+// return at once when the verdict is raised). Reads g only; a chunk that
+// finds a NaN or infinite scaled gradient raises the step's verdict word,
+// selected by the single pass's epoch, with one integer atomicOr.
+// ---------------------------------------------------------------------------
+
+template <bool kBf16>
+__global__ __launch_bounds__(kBlock) void finite_kernel(const TensorDesc *__restrict__ tensors,
+                                                       const ChunkDesc *__restrict__ chunks,
+                                                       uint32_t *__restrict__ flags,
+                                                       const uint32_t *__restrict__ ctl,
+                                                       float grad_scale) {
+    const ChunkDesc c = chunks[blockIdx.x];
+    const TensorDesc &t = tensors[c.tensor];
+    const GradView<kBf16> g(t.g, c.start, grad_scale);
+    bool bad = false;
+    const int n4 = c.len >> 2;
+#pragma unroll 4
+    for (int q = threadIdx.x; q < n4; q += kBlock) {
+        const f32x4 v = g.at4(4 * q);
+        bad |= !(isfinite(v.x) && isfinite(v.y) && isfinite(v.z) && isfinite(v.w));
+    }
+    const int tail = 4 * n4 + threadIdx.x;
+    if (tail < c.len)
+        bad |= !isfinite(g.at(tail));
+    if (__syncthreads_or(bad) && threadIdx.x == 0)
+        atomicOr(flags + kVerdictWord + (ctl[kCtlEpoch] & 1u), 1u);
+}
+
+// ---------------------------------------------------------------------------
 // Finalize, in two levels. The segment kernel gives each workgroup up to
 // kSegChunks consecutive chunk partials of one tensor: thread k folds slots
 // k + j * kSegBlock into kSegLanes independent accumulators (several loads in
@@ -593,7 +635,8 @@ __global__ __launch_bounds__(kSegBlock) void finalize_kernel(
 // are coherent across the XCDs' separate L2 caches. An empty slot holds
 // kEmptySlot, which no published value equals. Two slot buffers alternate by
 // the epoch word: a step fills buffer (epoch & 1) and empties the other for
-// the next step; the last workgroup to finish advances the epoch. Nothing
+// the next step; the last workgroup to finish advances the epoch (a step
+// skipped for a non-finite gradient touches no slot and leaves it). Nothing
 // depends on a host counter, so a captured graph replays correctly.
 // Every wait is bounded: after StepArgs::spin_limit polls, or once another workgroup
 // has given up, a workgroup raises the sticky fault word and abandons the
@@ -653,10 +696,11 @@ template <int kAlgo, bool kBf16, int kNorm>
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(kFusedWaves)))
 void fused_kernel(const TensorDesc *__restrict__ tensors, const ChunkDesc *__restrict__ tiles,
                   int32_t n_tiles, uint64_t *__restrict__ slots, uint32_t *__restrict__ ctl,
+                  uint32_t *__restrict__ flags, int32_t guarded, int32_t *__restrict__ nonfinite_out,
                   StepArgs a, FinalizeArgs f, double *__restrict__ ratio_out,
                   double *__restrict__ norms_out) {
     constexpr bool kV = kHasSecondMoment<kAlgo>;
-    __shared__ uint32_t sh_epoch, sh_fault;
+    __shared__ uint32_t sh_epoch, sh_fault, sh_skip;
     __shared__ float sh_scale;
     __shared__ Partial sh_tile, sh_layer;
     // The tile's x waits in LDS (32 KB), its update direction in registers.
@@ -664,6 +708,8 @@ void fused_kernel(const TensorDesc *__restrict__ tensors, const ChunkDesc *__res
     if (threadIdx.x == 0) {
         sh_epoch = ctl_load(ctl + kCtlEpoch);
         sh_fault = ctl_load(ctl + kCtlFault);
+        // skip_nonfinite step: the finiteness check's verdict
+        sh_skip = guarded ? flags[kVerdictWord + (sh_epoch & 1u)] : 0u;
     }
     __syncthreads();
     const uint32_t epoch = sh_epoch;
@@ -671,7 +717,7 @@ void fused_kernel(const TensorDesc *__restrict__ tensors, const ChunkDesc *__res
     // per buffer: partial ||x|| words, partial ||u|| words, broadcast scales
     uint64_t *cur = slots + size_t(epoch & 1u) * 3 * n;
     uint64_t *next = slots + size_t((epoch & 1u) ^ 1u) * 3 * n;
-    bool stop = sh_fault != 0;
+    bool stop = sh_fault != 0 || sh_skip != 0;
 
     const int32_t grid = static_cast<int32_t>(gridDim.x);
     for (int32_t r = 0; !stop; ++r) {
@@ -834,9 +880,21 @@ void fused_kernel(const TensorDesc *__restrict__ tensors, const ChunkDesc *__res
         const uint32_t done =
             __hip_atomic_fetch_add(ctl + kCtlDone, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         if (done == gridDim.x - 1) {
+            if (guarded && nonfinite_out)
+                *nonfinite_out = sh_skip ? 1 : 0;
             __hip_atomic_store(ctl + kCtlDone, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            __hip_atomic_store(ctl + kCtlEpoch, epoch + 1u, __ATOMIC_RELAXED,
-                               __HIP_MEMORY_SCOPE_AGENT);
+            if (sh_skip) {
+                // A skipped step touched no slot, so its buffer is still empty
+                // and the next step reuses it: the epoch stays, and the raised
+                // verdict word is cleared for that step.
+                flags[kVerdictWord + (epoch & 1u)] = 0u;
+            } else {
+                // Clear the verdict word of the next epoch (last used two
+                // steps ago, read by nothing now) and advance the epoch.
+                flags[kVerdictWord + ((epoch + 1u) & 1u)] = 0u;
+                __hip_atomic_store(ctl + kCtlEpoch, epoch + 1u, __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
+            }
         }
     }
 }
@@ -907,9 +965,10 @@ const void *fused_fn(const StepKind &k) {
 
 hipError_t launch_moments(const StepKind &kind, const TensorDesc *tensors,
                           const ChunkDesc *chunks, Partial *partials, int32_t n_chunks,
-                          uint32_t *flags, const StepArgs &args, hipStream_t stream) {
+                          uint32_t *flags, const uint32_t *guard_ctl, const StepArgs &args,
+                          hipStream_t stream) {
     StepArgs a = args;
-    void *params[] = {&tensors, &chunks, &partials, &flags, &a};
+    void *params[] = {&tensors, &chunks, &partials, &flags, &guard_ctl, &a};
     const void *fn;
     switch (kind.algo) {
     case kNLamb: fn = moments_fn<kNLamb>(kind); break;
@@ -922,10 +981,10 @@ hipError_t launch_moments(const StepKind &kind, const TensorDesc *tensors,
 
 hipError_t launch_apply(const StepKind &kind, const TensorDesc *tensors,
                         const ChunkDesc *chunks, const float *scale, int32_t n_chunks,
-                        uint32_t *flags, int32_t *nonfinite_out, const StepArgs &args,
-                        hipStream_t stream) {
+                        uint32_t *flags, const uint32_t *guard_ctl, int32_t *nonfinite_out,
+                        const StepArgs &args, hipStream_t stream) {
     StepArgs a = args;
-    void *params[] = {&tensors, &chunks, &scale, &flags, &nonfinite_out, &a};
+    void *params[] = {&tensors, &chunks, &scale, &flags, &guard_ctl, &nonfinite_out, &a};
     const void *fn;
     switch (kind.algo) {
     case kNLamb: fn = apply_fn<kNLamb>(kind); break;
@@ -958,16 +1017,28 @@ hipError_t launch_finalize(NormKind norm, const TensorDesc *tensors, int32_t n_t
 
 hipError_t launch_fused(const StepKind &kind, const TensorDesc *tensors, const ChunkDesc *tiles,
                         int32_t n_tiles, int32_t grid, uint64_t *slots, uint32_t *ctl,
+                        uint32_t *flags, bool guarded, int32_t *nonfinite_out,
                         const StepArgs &args, const FinalizeArgs &fargs, double *ratio_out,
                         double *norms_out, hipStream_t stream) {
     StepArgs a = args;
     FinalizeArgs f = fargs;
-    void *params[] = {&tensors, &tiles, &n_tiles, &slots, &ctl, &a, &f, &ratio_out, &norms_out};
+    int32_t guard = guarded ? 1 : 0;
+    void *params[] = {&tensors, &tiles, &n_tiles, &slots, &ctl, &flags, &guard, &nonfinite_out,
+                      &a, &f, &ratio_out, &norms_out};
     return hipLaunchKernel(fused_fn(kind), dim3(grid), dim3(kBlock), params, 0, stream);
 }
 
 hipError_t fused_blocks_per_cu(const StepKind &kind, int *blocks) {
     return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, fused_fn(kind), kBlock, 0);
+}
+
+hipError_t launch_finite(bool bf16_grad, const TensorDesc *tensors, const ChunkDesc *chunks,
+                         int32_t n_chunks, uint32_t *flags, const uint32_t *ctl, float grad_scale,
+                         hipStream_t stream) {
+    void *params[] = {&tensors, &chunks, &flags, &ctl, &grad_scale};
+    const void *fn = bf16_grad ? reinterpret_cast<const void *>(&finite_kernel<true>)
+                               : reinterpret_cast<const void *>(&finite_kernel<false>);
+    return hipLaunchKernel(fn, dim3(n_chunks), dim3(kBlock), params, 0, stream);
 }
 
 }  // namespace lamb_mi355x

@@ -106,16 +106,22 @@ def test_deferred_mode_equals_direct_mode(algo):
     assert torch.equal(r0, r1)
 
 
+@pytest.mark.parametrize("path", ["auto", "two-pass"])
 @pytest.mark.parametrize("algo", ALGOS)
 @pytest.mark.parametrize("g_dtype", ["f32", "bf16"])
-def test_skip_nonfinite_sequence(algo, g_dtype):
+def test_skip_nonfinite_sequence(algo, g_dtype, path):
     """Finite and non-finite steps interleaved: a skipped step changes nothing
     (bit for bit) and reports 1; the next finite step proceeds as the oracle
-    does. Covers +inf, NaN and an fp32 overflow caused by grad_scale."""
+    does. Covers +inf, NaN and an fp32 overflow caused by grad_scale. On the
+    single pass the verdict comes from a read-only check of g; on the
+    two-pass path from the deferred moment pass. The last layer has three
+    tiles, so its tiles meet through the slots, which a skipped step must
+    leave ready for the next one."""
     torch = H.torch_cuda()
     rng = np.random.default_rng(9)
-    xs = [(rng.standard_normal(n) * 0.2).astype(np.float32) for n in (700, 33, 4096, 5)]
-    pair = _pair(xs, [True, False, True, True], g_dtype, algo, chunk=256)
+    xs = [(rng.standard_normal(n) * 0.2).astype(np.float32)
+          for n in (700, 33, 4096, 5, 3 * 8192 + 77)]
+    pair = _pair(xs, [True, False, True, True, True], g_dtype, algo, chunk=256, path=path)
     flag = torch.full((1,), -1, dtype=torch.int32, device="cuda")
     plan_steps = [("ok", 1.0), ("inf", 1.0), ("ok", 1.0), ("nan", 1.0), ("ok", 1.0),
                   ("overflow", 3e38), ("overflow", 3e38), ("ok", 1.0)]
@@ -144,6 +150,66 @@ def test_skip_nonfinite_sequence(algo, g_dtype):
             assert skipped == (kind != "ok")
     finally:
         pair.close()
+
+
+def test_skip_nonfinite_with_two_pass_layer():
+    """The single-pass skip mode with a layer too large for the single pass:
+    the check's verdict also stops that layer's moment and apply passes."""
+    torch = H.torch_cuda()
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    big = 4 * cus * 8192 + 1029
+    rng = np.random.default_rng(19)
+    xs = [(rng.standard_normal(n) * 0.2).astype(np.float32) for n in (big, 3000, 7)]
+    pair = _pair(xs, [True, True, False], "bf16", "lamb", path="auto")
+    flag = torch.full((1,), -1, dtype=torch.int32, device="cuda")
+    try:
+        per, _ = _lib.lamb_plan_tiles(pair.plan)
+        assert per[0] == 0 and per[1] > 0 and per[2] > 0
+        for t, kind in enumerate(["ok", "nan_big", "ok", "inf_small", "ok"], start=1):
+            gs = _grads(rng, pair.X, "bf16")
+            if kind == "nan_big":
+                gs[0][big - 3] = float("nan")
+            elif kind == "inf_small":
+                gs[2][6] = float("inf")
+            hg = pair.set_grads(gs)
+            before = [x.clone() for x in pair.X + pair.M + pair.V]
+            ref = H.step_ex_both(pair, _hp("lamb", step=t, skip_nonfinite=1), hg, flag)
+            pair.compare(ref, "skip with a two-pass layer, step %d (%s)" % (t, kind))
+            torch.cuda.synchronize()
+            assert int(flag) == int(kind != "ok")
+            if kind != "ok":
+                after = pair.X + pair.M + pair.V
+                assert all(torch.equal(a, b) for a, b in zip(before, after))
+    finally:
+        pair.close()
+
+
+@pytest.mark.parametrize("algo", ["lamb", "nn-lamb", "lars"])
+def test_checked_skip_mode_equals_direct_mode(algo):
+    """With finite gradients, a skip_nonfinite step on the single pass runs
+    the direct kernels after the check: bit for bit the direct step."""
+    torch = H.torch_cuda()
+    ps = paramsets.get(3)
+    xs = paramsets.draw_params(ps, device="cuda")
+    runs = []
+    for skip in (0, 1):
+        pair = _pair([x.clone() for x in xs], ps.wd_mask(), "f32", algo, 0, "auto")
+        pair.subset = []
+        flag = torch.zeros(1, dtype=torch.int32, device="cuda")
+        for t in range(1, 4):
+            for G, g in zip(pair.G, paramsets.draw_grads(ps, t, device="cuda")):
+                G.copy_(g)
+            _lib.lamb_step_ex(pair.plan, _hp(algo, step=t, skip_nonfinite=skip),
+                              torch.cuda.current_stream().cuda_stream, pair.ratio.data_ptr(),
+                              pair.norms.data_ptr(), flag.data_ptr() if skip else 0)
+        _lib.lamb_plan_check(pair.plan)
+        runs.append(([x.clone() for x in pair.X], [m.clone() for m in pair.M],
+                     [v.clone() for v in pair.V] if pair.V else [], pair.ratio.clone(), int(flag)))
+        pair.close()
+    (x0, m0, v0, r0, _), (x1, m1, v1, r1, f1) = runs
+    assert f1 == 0
+    assert all(torch.equal(a, b) for a, b in zip(x0 + m0 + v0, x1 + m1 + v1))
+    assert torch.equal(r0, r1)
 
 
 def _with(hp, **fields):
