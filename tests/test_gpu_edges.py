@@ -341,3 +341,16 @@ def test_single_pass_layout_and_rounds():
             pair.compare(ref, "rounds step %d" % t)
     finally:
         pair.close()
+
+
+@pytest.mark.parametrize("path", PATHS)
+def test_many_small_layers(path):
+    """3000 layers of 1 to 300 elements plus two multi-tile layers: rounds
+    filled mostly with one-tile layers, against the oracle on every
+    element."""
+    rng = np.random.default_rng(41)
+    sizes = [int(v) for v in rng.integers(1, 301, size=3000)] + [5 * 8192 + 11, 2 * 8192]
+    xs = _xs(rng, sizes)
+    wd = [bool(v) for v in rng.integers(0, 2, size=len(sizes))]
+    H.log("many small layers: %d layers, path %s" % (len(sizes), path))
+    _run(xs, wd, "bf16", "lamb", 0, 2, DEFAULT, rng, path=path)
