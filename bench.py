@@ -10,6 +10,7 @@ to stderr.
                   [--path auto|two-pass] [--chunk ELEMS]
                   [--cpu-seconds S | --no-cpu-baseline]
   python bench.py --copy-probe      # plain copy of known size (counter scale)
+  python bench.py --stream-probe    # attainable GB/s of each kernel's access pattern
 """
 
 from __future__ import annotations
@@ -53,6 +54,10 @@ def bytes_per_param(algo: str, g_bytes: int, deferred: bool = False):
         return moment_reads, moment_reads + 4 + state
     needs_g = algo in ("nlamb", "nnlamb")
     return moment_reads + state, 4 + state + 4 + (g_bytes if needs_g else 0)
+
+
+def avg_one_ms(total_ms: float, recorded: int) -> float:
+    return total_ms / recorded if recorded else 0.0
 
 
 def single_pass_bytes(algo: str, g_bytes: int) -> int:
@@ -112,6 +117,65 @@ def copy_probe(args) -> None:
     ms = start.elapsed_time(end) / args.steps
     print(json.dumps({"probe": "copy", "bytes_read": 4 * n, "bytes_written": 4 * n,
                       "ms": ms, "GBps": 8 * n / ms / 1e6}), flush=True)
+
+
+PATTERNS = {"single_pass": 0, "moments": 1, "apply": 2, "read": 3, "copy": 4}
+
+
+def pattern_bytes(pattern: str, g_bytes: int) -> int:
+    """Bytes per element of a stream pattern (include/stream_probe.h)."""
+    return {"single_pass": 4 + g_bytes + 8 + 12, "moments": 4 + g_bytes + 8 + 8,
+            "apply": 12 + 4, "read": 12 + g_bytes, "copy": 8}[pattern]
+
+
+def stream_rate(pattern: str, n: int, g_bf16: bool, tile: int, reps: int = 20) -> float:
+    """Attainable GB/s of a stream with `pattern`'s access pattern over n
+    elements (the stream probe library), timed with events on torch's current
+    stream, on buffers of its own."""
+    import ctypes
+
+    import torch
+
+    from paper_1904_00962_amd import build as hb
+    if not os.path.exists(hb.PROBE_LIBRARY):
+        raise RuntimeError("stream probe library %s is missing; run the build" % hb.PROBE_LIBRARY)
+    lib = ctypes.CDLL(hb.PROBE_LIBRARY)
+    lib.stream_probe.argtypes = [ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
+                                 ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
+                                 ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p]
+    x, m, v = (torch.zeros(n, dtype=torch.float32, device="cuda") for _ in range(3))
+    g = torch.zeros(n, dtype=torch.bfloat16 if g_bf16 else torch.float32, device="cuda")
+    stream = torch.cuda.current_stream().cuda_stream
+
+    def run():
+        rc = lib.stream_probe(PATTERNS[pattern], x.data_ptr(), m.data_ptr(), v.data_ptr(),
+                              g.data_ptr(), int(g_bf16), n, tile, stream)
+        if rc != 0:
+            raise RuntimeError("stream_probe failed with %d" % rc)
+
+    for _ in range(3):
+        run()
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(reps):
+        run()
+    b.record()
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / reps
+    rate = pattern_bytes(pattern, 2 if g_bf16 else 4) * n / ms / 1e6
+    del x, m, v, g
+    torch.cuda.empty_cache()
+    return rate
+
+
+def stream_probe_all() -> None:
+    """Every pattern over the BERT-Large parameter count, one JSON line."""
+    out = {"probe": "stream", "elements": 335141888, "g": "bf16"}
+    for pattern, tile in (("single_pass", 8192), ("moments", 512), ("apply", 512),
+                          ("read", 2048), ("copy", 512)):
+        out[pattern + "_GBps"] = stream_rate(pattern, 335141888, True, tile)
+    print(json.dumps(out), flush=True)
 
 
 def cpu_sample(ps, xs, grads):
@@ -193,6 +257,8 @@ def main() -> int:
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", action="store_true")
+    ap.add_argument("--stream-probe", action="store_true",
+                    help="attainable GB/s of each kernel's access pattern, then exit")
     ap.add_argument("--copy-elems", type=int, default=1 << 28)
     args = ap.parse_args()
 
@@ -207,6 +273,9 @@ def main() -> int:
         return 1
     if args.copy_probe:
         copy_probe(args)
+        return 0
+    if args.stream_probe:
+        stream_probe_all()
         return 0
 
     from paper_1904_00962_amd import _lib, paramsets
@@ -245,6 +314,7 @@ def main() -> int:
     n_tensors, n_chunks, chunk = _lib.lamb_plan_info(opt.plan)
     tiles_per_tensor, n_tiles = _lib.lamb_plan_tiles(opt.plan)
     single = args.path == "auto"
+    P = sum(x.numel() for x in xs)
     P_single = sum(x.numel() for x, k in zip(xs, tiles_per_tensor) if k) if single else 0
     checked = single and args.skip_nonfinite and P_single > 0
 
@@ -273,6 +343,17 @@ def main() -> int:
     if not torch.isfinite(ratios).all():
         eprint("non-finite trust ratio after the timed steps")
         return 1
+    # The attainable rate of the dominant kernel's access pattern: a stream
+    # with the same reads, writes and elements per workgroup, no arithmetic.
+    dom_is_single = avg_one_ms(k_one, recorded) >= avg_one_ms(k_mom, recorded)
+    dom_pattern = "single_pass" if dom_is_single else "moments"
+    dom_elems = P_single if dom_is_single else P - P_single
+    attainable = None
+    if not args.skip_nonfinite and not args.bf16_copy and args.algo != "lars" and dom_elems:
+        attainable = stream_rate(dom_pattern, dom_elems, ps.g_dtype == "bf16",
+                                 8192 if dom_is_single else (chunk or 512))
+        eprint("stream probe (%s pattern, %d elements): %.0f GB/s"
+               % (dom_pattern, dom_elems, attainable))
     cpu = None
     if sample is not None:
         eprint("timing the CPU oracle (budget %.0f s)" % args.cpu_seconds)
@@ -280,7 +361,6 @@ def main() -> int:
         eprint("cpu baseline: %.3e params/s (%s)" % (cpu["value"], cpu["sample"]))
 
     ms_step = total_ms / args.steps
-    P = sum(x.numel() for x in xs)
     P_rest = P - P_single
     g_bytes = 2 if ps.g_dtype == "bf16" else 4
     copy_bytes = 2 if args.bf16_copy else 0  # the bf16 working copy of x
@@ -353,6 +433,10 @@ def main() -> int:
             "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": dom["achieved"] / HBM_PEAK_GBPS,
             "traffic": dom["traffic"], "bytes_per_launch": dom["bytes_per_launch"],
             "kernel_source_hash": src_hash,
+            "attainable": None if attainable is None else {
+                "GBps": attainable, "frac": dom["achieved"] / attainable,
+                "how": "stream with the kernel's reads, writes and elements per workgroup, "
+                       "no arithmetic (libstream_probe)"},
         },
         "cpu_baseline": cpu,
     }

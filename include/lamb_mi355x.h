@@ -352,9 +352,10 @@ LAMB_API lamb_status lamb_chunk_table(const int64_t *numel, int32_t n_tensors,
  * The single-pass schedule a plan would use (host only, no HIP call). The
  * single-pass kernel runs a persistent grid of `round` workgroups; workgroup
  * w takes entries w, w + round, ..., so the entry list falls into rounds of
- * `round` entries. A layer of at most `max_round` tiles of 8192 elements
- * takes the single pass: its tiles are consecutive entries inside one round,
- * tile j starting at element 8192 j. Layers are packed first-fit by
+ * `round` entries. A layer of n elements takes T = ceil(n / 8192) tiles; if
+ * T <= max_round it takes the single pass: its tiles are consecutive entries
+ * inside one round, and tile j holds the layer's 1024-element blocks j,
+ * j + T, ..., j + 7T (those inside the layer). Layers are packed first-fit by
  * decreasing tile count (ties in table order) into the fewest rounds of
  * `max_round` entries; `round` is then the narrowest width that packs into
  * as few rounds, so the rounds come out about equally full. The gap a
@@ -365,8 +366,8 @@ LAMB_API lamb_status lamb_chunk_table(const int64_t *numel, int32_t n_tensors,
  *   capacity      length of the three entry arrays (0 with NULL arrays to
  *                 query the count)
  *   entry_tensor  host, layer of each entry or -1
- *   entry_start   host, first element of each entry
- *   entry_len     host, elements of each entry (0 for an empty entry)
+ *   entry_start   host, first element of each entry (of its first block)
+ *   entry_len     host, elements each entry holds (0 for an empty entry)
  *   first_tile    host, n_tensors: the layer's first entry (0 if none)
  *   tiles         host, n_tensors: the layer's tile count, 0 when it takes
  *                 the two-pass kernels (more than `max_round` tiles)

@@ -19,6 +19,9 @@ INCLUDE = os.path.join(ROOT, "include")
 LIBRARY = os.path.join(PKG, "liblamb_mi355x.so")
 SOURCES = [os.path.join(CSRC, "lamb_kernels.hip"), os.path.join(CSRC, "lamb_api.cpp")]
 HEADERS = [os.path.join(INCLUDE, "lamb_mi355x.h"), os.path.join(CSRC, "lamb_internal.h")]
+# Measurement only: streams with the kernels' access patterns (bench.py).
+PROBE_LIBRARY = os.path.join(PKG, "libstream_probe.so")
+PROBE_SOURCES = [os.path.join(CSRC, "stream_probe.hip")]
 
 ARCH = "gfx950"
 HIPCC_FLAGS = [
@@ -50,6 +53,19 @@ def build(output: str = LIBRARY, verbose: bool = False, defines=()) -> str:
     return output
 
 
+def build_probe(output: str = PROBE_LIBRARY, verbose: bool = False) -> str:
+    """Compile the stream probe used by bench.py (not part of the optimizer)."""
+    tmp = output + ".tmp%d" % os.getpid()
+    cmd = [hipcc(), *HIPCC_FLAGS, "-I", INCLUDE, *PROBE_SOURCES, "-o", tmp]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    proc = subprocess.run(cmd, capture_output=True, text=True)
+    if proc.returncode != 0:
+        raise RuntimeError("hipcc failed (%d):\n%s\n%s" % (proc.returncode, proc.stdout, proc.stderr))
+    os.replace(tmp, output)
+    return output
+
+
 def is_stale(output: str = LIBRARY) -> bool:
     if not os.path.exists(output):
         return True
@@ -59,3 +75,4 @@ def is_stale(output: str = LIBRARY) -> bool:
 
 if __name__ == "__main__":
     print(build(verbose="-v" in sys.argv))
+    print(build_probe(verbose="-v" in sys.argv))

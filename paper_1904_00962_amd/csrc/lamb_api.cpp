@@ -393,9 +393,14 @@ lamb_status lamb_tile_schedule(const int64_t *numel, int32_t n_tensors, int32_t 
             for (int64_t j = 0; j < nt; ++j, ++k) {
                 if (!write)
                     continue;
+                // tile j holds the blocks j, j + nt, ... of kBlockElems each
+                int64_t held = 0;
+                for (int64_t b = j; b < int64_t(kTileGroups) * nt; b += nt)
+                    held += std::max<int64_t>(0, std::min<int64_t>(kBlockElems,
+                                                                   numel[i] - b * kBlockElems));
                 entry_tensor[k] = i;
-                entry_start[k] = j * kTileElems;
-                entry_len[k] = int32_t(std::min<int64_t>(kTileElems, numel[i] - j * kTileElems));
+                entry_start[k] = j * kBlockElems;
+                entry_len[k] = int32_t(held);
             }
         }
         if (r + 1 < fill.size()) {

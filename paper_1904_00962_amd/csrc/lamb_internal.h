@@ -26,10 +26,11 @@ constexpr int32_t kDefaultChunkElems = LAMB_DEFAULT_CHUNK;
 // and run faster with more work per workgroup).
 constexpr int32_t kCoarseFactor = 4;
 
-// Single-pass path: a layer is cut into tiles of kTileElems elements; one
-// workgroup keeps a tile's x (in LDS) and update direction (in registers,
-// kTileGroups float4 groups per thread) until the layer's step scale is
-// known. The persistent grid keeps kFusedBlocksPerCu workgroups on every CU,
+// Single-pass path: a layer of n elements takes T = ceil(n / kTileElems)
+// tiles; tile i holds the layer's (4 * kBlock)-element blocks i, i + T, ...,
+// i + (kTileGroups - 1) T. One workgroup keeps a tile's x (in LDS) and update
+// direction (in registers, kTileGroups float4 groups per thread) until the
+// layer's step scale is known. The persistent grid keeps kFusedBlocksPerCu workgroups on every CU,
 // so a layer of up to kFusedBlocksPerCu * (compute units) tiles can have
 // every tile resident at once.
 #ifndef LAMB_TILE_GROUPS
@@ -39,7 +40,8 @@ constexpr int32_t kCoarseFactor = 4;
 #define LAMB_FUSED_WAVES 4
 #endif
 constexpr int kTileGroups = LAMB_TILE_GROUPS;
-constexpr int32_t kTileElems = kBlock * 4 * kTileGroups;
+constexpr int32_t kBlockElems = kBlock * 4;  // one float4 per thread
+constexpr int32_t kTileElems = kBlockElems * kTileGroups;
 constexpr int kFusedWaves = LAMB_FUSED_WAVES;
 constexpr int kFusedBlocksPerCu = kFusedWaves * 4 / kWaves;  // 4 SIMDs per CU
 // Polls before a single-pass wait gives up (about a second); a plan reads an

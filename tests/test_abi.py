@@ -153,3 +153,25 @@ def test_null_plan_and_outputs(lib):
     assert lib.lamb_plan_set_timing(None, 4, 1) == _lib.LAMB_ENULL
     assert lib.lamb_plan_set_bf16_copies(None, None) == _lib.LAMB_ENULL
     assert lib.lamb_plan_create(None, 1, 0, 0, 0, None) == _lib.LAMB_ENULL
+
+
+def test_stream_probe_library_validates_on_the_host():
+    """The measurement-only stream library (include/stream_probe.h) exports
+    its entry point and rejects bad arguments before any launch."""
+    if not os.path.exists(build.PROBE_LIBRARY):
+        build.build_probe()
+    probe = ctypes.CDLL(build.PROBE_LIBRARY)
+    probe.stream_probe.argtypes = [ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
+                                   ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
+                                   ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p]
+    fake = 1 << 20  # aligned, never dereferenced: every case fails validation
+    bad = [
+        (9, fake, fake, fake, fake, 1, 100, 512),     # unknown pattern
+        (0, fake, fake, fake, fake, 1, 0, 512),       # n < 1
+        (0, fake, fake, fake, fake, 1, 100, 12),      # tile not a multiple of 8
+        (0, fake, fake, fake, fake, 2, 100, 512),     # g_bf16 not 0/1
+        (0, fake, fake, fake, None, 1, 100, 512),     # single pass reads g
+        (0, fake + 4, fake, fake, fake, 1, 100, 512), # misaligned
+    ]
+    for args in bad:
+        assert probe.stream_probe(*args, None) == -1, args

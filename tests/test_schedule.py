@@ -8,6 +8,7 @@ import pytest
 from paper_1904_00962_amd import _lib, paramsets
 
 TILE = 8192
+BLOCK = 1024
 
 
 def _check_layout(numel, max_round):
@@ -29,11 +30,16 @@ def _check_layout(numel, max_round):
         assert tiles[i] == nt
         f = first[i]
         assert f // round_ == (f + nt - 1) // round_, "layer %d straddles a round" % i
+        covered = 0
         for k in range(nt):
             j = f + k
             assert not seen[j]
             seen[j] = True
-            assert et[j] == i and es[j] == k * TILE and el[j] == min(TILE, size - k * TILE)
+            # tile k holds the 1024-element blocks k, k + nt, ..., k + 7 nt
+            held = sum(max(0, min(BLOCK, size - b * BLOCK)) for b in range(k, 8 * nt, nt))
+            assert et[j] == i and es[j] == k * BLOCK and el[j] == held > 0
+            covered += held
+        assert covered == size
     for j in range(n):
         if not seen[j]:  # an empty entry: only in a gap at the end of a full round
             assert et[j] == -1 and el[j] == 0
