@@ -358,19 +358,24 @@ lamb_status lamb_tile_schedule(const int64_t *numel, int32_t n_tensors, int32_t 
     // The fewest rounds, at the narrowest width that still needs no more:
     // the rounds come out about equally full instead of full rounds and a
     // short last one.
+    // Binary search over the width (at most ~10 packings): the smallest width
+    // in [lower bound, max_round] whose packing needs no more rounds.
     pack(max_round);
     const size_t n_rounds = fill.size();
     int64_t round = max_round;
     if (n_rounds > 0) {
-        int64_t width = std::max(largest, (total_tiles + int64_t(n_rounds) - 1) / int64_t(n_rounds));
-        for (; width < max_round; ++width) {
-            pack(width);
-            if (fill.size() == n_rounds)
-                break;
+        int64_t lo = std::max(largest, (total_tiles + int64_t(n_rounds) - 1) / int64_t(n_rounds));
+        int64_t hi = max_round;  // packs into n_rounds
+        while (lo < hi) {
+            const int64_t mid = lo + (hi - lo) / 2;
+            pack(mid);
+            if (fill.size() <= n_rounds)
+                hi = mid;
+            else
+                lo = mid + 1;
         }
-        if (width >= max_round)
-            pack(max_round);
-        round = std::min<int64_t>(width, max_round);
+        round = hi;
+        pack(round);
     }
     *round_out = int32_t(round);
     const int64_t total =
