@@ -1,6 +1,7 @@
 // Host side of the C ABI declared in include/lamb_mi355x.h: argument
-// validation, the chunk table (Section 2's layer blocks cut into work
-// chunks), plan buffers, per-step scalars and kernel launches.
+// validation, the chunk tables and the single-pass schedule (Section 2's
+// layer blocks cut into work units), plan buffers, per-step scalars, kernel
+// launches and timing hooks.
 
 #include "lamb_mi355x.h"
 
@@ -28,14 +29,14 @@ struct lamb_plan {
     int32_t n_tensors = 0;
     int32_t n_chunks = 0;
     int32_t chunk_elems = 0;
-    void *device_block = nullptr;  // one allocation holding the four buffers below
+    void *device_block = nullptr;  // one allocation holding every device buffer below
     int32_t n_coarse = 0;       // coarse chunks (kCoarseFactor * chunk_elems each)
     TensorDesc *tensors = nullptr;
     ChunkDesc *chunks = nullptr;
     ChunkDesc *coarse_chunks = nullptr;
     Partial *partials = nullptr;
     float *scale = nullptr;
-    uint32_t *flags = nullptr;     // deferred mode: raised by the moment pass, verdict
+    uint32_t *flags = nullptr;     // the four non-finite words (kVerdictWord)
     // Single-pass path: the tiles of the layers that fit, and a second tensor
     // and chunk table holding only the other layers (their two-pass work).
     lamb_path path = LAMB_PATH_AUTO;
