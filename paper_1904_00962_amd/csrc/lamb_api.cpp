@@ -311,7 +311,8 @@ lamb_status lamb_tile_schedule(const int64_t *numel, int32_t n_tensors, int32_t 
                                int32_t *entry_len, int32_t *first_tile, int32_t *tiles,
                                int32_t *n_entries, int32_t *round_out) {
     if (!numel || !n_entries || !first_tile || !tiles || !round_out)
-        return fail(LAMB_ENULL, "numel, first_tile, tiles, n_entries and round_out must not be NULL");
+        return fail(LAMB_ENULL,
+                    "numel, first_tile, tiles, n_entries and round_out must not be NULL");
     if (n_tensors < 1)
         return fail(LAMB_EINVAL, "n_tensors = %d, need >= 1", n_tensors);
     if (max_round < 1)
@@ -334,10 +335,9 @@ lamb_status lamb_tile_schedule(const int64_t *numel, int32_t n_tensors, int32_t 
             largest = std::max(largest, nt);
         }
     }
+    using Team = std::pair<int64_t, int32_t>;
     std::stable_sort(teams.begin(), teams.end(),
-                     [](const std::pair<int64_t, int32_t> &a, const std::pair<int64_t, int32_t> &b) {
-                         return a.first > b.first;
-                     });
+                     [](const Team &a, const Team &b) { return a.first > b.first; });
     // First-fit into rounds of `width` entries.
     std::vector<int64_t> fill;
     std::vector<std::vector<int32_t>> members;
@@ -509,12 +509,15 @@ lamb_status lamb_plan_create(const lamb_tensor *tensors, int32_t n_tensors,
             return fail(LAMB_EALIGN, "tensor %d: every buffer must be 16-byte aligned", i);
         numel[size_t(i)] = t.numel;
         const uintptr_t f32_bytes = uintptr_t(t.numel) * 4u;
-        ranges.push_back({reinterpret_cast<uintptr_t>(t.x), reinterpret_cast<uintptr_t>(t.x) + f32_bytes, i, "x"});
-        ranges.push_back({reinterpret_cast<uintptr_t>(t.g),
-                          reinterpret_cast<uintptr_t>(t.g) + uintptr_t(t.numel) * g_size, i, "g"});
-        ranges.push_back({reinterpret_cast<uintptr_t>(t.m), reinterpret_cast<uintptr_t>(t.m) + f32_bytes, i, "m"});
+        auto add = [&](const void *p, uintptr_t bytes, const char *what) {
+            const uintptr_t lo = reinterpret_cast<uintptr_t>(p);
+            ranges.push_back({lo, lo + bytes, i, what});
+        };
+        add(t.x, f32_bytes, "x");
+        add(t.g, uintptr_t(t.numel) * g_size, "g");
+        add(t.m, f32_bytes, "m");
         if (needs_v)
-            ranges.push_back({reinterpret_cast<uintptr_t>(t.v), reinterpret_cast<uintptr_t>(t.v) + f32_bytes, i, "v"});
+            add(t.v, f32_bytes, "v");
     }
     std::sort(ranges.begin(), ranges.end(),
               [](const Range &a, const Range &b) { return a.lo < b.lo; });
@@ -977,8 +980,9 @@ lamb_status lamb_step_ex(lamb_plan *plan, const lamb_hparams *hp, void *stream,
         // The tile list was packed in rounds of at most kFusedBlocksPerCu * CUs
         // entries; the grid is one round, so it must all be resident at once.
         if (per_cu < kFusedBlocksPerCu)
-            return fail(LAMB_EHIP, "single-pass kernel keeps %d workgroups per CU resident, needs %d",
-                        per_cu, kFusedBlocksPerCu);
+            return fail(LAMB_EHIP,
+                        "single-pass kernel keeps %d workgroups per CU resident, needs %d", per_cu,
+                        kFusedBlocksPerCu);
         grid = std::min(plan->n_tiles, plan->round);
     }
     hipStream_t s = static_cast<hipStream_t>(stream);

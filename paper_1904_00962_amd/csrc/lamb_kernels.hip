@@ -24,10 +24,10 @@
 //            too, unless the moment pass found a non-finite scaled gradient,
 //            in which case nothing changes.
 //
-// A layer small enough to sit in the registers of the resident workgroups
-// takes a single pass instead (fused_kernel below): each tile's x and u stay
-// in registers while the layer's partial norms meet, so x, g, m, v are read
-// and x, m, v written exactly once.
+// A layer small enough to sit on chip in the resident workgroups takes a
+// single pass instead (fused_kernel below): each tile's x (in LDS) and u (in
+// registers) stay there while the layer's partial norms meet, so x, g, m, v
+// are read and x, m, v written exactly once.
 //
 // Recomputing u instead of storing it saves 4 bytes per parameter of HBM
 // traffic. There are no float atomics: every reduction has a fixed order, so
@@ -641,9 +641,9 @@ __global__ __launch_bounds__(kSegBlock) void finalize_kernel(
 // the next step; the last workgroup to finish advances the epoch (a step
 // skipped for a non-finite gradient touches no slot and leaves it). Nothing
 // depends on a host counter, so a captured graph replays correctly.
-// Every wait is bounded: after StepArgs::spin_limit polls, or once another workgroup
-// has given up, a workgroup raises the sticky fault word and abandons the
-// step, and every later step of the plan does nothing.
+// Every wait is bounded: after StepArgs::spin_limit polls, or once another
+// workgroup has given up, a workgroup raises the sticky fault word and
+// abandons the step, and every later step of the plan does nothing.
 // ---------------------------------------------------------------------------
 
 // s_sleep argument between polls (units of 64 clocks): LAMB_SPIN_SLEEP for
@@ -699,7 +699,8 @@ template <int kAlgo, bool kBf16, int kNorm>
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(kFusedWaves)))
 void fused_kernel(const TensorDesc *__restrict__ tensors, const ChunkDesc *__restrict__ tiles,
                   int32_t n_tiles, uint64_t *__restrict__ slots, uint32_t *__restrict__ ctl,
-                  uint32_t *__restrict__ flags, int32_t guarded, int32_t *__restrict__ nonfinite_out,
+                  uint32_t *__restrict__ flags, int32_t guarded,
+                  int32_t *__restrict__ nonfinite_out,
                   StepArgs a, FinalizeArgs f, double *__restrict__ ratio_out,
                   double *__restrict__ norms_out) {
     constexpr bool kV = kHasSecondMoment<kAlgo>;
@@ -828,10 +829,12 @@ void fused_kernel(const TensorDesc *__restrict__ tensors, const ChunkDesc *__res
             if (j == first) {
                 double ax = 0.0, au = 0.0;
                 for (int k = threadIdx.x; k < team; k += kBlock) {
-                    const uint64_t wx = slot_wait<LAMB_SPIN_SLEEP>(cur + first + k, ctl, a.spin_limit);
-                    const uint64_t wu = wx == kEmptySlot
-                                            ? kEmptySlot
-                                            : slot_wait<LAMB_SPIN_SLEEP>(cur + n + first + k, ctl, a.spin_limit);
+                    const uint64_t wx =
+                        slot_wait<LAMB_SPIN_SLEEP>(cur + first + k, ctl, a.spin_limit);
+                    const uint64_t wu =
+                        wx == kEmptySlot
+                            ? kEmptySlot
+                            : slot_wait<LAMB_SPIN_SLEEP>(cur + n + first + k, ctl, a.spin_limit);
                     if (wu == kEmptySlot) {
                         give_up = 1;
                         break;
@@ -851,7 +854,8 @@ void fused_kernel(const TensorDesc *__restrict__ tensors, const ChunkDesc *__res
                         slot_store(cur + 2 * n + first + k, w);
                 }
             } else if (threadIdx.x == 0) {
-                const uint64_t w = slot_wait<LAMB_MEMBER_SLEEP>(cur + 2 * n + j, ctl, a.spin_limit);
+                const uint64_t w =
+                    slot_wait<LAMB_MEMBER_SLEEP>(cur + 2 * n + j, ctl, a.spin_limit);
                 if (w == kEmptySlot)
                     give_up = 1;
                 else
@@ -867,9 +871,9 @@ void fused_kernel(const TensorDesc *__restrict__ tensors, const ChunkDesc *__res
         gbf16 *copy = t.x_copy ? (gbf16 *)t.x_copy : nullptr;
 #pragma unroll
         for (int k = 0; k < kTileGroups; ++k) {
-            int64_t first;
+            int64_t at;
             int valid;
-            group(k, first, valid);
+            group(k, at, valid);
             if (valid > 0) {
                 const f32x4 xo = sh_x[k][threadIdx.x];
                 f32x4 xn;
@@ -877,17 +881,17 @@ void fused_kernel(const TensorDesc *__restrict__ tensors, const ChunkDesc *__res
                 for (int e = 0; e < 4; ++e)
                     xn[e] = fmaf(-s, us[k][e], xo[e]);
                 if (valid == 4) {
-                    store4(x + first, xn);
+                    store4(x + at, xn);
                     if (copy) {
                         const u32x2 packed = {bf16_bits(xn[0]) | (bf16_bits(xn[1]) << 16),
                                               bf16_bits(xn[2]) | (bf16_bits(xn[3]) << 16)};
-                        stream_store((LAMB_GLOBAL u32x2 *)(copy + first), packed);
+                        stream_store((LAMB_GLOBAL u32x2 *)(copy + at), packed);
                     }
                 } else {
                     for (int e = 0; e < valid; ++e) {
-                        x[first + e] = xn[e];
+                        x[at + e] = xn[e];
                         if (copy)
-                            copy[first + e] = uint16_t(bf16_bits(xn[e]));
+                            copy[at + e] = uint16_t(bf16_bits(xn[e]));
                     }
                 }
             }
@@ -1025,11 +1029,13 @@ hipError_t launch_finalize(NormKind norm, const TensorDesc *tensors, int32_t n_t
                          : norm == kLinf ? reinterpret_cast<const void *>(&segment_kernel<kLinf>)
                                          : reinterpret_cast<const void *>(&segment_kernel<kL2>);
     void *seg_params[] = {&partials, &segs, &seg_partials};
-    hipError_t err = hipLaunchKernel(seg_fn, dim3(n_segs), dim3(kSegBlock), seg_params, 0, stream);
+    hipError_t err =
+        hipLaunchKernel(seg_fn, dim3(n_segs), dim3(kSegBlock), seg_params, 0, stream);
     if (err != hipSuccess)
         return err;
     FinalizeArgs a = args;
-    void *params[] = {&tensors, &seg_partials, &ranges, &a, &scale, &ratio_out, &norms_out, &flags};
+    void *params[] = {&tensors, &seg_partials, &ranges,    &a,
+                      &scale,   &ratio_out,    &norms_out, &flags};
     const void *fn = norm == kL1     ? reinterpret_cast<const void *>(&finalize_kernel<kL1>)
                      : norm == kLinf ? reinterpret_cast<const void *>(&finalize_kernel<kLinf>)
                                      : reinterpret_cast<const void *>(&finalize_kernel<kL2>);

@@ -113,8 +113,9 @@ extern "C" int stream_probe(int32_t pattern, float *x, float *m, float *v, const
     if (pattern < STREAM_SINGLE_PASS || pattern > STREAM_COPY || n < 1 || tile < 8 ||
         tile > (1 << 24) || tile % 8 != 0 || (g_bf16 != 0 && g_bf16 != 1))
         return -1;
-    if (!x || !m || (pattern != STREAM_COPY && !v) ||
-        ((pattern == STREAM_SINGLE_PASS || pattern == STREAM_MOMENTS || pattern == STREAM_READ) && !g))
+    const bool reads_g =
+        pattern == STREAM_SINGLE_PASS || pattern == STREAM_MOMENTS || pattern == STREAM_READ;
+    if (!x || !m || (pattern != STREAM_COPY && !v) || (reads_g && !g))
         return -1;
     const uintptr_t mask = reinterpret_cast<uintptr_t>(x) | reinterpret_cast<uintptr_t>(m) |
                            reinterpret_cast<uintptr_t>(v) | reinterpret_cast<uintptr_t>(g);
