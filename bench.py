@@ -128,7 +128,8 @@ def pattern_bytes(pattern: str, g_bytes: int) -> int:
             "apply": 12 + 4, "read": 12 + g_bytes, "copy": 8}[pattern]
 
 
-def stream_rate(pattern: str, n: int, g_bf16: bool, tile: int, reps: int = 20) -> float:
+def stream_rate(pattern: str, n: int, g_bf16: bool, tile: int, layer_tiles: int = 0,
+                reps: int = 20) -> float:
     """Attainable GB/s of a stream with `pattern`'s access pattern over n
     elements (the stream probe library), timed with events on torch's current
     stream, on buffers of its own."""
@@ -142,14 +143,14 @@ def stream_rate(pattern: str, n: int, g_bf16: bool, tile: int, reps: int = 20) -
     lib = ctypes.CDLL(hb.PROBE_LIBRARY)
     lib.stream_probe.argtypes = [ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
                                  ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
-                                 ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p]
+                                 ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p]
     x, m, v = (torch.zeros(n, dtype=torch.float32, device="cuda") for _ in range(3))
     g = torch.zeros(n, dtype=torch.bfloat16 if g_bf16 else torch.float32, device="cuda")
     stream = torch.cuda.current_stream().cuda_stream
 
     def run():
         rc = lib.stream_probe(PATTERNS[pattern], x.data_ptr(), m.data_ptr(), v.data_ptr(),
-                              g.data_ptr(), int(g_bf16), n, tile, stream)
+                              g.data_ptr(), int(g_bf16), n, tile, layer_tiles, stream)
         if rc != 0:
             raise RuntimeError("stream_probe failed with %d" % rc)
 
@@ -175,6 +176,8 @@ def stream_probe_all() -> None:
     for pattern, tile in (("single_pass", 8192), ("moments", 512), ("apply", 512),
                           ("read", 2048), ("copy", 512)):
         out[pattern + "_GBps"] = stream_rate(pattern, 335141888, True, tile)
+    # the single pass's own layout: 1024-element blocks dealt over layers of 512 tiles
+    out["single_pass_dealt_GBps"] = stream_rate("single_pass", 335141888, True, 8192, 512)
     print(json.dumps(out), flush=True)
 
 
@@ -350,8 +353,11 @@ def main() -> int:
     dom_elems = P_single if dom_is_single else P - P_single
     attainable = None
     if not args.skip_nonfinite and not args.bf16_copy and args.algo != "lars" and dom_elems:
+        # the single pass deals its layers' blocks over their tiles; its largest
+        # layers on BERT-Large have 512 tiles
         attainable = stream_rate(dom_pattern, dom_elems, ps.g_dtype == "bf16",
-                                 8192 if dom_is_single else (chunk or 512))
+                                 8192 if dom_is_single else (chunk or 512),
+                                 512 if dom_is_single else 0)
         eprint("stream probe (%s pattern, %d elements): %.0f GB/s"
                % (dom_pattern, dom_elems, attainable))
     cpu = None

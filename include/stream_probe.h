@@ -45,9 +45,14 @@ typedef enum stream_pattern {
  * 256 threads (a multiple of 8 in [8, 2^24]; the single-pass kernel uses
  * 8192, the moment and apply kernels 512), enqueued on `stream`
  * (hipStream_t, NULL = null stream). g_bf16: 1 if g holds bf16.
+ * layer_tiles = 0: each workgroup streams a contiguous tile. layer_tiles > 0
+ * (tile a multiple of 1024): the single-pass kernel's layout, the array cut
+ * into layers of layer_tiles tiles, tile i of a layer holding the layer's
+ * 1024-element blocks i, i + layer_tiles, ....
  */
 PROBE_API int stream_probe(int32_t pattern, float *x, float *m, float *v, const void *g,
-                           int32_t g_bf16, int64_t n, int32_t tile, void *stream);
+                           int32_t g_bf16, int64_t n, int32_t tile, int32_t layer_tiles,
+                           void *stream);
 
 #ifdef __cplusplus
 }

@@ -2,7 +2,8 @@
 // their arithmetic: the attainable bandwidth for each kernel's traffic (see
 // include/stream_probe.h). Each workgroup of 256 threads streams one tile of
 // `tile` elements, two float4 groups per thread in flight, with nontemporal
-// 16-byte loads and stores (8-byte loads for bf16 g), like the kernels.
+// 16-byte loads and stores (8-byte loads for bf16 g), like the kernels. A
+// partial last float4 group is skipped (the probe measures rates, n is large).
 
 #include <hip/hip_runtime.h>
 
@@ -41,22 +42,35 @@ __device__ __forceinline__ f32x4 ldg(const void *g, int64_t i) {
 // `keep`, which is 0 at run time: the term is then exactly -0.0, so every
 // array keeps its values (NaN payloads aside) while the compiler cannot drop
 // a load or a store.
+// Element offset of float4 group q of workgroup b: contiguous tiles, or,
+// with `layer_tiles` > 0, the layer-cyclic deal of the single-pass kernel
+// (the array cut into layers of layer_tiles tiles; tile i of a layer holds
+// its 1024-element blocks i, i + layer_tiles, ...).
+__device__ __forceinline__ int64_t element(int64_t b, int q, int32_t tile, int32_t layer_tiles) {
+    if (layer_tiles <= 0)
+        return b * tile + 4 * int64_t(q);
+    const int64_t layer = b / layer_tiles, i = b % layer_tiles;
+    const int64_t block = int64_t(q / kThreads) * layer_tiles + i;
+    return (layer * layer_tiles) * int64_t(tile) + block * (4 * kThreads) + 4 * (q % kThreads);
+}
+
 template <bool kBf16, bool kRX, bool kWX, bool kRM, bool kWM, bool kRV, bool kWV, bool kRG>
 __global__ __launch_bounds__(kThreads) void stream_kernel(float *x, float *m, float *v,
                                                         const void *g, int64_t n, int32_t tile,
-                                                        uint32_t keep, float *sink) {
-    const int64_t start = int64_t(blockIdx.x) * tile;
-    const int64_t len = n - start < tile ? n - start : tile;
-    const int n4 = int(len >> 2);
+                                                        int32_t layer_tiles, uint32_t keep,
+                                                        float *sink) {
+    const int n4 = tile >> 2;
     f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
     for (int base = threadIdx.x; base < n4; base += kThreads * kUnroll) {
         f32x4 xr[kUnroll], mr[kUnroll], vr[kUnroll], gr[kUnroll];
+        int64_t at[kUnroll];
 #pragma unroll
         for (int k = 0; k < kUnroll; ++k) {
             const int q = base + k * kThreads;
+            at[k] = element(blockIdx.x, q, tile, layer_tiles);
             xr[k] = mr[k] = vr[k] = gr[k] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-            if (q < n4) {
-                const int64_t i = start + 4 * int64_t(q);
+            if (q < n4 && at[k] + 4 <= n) {
+                const int64_t i = at[k];
                 if constexpr (kRX) xr[k] = ld4(x + i);
                 if constexpr (kRM) mr[k] = ld4(m + i);
                 if constexpr (kRV) vr[k] = ld4(v + i);
@@ -66,8 +80,8 @@ __global__ __launch_bounds__(kThreads) void stream_kernel(float *x, float *m, fl
 #pragma unroll
         for (int k = 0; k < kUnroll; ++k) {
             const int q = base + k * kThreads;
-            if (q < n4) {
-                const int64_t i = start + 4 * int64_t(q);
+            if (q < n4 && at[k] + 4 <= n) {
+                const int64_t i = at[k];
                 const f32x4 sum = xr[k] + mr[k] + vr[k] + gr[k];
                 f32x4 t;
 #pragma unroll
@@ -109,9 +123,11 @@ const void *pick(int pattern) {
 }  // namespace
 
 extern "C" int stream_probe(int32_t pattern, float *x, float *m, float *v, const void *g,
-                            int32_t g_bf16, int64_t n, int32_t tile, void *stream) {
+                            int32_t g_bf16, int64_t n, int32_t tile, int32_t layer_tiles,
+                            void *stream) {
     if (pattern < STREAM_SINGLE_PASS || pattern > STREAM_COPY || n < 1 || tile < 8 ||
-        tile > (1 << 24) || tile % 8 != 0 || (g_bf16 != 0 && g_bf16 != 1))
+        tile > (1 << 24) || tile % 8 != 0 || (g_bf16 != 0 && g_bf16 != 1) || layer_tiles < 0 ||
+        (layer_tiles > 0 && tile % (4 * kThreads) != 0))
         return -1;
     const bool reads_g =
         pattern == STREAM_SINGLE_PASS || pattern == STREAM_MOMENTS || pattern == STREAM_READ;
@@ -121,12 +137,14 @@ extern "C" int stream_probe(int32_t pattern, float *x, float *m, float *v, const
                            reinterpret_cast<uintptr_t>(v) | reinterpret_cast<uintptr_t>(g);
     if (mask & 15u)
         return -1;
-    const int64_t blocks = (n + tile - 1) / tile;
+    int64_t blocks = (n + tile - 1) / tile;
+    if (layer_tiles > 0)  // whole layers: tiles past the end find no element
+        blocks = (blocks + layer_tiles - 1) / layer_tiles * layer_tiles;
     if (blocks > 0x7fffffff)
         return -1;
     uint32_t keep = 0u;
     float *sink = nullptr;
-    void *params[] = {&x, &m, &v, &g, &n, &tile, &keep, &sink};
+    void *params[] = {&x, &m, &v, &g, &n, &tile, &layer_tiles, &keep, &sink};
     const void *fn = g_bf16 ? pick<true>(pattern) : pick<false>(pattern);
     hipError_t err = hipLaunchKernel(fn, dim3(unsigned(blocks)), dim3(kThreads), params, 0,
                                      static_cast<hipStream_t>(stream));

@@ -163,15 +163,18 @@ def test_stream_probe_library_validates_on_the_host():
     probe = ctypes.CDLL(build.PROBE_LIBRARY)
     probe.stream_probe.argtypes = [ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
                                    ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
-                                   ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p]
+                                   ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
+                                   ctypes.c_void_p]
     fake = 1 << 20  # aligned, never dereferenced: every case fails validation
     bad = [
-        (9, fake, fake, fake, fake, 1, 100, 512),     # unknown pattern
-        (0, fake, fake, fake, fake, 1, 0, 512),       # n < 1
-        (0, fake, fake, fake, fake, 1, 100, 12),      # tile not a multiple of 8
-        (0, fake, fake, fake, fake, 2, 100, 512),     # g_bf16 not 0/1
-        (0, fake, fake, fake, None, 1, 100, 512),     # single pass reads g
-        (0, fake + 4, fake, fake, fake, 1, 100, 512), # misaligned
+        (9, fake, fake, fake, fake, 1, 100, 512, 0),     # unknown pattern
+        (0, fake, fake, fake, fake, 1, 0, 512, 0),       # n < 1
+        (0, fake, fake, fake, fake, 1, 100, 12, 0),      # tile not a multiple of 8
+        (0, fake, fake, fake, fake, 2, 100, 512, 0),     # g_bf16 not 0/1
+        (0, fake, fake, fake, None, 1, 100, 512, 0),     # single pass reads g
+        (0, fake + 4, fake, fake, fake, 1, 100, 512, 0), # misaligned
+        (0, fake, fake, fake, fake, 1, 100, 512, 4),     # dealt tiles need 1024 | tile
+        (0, fake, fake, fake, fake, 1, 100, 8192, -1),   # negative layer_tiles
     ]
     for args in bad:
         assert probe.stream_probe(*args, None) == -1, args
