@@ -36,7 +36,7 @@ def test_library_exports_every_declared_symbol(lib):
 
 
 def test_status_strings(lib):
-    for code in range(-7, 1):
+    for code in range(-8, 1):
         assert _lib.status_str(code) != "unknown status"
     assert _lib.status_str(-99) == "unknown status"
 
@@ -153,6 +153,12 @@ def test_null_plan_and_outputs(lib):
     assert lib.lamb_plan_set_timing(None, 4, 1) == _lib.LAMB_ENULL
     assert lib.lamb_plan_set_bf16_copies(None, None) == _lib.LAMB_ENULL
     assert lib.lamb_plan_create(None, 1, 0, 0, 0, None) == _lib.LAMB_ENULL
+    assert lib.lamb_plan_set_path(None, 0) == _lib.LAMB_ENULL
+    assert lib.lamb_plan_tiles(None, None, None) == _lib.LAMB_ENULL
+    assert lib.lamb_plan_check(None, None) == _lib.LAMB_ENULL
+    per = (ctypes.c_double * 5)()
+    steps = ctypes.c_int64()
+    assert lib.lamb_plan_timing(None, per, ctypes.byref(steps)) == _lib.LAMB_ENULL
 
 
 def test_stream_probe_library_validates_on_the_host():
