@@ -80,3 +80,33 @@ def test_abandoned_wait_is_reported(monkeypatch):
         pair.compare(ref, "after a give-up")
     finally:
         pair.close()
+
+
+def test_single_pass_beside_other_work():
+    """Single-pass steps while another stream keeps the GPU busy with large
+    fp32 matrix products: the grid may wait for residency, but every wait
+    ends, nothing is given up, and the result matches the oracle."""
+    torch = H.torch_cuda()
+    ps = paramsets.get(1)
+    subset = [0, 3, 4, 5, 6, 7, 8, ps.n_tensors - 1]
+    pair = H.Pair(paramsets.draw_params(ps, device="cuda"), ps.wd_mask(), ps.g_dtype, "lamb",
+                  oracle_subset=subset, path="auto")
+    side = torch.cuda.Stream()
+    a = torch.randn(4096, 4096, device="cuda")
+    b = torch.randn(4096, 4096, device="cuda")
+    try:
+        hp = H.lamb_hp(ps)
+        for t in range(1, 4):
+            hg = pair.set_grads(paramsets.draw_grads(ps, t, device="cuda"))
+            torch.cuda.synchronize()
+            side.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.stream(side):
+                for _ in range(6):
+                    c = torch.mm(a, b)
+            pair.gpu_lamb(hp, t)
+            ref = pair.oracle_lamb(hg, hp, t)
+            torch.cuda.current_stream().wait_stream(side)
+            pair.compare(ref, "beside other work, step %d" % t)
+        del c
+    finally:
+        pair.close()
