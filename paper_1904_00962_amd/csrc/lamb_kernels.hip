@@ -58,7 +58,8 @@ __device__ __forceinline__ gfloat *global_view(float *p) { return (gfloat *)p; }
 __device__ __forceinline__ gcfloat *global_view(const float *p) { return (gcfloat *)p; }
 
 // Tuning knobs (compile-time; the defaults are the measured best on MI355X).
-// LAMB_UNROLL: float4 groups each thread keeps in flight per loop trip.
+// LAMB_UNROLL: float4 groups each thread of the two-pass kernels keeps in
+//   flight per loop trip.
 // LAMB_NONTEMPORAL: stream x, g, m, v with nontemporal loads and stores; the
 //   data is touched once per pass, so it should not displace cache lines.
 // LAMB_APPLY_REVERSE: the apply pass walks chunks last-to-first, so its first
@@ -655,7 +656,15 @@ __global__ __launch_bounds__(kSegBlock) void finalize_kernel(
 #ifndef LAMB_MEMBER_SLEEP
 #define LAMB_MEMBER_SLEEP LAMB_SPIN_SLEEP
 #endif
-static_assert(kTileGroups % kUnroll == 0, "tile groups must be a multiple of the unroll");
+// LAMB_FUSED_UNROLL: float4 groups each thread of the single pass loads per
+// trip. One beats two there (about half a percent on BERT-Large): it leaves
+// more registers free, and a round's many resident tiles already keep enough
+// loads in flight.
+#ifndef LAMB_FUSED_UNROLL
+#define LAMB_FUSED_UNROLL 1
+#endif
+constexpr int kFusedUnroll = LAMB_FUSED_UNROLL;
+static_assert(kTileGroups % kFusedUnroll == 0, "tile groups must be a multiple of the unroll");
 
 __device__ __forceinline__ uint64_t slot_load(const uint64_t *p) {
     return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -753,12 +762,12 @@ void fused_kernel(const TensorDesc *__restrict__ tensors, const ChunkDesc *__res
         f32x4 us[kTileGroups];
         double sum_xx = 0.0, sum_uu = 0.0;
 #pragma unroll
-        for (int k0 = 0; k0 < kTileGroups; k0 += kUnroll) {
-            f32x4 xr[kUnroll], gr[kUnroll], mr[kUnroll], vr[kUnroll];
-            int64_t at[kUnroll];
-            int ok[kUnroll];
+        for (int k0 = 0; k0 < kTileGroups; k0 += kFusedUnroll) {
+            f32x4 xr[kFusedUnroll], gr[kFusedUnroll], mr[kFusedUnroll], vr[kFusedUnroll];
+            int64_t at[kFusedUnroll];
+            int ok[kFusedUnroll];
 #pragma unroll
-            for (int k = 0; k < kUnroll; ++k) {
+            for (int k = 0; k < kFusedUnroll; ++k) {
                 group(k0 + k, at[k], ok[k]);
                 xr[k] = gr[k] = mr[k] = vr[k] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
                 if (ok[k] == 4) {
@@ -778,7 +787,7 @@ void fused_kernel(const TensorDesc *__restrict__ tensors, const ChunkDesc *__res
                 }
             }
 #pragma unroll
-            for (int k = 0; k < kUnroll; ++k) {
+            for (int k = 0; k < kFusedUnroll; ++k) {
                 f32x4 ur = {0.0f, 0.0f, 0.0f, 0.0f};
                 if (ok[k] > 0) {
 #pragma unroll
