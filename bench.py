@@ -315,7 +315,7 @@ def main() -> int:
     if args.bf16_copy:
         opt.attach_bf16_copies("allocate")
     n_tensors, n_chunks, chunk = _lib.lamb_plan_info(opt.plan)
-    tiles_per_tensor, n_tiles = _lib.lamb_plan_tiles(opt.plan)
+    tiles_per_tensor, n_tiles, tile_groups = _lib.lamb_plan_tiles(opt.plan)
     single = args.path == "auto"
     P = sum(x.numel() for x in xs)
     P_single = sum(x.numel() for x, k in zip(xs, tiles_per_tensor) if k) if single else 0
@@ -356,7 +356,7 @@ def main() -> int:
         # the single pass deals its layers' blocks over their tiles; its largest
         # layers on BERT-Large have 512 tiles
         attainable = stream_rate(dom_pattern, dom_elems, ps.g_dtype == "bf16",
-                                 8192 if dom_is_single else (chunk or 512),
+                                 1024 * tile_groups if dom_is_single else (chunk or 512),
                                  512 if dom_is_single else 0)
         eprint("stream probe (%s pattern, %d elements): %.0f GB/s"
                % (dom_pattern, dom_elems, attainable))
@@ -391,7 +391,8 @@ def main() -> int:
     g_name = "bf16" if g_bytes == 2 else "f32"
     # the roofline entry covers the kernel that takes the most time
     if avg_one >= avg_mom:
-        dom = dict(kernel="fused_kernel<%s, %s, %s>" % (algo_name, g_name, args.norm),
+        dom = dict(kernel="fused_kernel<%s, %s, %s, %d groups>" % (algo_name, g_name, args.norm,
+                                                                  tile_groups),
                    achieved=one_gbps, bytes_per_launch=b_one * P_single,
                    traffic=counter_traffic("single_pass", workload, src_hash)
                    if default_mode else None)
@@ -423,6 +424,7 @@ def main() -> int:
                         % (workload, algo_name, n_tensors, P, ps.g_dtype),
             "algo": args.algo, "tensors": n_tensors, "params": P, "grad_dtype": ps.g_dtype,
             "path": args.path, "single_pass_params": P_single, "single_pass_tiles": n_tiles,
+            "tile_elems": 1024 * tile_groups if single else 0,
             "chunk_elems": chunk, "chunks": n_chunks, "norm": args.norm,
             "grad_scale": args.grad_scale, "skip_nonfinite": args.skip_nonfinite,
             "bf16_copy": args.bf16_copy,

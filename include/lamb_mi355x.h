@@ -105,11 +105,17 @@ typedef enum lamb_norm {
 /*
  * How a plan's direct-mode steps (skip_nonfinite = 0) run.
  *  LAMB_PATH_AUTO      (default) every layer of at most 4 * (compute units)
- *                      tiles of 8192 elements (8M elements on MI355X) takes
- *                      one single-pass kernel that reads x, g, m, v and
- *                      writes x, m, v once: a persistent grid keeps each
- *                      tile's x and update direction in registers while the
- *                      layer's norms are combined. Larger layers take the
+ *                      tiles takes one single-pass kernel that reads x, g,
+ *                      m, v and writes x, m, v once: a persistent grid keeps
+ *                      each tile's x and update direction on chip while the
+ *                      layer's norms are combined. A tile holds 8192
+ *                      elements, or 10240 when that puts more parameters on
+ *                      the single pass (lamb_tile_schedule): layers of up to
+ *                      8M or 10M elements on MI355X. The environment
+ *                      variable LAMB_MI355X_TILE_GROUPS (8 or 10), read by
+ *                      lamb_plan_create, fixes the tile instead; tests use
+ *                      it to run the wider tile on small layers (any other
+ *                      value fails with LAMB_EINVAL). Larger layers take the
  *                      two-pass kernels. Needs the device's full occupancy
  *                      for the length of that kernel: the library runs the
  *                      single-pass kernels of one process one at a time
@@ -229,14 +235,16 @@ LAMB_API lamb_status lamb_plan_info(const lamb_plan *plan, int32_t *n_tensors,
 LAMB_API lamb_status lamb_plan_set_path(lamb_plan *plan, int32_t path);
 
 /*
- * The single-pass layout (host outputs; either may be NULL):
+ * The single-pass layout (host outputs; any may be NULL):
  *   tiles_per_tensor  n_tensors entries: the layer's tile count, or 0 when
  *                     the layer takes the two-pass kernels
  *   n_tiles           total tiles of the single pass
+ *   tile_groups       the tile shape lamb_tile_schedule chose: 8 (tiles of
+ *                     8192 elements) or 10 (10240 elements)
  * Errors: LAMB_ENULL (plan).
  */
 LAMB_API lamb_status lamb_plan_tiles(const lamb_plan *plan, int32_t *tiles_per_tensor,
-                            int32_t *n_tiles);
+                            int32_t *n_tiles, int32_t *tile_groups);
 
 /*
  * Wait for `stream` and report whether a single-pass step of the plan gave
@@ -352,17 +360,20 @@ LAMB_API lamb_status lamb_chunk_table(const int64_t *numel, int32_t n_tensors,
  * The single-pass schedule a plan would use (host only, no HIP call). The
  * single-pass kernel runs a persistent grid of `round` workgroups; workgroup
  * w takes entries w, w + round, ..., so the entry list falls into rounds of
- * `round` entries. A layer of n elements takes T = ceil(n / 8192) tiles; if
- * T <= max_round it takes the single pass: its tiles are consecutive entries
- * inside one round, and tile j holds the layer's 1024-element blocks j,
- * j + T, ..., j + 7T (those inside the layer). Layers are packed first-fit by
- * decreasing tile count (ties in table order) into the fewest rounds of
- * `max_round` entries; `round` is then the narrowest width that packs into
- * as few rounds, so the rounds come out about equally full. The gap a
- * round leaves is filled with empty entries (tensor -1, length 0). A plan
- * uses max_round = 4 * (compute units).
+ * `round` entries. A tile holds G blocks of 1024 elements (G = 8 or 10). A
+ * layer of n elements takes T = ceil(n / (1024 G)) tiles; if T <= max_round
+ * it takes the single pass: its tiles are consecutive entries inside one
+ * round, and tile j holds the layer's blocks j, j + T, ..., j + (G - 1) T
+ * (those inside the layer). Layers are packed first-fit by decreasing tile
+ * count (ties in table order) into the fewest rounds of `max_round`
+ * entries; `round` is then the narrowest width that packs into as few
+ * rounds, so the rounds come out about equally full. The gap a round leaves
+ * is filled with empty entries (tensor -1, length 0). A plan uses
+ * max_round = 4 * (compute units) and tile_groups = 0.
  *   numel         host, n_tensors sizes (>= 1 each)
  *   max_round     widest round, >= 1
+ *   tile_groups   G: 8, 10, or 0 for a plan's choice, which is 10 only if
+ *                 that puts more parameters on the single pass than 8
  *   capacity      length of the three entry arrays (0 with NULL arrays to
  *                 query the count)
  *   entry_tensor  host, layer of each entry or -1
@@ -373,13 +384,16 @@ LAMB_API lamb_status lamb_chunk_table(const int64_t *numel, int32_t n_tensors,
  *                 the two-pass kernels (more than `max_round` tiles)
  *   n_entries     receives the length of the list
  *   round_out     receives the round width (the single-pass grid)
+ *   groups_out    receives G (may be NULL)
  * Errors: LAMB_ENULL, LAMB_EINVAL (including capacity too small, in which
- * case *n_entries, *round_out, first_tile and tiles are still filled).
+ * case *n_entries, *round_out, *groups_out, first_tile and tiles are still
+ * filled).
  */
 LAMB_API lamb_status lamb_tile_schedule(const int64_t *numel, int32_t n_tensors,
-                               int32_t max_round, int32_t capacity, int32_t *entry_tensor,
-                               int64_t *entry_start, int32_t *entry_len, int32_t *first_tile,
-                               int32_t *tiles, int32_t *n_entries, int32_t *round_out);
+                               int32_t max_round, int32_t tile_groups, int32_t capacity,
+                               int32_t *entry_tensor, int64_t *entry_start, int32_t *entry_len,
+                               int32_t *first_tile, int32_t *tiles, int32_t *n_entries,
+                               int32_t *round_out, int32_t *groups_out);
 
 /*
  * Per-kernel timing with HIP events, for measurement. max_steps > 0 creates

@@ -121,10 +121,10 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
     lib.lamb_plan_set_timing.argtypes = [vp, i32, i32]
     lib.lamb_plan_timing.argtypes = [vp, P(ctypes.c_double), P(i64)]
     lib.lamb_plan_set_path.argtypes = [vp, i32]
-    lib.lamb_plan_tiles.argtypes = [vp, P(i32), P(i32)]
+    lib.lamb_plan_tiles.argtypes = [vp, P(i32), P(i32), P(i32)]
     lib.lamb_plan_check.argtypes = [vp, vp]
-    lib.lamb_tile_schedule.argtypes = [P(i64), i32, i32, i32, P(i32), P(i64), P(i32), P(i32),
-                                       P(i32), P(i32), P(i32)]
+    lib.lamb_tile_schedule.argtypes = [P(i64), i32, i32, i32, i32, P(i32), P(i64), P(i32),
+                                       P(i32), P(i32), P(i32), P(i32), P(i32)]
     lib.lamb_status_str.argtypes = [i32]
     lib.lamb_status_str.restype = ctypes.c_char_p
     lib.lamb_last_error.argtypes = []
@@ -319,32 +319,37 @@ def lamb_plan_set_path(plan: Plan, path="auto") -> None:
     _check(load().lamb_plan_set_path(_vp(plan.handle), code), "lamb_plan_set_path")
 
 
-def lamb_plan_tiles(plan: Plan) -> Tuple[list, int]:
-    """(tiles per tensor, 0 for a two-pass layer; total single-pass tiles)."""
+def lamb_plan_tiles(plan: Plan) -> Tuple[list, int, int]:
+    """(tiles per tensor, 0 for a two-pass layer; total single-pass tiles;
+    tile shape in float4 groups per thread, 8 or 10)."""
     n = lamb_plan_info(plan)[0]
     per = (ctypes.c_int32 * n)()
-    total = ctypes.c_int32()
-    _check(load().lamb_plan_tiles(_vp(plan.handle), per, ctypes.byref(total)), "lamb_plan_tiles")
-    return list(per), total.value
+    total, groups = ctypes.c_int32(), ctypes.c_int32()
+    _check(load().lamb_plan_tiles(_vp(plan.handle), per, ctypes.byref(total),
+                                  ctypes.byref(groups)), "lamb_plan_tiles")
+    return list(per), total.value, groups.value
 
 
-def lamb_tile_schedule(numel: Sequence[int], max_round: int):
+def lamb_tile_schedule(numel: Sequence[int], max_round: int, tile_groups: int = 0):
     """The single-pass schedule (host only): (entry_tensor, entry_start,
-    entry_len, first_tile, tiles, round) with lists for the first five;
-    entry_tensor -1 marks an empty entry, ``round`` is the grid width."""
+    entry_len, first_tile, tiles, round, groups) with lists for the first
+    five; entry_tensor -1 marks an empty entry, ``round`` is the grid width,
+    ``groups`` the tile shape (``tile_groups`` 0: a plan's choice)."""
     n = len(numel)
     arr = (ctypes.c_int64 * n)(*[int(v) for v in numel])
     first = (ctypes.c_int32 * n)()
     tiles = (ctypes.c_int32 * n)()
-    count, width = ctypes.c_int32(), ctypes.c_int32()
+    count, width, groups = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
     lib = load()
-    _check(lib.lamb_tile_schedule(arr, n, int(max_round), 0, None, None, None, first, tiles,
-                                  ctypes.byref(count), ctypes.byref(width)), "lamb_tile_schedule")
+    _check(lib.lamb_tile_schedule(arr, n, int(max_round), int(tile_groups), 0, None, None, None,
+                                  first, tiles, ctypes.byref(count), ctypes.byref(width),
+                                  ctypes.byref(groups)), "lamb_tile_schedule")
     k = count.value
     et, es, el = (ctypes.c_int32 * k)(), (ctypes.c_int64 * k)(), (ctypes.c_int32 * k)()
-    _check(lib.lamb_tile_schedule(arr, n, int(max_round), k, et, es, el, first, tiles,
-                                  ctypes.byref(count), ctypes.byref(width)), "lamb_tile_schedule")
-    return list(et), list(es), list(el), list(first), list(tiles), width.value
+    _check(lib.lamb_tile_schedule(arr, n, int(max_round), groups.value, k, et, es, el, first,
+                                  tiles, ctypes.byref(count), ctypes.byref(width), None),
+           "lamb_tile_schedule")
+    return list(et), list(es), list(el), list(first), list(tiles), width.value, groups.value
 
 
 def lamb_plan_check(plan: Plan, stream: int = 0) -> None:

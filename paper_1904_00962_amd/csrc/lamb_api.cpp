@@ -42,6 +42,7 @@ struct lamb_plan {
     lamb_path path = LAMB_PATH_AUTO;
     int32_t cu_count = 0;
     int32_t round = 0;             // single-pass grid: workgroups per round of the tile list
+    int32_t tile_groups = kTileGroups;  // single-pass tile shape (float4 groups per thread)
     uint32_t spin_limit = kDefaultSpinLimit;
     int32_t n_tiles = 0;
     int32_t n_rest = 0;            // layers outside the single pass
@@ -195,9 +196,9 @@ hipError_t gated_fused_launch(int device, hipStream_t stream, const StepKind &ki
     if (err != hipSuccess)
         return err;
     if (capture != hipStreamCaptureStatusNone)
-        return launch_fused(kind, plan->tensors, plan->tiles, plan->n_tiles, grid, plan->slots,
-                            plan->ctl, plan->flags, guarded, nonfinite_out, a, f, ratio_out,
-                            norms_out, stream);
+        return launch_fused(kind, plan->tile_groups, plan->tensors, plan->tiles, plan->n_tiles,
+                            grid, plan->slots, plan->ctl, plan->flags, guarded, nonfinite_out, a,
+                            f, ratio_out, norms_out, stream);
     std::lock_guard<std::mutex> lock(g_gate_mutex);
     if (g_gates.size() <= size_t(device))
         g_gates.resize(size_t(device) + 1);
@@ -212,9 +213,9 @@ hipError_t gated_fused_launch(int device, hipStream_t stream, const StepKind &ki
         if (err != hipSuccess)
             return err;
     }
-    err = launch_fused(kind, plan->tensors, plan->tiles, plan->n_tiles, grid, plan->slots,
-                       plan->ctl, plan->flags, guarded, nonfinite_out, a, f, ratio_out, norms_out,
-                       stream);
+    err = launch_fused(kind, plan->tile_groups, plan->tensors, plan->tiles, plan->n_tiles, grid,
+                       plan->slots, plan->ctl, plan->flags, guarded, nonfinite_out, a, f,
+                       ratio_out, norms_out, stream);
     if (err != hipSuccess)
         return err;
     err = hipEventRecord(gate.done, stream);
@@ -306,10 +307,27 @@ lamb_status lamb_chunk_table(const int64_t *numel, int32_t n_tensors, int32_t ch
     return LAMB_OK;
 }
 
+namespace {
+
+// Parameters a tile shape of `groups` puts on the single pass: those of the
+// layers of at most `max_round` tiles.
+int64_t single_pass_params(const int64_t *numel, int32_t n_tensors, int32_t max_round,
+                           int groups) {
+    const int64_t te = tile_elems(groups);
+    int64_t total = 0;
+    for (int32_t i = 0; i < n_tensors; ++i)
+        if ((numel[i] + te - 1) / te <= max_round)
+            total += numel[i];
+    return total;
+}
+
+}  // namespace
+
 lamb_status lamb_tile_schedule(const int64_t *numel, int32_t n_tensors, int32_t max_round,
-                               int32_t capacity, int32_t *entry_tensor, int64_t *entry_start,
-                               int32_t *entry_len, int32_t *first_tile, int32_t *tiles,
-                               int32_t *n_entries, int32_t *round_out) {
+                               int32_t tile_groups, int32_t capacity, int32_t *entry_tensor,
+                               int64_t *entry_start, int32_t *entry_len, int32_t *first_tile,
+                               int32_t *tiles, int32_t *n_entries, int32_t *round_out,
+                               int32_t *groups_out) {
     if (!numel || !n_entries || !first_tile || !tiles || !round_out)
         return fail(LAMB_ENULL,
                     "numel, first_tile, tiles, n_entries and round_out must not be NULL");
@@ -317,16 +335,30 @@ lamb_status lamb_tile_schedule(const int64_t *numel, int32_t n_tensors, int32_t 
         return fail(LAMB_EINVAL, "n_tensors = %d, need >= 1", n_tensors);
     if (max_round < 1)
         return fail(LAMB_EINVAL, "max_round = %d, need >= 1", max_round);
+    if (tile_groups != 0 && tile_groups != kTileGroups && tile_groups != kWideGroups)
+        return fail(LAMB_EINVAL, "tile_groups = %d, need 0, %d or %d", tile_groups, kTileGroups,
+                    kWideGroups);
     for (int32_t i = 0; i < n_tensors; ++i)
         if (numel[i] < 1)
             return fail(LAMB_EINVAL, "tensor %d has numel %lld, need >= 1", i,
                         static_cast<long long>(numel[i]));
+    // A plan's choice: the wide tile only if it puts more parameters on the
+    // single pass (with as many, the narrow tile streams slightly faster).
+    int groups = tile_groups;
+    if (groups == 0)
+        groups = single_pass_params(numel, n_tensors, max_round, kWideGroups) >
+                         single_pass_params(numel, n_tensors, max_round, kTileGroups)
+                     ? kWideGroups
+                     : kTileGroups;
+    if (groups_out)
+        *groups_out = groups;
+    const int64_t te = tile_elems(groups);
     // Layers of at most `max_round` tiles, in decreasing tile count (ties in
     // table order).
     std::vector<std::pair<int64_t, int32_t>> teams;
     int64_t total_tiles = 0, largest = 0;
     for (int32_t i = 0; i < n_tensors; ++i) {
-        const int64_t nt = (numel[i] + kTileElems - 1) / kTileElems;
+        const int64_t nt = (numel[i] + te - 1) / te;
         first_tile[i] = 0;
         tiles[i] = 0;
         if (nt <= max_round) {
@@ -393,7 +425,7 @@ lamb_status lamb_tile_schedule(const int64_t *numel, int32_t n_tensors, int32_t 
     int32_t k = 0;
     for (size_t r = 0; r < fill.size(); ++r) {
         for (int32_t i : members[r]) {
-            const int64_t nt = (numel[i] + kTileElems - 1) / kTileElems;
+            const int64_t nt = (numel[i] + te - 1) / te;
             first_tile[i] = k;
             tiles[i] = int32_t(nt);
             for (int64_t j = 0; j < nt; ++j, ++k) {
@@ -401,7 +433,7 @@ lamb_status lamb_tile_schedule(const int64_t *numel, int32_t n_tensors, int32_t 
                     continue;
                 // tile j holds the blocks j, j + nt, ... of kBlockElems each
                 int64_t held = 0;
-                for (int64_t b = j; b < int64_t(kTileGroups) * nt; b += nt)
+                for (int64_t b = j; b < int64_t(groups) * nt; b += nt)
                     held += std::max<int64_t>(0, std::min<int64_t>(kBlockElems,
                                                                    numel[i] - b * kBlockElems));
                 entry_tensor[k] = i;
@@ -562,16 +594,26 @@ lamb_status lamb_plan_create(const lamb_tensor *tensors, int32_t n_tensors,
     const int32_t max_round = int32_t(std::max<int64_t>(1, int64_t(kFusedBlocksPerCu) * cu_count));
     std::vector<int32_t> first_tile(static_cast<size_t>(n_tensors)),
         tile_count(static_cast<size_t>(n_tensors));
-    int32_t n_entries = 0, round = 0;
-    st = lamb_tile_schedule(numel.data(), n_tensors, max_round, 0, nullptr, nullptr, nullptr,
-                            first_tile.data(), tile_count.data(), &n_entries, &round);
+    int32_t n_entries = 0, round = 0, groups = 0;
+    if (const char *env = std::getenv("LAMB_MI355X_TILE_GROUPS")) {
+        char *end = nullptr;
+        const long v = std::strtol(env, &end, 10);
+        if (end == env || *end != '\0' || (v != kTileGroups && v != kWideGroups))
+            return fail(LAMB_EINVAL, "LAMB_MI355X_TILE_GROUPS = \"%s\", need %d or %d", env,
+                        kTileGroups, kWideGroups);
+        groups = int32_t(v);
+    }
+    st = lamb_tile_schedule(numel.data(), n_tensors, max_round, groups, 0, nullptr, nullptr,
+                            nullptr, first_tile.data(), tile_count.data(), &n_entries, &round,
+                            &groups);
     std::vector<int32_t> entry_tensor(static_cast<size_t>(n_entries)),
         entry_len(static_cast<size_t>(n_entries));
     std::vector<int64_t> entry_start(static_cast<size_t>(n_entries));
     if (st == LAMB_OK)
-        st = lamb_tile_schedule(numel.data(), n_tensors, max_round, n_entries,
+        st = lamb_tile_schedule(numel.data(), n_tensors, max_round, groups, n_entries,
                                 entry_tensor.data(), entry_start.data(), entry_len.data(),
-                                first_tile.data(), tile_count.data(), &n_entries, &round);
+                                first_tile.data(), tile_count.data(), &n_entries, &round,
+                                nullptr);
     if (st != LAMB_OK)
         return st;
     std::vector<ChunkDesc> host_tiles(static_cast<size_t>(n_entries));
@@ -634,6 +676,7 @@ lamb_status lamb_plan_create(const lamb_tensor *tensors, int32_t n_tensors,
     plan->device = device;
     plan->cu_count = cu_count;
     plan->round = round;
+    plan->tile_groups = groups;
     if (const char *env = std::getenv("LAMB_MI355X_SPIN_LIMIT")) {
         const long long v = std::atoll(env);
         plan->spin_limit = uint32_t(std::min<long long>(std::max<long long>(v, 1), 1LL << 30));
@@ -757,7 +800,7 @@ lamb_status lamb_plan_create(const lamb_tensor *tensors, int32_t n_tensors,
                 kind.bf16_grad = g_dtype == LAMB_GRAD_BF16;
                 kind.deferred = false;
                 int per_cu = 0;
-                err = fused_blocks_per_cu(kind, &per_cu);
+                err = fused_blocks_per_cu(kind, plan->tile_groups, &per_cu);
                 plan->fused_per_cu[int(kind.algo)][kind.bf16_grad ? 1 : 0][nk] = per_cu;
             }
         }
@@ -1143,7 +1186,8 @@ lamb_status lamb_plan_set_path(lamb_plan *plan, int32_t path) {
     return LAMB_OK;
 }
 
-lamb_status lamb_plan_tiles(const lamb_plan *plan, int32_t *tiles_per_tensor, int32_t *n_tiles) {
+lamb_status lamb_plan_tiles(const lamb_plan *plan, int32_t *tiles_per_tensor, int32_t *n_tiles,
+                            int32_t *tile_groups) {
     if (!plan)
         return fail(LAMB_ENULL, "plan must not be NULL");
     if (tiles_per_tensor)
@@ -1151,6 +1195,8 @@ lamb_status lamb_plan_tiles(const lamb_plan *plan, int32_t *tiles_per_tensor, in
             tiles_per_tensor[i] = plan->host_tensors[size_t(i)].n_tiles;
     if (n_tiles)
         *n_tiles = plan->n_tiles;
+    if (tile_groups)
+        *tile_groups = plan->tile_groups;
     return LAMB_OK;
 }
 

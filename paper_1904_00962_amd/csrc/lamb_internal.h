@@ -26,22 +26,30 @@ constexpr int32_t kDefaultChunkElems = LAMB_DEFAULT_CHUNK;
 // and run faster with more work per workgroup).
 constexpr int32_t kCoarseFactor = 4;
 
-// Single-pass path: a layer of n elements takes T = ceil(n / kTileElems)
-// tiles; tile i holds the layer's (4 * kBlock)-element blocks i, i + T, ...,
-// i + (kTileGroups - 1) T. One workgroup keeps a tile's x (in LDS) and update
-// direction (in registers, kTileGroups float4 groups per thread) until the
-// layer's step scale is known. The persistent grid keeps kFusedBlocksPerCu workgroups on every CU,
-// so a layer of up to kFusedBlocksPerCu * (compute units) tiles can have
-// every tile resident at once.
+// Single-pass path: with tiles of G float4 groups per thread, a layer of n
+// elements takes T = ceil(n / (G * kBlockElems)) tiles; tile i holds the
+// layer's (4 * kBlock)-element blocks i, i + T, ..., i + (G - 1) T. One
+// workgroup keeps a tile's x (the first kLdsGroups groups in LDS, any others
+// in registers) and update direction (in registers) until the layer's step
+// scale is known. The persistent grid keeps kFusedBlocksPerCu workgroups on
+// every CU, so a layer of up to kFusedBlocksPerCu * (compute units) tiles can
+// have every tile resident at once. A plan uses kTileGroups, or kWideGroups
+// when the wider tile puts more parameters on the single pass.
 #ifndef LAMB_TILE_GROUPS
 #define LAMB_TILE_GROUPS 8
+#endif
+#ifndef LAMB_WIDE_GROUPS
+#define LAMB_WIDE_GROUPS 10
 #endif
 #ifndef LAMB_FUSED_WAVES
 #define LAMB_FUSED_WAVES 4
 #endif
 constexpr int kTileGroups = LAMB_TILE_GROUPS;
+constexpr int kWideGroups = LAMB_WIDE_GROUPS;
+constexpr int kLdsGroups = kTileGroups;
+static_assert(kWideGroups > kTileGroups, "the wide tile is the larger one");
 constexpr int32_t kBlockElems = kBlock * 4;  // one float4 per thread
-constexpr int32_t kTileElems = kBlockElems * kTileGroups;
+constexpr int64_t tile_elems(int groups) { return int64_t(groups) * kBlockElems; }
 constexpr int kFusedWaves = LAMB_FUSED_WAVES;
 constexpr int kFusedBlocksPerCu = kFusedWaves * 4 / kWaves;  // 4 SIMDs per CU
 // Polls before a single-pass wait gives up (about a second); a plan reads an
@@ -197,12 +205,14 @@ constexpr uint64_t kEmptySlot = ~uint64_t(0);
 // raised or not; the last workgroup writes it to `nonfinite_out` (may be
 // null). Every step's last workgroup clears the verdict word of the next
 // epoch.
-hipError_t launch_fused(const StepKind &kind, const TensorDesc *tensors, const ChunkDesc *tiles,
-                        int32_t n_tiles, int32_t grid, uint64_t *slots, uint32_t *ctl,
-                        uint32_t *flags, bool guarded, int32_t *nonfinite_out,
+// `groups` is the plan's tile shape, kTileGroups or kWideGroups.
+hipError_t launch_fused(const StepKind &kind, int groups, const TensorDesc *tensors,
+                        const ChunkDesc *tiles, int32_t n_tiles, int32_t grid, uint64_t *slots,
+                        uint32_t *ctl, uint32_t *flags, bool guarded, int32_t *nonfinite_out,
                         const StepArgs &args, const FinalizeArgs &fargs, double *ratio_out,
                         double *norms_out, hipStream_t stream);
-// Workgroups of the single-pass kernel for `kind` that fit on one CU at once.
-hipError_t fused_blocks_per_cu(const StepKind &kind, int *blocks);
+// Workgroups of the single-pass kernel for `kind` and tile shape `groups`
+// that fit on one CU at once.
+hipError_t fused_blocks_per_cu(const StepKind &kind, int groups, int *blocks);
 
 }  // namespace lamb_mi355x

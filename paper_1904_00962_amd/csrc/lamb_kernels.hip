@@ -622,11 +622,13 @@ __global__ __launch_bounds__(kSegBlock) void finalize_kernel(
 // tile list: workgroup w takes entries w, w + grid, w + 2 grid, ..., so the
 // list falls into rounds of `grid` entries. The host packs every layer's
 // tiles consecutively inside one round (empty entries pad a round's gap).
+// A tile is G = kGroups float4 groups per thread (8 or 10; the plan picks).
 // Tile i of a layer of T tiles holds the layer's 1024-element blocks i,
-// i + T, ..., i + 7T, so the layer's tiles stream one dense stretch of it at
-// a time (contiguous 8192-element tiles, 32 KB apart, streamed 2.3% slower).
-// For each tile a workgroup reads x, g, m, v once, writes the new moments at
-// once, and keeps x in LDS and u in registers. The tile's partial norms go
+// i + T, ..., i + (G - 1) T, so the layer's tiles stream one dense stretch of
+// it at a time (contiguous 8192-element tiles, 32 KB apart, streamed 2.3%
+// slower). For each tile a workgroup reads x, g, m, v once, writes the new
+// moments at once, and keeps x in LDS (a 10-group tile keeps the x of its
+// last two groups in registers) and u in registers. The tile's partial norms go
 // to a slot; the layer's first tile (its leader) waits for every slot of the
 // layer, combines them in tile order, forms the step scale exactly as the
 // finalize kernel does and writes it to each member's broadcast slot; every
@@ -664,7 +666,8 @@ __global__ __launch_bounds__(kSegBlock) void finalize_kernel(
 #define LAMB_FUSED_UNROLL 1
 #endif
 constexpr int kFusedUnroll = LAMB_FUSED_UNROLL;
-static_assert(kTileGroups % kFusedUnroll == 0, "tile groups must be a multiple of the unroll");
+static_assert(kTileGroups % kFusedUnroll == 0 && kWideGroups % kFusedUnroll == 0,
+              "tile groups must be a multiple of the unroll");
 
 __device__ __forceinline__ uint64_t slot_load(const uint64_t *p) {
     return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -704,7 +707,7 @@ __device__ uint64_t slot_wait(const uint64_t *p, uint32_t *ctl, uint32_t limit) 
     }
 }
 
-template <int kAlgo, bool kBf16, int kNorm>
+template <int kAlgo, bool kBf16, int kNorm, int kGroups>
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(kFusedWaves)))
 void fused_kernel(const TensorDesc *__restrict__ tensors, const ChunkDesc *__restrict__ tiles,
                   int32_t n_tiles, uint64_t *__restrict__ slots, uint32_t *__restrict__ ctl,
@@ -716,8 +719,11 @@ void fused_kernel(const TensorDesc *__restrict__ tensors, const ChunkDesc *__res
     __shared__ uint32_t sh_epoch, sh_fault, sh_skip;
     __shared__ float sh_scale;
     __shared__ Partial sh_tile, sh_layer;
-    // The tile's x waits in LDS (32 KB), its update direction in registers.
-    __shared__ f32x4 sh_x[kTileGroups][kBlock];
+    // The tile's x waits in LDS (32 KB for the first kLdsGroups groups) and,
+    // past those, in registers; its update direction waits in registers.
+    constexpr int kInLds = kGroups < kLdsGroups ? kGroups : kLdsGroups;
+    constexpr int kInRegs = kGroups - kInLds;
+    __shared__ f32x4 sh_x[kInLds][kBlock];
     if (threadIdx.x == 0) {
         sh_epoch = ctl_load(ctl + kCtlEpoch);
         sh_fault = ctl_load(ctl + kCtlFault);
@@ -759,10 +765,11 @@ void fused_kernel(const TensorDesc *__restrict__ tensors, const ChunkDesc *__res
         };
 
         // Read once, write the new moments, keep x and u.
-        f32x4 us[kTileGroups];
+        f32x4 us[kGroups];
+        f32x4 x_keep[kInRegs > 0 ? kInRegs : 1];
         double sum_xx = 0.0, sum_uu = 0.0;
 #pragma unroll
-        for (int k0 = 0; k0 < kTileGroups; k0 += kFusedUnroll) {
+        for (int k0 = 0; k0 < kGroups; k0 += kFusedUnroll) {
             f32x4 xr[kFusedUnroll], gr[kFusedUnroll], mr[kFusedUnroll], vr[kFusedUnroll];
             int64_t at[kFusedUnroll];
             int ok[kFusedUnroll];
@@ -814,7 +821,10 @@ void fused_kernel(const TensorDesc *__restrict__ tensors, const ChunkDesc *__res
                         }
                     }
                 }
-                sh_x[k0 + k][threadIdx.x] = xr[k];
+                if (k0 + k < kInLds)
+                    sh_x[k0 + k][threadIdx.x] = xr[k];
+                else
+                    x_keep[k0 + k - kInLds] = xr[k];
                 us[k0 + k] = ur;
             }
         }
@@ -879,12 +889,12 @@ void fused_kernel(const TensorDesc *__restrict__ tensors, const ChunkDesc *__res
         const float s = sh_scale;
         gbf16 *copy = t.x_copy ? (gbf16 *)t.x_copy : nullptr;
 #pragma unroll
-        for (int k = 0; k < kTileGroups; ++k) {
+        for (int k = 0; k < kGroups; ++k) {
             int64_t at;
             int valid;
             group(k, at, valid);
             if (valid > 0) {
-                const f32x4 xo = sh_x[k][threadIdx.x];
+                const f32x4 xo = k < kInLds ? sh_x[k][threadIdx.x] : x_keep[k - kInLds];
                 f32x4 xn;
 #pragma unroll
                 for (int e = 0; e < 4; ++e)
@@ -968,27 +978,39 @@ const void *apply_fn(const StepKind &k) {
                       : reinterpret_cast<const void *>(&apply_kernel<kAlgo, false, false>);
 }
 
-template <int kAlgo, bool kBf16>
+template <int kAlgo, bool kBf16, int kGroups>
 const void *fused_fn(int norm) {
     switch (norm) {
-    case kL1: return reinterpret_cast<const void *>(&fused_kernel<kAlgo, kBf16, kL1>);
-    case kLinf: return reinterpret_cast<const void *>(&fused_kernel<kAlgo, kBf16, kLinf>);
-    default: return reinterpret_cast<const void *>(&fused_kernel<kAlgo, kBf16, kL2>);
+    case kL1: return reinterpret_cast<const void *>(&fused_kernel<kAlgo, kBf16, kL1, kGroups>);
+    case kLinf:
+        return reinterpret_cast<const void *>(&fused_kernel<kAlgo, kBf16, kLinf, kGroups>);
+    default: return reinterpret_cast<const void *>(&fused_kernel<kAlgo, kBf16, kL2, kGroups>);
     }
 }
 
-template <int kAlgo>
+template <int kAlgo, int kGroups>
 const void *fused_fn(const StepKind &k) {
-    return k.bf16_grad ? fused_fn<kAlgo, true>(k.norm) : fused_fn<kAlgo, false>(k.norm);
+    return k.bf16_grad ? fused_fn<kAlgo, true, kGroups>(k.norm)
+                       : fused_fn<kAlgo, false, kGroups>(k.norm);
 }
 
+template <int kGroups>
 const void *fused_fn(const StepKind &k) {
     switch (k.algo) {
-    case kNLamb: return fused_fn<kNLamb>(k);
-    case kNNLamb: return fused_fn<kNNLamb>(k);
-    case kLars: return fused_fn<kLars>(k);
-    default: return fused_fn<kLamb>(k);
+    case kNLamb: return fused_fn<kNLamb, kGroups>(k);
+    case kNNLamb: return fused_fn<kNNLamb, kGroups>(k);
+    case kLars: return fused_fn<kLars, kGroups>(k);
+    default: return fused_fn<kLamb, kGroups>(k);
     }
+}
+
+// Null for a tile shape other than the two a plan may pick.
+const void *fused_fn(const StepKind &k, int groups) {
+    if (groups == kTileGroups)
+        return fused_fn<kTileGroups>(k);
+    if (groups == kWideGroups)
+        return fused_fn<kWideGroups>(k);
+    return nullptr;
 }
 
 }  // namespace
@@ -1051,21 +1073,27 @@ hipError_t launch_finalize(NormKind norm, const TensorDesc *tensors, int32_t n_t
     return hipLaunchKernel(fn, dim3(n_tensors), dim3(kSegBlock), params, 0, stream);
 }
 
-hipError_t launch_fused(const StepKind &kind, const TensorDesc *tensors, const ChunkDesc *tiles,
-                        int32_t n_tiles, int32_t grid, uint64_t *slots, uint32_t *ctl,
-                        uint32_t *flags, bool guarded, int32_t *nonfinite_out,
+hipError_t launch_fused(const StepKind &kind, int groups, const TensorDesc *tensors,
+                        const ChunkDesc *tiles, int32_t n_tiles, int32_t grid, uint64_t *slots,
+                        uint32_t *ctl, uint32_t *flags, bool guarded, int32_t *nonfinite_out,
                         const StepArgs &args, const FinalizeArgs &fargs, double *ratio_out,
                         double *norms_out, hipStream_t stream) {
+    const void *fn = fused_fn(kind, groups);
+    if (!fn)
+        return hipErrorInvalidValue;
     StepArgs a = args;
     FinalizeArgs f = fargs;
     int32_t guard = guarded ? 1 : 0;
     void *params[] = {&tensors, &tiles, &n_tiles, &slots, &ctl, &flags, &guard, &nonfinite_out,
                       &a, &f, &ratio_out, &norms_out};
-    return hipLaunchKernel(fused_fn(kind), dim3(grid), dim3(kBlock), params, 0, stream);
+    return hipLaunchKernel(fn, dim3(grid), dim3(kBlock), params, 0, stream);
 }
 
-hipError_t fused_blocks_per_cu(const StepKind &kind, int *blocks) {
-    return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, fused_fn(kind), kBlock, 0);
+hipError_t fused_blocks_per_cu(const StepKind &kind, int groups, int *blocks) {
+    const void *fn = fused_fn(kind, groups);
+    if (!fn)
+        return hipErrorInvalidValue;
+    return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, fn, kBlock, 0);
 }
 
 hipError_t launch_finite(bool bf16_grad, const TensorDesc *tensors, const ChunkDesc *chunks,

@@ -62,17 +62,19 @@ static void chunk_table(void) {
 }
 
 /*
- * Three layers of 3, 1 and 2 tiles with rounds of at most 4 entries: two
- * rounds are needed, and the narrowest width that still packs into two is 3:
- * [layer 0 x3][layer 2 x2, layer 1 x1]. Every element of every layer is held
- * by exactly one entry.
+ * Three layers of 3, 1 and 2 tiles of 8192 elements with rounds of at most 4
+ * entries (the wide tile puts no more of them on the single pass, so a plan
+ * keeps the narrow one): two rounds are needed, and the narrowest width that
+ * still packs into two is 3: [layer 0 x3][layer 2 x2, layer 1 x1]. Every
+ * element of every layer is held by exactly one entry.
  */
 static void tile_schedule(void) {
     const int64_t numel[3] = {3 * 8192 - 100, 8192, 2 * 8192};
-    int32_t et[8], el[8], first[3], tiles[3], n = -1, round = -1, i, k;
+    int32_t et[8], el[8], first[3], tiles[3], n = -1, round = -1, groups = -1, i, k;
     int64_t es[8], covered[3] = {0, 0, 0};
-    CHECK(lamb_tile_schedule(numel, 3, 4, 8, et, es, el, first, tiles, &n, &round) == LAMB_OK);
-    CHECK(n == 6 && round == 3);
+    CHECK(lamb_tile_schedule(numel, 3, 4, 0, 8, et, es, el, first, tiles, &n, &round,
+                             &groups) == LAMB_OK);
+    CHECK(groups == 8 && n == 6 && round == 3);
     CHECK(tiles[0] == 3 && tiles[1] == 1 && tiles[2] == 2);
     CHECK(first[0] == 0 && first[2] == 3 && first[1] == 5);
     for (k = 0; k < n; ++k) {
@@ -87,12 +89,18 @@ static void tile_schedule(void) {
     }
     for (i = 0; i < 3; ++i)
         CHECK(covered[i] == numel[i]);
-    /* a layer too large for one round takes the two-pass kernels */
+    /* five 8192-element tiles are too many for a round of 4, four of 10240
+     * are not: a plan picks the wide tile for this layer */
     {
         const int64_t big[1] = {5 * 8192};
-        CHECK(lamb_tile_schedule(big, 1, 4, 8, et, es, el, first, tiles, &n, &round) ==
-              LAMB_OK);
+        CHECK(lamb_tile_schedule(big, 1, 4, 8, 8, et, es, el, first, tiles, &n, &round,
+                                 NULL) == LAMB_OK);
         CHECK(tiles[0] == 0 && n == 0);
+        CHECK(lamb_tile_schedule(big, 1, 4, 0, 8, et, es, el, first, tiles, &n, &round,
+                                 &groups) == LAMB_OK);
+        CHECK(groups == 10 && tiles[0] == 4 && n == 4 && el[3] == 10 * 1024);
+        CHECK(lamb_tile_schedule(big, 1, 4, 9, 8, et, es, el, first, tiles, &n, &round,
+                                 NULL) == LAMB_EINVAL);
     }
 }
 

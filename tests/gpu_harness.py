@@ -13,6 +13,7 @@ exactly 0 wherever the oracle reports 0.
 from __future__ import annotations
 
 import dataclasses
+import os
 from typing import Callable, List, Optional, Sequence
 
 import numpy as np
@@ -103,6 +104,32 @@ def compare_ratios(gpu: np.ndarray, ref: np.ndarray, what: str, tol: float = RAT
     return 0.0
 
 
+# Environment variable a plan reads for its single-pass tile shape (8 or 10).
+TILE_ENV = "LAMB_MI355X_TILE_GROUPS"
+
+
+def create_plan(rows, g_dtype: int, algo: int, chunk_elems: int, path: str) -> "_lib.Plan":
+    """A plan on ``path``: "auto", "two-pass", or "wide", the single pass with
+    10-group tiles, forced through the environment override so that small
+    layers exercise that kernel."""
+    wide = path == "wide"
+    saved = os.environ.get(TILE_ENV)
+    if wide:
+        os.environ[TILE_ENV] = "10"
+    try:
+        plan = _lib.lamb_plan_create(rows, g_dtype, algo, chunk_elems)
+    finally:
+        if wide:
+            if saved is None:
+                del os.environ[TILE_ENV]
+            else:
+                os.environ[TILE_ENV] = saved
+    _lib.lamb_plan_set_path(plan, "auto" if wide else path)
+    if wide:
+        assert _lib.lamb_plan_tiles(plan)[2] == 10
+    return plan
+
+
 class Pair:
     """Device state + plan for the HIP path, and host state for the oracle."""
 
@@ -131,8 +158,7 @@ class Pair:
                  int(self.wd[i])) for i in range(self.n)]
         kind = _lib.LAMB_GRAD_BF16 if g_dtype == "bf16" else _lib.LAMB_GRAD_F32
         algo_id = _lib.LAMB_ALGO_LARS if algo == "lars" else _lib.LAMB_ALGO_LAMB
-        self.plan = _lib.lamb_plan_create(rows, kind, algo_id, chunk_elems)
-        _lib.lamb_plan_set_path(self.plan, path)
+        self.plan = create_plan(rows, kind, algo_id, chunk_elems, path)
         self.path = path
         self.oracle = oracle.load()
 
@@ -278,9 +304,9 @@ def run_config(cfg: int, steps: int, algo: str = "lamb", chunk_elems: int = 0,
         % (cfg, ps.name, algo, steps, chunk_elems, path))
     pair = Pair(paramsets.draw_params(ps, device=device), ps.wd_mask(), ps.g_dtype, algo,
                 chunk_elems, oracle_subset, path)
-    per, total = _lib.lamb_plan_tiles(pair.plan)
-    log("  single-pass layers %d of %d, %d tiles"
-        % (sum(1 for k in per if k), len(per), total))
+    per, total, groups = _lib.lamb_plan_tiles(pair.plan)
+    log("  single-pass layers %d of %d, %d tiles of %d groups"
+        % (sum(1 for k in per if k), len(per), total, groups))
     rep = Report()
     hp = {"lamb": lamb_hp, "lars": lars_hp, "nlamb": nlamb_hp, "nnlamb": nlamb_hp}[algo](ps)
     try:

@@ -29,7 +29,7 @@ def _gs(rng, sizes, g_dtype="f32", scale=1e-3):
     return out
 
 
-PATHS = ["auto", "two-pass"]
+PATHS = ["auto", "wide", "two-pass"]
 
 
 def _run(xs, wd, g_dtype, algo, chunk, steps, hp, rng, grads=None, bias_correction=True,
@@ -58,19 +58,21 @@ NLAMB = dict(DEFAULT, beta1=0.975, eps=1e-8)
                                           ("lars", "bf16"), ("nlamb", "bf16"),
                                           ("nnlamb", "f32")])
 @pytest.mark.parametrize("chunk,path", [(8, "two-pass"), (64, "two-pass"), (1024, "two-pass"),
-                                        (0, "two-pass"), (0, "auto")])
+                                        (0, "two-pass"), (0, "auto"), (0, "wide")])
 def test_ragged_sizes(algo, g_dtype, chunk, path):
     """Every tensor length around the 4-element group, the 256-thread tile,
     the unrolled loop trip and the chunk boundary; on the single pass, around
-    the 8192-element tile and its multiples (layers of several tiles)."""
+    the 8192- and 10240-element tiles and their multiples (layers of several
+    tiles)."""
     rng = np.random.default_rng(1000 + chunk)
     sizes = list(RAGGED)
     if chunk:
         sizes += [chunk - 1, chunk, chunk + 1, 4 * chunk + 5]
     else:
         sizes += [32767, 32768, 32769, 4 * 32768 + 5]
-    if path == "auto":
+    if path in ("auto", "wide"):
         sizes += [8191, 8192, 8193, 2 * 8192 - 3, 3 * 8192, 5 * 8192 + 7]
+        sizes += [10239, 10240, 10241, 3 * 10240 + 11]
     xs = _xs(rng, sizes)
     wd = [i % 3 != 0 for i in range(len(sizes))]
     hp = {"lamb": DEFAULT, "lars": LARS, "nlamb": NLAMB, "nnlamb": NLAMB}[algo]
@@ -190,8 +192,7 @@ def test_guard_bands_untouched(path):
             mask[start:start + v.numel()] = False
     rows = [(views["x"][i].data_ptr(), views["g"][i].data_ptr(), views["m"][i].data_ptr(),
              views["v"][i].data_ptr(), sizes[i], 1) for i in range(len(sizes))]
-    with _lib.lamb_plan_create(rows, _lib.LAMB_GRAD_F32, _lib.LAMB_ALGO_LAMB, 8) as plan:
-        _lib.lamb_plan_set_path(plan, path)
+    with H.create_plan(rows, _lib.LAMB_GRAD_F32, _lib.LAMB_ALGO_LAMB, 8, path) as plan:
         for t in range(1, 4):
             _lib.lamb_step(plan, 0.01, 0.9, 0.999, 1e-6, 0.01, 0.0, 10.0, t, True,
                            torch.cuda.current_stream().cuda_stream)
@@ -312,24 +313,30 @@ def test_subnormal_and_zero_gradients():
              ratio_tol=tol)
 
 
-def test_single_pass_layout_and_rounds():
+@pytest.mark.parametrize("groups", [8, 10])
+def test_single_pass_layout_and_rounds(groups):
     """The single pass runs in rounds of one workgroup per tile, four per CU.
-    A layer of exactly one round of 8192-element tiles takes it, a layer of
-    one element more takes the two-pass kernels; layers that leave a gap in
-    a round (padded with empty entries) and a layer that fills the last
-    round still match the oracle on every element."""
+    A layer of exactly one round of tiles takes it, a layer of one element
+    more than a round of the wider tile takes the two-pass kernels; layers
+    that leave a gap in a round (padded with empty entries) and a layer that
+    fills the last round still match the oracle on every element. With a
+    layer that only the 10240-element tile fits in a round, the plan picks
+    that tile; without one it keeps the 8192-element tile."""
     torch = H.torch_cuda()
     cus = torch.cuda.get_device_properties(0).multi_processor_count
-    R, T = 4 * cus, 8192
-    sizes = [R * T, R * T + 1, int(0.68 * R) * T - 3, int(0.39 * R) * T + 5, int(0.29 * R) * T,
+    R, T, W = 4 * cus, 1024 * groups, 10240
+    sizes = [R * T, R * W + 1, int(0.68 * R) * T - 3, int(0.39 * R) * T + 5, int(0.29 * R) * T,
              30 * T - 1, 100, 7]
+    if groups == 10:
+        sizes.append(R * 8192 + 1)  # fits a round of the wide tile only
     rng = np.random.default_rng(21)
     xs = _xs(rng, sizes)
     wd = [i % 2 == 0 for i in range(len(sizes))]
-    H.log("single-pass rounds: R=%d sizes=%s" % (R, sizes))
+    H.log("single-pass rounds: R=%d groups=%d sizes=%s" % (R, groups, sizes))
     pair = H.Pair(xs, wd, "bf16", "lamb", path="auto")
     try:
-        per, total = _lib.lamb_plan_tiles(pair.plan)
+        per, total, got = _lib.lamb_plan_tiles(pair.plan)
+        assert got == groups
         want = [(n + T - 1) // T for n in sizes]
         want[1] = 0
         assert per == want
@@ -338,7 +345,7 @@ def test_single_pass_layout_and_rounds():
             gs = _gs(rng, sizes, "bf16")
             hg = pair.set_grads(gs)
             ref = H.step_both(pair, "lamb", hg, DEFAULT, t)
-            pair.compare(ref, "rounds step %d" % t)
+            pair.compare(ref, "rounds groups %d step %d" % (groups, t))
     finally:
         pair.close()
 

@@ -45,7 +45,8 @@ def test_other_norms(algo, norm):
     rwd = [i % 2 == 0 for i in range(len(ragged))]
     for xs, wd, g_dtype, chunk, path in ((paramsets.draw_params(ps), ps.wd_mask(), "f32", 0, "auto"),
                                          (ragged, rwd, "bf16", 64, "two-pass"),
-                                         (ragged, rwd, "bf16", 0, "auto")):
+                                         (ragged, rwd, "bf16", 0, "auto"),
+                                         (ragged, rwd, "f32", 0, "wide")):
         H.log("norm=%s algo=%s tensors=%d chunk=%d path=%s" % (norm, algo, len(xs), chunk, path))
         pair = _pair(xs, wd, g_dtype, algo, chunk, path)
         try:
@@ -106,7 +107,7 @@ def test_deferred_mode_equals_direct_mode(algo):
     assert torch.equal(r0, r1)
 
 
-@pytest.mark.parametrize("path", ["auto", "two-pass"])
+@pytest.mark.parametrize("path", ["auto", "wide", "two-pass"])
 @pytest.mark.parametrize("algo", ALGOS)
 @pytest.mark.parametrize("g_dtype", ["f32", "bf16"])
 def test_skip_nonfinite_sequence(algo, g_dtype, path):
@@ -152,18 +153,20 @@ def test_skip_nonfinite_sequence(algo, g_dtype, path):
         pair.close()
 
 
-def test_skip_nonfinite_with_two_pass_layer():
-    """The single-pass skip mode with a layer too large for the single pass:
-    the check's verdict also stops that layer's moment and apply passes."""
+@pytest.mark.parametrize("path", ["auto", "wide"])
+def test_skip_nonfinite_with_two_pass_layer(path):
+    """The single-pass skip mode with a layer too large for the single pass
+    (with either tile): the check's verdict also stops that layer's moment
+    and apply passes."""
     torch = H.torch_cuda()
     cus = torch.cuda.get_device_properties(0).multi_processor_count
-    big = 4 * cus * 8192 + 1029
+    big = 4 * cus * 10240 + 1029
     rng = np.random.default_rng(19)
     xs = [(rng.standard_normal(n) * 0.2).astype(np.float32) for n in (big, 3000, 7)]
-    pair = _pair(xs, [True, True, False], "bf16", "lamb", path="auto")
+    pair = _pair(xs, [True, True, False], "bf16", "lamb", path=path)
     flag = torch.full((1,), -1, dtype=torch.int32, device="cuda")
     try:
-        per, _ = _lib.lamb_plan_tiles(pair.plan)
+        per, _, _ = _lib.lamb_plan_tiles(pair.plan)
         assert per[0] == 0 and per[1] > 0 and per[2] > 0
         for t, kind in enumerate(["ok", "nan_big", "ok", "inf_small", "ok"], start=1):
             gs = _grads(rng, pair.X, "bf16")
@@ -259,7 +262,8 @@ def _bf16_bits(t):
 
 @pytest.mark.parametrize("algo,skip,g_dtype,path", [
     ("lamb", 0, "bf16", "auto"), ("lamb", 0, "bf16", "two-pass"), ("nn-lamb", 0, "f32", "auto"),
-    ("lars", 0, "f32", "auto"), ("lars", 1, "bf16", "auto"), ("lamb", 1, "f32", "auto")])
+    ("lars", 0, "f32", "auto"), ("lars", 1, "bf16", "auto"), ("lamb", 1, "f32", "auto"),
+    ("lamb", 0, "bf16", "wide"), ("lars", 1, "f32", "wide")])
 def test_bf16_copies(algo, skip, g_dtype, path):
     """The apply pass writes bf16(x_{t+1}): bit for bit torch's cast of the
     GPU's own x, within one bf16 ulp of the oracle's rounding of the oracle's
@@ -290,7 +294,7 @@ def test_bf16_copies(algo, skip, g_dtype, path):
         pair.close()
 
 
-@pytest.mark.parametrize("path", ["auto", "two-pass"])
+@pytest.mark.parametrize("path", ["auto", "wide", "two-pass"])
 def test_bf16_copy_guard_bands_and_detach(path):
     torch = H.torch_cuda()
     rng = np.random.default_rng(12)

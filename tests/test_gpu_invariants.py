@@ -33,7 +33,7 @@ def _steps(cfg, algo, chunk, steps, device="cuda", subset=None, path="auto"):
     return pair
 
 
-@pytest.mark.parametrize("path", ["auto", "two-pass"])
+@pytest.mark.parametrize("path", ["auto", "wide", "two-pass"])
 @pytest.mark.parametrize("cfg,algo", [(2, "lamb"), (3, "lars")])
 def test_bitwise_deterministic(cfg, algo, path):
     torch = H.torch_cuda()
@@ -49,9 +49,10 @@ def test_bitwise_deterministic(cfg, algo, path):
 def test_chunk_size_invariance():
     """m and v are elementwise, so they do not depend on the chunking or on
     the path at all; x and the ratios agree to rounding of the reduction
-    order. The first run is the single pass."""
+    order. The first runs are the single pass with either tile."""
     torch = H.torch_cuda()
     runs = [_state(_steps(1, "lamb", 0, 2))]
+    runs += [_state(_steps(1, "lamb", 0, 2, path="wide"))]
     runs += [_state(_steps(1, "lamb", c, 2, path="two-pass")) for c in (0, 4096, 65536)]
     n = paramsets.get(1).n_tensors
     for other in runs[1:]:
@@ -62,7 +63,7 @@ def test_chunk_size_invariance():
         H.compare_ratios(other[-1].cpu().numpy(), runs[0][-1].cpu().numpy(), "ratio")
 
 
-@pytest.mark.parametrize("path,chunk", [("two-pass", 1024), ("auto", 0)])
+@pytest.mark.parametrize("path,chunk", [("two-pass", 1024), ("auto", 0), ("wide", 0)])
 def test_layer_independence(path, chunk):
     """A step on {A, B} equals a step on {A} and a step on {B}, bit for bit
     (on the single pass, wherever the packing puts each layer)."""
@@ -223,7 +224,8 @@ def test_independent_plans_on_concurrent_streams():
         assert all(torch.equal(u, w) for u, w in zip(a, b))
 
 
-@pytest.mark.parametrize("path,skip", [("auto", 0), ("two-pass", 0), ("two-pass", 1), ("auto", 1)])
+@pytest.mark.parametrize("path,skip", [("auto", 0), ("two-pass", 0), ("two-pass", 1), ("auto", 1),
+                                       ("wide", 0), ("wide", 1)])
 def test_graph_capture_replays_match_eager(path, skip):
     """A captured step (fixed scalars, gradients read from the same buffers)
     replayed three times, with eager work between replays, equals three eager

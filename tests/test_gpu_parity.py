@@ -11,7 +11,7 @@ import numpy as np
 import pytest
 
 import gpu_harness as H
-from paper_1904_00962_amd import paramsets
+from paper_1904_00962_amd import _lib, paramsets
 
 pytestmark = pytest.mark.gpu
 
@@ -24,6 +24,12 @@ def test_tiny_lamb_ten_steps(chunk):
 
 def test_tiny_lars_ten_steps():
     H.run_config(0, 10, "lars", chunk_elems=512)
+
+
+@pytest.mark.parametrize("algo", ["lamb", "lars", "nlamb", "nnlamb"])
+def test_tiny_wide_tiles(algo):
+    """The single pass with 10240-element tiles (forced on the tiny set)."""
+    H.run_config(0, 6, algo, path="wide")
 
 
 def test_bert_base_lamb():
@@ -66,7 +72,9 @@ def test_bert_large_lars_bf16_grad():
 def test_gpt_1p5b_lamb_sampled():
     """1.56e9 parameters: one step; whole-tensor parity on a sample (the 80M
     token embedding, the first layer, the final norm), and on every tensor
-    the Section 3 identity ||x_{t+1} - x_t|| = eta * phi(||x_t||)."""
+    the Section 3 identity ||x_{t+1} - x_t|| = eta * phi(||x_t||). The plan
+    takes 10240-element tiles, which put the 10.24M-element FFN layers on
+    the single pass."""
     torch = H.torch_cuda()
     ps = paramsets.get(4)
     sample = [0, 1, 2, 3, 4, 5, 6, 7, 8, 9, 10, 11, 12, 13, ps.n_tensors - 2, ps.n_tensors - 1]
@@ -74,6 +82,9 @@ def test_gpt_1p5b_lamb_sampled():
     pair = H.Pair(paramsets.draw_params(ps, device="cuda"), ps.wd_mask(), ps.g_dtype, "lamb",
                   oracle_subset=sample)
     try:
+        per, _, groups = _lib.lamb_plan_tiles(pair.plan)
+        assert groups == 10
+        assert [i for i, k in enumerate(per) if k == 0] == [0]  # the token embedding only
         hp = H.lamb_hp(ps)
         x_old = [x.clone() for x in pair.X]
         hg = pair.set_grads(paramsets.draw_grads(ps, 1, device="cuda"))

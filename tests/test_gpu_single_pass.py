@@ -30,11 +30,13 @@ def _run_path(cfg, path, steps=2):
     return state
 
 
-def test_single_pass_agrees_with_two_pass():
-    """BERT-Base: 198 layers on the single pass, the token embedding on the
-    two-pass kernels, against the two-pass path for everything."""
+@pytest.mark.parametrize("path", ["auto", "wide"])
+def test_single_pass_agrees_with_two_pass(path):
+    """BERT-Base: 198 layers on the single pass (with either tile), the token
+    embedding on the two-pass kernels, against the two-pass path for
+    everything."""
     torch = H.torch_cuda()
-    x1, m1, v1, r1, n1 = _run_path(1, "auto")
+    x1, m1, v1, r1, n1 = _run_path(1, path)
     x2, m2, v2, r2, n2 = _run_path(1, "two-pass")
     assert all(torch.equal(a, b) for a, b in zip(m1 + v1, m2 + v2))
     for k, (a, b) in enumerate(zip(x1, x2)):

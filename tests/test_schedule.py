@@ -1,6 +1,8 @@
 """The single-pass schedule (lamb_tile_schedule, host only): every layer's
 tiles cover it exactly, sit consecutively inside one round, and a simulation
-of the persistent grid's waits always runs to the end."""
+of the persistent grid's waits always runs to the end. A plan's tile shape is
+the wide one (10 groups of 1024 elements) exactly when that puts more
+parameters on the single pass than the narrow one (8 groups)."""
 
 import numpy as np
 import pytest
@@ -9,10 +11,22 @@ from paper_1904_00962_amd import _lib, paramsets
 
 TILE = 8192
 BLOCK = 1024
+NARROW, WIDE = 8, 10
 
 
-def _check_layout(numel, max_round):
-    et, es, el, first, tiles, round_ = _lib.lamb_tile_schedule(numel, max_round)
+def _single_pass_params(numel, max_round, groups):
+    return sum(n for n in numel if -(-n // (groups * BLOCK)) <= max_round)
+
+
+def _check_layout(numel, max_round, tile_groups=0):
+    et, es, el, first, tiles, round_, groups = _lib.lamb_tile_schedule(numel, max_round,
+                                                                      tile_groups)
+    if tile_groups:
+        assert groups == tile_groups
+    else:
+        wide = _single_pass_params(numel, max_round, WIDE)
+        assert groups == (WIDE if wide > _single_pass_params(numel, max_round, NARROW) else NARROW)
+    tile = groups * BLOCK
     n = len(et)
     assert 1 <= round_ <= max_round
     n_rounds = -(-n // round_)
@@ -23,7 +37,7 @@ def _check_layout(numel, max_round):
     assert all(k <= round_ for k in tiles)
     seen = [False] * n
     for i, size in enumerate(numel):
-        nt = -(-size // TILE)
+        nt = -(-size // tile)
         if nt > max_round:
             assert tiles[i] == 0, "layer %d of %d tiles must take the two-pass path" % (i, nt)
             continue
@@ -35,8 +49,8 @@ def _check_layout(numel, max_round):
             j = f + k
             assert not seen[j]
             seen[j] = True
-            # tile k holds the 1024-element blocks k, k + nt, ..., k + 7 nt
-            held = sum(max(0, min(BLOCK, size - b * BLOCK)) for b in range(k, 8 * nt, nt))
+            # tile k holds the 1024-element blocks k, k + nt, ..., k + (groups - 1) nt
+            held = sum(max(0, min(BLOCK, size - b * BLOCK)) for b in range(k, groups * nt, nt))
             assert et[j] == i and es[j] == k * BLOCK and el[j] == held > 0
             covered += held
         assert covered == size
@@ -45,7 +59,7 @@ def _check_layout(numel, max_round):
             assert et[j] == -1 and el[j] == 0
             assert j // round_ < (n - 1) // round_
             assert all(not seen[k] for k in range(j, (j // round_ + 1) * round_))
-    return et, first, tiles, round_
+    return et, first, tiles, round_, groups
 
 
 def _simulate(et, first, tiles, round_):
@@ -90,7 +104,7 @@ def _simulate(et, first, tiles, round_):
 def test_paramset_schedules(cfg):
     ps = paramsets.get(cfg)
     numel = [t.numel for t in ps.tensors]
-    et, first, tiles, round_ = _check_layout(numel, 1024)
+    et, first, tiles, round_, _ = _check_layout(numel, 1024)
     _simulate(et, first, tiles, round_)
 
 
@@ -100,8 +114,8 @@ def test_bert_large_layout():
     fill a round, so no narrower round would do."""
     ps = paramsets.get(2)
     numel = [t.numel for t in ps.tensors]
-    et, first, tiles, round_ = _check_layout(numel, 1024)
-    assert sum(1 for k in tiles if k == 0) == 1
+    et, first, tiles, round_, groups = _check_layout(numel, 1024)
+    assert groups == NARROW and sum(1 for k in tiles if k == 0) == 1
     assert round_ == 1024 and -(-len(et) // round_) == 37 and -1 not in et
 
 
@@ -110,32 +124,57 @@ def test_resnet50_rounds_are_balanced():
     equal rounds instead of three full ones and a short one."""
     ps = paramsets.get(3)
     numel = [t.numel for t in ps.tensors]
-    et, first, tiles, round_ = _check_layout(numel, 1024)
-    assert -(-len(et) // round_) == 4 and sum(tiles) == 3223
+    et, first, tiles, round_, groups = _check_layout(numel, 1024)
+    assert groups == NARROW and -(-len(et) // round_) == 4 and sum(tiles) == 3223
     assert round_ < 900
 
 
+def test_gpt_1p5b_takes_wide_tiles():
+    """The 1.5B set's 10.24M-element FFN layers need 1250 narrow tiles but
+    only 1000 wide ones: with wide tiles they join the single pass, and only
+    the token embedding stays on the two-pass kernels."""
+    ps = paramsets.get(4)
+    numel = [t.numel for t in ps.tensors]
+    et, first, tiles, round_, groups = _check_layout(numel, 1024)
+    assert groups == WIDE
+    two_pass = [n for n, k in zip(numel, tiles) if k == 0]
+    assert two_pass == [max(numel)] and max(numel) > WIDE * BLOCK * 1024
+    ffn = [k for n, k in zip(numel, tiles) if n == 1600 * 6400]
+    assert ffn and all(k == 1000 for k in ffn)
+    _, _, narrow_tiles, _, _ = _check_layout(numel, 1024, NARROW)
+    assert all(k == 0 for n, k in zip(numel, narrow_tiles) if n == 1600 * 6400)
+
+
+@pytest.mark.parametrize("tile_groups", [0, NARROW, WIDE])
 @pytest.mark.parametrize("seed", range(12))
-def test_random_layers_small_rounds(seed):
+def test_random_layers_small_rounds(seed, tile_groups):
     rng = np.random.default_rng(seed)
     round_ = int(rng.integers(1, 40))
     n = int(rng.integers(1, 60))
     numel = [int(v) for v in rng.integers(1, TILE * (round_ + 3), size=n)]
-    numel += [TILE * round_, TILE * round_ + 1, 1, TILE]
-    et, first, tiles, width = _check_layout(numel, round_)
+    numel += [TILE * round_, TILE * round_ + 1, 1, TILE, WIDE * BLOCK * round_ + 1]
+    et, first, tiles, width, _ = _check_layout(numel, round_, tile_groups)
     if et:
         _simulate(et, first, tiles, width)
 
 
 def test_round_boundary_and_errors():
-    et, es, el, first, tiles, width = _lib.lamb_tile_schedule([TILE * 4, TILE * 4 + 1, 5], 4)
+    sizes = [TILE * 4, TILE * 4 + 1, 5]
+    et, es, el, first, tiles, width, groups = _lib.lamb_tile_schedule(sizes, 4, NARROW)
     assert tiles == [4, 0, 1] and first == [0, 0, 4] and len(et) == 5 and width == 4
+    # the wide tile takes the second layer too (4 tiles of 10240), so a plan
+    # picks it: rounds {4}, {4}, {1}
+    et, es, el, first, tiles, width, groups = _lib.lamb_tile_schedule(sizes, 4)
+    assert groups == WIDE and tiles == [4, 4, 1] and width == 4 and len(et) == 9
     # three layers of 3, 3 and 2 tiles fill two rounds of 6 as {3, 3}, {2}; the
     # narrowest width that still needs two rounds is 5: {3, 2}, {3}
-    et, es, el, first, tiles, width = _lib.lamb_tile_schedule([3 * TILE, 3 * TILE, 2 * TILE], 6)
-    assert width == 5 and tiles == [3, 3, 2] and len(et) == 8
+    et, es, el, first, tiles, width, groups = _lib.lamb_tile_schedule(
+        [3 * TILE, 3 * TILE, 2 * TILE], 6)
+    assert groups == NARROW and width == 5 and tiles == [3, 3, 2] and len(et) == 8
     assert et == [0, 0, 0, 2, 2, 1, 1, 1]
     with pytest.raises(_lib.LambError):
         _lib.lamb_tile_schedule([TILE], 0)
     with pytest.raises(_lib.LambError):
         _lib.lamb_tile_schedule([0], 4)
+    with pytest.raises(_lib.LambError):
+        _lib.lamb_tile_schedule([TILE], 4, 9)
