@@ -658,15 +658,20 @@ __global__ __launch_bounds__(kSegBlock) void finalize_kernel(
 #ifndef LAMB_MEMBER_SLEEP
 #define LAMB_MEMBER_SLEEP LAMB_SPIN_SLEEP
 #endif
-// LAMB_FUSED_UNROLL: float4 groups each thread of the single pass loads per
-// trip. One beats two there (about half a percent on BERT-Large): it leaves
-// more registers free, and a round's many resident tiles already keep enough
-// loads in flight.
+// LAMB_FUSED_UNROLL / LAMB_FUSED_UNROLL_LARS: float4 groups each thread of
+// the single pass loads per trip, for the LAMB family (four streams) and for
+// LARS (three). For LAMB one beats two (0.3-1% on BERT and ResNet-50): a
+// round's resident tiles already keep enough loads in flight. LARS, with
+// no v to stream, needs two (3-5% faster).
 #ifndef LAMB_FUSED_UNROLL
 #define LAMB_FUSED_UNROLL 1
 #endif
-constexpr int kFusedUnroll = LAMB_FUSED_UNROLL;
-static_assert(kTileGroups % kFusedUnroll == 0 && kWideGroups % kFusedUnroll == 0,
+#ifndef LAMB_FUSED_UNROLL_LARS
+#define LAMB_FUSED_UNROLL_LARS 2
+#endif
+static_assert(kTileGroups % LAMB_FUSED_UNROLL == 0 && kWideGroups % LAMB_FUSED_UNROLL == 0 &&
+                  kTileGroups % LAMB_FUSED_UNROLL_LARS == 0 &&
+                  kWideGroups % LAMB_FUSED_UNROLL_LARS == 0,
               "tile groups must be a multiple of the unroll");
 
 __device__ __forceinline__ uint64_t slot_load(const uint64_t *p) {
@@ -716,6 +721,7 @@ void fused_kernel(const TensorDesc *__restrict__ tensors, const ChunkDesc *__res
                   StepArgs a, FinalizeArgs f, double *__restrict__ ratio_out,
                   double *__restrict__ norms_out) {
     constexpr bool kV = kHasSecondMoment<kAlgo>;
+    constexpr int kFusedUnroll = kV ? LAMB_FUSED_UNROLL : LAMB_FUSED_UNROLL_LARS;
     __shared__ uint32_t sh_epoch, sh_fault, sh_skip;
     __shared__ float sh_scale;
     __shared__ Partial sh_tile, sh_layer;
