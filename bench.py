@@ -4,7 +4,10 @@ Default workload: the BERT-Large-shaped parameter set (391 tensors,
 335,141,888 fp32 parameters, bf16 gradients), LAMB with the paper's
 hyperparameters. Inputs are synthetic, seeded, drawn on the GPU and resident
 in HBM before timing starts. Prints ONE JSON line on stdout; diagnostics go
-to stderr.
+to stderr. Besides the contract's fields the line holds the per-kernel times,
+the dominant kernel's roofline, the CPU oracle's rate on a bounded sample,
+the latency of single steps timed one by one after the timed region (median,
+min, max) and the GPU, runtime and host it ran on.
 
   python bench.py [--steps K] [--warmup W] [--config 2] [--algo lamb|lars]
                   [--path auto|two-pass] [--chunk ELEMS]
@@ -32,6 +35,7 @@ HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, published
 PROFILES = os.path.join(ROOT, "profiles")
 NLAMB_BETA1, NLAMB_EPS = 0.975, 1e-8  # N-LAMB / NN-LAMB settings (Appendix D)
 TIMING_EVERY = 4  # kernel-level events on one timed step in four
+LATENCY_STEPS = 50  # steps timed one by one after the timed region
 
 
 def eprint(*a):
@@ -179,6 +183,44 @@ def stream_probe_all() -> None:
     # the single pass's own layout: 1024-element blocks dealt over layers of 512 tiles
     out["single_pass_dealt_GBps"] = stream_rate("single_pass", 335141888, True, 8192, 512)
     print(json.dumps(out), flush=True)
+
+
+def step_latencies(opt, n: int) -> dict:
+    """Latency of single steps: an event pair on the step's stream around
+    each of ``n`` more steps, after the timed region (the events add a little
+    to each step, so the timed region keeps the throughput figure)."""
+    import torch
+    stream = torch.cuda.current_stream()
+    pairs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+             for _ in range(n)]
+    torch.cuda.synchronize()
+    for a, b in pairs:
+        a.record(stream)
+        opt.step()
+        b.record(stream)
+    torch.cuda.synchronize()
+    ms = sorted(a.elapsed_time(b) for a, b in pairs)
+    mid = len(ms) // 2
+    median = ms[mid] if len(ms) % 2 else 0.5 * (ms[mid - 1] + ms[mid])
+    return {"median_ms": median, "min_ms": ms[0], "max_ms": ms[-1], "steps": n}
+
+
+def environment() -> dict:
+    """The GPU, runtime and host the line was measured on."""
+    import torch
+    props = torch.cuda.get_device_properties(0)
+    host = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for ln in f:
+                if ln.startswith("model name"):
+                    host = ln.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"gpu": props.name, "arch": getattr(props, "gcnArchName", ""),
+            "compute_units": props.multi_processor_count, "hip": torch.version.hip,
+            "torch": torch.__version__, "host_cpu": host}
 
 
 def cpu_sample(ps, xs, grads):
@@ -346,6 +388,10 @@ def main() -> int:
     if not torch.isfinite(ratios).all():
         eprint("non-finite trust ratio after the timed steps")
         return 1
+    latency = step_latencies(opt, LATENCY_STEPS)
+    opt.check()
+    eprint("single-step latency over %d steps: median %.4f ms, min %.4f ms, max %.4f ms"
+           % (latency["steps"], latency["median_ms"], latency["min_ms"], latency["max_ms"]))
     # The attainable rate of the dominant kernel's access pattern: a stream
     # with the same reads, writes and elements per workgroup, no arithmetic.
     dom_is_single = avg_one_ms(k_one, recorded) >= avg_one_ms(k_mom, recorded)
@@ -447,7 +493,11 @@ def main() -> int:
                        "no arithmetic (libstream_probe)"},
         },
         "cpu_baseline": cpu,
+        "latency": latency,
+        "env": environment(),
     }
+    if cpu:
+        cpu["gpu_speedup"] = line["value"] / cpu["value"]
     print(json.dumps(line), flush=True)
     opt.close()
     return 0
