@@ -658,6 +658,13 @@ __global__ __launch_bounds__(kSegBlock) void finalize_kernel(
 #ifndef LAMB_MEMBER_SLEEP
 #define LAMB_MEMBER_SLEEP LAMB_SPIN_SLEEP
 #endif
+// LAMB_PREFETCH: load group 0 of a workgroup's next tile before the wait for
+// the current layer's scale (0.2-0.55% faster on BERT, ResNet-50 and LARS;
+// neutral where a round is one layer, whose stragglers then share HBM with
+// the prefetch). It takes 16 more VGPRs, at most 127 in all.
+#ifndef LAMB_PREFETCH
+#define LAMB_PREFETCH 1
+#endif
 // LAMB_FUSED_UNROLL / LAMB_FUSED_UNROLL_LARS: float4 groups each thread of
 // the single pass loads per trip, for the LAMB family (four streams) and for
 // LARS (three). For LAMB one beats two (0.3-1% on BERT and ResNet-50): a
@@ -745,6 +752,13 @@ void fused_kernel(const TensorDesc *__restrict__ tensors, const ChunkDesc *__res
     bool stop = sh_fault != 0 || sh_skip != 0;
 
     const int32_t grid = static_cast<int32_t>(gridDim.x);
+#if LAMB_PREFETCH
+    // Group 0 of this workgroup's next tile, loaded before the current tile
+    // waits for its layer's scale, so that HBM keeps streaming through the
+    // wait. p_j: the entry it belongs to (-1: none for this thread).
+    f32x4 px = {0.0f, 0.0f, 0.0f, 0.0f}, pg = px, pm = px, pv = px;
+    int32_t p_j = -1;
+#endif
     for (int32_t r = 0; !stop; ++r) {
         const int32_t j = r * grid + static_cast<int32_t>(blockIdx.x);  // entry of round r
         if (j >= n_tiles)
@@ -783,6 +797,14 @@ void fused_kernel(const TensorDesc *__restrict__ tensors, const ChunkDesc *__res
             for (int k = 0; k < kFusedUnroll; ++k) {
                 group(k0 + k, at[k], ok[k]);
                 xr[k] = gr[k] = mr[k] = vr[k] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+#if LAMB_PREFETCH
+                if (k0 + k == 0 && p_j == j) {
+                    xr[k] = px;
+                    gr[k] = pg;
+                    mr[k] = pm;
+                    vr[k] = pv;
+                } else
+#endif
                 if (ok[k] == 4) {
                     xr[k] = load4(x + at[k]);
                     gr[k] = g.at4(at[k]);
@@ -836,6 +858,26 @@ void fused_kernel(const TensorDesc *__restrict__ tensors, const ChunkDesc *__res
         }
         block_combine<kNorm, kWaves>(sum_xx, sum_uu, &sh_tile);
         __syncthreads();
+#if LAMB_PREFETCH
+        p_j = -1;
+        if (j + grid < n_tiles) {
+            const int32_t jn = j + grid;
+            const ChunkDesc cn = tiles[jn];
+            if (cn.len != 0) {
+                const TensorDesc &tn = tensors[cn.tensor];
+                // block 0 of tile jn - first_tile of its layer
+                const int64_t at0 = int64_t(jn - tn.first_tile) * (4 * kBlock) + 4 * threadIdx.x;
+                if (tn.numel - at0 >= 4) {
+                    px = load4(global_view(tn.x) + at0);
+                    pg = GradView<kBf16>(tn.g, 0, a.grad_scale).at4(at0);
+                    pm = load4(global_view(tn.m) + at0);
+                    if constexpr (kV)
+                        pv = load4(global_view(tn.v) + at0);
+                    p_j = jn;
+                }
+            }
+        }
+#endif
 
         // The layer's step scale.
         const int32_t first = t.first_tile, team = t.n_tiles;
