@@ -112,3 +112,24 @@ def test_single_pass_beside_other_work():
         del c
     finally:
         pair.close()
+
+
+@pytest.mark.parametrize("value", ["9", "8x", "", "-10"])
+def test_tile_override_rejects_other_values(monkeypatch, value):
+    """The tile override takes 8 or 10; anything else fails plan creation with
+    LAMB_EINVAL and a message naming the variable, and creates nothing."""
+    torch = H.torch_cuda()
+    x = torch.zeros(4096, device="cuda")
+    g = torch.zeros(4096, device="cuda")
+    m = torch.zeros(4096, device="cuda")
+    v = torch.zeros(4096, device="cuda")
+    rows = [(x.data_ptr(), g.data_ptr(), m.data_ptr(), v.data_ptr(), 4096, 1)]
+    monkeypatch.setenv(H.TILE_ENV, value)
+    with pytest.raises(_lib.LambError) as e:
+        _lib.lamb_plan_create(rows, _lib.LAMB_GRAD_F32, _lib.LAMB_ALGO_LAMB, 0)
+    assert e.value.status == _lib.LAMB_EINVAL
+    assert H.TILE_ENV in _lib.last_error()
+    for ok, groups in (("8", 8), ("10", 10)):
+        monkeypatch.setenv(H.TILE_ENV, ok)
+        with _lib.lamb_plan_create(rows, _lib.LAMB_GRAD_F32, _lib.LAMB_ALGO_LAMB, 0) as plan:
+            assert _lib.lamb_plan_tiles(plan)[2] == groups
