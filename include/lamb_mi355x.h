@@ -251,7 +251,9 @@ LAMB_API lamb_status lamb_plan_tiles(const lamb_plan *plan, int32_t *tiles_per_t
  * up a wait (a layer's tiles were not all resident within about a second:
  * 2^22 polls, or the count in the environment variable
  * LAMB_MI355X_SPIN_LIMIT when lamb_plan_create ran, which tests use to
- * exercise this path).
+ * exercise this path; a value that is not a positive integer makes
+ * lamb_plan_create fail with LAMB_EINVAL, and values above 2^30 count as
+ * 2^30).
  * That step's state is then undefined and the plan's single pass does no
  * further work: restore the state and build a new plan. Synchronises the
  * stream. Errors: LAMB_ENULL, LAMB_EHIP, LAMB_ESYNC.

@@ -594,6 +594,15 @@ lamb_status lamb_plan_create(const lamb_tensor *tensors, int32_t n_tensors,
     const int32_t max_round = int32_t(std::max<int64_t>(1, int64_t(kFusedBlocksPerCu) * cu_count));
     std::vector<int32_t> first_tile(static_cast<size_t>(n_tensors)),
         tile_count(static_cast<size_t>(n_tensors));
+    uint32_t spin_limit = kDefaultSpinLimit;
+    if (const char *env = std::getenv("LAMB_MI355X_SPIN_LIMIT")) {
+        char *end = nullptr;
+        const long long v = std::strtoll(env, &end, 10);
+        if (end == env || *end != '\0' || v < 1)
+            return fail(LAMB_EINVAL, "LAMB_MI355X_SPIN_LIMIT = \"%s\", need a positive integer",
+                        env);
+        spin_limit = uint32_t(std::min<long long>(v, 1LL << 30));
+    }
     int32_t n_entries = 0, round = 0, groups = 0;
     if (const char *env = std::getenv("LAMB_MI355X_TILE_GROUPS")) {
         char *end = nullptr;
@@ -677,10 +686,7 @@ lamb_status lamb_plan_create(const lamb_tensor *tensors, int32_t n_tensors,
     plan->cu_count = cu_count;
     plan->round = round;
     plan->tile_groups = groups;
-    if (const char *env = std::getenv("LAMB_MI355X_SPIN_LIMIT")) {
-        const long long v = std::atoll(env);
-        plan->spin_limit = uint32_t(std::min<long long>(std::max<long long>(v, 1), 1LL << 30));
-    }
+    plan->spin_limit = spin_limit;
     auto round256 = [](size_t b) { return (b + 255) & ~size_t(255); };
     const size_t tensors_bytes = round256(sizeof(TensorDesc) * size_t(n_tensors));
     const size_t chunks_bytes = round256(sizeof(ChunkDesc) * size_t(n_chunks));

@@ -133,3 +133,20 @@ def test_tile_override_rejects_other_values(monkeypatch, value):
         monkeypatch.setenv(H.TILE_ENV, ok)
         with _lib.lamb_plan_create(rows, _lib.LAMB_GRAD_F32, _lib.LAMB_ALGO_LAMB, 0) as plan:
             assert _lib.lamb_plan_tiles(plan)[2] == groups
+
+
+@pytest.mark.parametrize("value", ["abc", "0", "-5", "12 "])
+def test_spin_limit_rejects_other_values(monkeypatch, value):
+    """The spin limit takes a positive integer; anything else fails plan
+    creation with LAMB_EINVAL instead of silently becoming a one-poll budget."""
+    torch = H.torch_cuda()
+    bufs = [torch.zeros(4096, device="cuda") for _ in range(4)]
+    rows = [tuple(b.data_ptr() for b in bufs) + (4096, 1)]
+    monkeypatch.setenv("LAMB_MI355X_SPIN_LIMIT", value)
+    with pytest.raises(_lib.LambError) as e:
+        _lib.lamb_plan_create(rows, _lib.LAMB_GRAD_F32, _lib.LAMB_ALGO_LAMB, 0)
+    assert e.value.status == _lib.LAMB_EINVAL
+    assert "LAMB_MI355X_SPIN_LIMIT" in _lib.last_error()
+    monkeypatch.setenv("LAMB_MI355X_SPIN_LIMIT", "1000")
+    with _lib.lamb_plan_create(rows, _lib.LAMB_GRAD_F32, _lib.LAMB_ALGO_LAMB, 0):
+        pass
