@@ -46,6 +46,21 @@ def _check_tensors(params, grads):
     return g_dtype, device
 
 
+def _check_state(state, buffers) -> None:
+    """A saved state must hold one tensor of the right size per parameter for
+    every buffer, and a step count >= 0."""
+    if int(state["step"]) < 0:
+        raise ValueError("step must be >= 0")
+    for name, dst in buffers.items():
+        src = state[name]
+        if len(src) != len(dst):
+            raise ValueError("state %r has %d tensors, the optimizer %d" % (name, len(src), len(dst)))
+        for i, (d, t) in enumerate(zip(dst, src)):
+            if t.numel() != d.numel():
+                raise ValueError("state %r tensor %d has %d elements, need %d"
+                                 % (name, i, t.numel(), d.numel()))
+
+
 class _LayerwiseOptimizer:
     algo = _lib.LAMB_ALGO_LAMB
 
@@ -169,8 +184,9 @@ class LAMB(_LayerwiseOptimizer):
         holds a NaN or infinity changes nothing and sets ``found_nonfinite``.
         ``schedule``: stages (steps, warmup_steps, peak_lr, power) that set the
         learning rate of each step (warmup, then polynomial decay, Section 4).
-        ``path``: "auto" (layers of up to 8M elements take the single-pass
-        kernel) or "two-pass"."""
+        ``path``: "auto" (layers of up to 8.4M elements, or 10.5M where the
+        plan takes the wider tile, take the single-pass kernel) or
+        "two-pass"."""
         if variant not in self.VARIANTS:
             raise ValueError("variant must be one of %s" % (self.VARIANTS,))
         if variant != "lamb" and not bias_correction:
@@ -196,6 +212,7 @@ class LAMB(_LayerwiseOptimizer):
         return {"step": self.t, "m": [m.clone() for m in self.m], "v": [v.clone() for v in self.v]}
 
     def load_state_dict(self, state) -> None:
+        _check_state(state, {"m": self.m, "v": self.v})
         self.t = int(state["step"])
         for dst, src in zip(self.m, state["m"]):
             dst.copy_(src)
@@ -228,6 +245,7 @@ class LARS(_LayerwiseOptimizer):
         return {"step": self.t, "m": [m.clone() for m in self.m]}
 
     def load_state_dict(self, state) -> None:
+        _check_state(state, {"m": self.m})
         self.t = int(state["step"])
         for dst, src in zip(self.m, state["m"]):
             dst.copy_(src)

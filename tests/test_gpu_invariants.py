@@ -80,7 +80,8 @@ def test_layer_independence(path, chunk):
 
 def test_resume_is_bitwise():
     """The caller owns x, m, v and t: 6 steps equal 3 steps, a copy out and
-    into a fresh optimizer, and 3 more."""
+    into a fresh optimizer, and 3 more. A state that does not fit the
+    optimizer's tensors is refused and changes nothing."""
     torch = H.torch_cuda()
     from paper_1904_00962_amd.optim import LAMB
     ps = paramsets.get(3)
@@ -104,6 +105,14 @@ def test_resume_is_bitwise():
     b.close()
     p3 = [x.clone() for x in saved[0]]
     c = LAMB(p3, grads, lr=ps.lr, wd_mask=mask)
+    # a state of another parameter set is refused before anything is copied
+    bad = dict(saved[1], m=saved[1]["m"][:-1])
+    with pytest.raises(ValueError):
+        c.load_state_dict(bad)
+    bad = dict(saved[1], v=[v[:-1] for v in saved[1]["v"]])
+    with pytest.raises(ValueError):
+        c.load_state_dict(bad)
+    assert c.t == 0 and all(int(torch.count_nonzero(m)) == 0 for m in c.m)
     c.load_state_dict(saved[1])
     run(c, 4, 7)
     torch.cuda.synchronize()
