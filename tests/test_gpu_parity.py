@@ -26,6 +26,15 @@ def test_tiny_lars_ten_steps():
     H.run_config(0, 10, "lars", chunk_elems=512)
 
 
+@pytest.mark.parametrize("path", ["auto", "wide"])
+def test_tiny_lamb_hundred_steps(path):
+    """100 steps compared with the oracle after every one: no drift between
+    the two trajectories, and 100 alternations of the single pass's slot
+    buffers on layers of up to 32 tiles."""
+    r = H.run_config(0, 100, "lamb", path=path)
+    assert r.max_err <= H.STATE_TOL
+
+
 @pytest.mark.parametrize("algo", ["lamb", "lars", "nlamb", "nnlamb"])
 def test_tiny_wide_tiles(algo):
     """The single pass with 10240-element tiles (forced on the tiny set)."""
