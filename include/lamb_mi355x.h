@@ -193,8 +193,10 @@ typedef struct lamb_hparams {
  * The table is copied; the tensor pointers must stay valid and unchanged for
  * the plan's life (rebuild the plan if the buffers move).
  *   tensors      host array of n_tensors descriptors, n_tensors >= 1
- *   g_dtype      dtype of every g
- *   algo         which step the plan serves
+ *   g_dtype      dtype of every g, a lamb_grad_dtype value
+ *   algo         which step the plan serves, a lamb_algo value
+ * (The enum parameters travel as int32_t so that any value a caller passes
+ * is well defined and rejected with LAMB_EINVAL when out of range.)
  *   chunk_elems  elements per work chunk: 0 picks the default, otherwise a
  *                multiple of 8 in [8, 2^30]. Results are deterministic for a
  *                given chunk size and agree across sizes to rounding.
@@ -204,7 +206,7 @@ typedef struct lamb_hparams {
  * LAMB_EHIP (device allocation or copy failed).
  */
 LAMB_API lamb_status lamb_plan_create(const lamb_tensor *tensors, int32_t n_tensors,
-                             lamb_grad_dtype g_dtype, lamb_algo algo,
+                             int32_t g_dtype, int32_t algo,
                              int32_t chunk_elems, lamb_plan **out);
 
 /* Free the plan's device buffers. NULL is accepted. Waits for nothing: the
@@ -454,7 +456,7 @@ LAMB_API lamb_status lamb_sqrt_scaled_lr(double base_lr, int64_t base_batch, int
                                 double *lr_out);
 
 /* Static description of a status code. */
-LAMB_API const char *lamb_status_str(lamb_status status);
+LAMB_API const char *lamb_status_str(int32_t status);
 
 /* Detail of the calling thread's last failure ("" if none). */
 LAMB_API const char *lamb_last_error(void);

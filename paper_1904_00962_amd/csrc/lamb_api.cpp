@@ -252,7 +252,7 @@ void release_events(lamb_plan *plan) {
 
 extern "C" {
 
-const char *lamb_status_str(lamb_status status) {
+const char *lamb_status_str(int32_t status) {
     switch (status) {
     case LAMB_OK: return "ok";
     case LAMB_EINVAL: return "invalid argument";
@@ -494,7 +494,7 @@ void build_segments(const std::vector<std::pair<int32_t, int32_t>> &tensor_chunk
 extern "C" {
 
 lamb_status lamb_plan_create(const lamb_tensor *tensors, int32_t n_tensors,
-                             lamb_grad_dtype g_dtype, lamb_algo algo, int32_t chunk_elems,
+                             int32_t g_dtype_in, int32_t algo_in, int32_t chunk_elems,
                              lamb_plan **out) {
     if (!out)
         return fail(LAMB_ENULL, "out must not be NULL");
@@ -503,10 +503,12 @@ lamb_status lamb_plan_create(const lamb_tensor *tensors, int32_t n_tensors,
         return fail(LAMB_ENULL, "tensors must not be NULL");
     if (n_tensors < 1)
         return fail(LAMB_EINVAL, "n_tensors = %d, need >= 1", n_tensors);
-    if (g_dtype != LAMB_GRAD_F32 && g_dtype != LAMB_GRAD_BF16)
-        return fail(LAMB_EINVAL, "unknown gradient dtype %d", int(g_dtype));
-    if (algo != LAMB_ALGO_LAMB && algo != LAMB_ALGO_LARS)
-        return fail(LAMB_EINVAL, "unknown algorithm %d", int(algo));
+    if (g_dtype_in != LAMB_GRAD_F32 && g_dtype_in != LAMB_GRAD_BF16)
+        return fail(LAMB_EINVAL, "unknown gradient dtype %d", g_dtype_in);
+    if (algo_in != LAMB_ALGO_LAMB && algo_in != LAMB_ALGO_LARS)
+        return fail(LAMB_EINVAL, "unknown algorithm %d", algo_in);
+    const lamb_grad_dtype g_dtype = static_cast<lamb_grad_dtype>(g_dtype_in);
+    const lamb_algo algo = static_cast<lamb_algo>(algo_in);
     int32_t chunk = 0;
     lamb_status st = resolve_chunk_elems(chunk_elems, &chunk);
     if (st != LAMB_OK)

@@ -24,10 +24,10 @@ static int failures = 0;
 static void status_strings(void) {
     int code;
     for (code = LAMB_ESYNC; code <= LAMB_OK; ++code) {
-        const char *s = lamb_status_str((lamb_status)code);
+        const char *s = lamb_status_str(code);
         CHECK(s != NULL && s[0] != '\0' && strcmp(s, "unknown status") != 0);
     }
-    CHECK(strcmp(lamb_status_str((lamb_status)-99), "unknown status") == 0);
+    CHECK(strcmp(lamb_status_str(-99), "unknown status") == 0);
 }
 
 /* Section 4 / Appendix H defaults as the header documents them. */
@@ -132,6 +132,11 @@ static void rejected_calls(void) {
     CHECK(plan == NULL && lamb_last_error()[0] != '\0');
     CHECK(lamb_plan_create(&t, 1, LAMB_GRAD_F32, LAMB_ALGO_LAMB, 0, &plan) == LAMB_ENULL);
     CHECK(lamb_plan_create(NULL, 1, LAMB_GRAD_F32, LAMB_ALGO_LAMB, 0, &plan) == LAMB_ENULL);
+    /* out-of-range enum values are rejected, not assumed away */
+    CHECK(lamb_plan_create(&t, 1, 2, LAMB_ALGO_LAMB, 0, &plan) == LAMB_EINVAL);
+    CHECK(lamb_plan_create(&t, 1, -1, LAMB_ALGO_LAMB, 0, &plan) == LAMB_EINVAL);
+    CHECK(lamb_plan_create(&t, 1, LAMB_GRAD_F32, 7, 0, &plan) == LAMB_EINVAL);
+    CHECK(plan == NULL);
     CHECK(lamb_plan_destroy(NULL) == LAMB_OK);
     CHECK(lamb_step(NULL, 1e-3f, 0.9f, 0.999f, 1e-6f, 0.01f, 0.0f, 10.0f, 1, 1, NULL, NULL,
                     NULL) == LAMB_ENULL);
