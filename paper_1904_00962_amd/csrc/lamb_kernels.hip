@@ -658,6 +658,14 @@ __global__ __launch_bounds__(kSegBlock) void finalize_kernel(
 #ifndef LAMB_MEMBER_SLEEP
 #define LAMB_MEMBER_SLEEP LAMB_SPIN_SLEEP
 #endif
+// LAMB_WAVE_PRIORITY: a workgroup that waits for its layer's scale drops its
+// waves to the lowest issue priority (s_setprio 0) and raises them (to 3)
+// once the scale is known, so that waves with reads and writes to issue go
+// first (1.2-1.4% faster on BERT-Large, 0.5-0.6% on LARS; within 0.5% either
+// way on the other sets).
+#ifndef LAMB_WAVE_PRIORITY
+#define LAMB_WAVE_PRIORITY 1
+#endif
 // LAMB_PREFETCH: load group 0 of a workgroup's next tile before the wait for
 // the current layer's scale (0.2-0.55% faster on BERT, ResNet-50 and LARS;
 // neutral where a round is one layer, whose stragglers then share HBM with
@@ -858,6 +866,9 @@ void fused_kernel(const TensorDesc *__restrict__ tensors, const ChunkDesc *__res
         }
         block_combine<kNorm, kWaves>(sum_xx, sum_uu, &sh_tile);
         __syncthreads();
+#if LAMB_WAVE_PRIORITY
+        __builtin_amdgcn_s_setprio(0);
+#endif
 #if LAMB_PREFETCH
         p_j = -1;
         if (j + grid < n_tiles) {
@@ -933,6 +944,9 @@ void fused_kernel(const TensorDesc *__restrict__ tensors, const ChunkDesc *__res
         if (stop)
             break;
 
+#if LAMB_WAVE_PRIORITY
+        __builtin_amdgcn_s_setprio(3);
+#endif
         // x - scale * u from LDS and the registers.
         const float s = sh_scale;
         gbf16 *copy = t.x_copy ? (gbf16 *)t.x_copy : nullptr;
