@@ -14,7 +14,7 @@ from __future__ import annotations
 
 import dataclasses
 import os
-from typing import Callable, List, Optional, Sequence
+from typing import List, Optional, Sequence
 
 import numpy as np
 import pytest
