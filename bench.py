@@ -75,14 +75,24 @@ def algo_label(algo: str) -> str:
     return {"lamb": "LAMB", "lars": "LARS", "nlamb": "N-LAMB", "nnlamb": "NN-LAMB"}[algo]
 
 
+def _strip_comments(src: str) -> str:
+    """C/C++ source without // and /* */ comments, blank lines and trailing
+    blanks (the sources hashed here hold no string literal with either
+    comment sequence)."""
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    src = re.sub(r"//[^\n]*", "", src)
+    return "\n".join(line.rstrip() for line in src.splitlines() if line.strip())
+
+
 def kernel_source_hash() -> str:
     """Hash of what the kernels' machine code depends on: the kernel source,
-    the layout header it shares with the host side, and the compile flags."""
+    the layout header it shares with the host side (both without comments),
+    and the compile flags."""
     from paper_1904_00962_amd import build as hb
     h = hashlib.sha256()
     for p in (os.path.join(hb.CSRC, "lamb_kernels.hip"), os.path.join(hb.CSRC, "lamb_internal.h")):
-        with open(p, "rb") as f:
-            h.update(f.read())
+        with open(p) as f:
+            h.update(_strip_comments(f.read()).encode())
     h.update(" ".join(hb.HIPCC_FLAGS).encode())
     return h.hexdigest()[:16]
 

@@ -25,9 +25,12 @@
 //            in which case nothing changes.
 //
 // A layer small enough to sit on chip in the resident workgroups takes a
-// single pass instead (fused_kernel below): each tile's x (in LDS) and u (in
-// registers) stay there while the layer's partial norms meet, so x, g, m, v
-// are read and x, m, v written exactly once.
+// single pass instead (fused_kernel below): each tile's x (in LDS, part of it
+// in registers for the wider tile) and u (in registers) stay there while the
+// layer's partial norms meet, so x, g, m, v are read and x, m, v written
+// exactly once. A step that skips on a non-finite gradient first runs a
+// read-only check of g (finite_kernel) whose verdict every later kernel of
+// the step reads.
 //
 // Recomputing u instead of storing it saves 4 bytes per parameter of HBM
 // traffic. There are no float atomics: every reduction has a fixed order, so

@@ -67,3 +67,11 @@ def test_counter_traffic_only_for_the_profiled_kernel(tmp_path, monkeypatch):
     assert bench.counter_traffic("single_pass", "bert-large", h) == pytest.approx(7.9e9)
     path.write_text("kernel_source_hash: 0123456789abcdef\nhbm_bytes_per_launch: 7.9e+09\n")
     assert bench.counter_traffic("single_pass", "bert-large", h) is None  # stale
+
+
+def test_source_hash_ignores_comments_and_blank_lines():
+    code = "int f(int a) {\n    return a + 1;  // one more\n}\n"
+    same = "/* header\n   comment */\n\nint f(int a) {\n    // note\n    return a + 1;\n}\n\n"
+    other = "int f(int a) {\n    return a + 2;\n}\n"
+    assert bench._strip_comments(code) == bench._strip_comments(same)
+    assert bench._strip_comments(code) != bench._strip_comments(other)
