@@ -67,7 +67,8 @@ typedef enum lamb_algo {
 
 /*
  * One layer block x^(i) (Section 2). Every buffer holds `numel` contiguous
- * elements and is 16-byte aligned; no two buffers of a table may overlap.
+ * elements (1 to 2^40) and is 16-byte aligned; no two buffers of a table may
+ * overlap.
  *   x  fp32 parameters, updated in place
  *   g  gradient g_t (fp32 or bf16, fixed per plan), read only
  *   m  fp32 first moment (LAMB) / momentum (LARS), updated in place; start at 0
@@ -348,7 +349,7 @@ LAMB_API lamb_status lars_step(lamb_plan *plan, float lr, float momentum,
  * into ceil(numel[i] / chunk_elems) chunks in table order; chunk k of it
  * starts at k * chunk_elems and holds min(chunk_elems, numel[i] - start)
  * elements. chunk_elems = 0 picks the default.
- *   numel        host, n_tensors sizes (>= 1 each)
+ *   numel        host, n_tensors sizes (each in [1, 2^40])
  *   capacity     length of the three host output arrays (may be 0 with NULL
  *                outputs to query the count)
  *   n_chunks     receives the number of chunks
@@ -374,7 +375,7 @@ LAMB_API lamb_status lamb_chunk_table(const int64_t *numel, int32_t n_tensors,
  * rounds, so the rounds come out about equally full. The gap a round leaves
  * is filled with empty entries (tensor -1, length 0). A plan uses
  * max_round = 4 * (compute units) and tile_groups = 0.
- *   numel         host, n_tensors sizes (>= 1 each)
+ *   numel         host, n_tensors sizes (each in [1, 2^40])
  *   max_round     widest round, >= 1
  *   tile_groups   G: 8, 10, or 0 for a plan's choice, which is 10 only if
  *                 that puts more parameters on the single pass than 8

@@ -103,6 +103,17 @@ bool aligned16(const void *p) {
 }
 
 constexpr int64_t kMaxChunkElems = int64_t(1) << 30;
+constexpr int64_t kMaxNumel = int64_t(1) << 40;  // elements per tensor
+
+// Every size in [1, kMaxNumel]: chunk and tile counts then stay far from
+// int64 overflow.
+lamb_status check_numel(const int64_t *numel, int32_t n) {
+    for (int32_t i = 0; i < n; ++i)
+        if (numel[i] < 1 || numel[i] > kMaxNumel)
+            return fail(LAMB_EINVAL, "tensor %d has numel %lld, need 1 to 2^40", i,
+                        static_cast<long long>(numel[i]));
+    return LAMB_OK;
+}
 
 lamb_status resolve_chunk_elems(int32_t requested, int32_t *out) {
     if (requested == 0) {
@@ -280,10 +291,9 @@ lamb_status lamb_chunk_table(const int64_t *numel, int32_t n_tensors, int32_t ch
     lamb_status st = resolve_chunk_elems(chunk_elems, &chunk);
     if (st != LAMB_OK)
         return st;
-    for (int32_t i = 0; i < n_tensors; ++i)
-        if (numel[i] < 1)
-            return fail(LAMB_EINVAL, "tensor %d has numel %lld, need >= 1", i,
-                        static_cast<long long>(numel[i]));
+    st = check_numel(numel, n_tensors);
+    if (st != LAMB_OK)
+        return st;
     const int64_t total = count_chunks(numel, n_tensors, chunk);
     if (total < 0)
         return fail(LAMB_EINVAL, "more than 2^31-1 chunks; raise chunk_elems");
@@ -338,10 +348,9 @@ lamb_status lamb_tile_schedule(const int64_t *numel, int32_t n_tensors, int32_t 
     if (tile_groups != 0 && tile_groups != kTileGroups && tile_groups != kWideGroups)
         return fail(LAMB_EINVAL, "tile_groups = %d, need 0, %d or %d", tile_groups, kTileGroups,
                     kWideGroups);
-    for (int32_t i = 0; i < n_tensors; ++i)
-        if (numel[i] < 1)
-            return fail(LAMB_EINVAL, "tensor %d has numel %lld, need >= 1", i,
-                        static_cast<long long>(numel[i]));
+    const lamb_status st = check_numel(numel, n_tensors);
+    if (st != LAMB_OK)
+        return st;
     // A plan's choice: the wide tile only if it puts more parameters on the
     // single pass (with as many, the narrow tile streams slightly faster).
     int groups = tile_groups;
@@ -529,11 +538,9 @@ lamb_status lamb_plan_create(const lamb_tensor *tensors, int32_t n_tensors,
         if (!t.x || !t.g || !t.m || (needs_v && !t.v))
             return fail(LAMB_ENULL, "tensor %d: x, g, m%s must not be NULL", i,
                         needs_v ? ", v" : "");
-        if (t.numel < 1)
-            return fail(LAMB_EINVAL, "tensor %d: numel %lld, need >= 1", i,
-                        static_cast<long long>(t.numel));
-        if (t.numel > (int64_t(1) << 40))
-            return fail(LAMB_EINVAL, "tensor %d: numel %lld too large", i,
+        st = check_numel(&t.numel, 1);
+        if (st != LAMB_OK)
+            return fail(LAMB_EINVAL, "tensor %d: numel %lld, need 1 to 2^40", i,
                         static_cast<long long>(t.numel));
         if (t.wd != 0 && t.wd != 1)
             return fail(LAMB_EINVAL, "tensor %d: wd must be 0 or 1", i);

@@ -6,6 +6,7 @@
  * any failure.
  */
 #include <math.h>
+#include <stdint.h>
 #include <stdio.h>
 #include <string.h>
 
@@ -59,6 +60,11 @@ static void chunk_table(void) {
     CHECK(lamb_chunk_table(numel, 3, 512, 5, ct, cs, cl, &n) == LAMB_EINVAL && n == 6);
     CHECK(lamb_chunk_table(numel, 3, 12, 8, ct, cs, cl, &n) == LAMB_EINVAL);
     CHECK(lamb_chunk_table(NULL, 3, 512, 8, ct, cs, cl, &n) == LAMB_ENULL);
+    /* sizes beyond 2^40 are rejected before anything is counted */
+    {
+        const int64_t huge[2] = {5, INT64_MAX};
+        CHECK(lamb_chunk_table(huge, 2, 8, 0, NULL, NULL, NULL, &n) == LAMB_EINVAL);
+    }
 }
 
 /*
@@ -100,6 +106,11 @@ static void tile_schedule(void) {
                                  &groups) == LAMB_OK);
         CHECK(groups == 10 && tiles[0] == 4 && n == 4 && el[3] == 10 * 1024);
         CHECK(lamb_tile_schedule(big, 1, 4, 9, 8, et, es, el, first, tiles, &n, &round,
+                                 NULL) == LAMB_EINVAL);
+    }
+    {
+        const int64_t huge[1] = {((int64_t)1 << 40) + 1};
+        CHECK(lamb_tile_schedule(huge, 1, 4, 0, 8, et, es, el, first, tiles, &n, &round,
                                  NULL) == LAMB_EINVAL);
     }
 }

@@ -78,6 +78,12 @@ def test_chunk_table_errors(lib):
     with pytest.raises(_lib.LambError) as e:
         _lib.lamb_chunk_table([1 << 40] * 3, 8)  # more than 2^31 - 1 chunks
     assert e.value.status == _lib.LAMB_EINVAL
+    for numel in ([(1 << 40) + 1], [5, (1 << 63) - 1]):  # beyond 2^40 elements
+        for call in (lambda: _lib.lamb_chunk_table(numel, 8),
+                     lambda: _lib.lamb_tile_schedule(numel, 1024)):
+            with pytest.raises(_lib.LambError) as e:
+                call()
+            assert e.value.status == _lib.LAMB_EINVAL and "2^40" in str(e.value)
     n = ctypes.c_int32()
     sizes = (ctypes.c_int64 * 2)(100, 100)
     arr32 = (ctypes.c_int32 * 1)()
