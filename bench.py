@@ -142,6 +142,9 @@ def pattern_bytes(pattern: str, g_bytes: int) -> int:
             "apply": 12 + 4, "read": 12 + g_bytes, "copy": 8}[pattern]
 
 
+BEST_STREAM_TILES = (256, 512, 1024, 2048)
+
+
 def stream_rate(pattern: str, n: int, g_bf16: bool, tile: int, layer_tiles: int = 0,
                 reps: int = 20) -> float:
     """Attainable GB/s of a stream with `pattern`'s access pattern over n
@@ -192,6 +195,8 @@ def stream_probe_all() -> None:
         out[pattern + "_GBps"] = stream_rate(pattern, 335141888, True, tile)
     # the single pass's own layout: 1024-element blocks dealt over layers of 512 tiles
     out["single_pass_dealt_GBps"] = stream_rate("single_pass", 335141888, True, 8192, 512)
+    for tile in BEST_STREAM_TILES:
+        out["single_pass_tile%d_GBps" % tile] = stream_rate("single_pass", 335141888, True, tile)
     print(json.dumps(out), flush=True)
 
 
@@ -408,7 +413,7 @@ def main() -> int:
     dom_is_single = avg_one_ms(k_one, recorded) >= avg_one_ms(k_mom, recorded)
     dom_pattern = "single_pass" if dom_is_single else "moments"
     dom_elems = P_single if dom_is_single else P - P_single
-    attainable = None
+    attainable = best_stream = None
     if not args.skip_nonfinite and not args.bf16_copy and args.algo != "lars" and dom_elems:
         # the single pass deals its layers' blocks over their tiles; its largest
         # layers on BERT-Large have 512 tiles
@@ -417,6 +422,12 @@ def main() -> int:
                                  512 if dom_is_single else 0)
         eprint("stream probe (%s pattern, %d elements): %.0f GB/s"
                % (dom_pattern, dom_elems, attainable))
+        # The best plain stream of the same traffic: contiguous tiles of
+        # 256 to 2048 elements per workgroup, the fastest of them.
+        best_stream = max((stream_rate(dom_pattern, dom_elems, ps.g_dtype == "bf16", t), t)
+                          for t in BEST_STREAM_TILES)
+        eprint("best plain stream of that traffic: %.0f GB/s (%d elements per workgroup)"
+               % best_stream)
     cpu = None
     if sample is not None:
         eprint("timing the CPU oracle (budget %.0f s)" % args.cpu_seconds)
@@ -501,7 +512,12 @@ def main() -> int:
             "attainable": None if attainable is None else {
                 "GBps": attainable, "frac": dom["achieved"] / attainable,
                 "how": "stream with the kernel's reads, writes and elements per workgroup, "
-                       "no arithmetic (libstream_probe)"},
+                       "no arithmetic (libstream_probe)",
+                "best_stream_GBps": best_stream[0],
+                "best_stream_frac": dom["achieved"] / best_stream[0],
+                "best_stream_how": "the same reads and writes in contiguous tiles of %d "
+                                   "elements per workgroup, the fastest of %s"
+                                   % (best_stream[1], list(BEST_STREAM_TILES))},
         },
         "cpu_baseline": cpu,
         "latency": latency,

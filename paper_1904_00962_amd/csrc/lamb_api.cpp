@@ -1069,8 +1069,13 @@ lamb_status lamb_step_ex(lamb_plan *plan, const lamb_hparams *hp, void *stream,
         // Deferred moment passes only read, and use the coarse chunk table.
         const ChunkDesc *moment_chunks = k2.deferred ? plan->coarse_chunks : chunks;
         const int32_t n_moment_chunks = k2.deferred ? plan->n_coarse : n_chunks;
+        const int64_t coarse_elems =
+            std::min<int64_t>(int64_t(plan->chunk_elems) * kCoarseFactor, kMaxChunkElems);
+        const int32_t moment_threads =
+            two_pass_threads(k2.deferred ? coarse_elems : plan->chunk_elems);
         hipError_t err = launch_moments(k2, tensors, moment_chunks, plan->partials,
-                                        n_moment_chunks, plan->flags, guard_ctl, a, s);
+                                        n_moment_chunks, moment_threads, plan->flags, guard_ctl,
+                                        a, s);
         if (err != hipSuccess)
             return fail_hip(err, "launching the moment kernel");
         mark(plan, kTimedMoments, s);
@@ -1082,7 +1087,8 @@ lamb_status lamb_step_ex(lamb_plan *plan, const lamb_hparams *hp, void *stream,
         if (err != hipSuccess)
             return fail_hip(err, "launching the finalize kernel");
         mark(plan, kTimedFinalize, s);
-        err = launch_apply(k2, tensors, chunks, plan->scale, n_chunks, plan->flags, guard_ctl,
+        err = launch_apply(k2, tensors, chunks, plan->scale, n_chunks,
+                           two_pass_threads(plan->chunk_elems), plan->flags, guard_ctl,
                            k2.deferred ? nonfinite_out : nullptr, a, s);
         if (err != hipSuccess)
             return fail_hip(err, "launching the apply kernel");

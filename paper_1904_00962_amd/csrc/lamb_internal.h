@@ -9,22 +9,39 @@
 namespace lamb_mi355x {
 
 // Work is cut into chunks of at most `chunk_elems` elements of one tensor;
-// one workgroup of kBlock threads handles one chunk.
+// one workgroup of two_pass_threads(chunk_elems) threads (at most kBlock)
+// handles one chunk.
 #ifndef LAMB_BLOCK
 #define LAMB_BLOCK 256
 #endif
 #ifndef LAMB_DEFAULT_CHUNK
-#define LAMB_DEFAULT_CHUNK 512
+#define LAMB_DEFAULT_CHUNK 256
 #endif
 constexpr int kBlock = LAMB_BLOCK;
 constexpr int kWaves = kBlock / 64;
 constexpr int32_t kDefaultChunkElems = LAMB_DEFAULT_CHUNK;
 
+// Threads per workgroup of the moment and apply passes over chunks of `chunk`
+// elements: LAMB_TWO_PASS_F4 float4 groups per thread, whole waves, at least
+// one wave and at most kBlock threads (0: always kBlock). A default chunk is
+// one wave's float4 each: no thread of the workgroup idles.
+#ifndef LAMB_TWO_PASS_F4
+#define LAMB_TWO_PASS_F4 1
+#endif
+constexpr int32_t two_pass_threads(int64_t chunk) {
+    if (LAMB_TWO_PASS_F4 == 0)
+        return kBlock;
+    const int64_t groups = (chunk + 3) / 4;
+    const int64_t threads = (groups + LAMB_TWO_PASS_F4 - 1) / LAMB_TWO_PASS_F4;
+    const int64_t waves = (threads + 63) / 64;
+    return int32_t(waves < 1 ? 64 : waves * 64 > kBlock ? kBlock : waves * 64);
+}
+
 // A plan cuts every tensor twice: into fine chunks of chunk_elems elements
 // (direct-mode moment passes and every apply pass) and into coarse chunks of
 // kCoarseFactor times as many (deferred-mode moment passes, which only read
 // and run faster with more work per workgroup).
-constexpr int32_t kCoarseFactor = 4;
+constexpr int32_t kCoarseFactor = 8;
 
 // Single-pass path: with tiles of G float4 groups per thread, a layer of n
 // elements takes T = ceil(n / (G * kBlockElems)) tiles; tile i holds the
@@ -177,8 +194,8 @@ constexpr int32_t kCheckElems = 16384;
 // word of the epoch in guard_ctl is raised.
 hipError_t launch_moments(const StepKind &kind, const TensorDesc *tensors,
                           const ChunkDesc *chunks, Partial *partials, int32_t n_chunks,
-                          uint32_t *flags, const uint32_t *guard_ctl, const StepArgs &args,
-                          hipStream_t stream);
+                          int32_t threads, uint32_t *flags, const uint32_t *guard_ctl,
+                          const StepArgs &args, hipStream_t stream);
 // Both levels of the finalize: `segs` (n_segs entries) over `partials` into
 // `seg_partials`, then per tensor over its `ranges` entry of the segments.
 hipError_t launch_finalize(NormKind norm, const TensorDesc *tensors, int32_t n_tensors,
@@ -188,8 +205,8 @@ hipError_t launch_finalize(NormKind norm, const TensorDesc *tensors, int32_t n_t
                            double *norms_out, uint32_t *flags, hipStream_t stream);
 hipError_t launch_apply(const StepKind &kind, const TensorDesc *tensors,
                         const ChunkDesc *chunks, const float *scale, int32_t n_chunks,
-                        uint32_t *flags, const uint32_t *guard_ctl, int32_t *nonfinite_out,
-                        const StepArgs &args, hipStream_t stream);
+                        int32_t threads, uint32_t *flags, const uint32_t *guard_ctl,
+                        int32_t *nonfinite_out, const StepArgs &args, hipStream_t stream);
 // The finiteness check over `chunks` (all tensors, kCheckElems each).
 hipError_t launch_finite(bool bf16_grad, const TensorDesc *tensors, const ChunkDesc *chunks,
                          int32_t n_chunks, uint32_t *flags, const uint32_t *ctl, float grad_scale,

@@ -282,6 +282,42 @@ __device__ __forceinline__ void block_combine(double a, double b, Partial *out) 
     }
 }
 
+// block_combine over a workgroup of blockDim.x threads (whole waves, at most
+// kWaves of them): the same fixed tree; a single wave needs no LDS.
+template <int kNorm>
+__device__ __forceinline__ void block_combine_any(double a, double b, Partial *out) {
+    if (blockDim.x == 64) {
+        a = wave_combine<kNorm>(a);
+        b = wave_combine<kNorm>(b);
+        if (threadIdx.x == 0) {
+            out->sum_xx = a;
+            out->sum_uu = b;
+        }
+        return;
+    }
+    __shared__ double red_a[kWaves];
+    __shared__ double red_b[kWaves];
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int waves = int(blockDim.x >> 6);
+    a = wave_combine<kNorm>(a);
+    b = wave_combine<kNorm>(b);
+    if (lane == 0) {
+        red_a[wave] = a;
+        red_b[wave] = b;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        double sa = red_a[0], sb = red_b[0];
+        for (int w = 1; w < waves; ++w) {
+            sa = norm_combine<kNorm>(sa, red_a[w]);
+            sb = norm_combine<kNorm>(sb, red_b[w]);
+        }
+        out->sum_xx = sa;
+        out->sum_uu = sb;
+    }
+}
+
 // Workgroups are dispatched round-robin over the 8 XCDs.
 __device__ __forceinline__ uint32_t dispatch_rank() {
 #if LAMB_XCD_CONTIGUOUS
@@ -336,11 +372,12 @@ __global__ __launch_bounds__(kBlock) void moments_kernel(
     double sum_xx = 0.0, sum_uu = 0.0;
     bool nonfinite = false;
     const int n4 = c.len >> 2;
-    for (int base = threadIdx.x; base < n4; base += kBlock * kUnroll) {
+    const int stride = int(blockDim.x);
+    for (int base = threadIdx.x; base < n4; base += stride * kUnroll) {
         f32x4 xr[kUnroll], gr[kUnroll], mr[kUnroll], vr[kUnroll];
 #pragma unroll
         for (int k = 0; k < kUnroll; ++k) {
-            const int q = base + k * kBlock;
+            const int q = base + k * stride;
             if (q < n4) {
                 xr[k] = load4(x + 4 * q);
                 gr[k] = g.at4(4 * q);
@@ -353,7 +390,7 @@ __global__ __launch_bounds__(kBlock) void moments_kernel(
         }
 #pragma unroll
         for (int k = 0; k < kUnroll; ++k) {
-            const int q = base + k * kBlock;
+            const int q = base + k * stride;
             if (q < n4) {
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
@@ -398,7 +435,7 @@ __global__ __launch_bounds__(kBlock) void moments_kernel(
         if (__syncthreads_or(nonfinite) && threadIdx.x == 0)
             atomicOr(flags, 1u);
     }
-    block_combine<kNorm, kWaves>(sum_xx, sum_uu, partials + chunk_index());
+    block_combine_any<kNorm>(sum_xx, sum_uu, partials + chunk_index());
 }
 
 // ---------------------------------------------------------------------------
@@ -434,11 +471,12 @@ __global__ __launch_bounds__(kBlock) void apply_kernel(
     const float s = scale[c.tensor];
 
     const int n4 = c.len >> 2;
-    for (int base = threadIdx.x; base < n4; base += kBlock * kUnroll) {
+    const int stride = int(blockDim.x);
+    for (int base = threadIdx.x; base < n4; base += stride * kUnroll) {
         f32x4 xr[kUnroll], gr[kUnroll], mr[kUnroll], vr[kUnroll];
 #pragma unroll
         for (int k = 0; k < kUnroll; ++k) {
-            const int q = base + k * kBlock;
+            const int q = base + k * stride;
             if (q < n4) {
                 xr[k] = load4(x + 4 * q);
                 if constexpr (kReadsGrad)
@@ -454,7 +492,7 @@ __global__ __launch_bounds__(kBlock) void apply_kernel(
         }
 #pragma unroll
         for (int k = 0; k < kUnroll; ++k) {
-            const int q = base + k * kBlock;
+            const int q = base + k * stride;
             if (q < n4) {
                 f32x4 xn;
 #pragma unroll
@@ -1086,8 +1124,10 @@ const void *fused_fn(const StepKind &k, int groups) {
 
 hipError_t launch_moments(const StepKind &kind, const TensorDesc *tensors,
                           const ChunkDesc *chunks, Partial *partials, int32_t n_chunks,
-                          uint32_t *flags, const uint32_t *guard_ctl, const StepArgs &args,
-                          hipStream_t stream) {
+                          int32_t threads, uint32_t *flags, const uint32_t *guard_ctl,
+                          const StepArgs &args, hipStream_t stream) {
+    if (threads < 64 || threads > kBlock || threads % 64 != 0)
+        return hipErrorInvalidValue;
     StepArgs a = args;
     void *params[] = {&tensors, &chunks, &partials, &flags, &guard_ctl, &a};
     const void *fn;
@@ -1097,13 +1137,15 @@ hipError_t launch_moments(const StepKind &kind, const TensorDesc *tensors,
     case kLars: fn = moments_fn<kLars>(kind); break;
     default: fn = moments_fn<kLamb>(kind); break;
     }
-    return hipLaunchKernel(fn, dim3(n_chunks), dim3(kBlock), params, 0, stream);
+    return hipLaunchKernel(fn, dim3(n_chunks), dim3(threads), params, 0, stream);
 }
 
 hipError_t launch_apply(const StepKind &kind, const TensorDesc *tensors,
                         const ChunkDesc *chunks, const float *scale, int32_t n_chunks,
-                        uint32_t *flags, const uint32_t *guard_ctl, int32_t *nonfinite_out,
-                        const StepArgs &args, hipStream_t stream) {
+                        int32_t threads, uint32_t *flags, const uint32_t *guard_ctl,
+                        int32_t *nonfinite_out, const StepArgs &args, hipStream_t stream) {
+    if (threads < 64 || threads > kBlock || threads % 64 != 0)
+        return hipErrorInvalidValue;
     StepArgs a = args;
     void *params[] = {&tensors, &chunks, &scale, &flags, &guard_ctl, &nonfinite_out, &a};
     const void *fn;
@@ -1113,7 +1155,7 @@ hipError_t launch_apply(const StepKind &kind, const TensorDesc *tensors,
     case kLars: fn = apply_fn<kLars>(kind); break;
     default: fn = apply_fn<kLamb>(kind); break;
     }
-    return hipLaunchKernel(fn, dim3(n_chunks), dim3(kBlock), params, 0, stream);
+    return hipLaunchKernel(fn, dim3(n_chunks), dim3(threads), params, 0, stream);
 }
 
 hipError_t launch_finalize(NormKind norm, const TensorDesc *tensors, int32_t n_tensors,

@@ -8,7 +8,8 @@
 namespace lamb_mi355x {
 
 hipError_t launch_moments(const StepKind &, const TensorDesc *, const ChunkDesc *, Partial *,
-                          int32_t, uint32_t *, const uint32_t *, const StepArgs &, hipStream_t) {
+                          int32_t, int32_t, uint32_t *, const uint32_t *, const StepArgs &,
+                          hipStream_t) {
     return hipErrorNotSupported;
 }
 
@@ -19,8 +20,8 @@ hipError_t launch_finalize(NormKind, const TensorDesc *, int32_t, const Partial 
 }
 
 hipError_t launch_apply(const StepKind &, const TensorDesc *, const ChunkDesc *, const float *,
-                        int32_t, uint32_t *, const uint32_t *, int32_t *, const StepArgs &,
-                        hipStream_t) {
+                        int32_t, int32_t, uint32_t *, const uint32_t *, int32_t *,
+                        const StepArgs &, hipStream_t) {
     return hipErrorNotSupported;
 }
 

@@ -63,10 +63,11 @@ def test_chunk_table_is_the_documented_split(lib, chunk):
 
 
 def test_chunk_table_default_and_large_tensor(lib):
-    ct, cs, cl = _lib.lamb_chunk_table([(1 << 33) + 3], 0)
+    big = (1 << 31) + 1000
+    ct, cs, cl = _lib.lamb_chunk_table([big], 0)
     default = int(cl[0])
     assert default % 8 == 0 and cs[1] == default
-    assert cs[-1] + cl[-1] == (1 << 33) + 3 and cl[-1] == ((1 << 33) + 3) % default
+    assert cs[-1] + cl[-1] == big and cl[-1] == big % default
     assert cs.dtype == np.int64 and cs[-1] > 2 ** 31
 
 

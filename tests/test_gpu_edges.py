@@ -57,11 +57,13 @@ NLAMB = dict(DEFAULT, beta1=0.975, eps=1e-8)
 @pytest.mark.parametrize("algo,g_dtype", [("lamb", "f32"), ("lamb", "bf16"), ("lars", "f32"),
                                           ("lars", "bf16"), ("nlamb", "bf16"),
                                           ("nnlamb", "f32")])
-@pytest.mark.parametrize("chunk,path", [(8, "two-pass"), (64, "two-pass"), (1024, "two-pass"),
-                                        (0, "two-pass"), (0, "auto"), (0, "wide")])
+@pytest.mark.parametrize("chunk,path", [(8, "two-pass"), (64, "two-pass"), (520, "two-pass"),
+                                        (1024, "two-pass"), (0, "two-pass"), (0, "auto"),
+                                        (0, "wide")])
 def test_ragged_sizes(algo, g_dtype, chunk, path):
-    """Every tensor length around the 4-element group, the 256-thread tile,
-    the unrolled loop trip and the chunk boundary; on the single pass, around
+    """Every tensor length around the 4-element group, the workgroup's span
+    (one to four waves, by chunk size), the unrolled loop trip and the chunk
+    boundary; on the single pass, around
     the 8192- and 10240-element tiles and their multiples (layers of several
     tiles)."""
     rng = np.random.default_rng(1000 + chunk)

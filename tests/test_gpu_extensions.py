@@ -80,14 +80,14 @@ def test_grad_scale(algo, scale, g_mult):
 
 @pytest.mark.parametrize("algo", ALGOS)
 def test_deferred_mode_equals_direct_mode(algo):
-    """With finite gradients, the deferred mode (moment pass over chunks 4x as
+    """With finite gradients, the deferred mode (moment pass over chunks 8x as
     large, moments written by the apply pass) gives bit for bit the x, m, v
-    and ratios of the direct mode on a plan with 4x larger chunks."""
+    and ratios of the direct mode on a plan with 8x larger chunks."""
     torch = H.torch_cuda()
     ps = paramsets.get(3)
     xs = paramsets.draw_params(ps, device="cuda")
     runs = []
-    for skip, chunk in ((0, 2048), (1, 512)):
+    for skip, chunk in ((0, 2048), (1, 256)):
         pair = _pair([x.clone() for x in xs], ps.wd_mask(), "f32", algo, chunk, "two-pass")
         pair.subset = []
         flag = torch.zeros(1, dtype=torch.int32, device="cuda")
