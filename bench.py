@@ -190,7 +190,9 @@ def stream_rate(pattern: str, n: int, g_bf16: bool, tile: int, layer_tiles: int 
 def stream_probe_all() -> None:
     """Every pattern over the BERT-Large parameter count, one JSON line."""
     out = {"probe": "stream", "elements": 335141888, "g": "bf16"}
-    for pattern, tile in (("single_pass", 8192), ("moments", 512), ("apply", 512),
+    from paper_1904_00962_amd import _lib
+    chunk = int(_lib.lamb_chunk_table([1 << 20], 0)[2][0])  # a plan's default chunk
+    for pattern, tile in (("single_pass", 8192), ("moments", chunk), ("apply", chunk),
                           ("read", 2048), ("copy", 512)):
         out[pattern + "_GBps"] = stream_rate(pattern, 335141888, True, tile)
     # the single pass's own layout: 1024-element blocks dealt over layers of 512 tiles
@@ -418,7 +420,7 @@ def main() -> int:
         # the single pass deals its layers' blocks over their tiles; its largest
         # layers on BERT-Large have 512 tiles
         attainable = stream_rate(dom_pattern, dom_elems, ps.g_dtype == "bf16",
-                                 1024 * tile_groups if dom_is_single else (chunk or 512),
+                                 1024 * tile_groups if dom_is_single else chunk,
                                  512 if dom_is_single else 0)
         eprint("stream probe (%s pattern, %d elements): %.0f GB/s"
                % (dom_pattern, dom_elems, attainable))

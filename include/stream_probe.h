@@ -43,8 +43,9 @@ typedef enum stream_pattern {
 /*
  * One stream of `pattern` over n elements, `tile` elements per workgroup of
  * 256 threads (a multiple of 8 in [8, 2^24]; the single-pass kernel uses
- * 8192, the moment and apply kernels 512), enqueued on `stream`
- * (hipStream_t, NULL = null stream). g_bf16: 1 if g holds bf16.
+ * 8192, the moment and apply kernels the plan's chunk size, 256 by default),
+ * enqueued on `stream` (hipStream_t, NULL = null stream). g_bf16: 1 if g
+ * holds bf16.
  * layer_tiles = 0: each workgroup streams a contiguous tile. layer_tiles > 0
  * (tile a multiple of 1024): the single-pass kernel's layout, the array cut
  * into layers of layer_tiles tiles, tile i of a layer holding the layer's
