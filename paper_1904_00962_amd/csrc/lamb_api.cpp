@@ -29,11 +29,12 @@ struct lamb_plan {
     int32_t n_tensors = 0;
     int32_t n_chunks = 0;
     int32_t chunk_elems = 0;
+    int32_t coarse_elems = 0;       // elements per coarse chunk
     void *device_block = nullptr;  // one allocation holding every device buffer below
     int32_t n_coarse = 0;       // coarse chunks (kCoarseFactor * chunk_elems each)
     TensorDesc *tensors = nullptr;
-    ChunkDesc *chunks = nullptr;
-    ChunkDesc *coarse_chunks = nullptr;
+    int32_t *chunk_ids = nullptr;   // tensor id of every fine chunk
+    int32_t *coarse_ids = nullptr;  // tensor id of every coarse chunk
     Partial *partials = nullptr;
     float *scale = nullptr;
     uint32_t *flags = nullptr;     // the four non-finite words (kVerdictWord)
@@ -51,7 +52,7 @@ struct lamb_plan {
     uint64_t *slots = nullptr;     // 2 x 3 x n_tiles slot words
     uint32_t *ctl = nullptr;       // FusedCtl words
     TensorDesc *rest_tensors = nullptr;
-    ChunkDesc *rest_chunks = nullptr;
+    int32_t *rest_ids = nullptr;    // tensor id (in rest_tensors) of every fine chunk of those
     // Finalize segments of the fine, the coarse and the other-layers table.
     SegDesc *segs[3] = {};
     SegRange *seg_ranges[3] = {};
@@ -484,6 +485,15 @@ lamb_status build_chunks(const std::vector<int64_t> &numel, int32_t chunk, int32
 
 enum SegTable { kSegFine = 0, kSegCoarse = 1, kSegRest = 2 };
 
+// The tensor id of every chunk of a table (what the moment and apply passes
+// read; start and length follow from the tensor and the chunk size).
+std::vector<int32_t> ids_of(const std::vector<ChunkDesc> &chunks) {
+    std::vector<int32_t> ids(chunks.size());
+    for (size_t k = 0; k < chunks.size(); ++k)
+        ids[k] = chunks[k].tensor;
+    return ids;
+}
+
 // Finalize segments of a chunk table: tensor k's chunk partials
 // [first_k, first_k + count_k) cut into runs of kSegChunks.
 void build_segments(const std::vector<std::pair<int32_t, int32_t>> &tensor_chunks,
@@ -698,8 +708,8 @@ lamb_status lamb_plan_create(const lamb_tensor *tensors, int32_t n_tensors,
     plan->spin_limit = spin_limit;
     auto round256 = [](size_t b) { return (b + 255) & ~size_t(255); };
     const size_t tensors_bytes = round256(sizeof(TensorDesc) * size_t(n_tensors));
-    const size_t chunks_bytes = round256(sizeof(ChunkDesc) * size_t(n_chunks));
-    const size_t coarse_bytes = round256(sizeof(ChunkDesc) * size_t(n_coarse));
+    const size_t chunks_bytes = round256(sizeof(int32_t) * size_t(n_chunks));
+    const size_t coarse_bytes = round256(sizeof(int32_t) * size_t(n_coarse));
     const size_t partial_bytes = round256(sizeof(Partial) * size_t(n_chunks));
     const size_t scale_bytes = round256(sizeof(float) * size_t(n_tensors));
     const size_t flag_bytes = 256;
@@ -707,7 +717,7 @@ lamb_status lamb_plan_create(const lamb_tensor *tensors, int32_t n_tensors,
     const size_t slot_bytes = round256(sizeof(uint64_t) * 6 * size_t(n_tiles));
     const size_t ctl_bytes = 256;
     const size_t rest_bytes = round256(sizeof(TensorDesc) * size_t(n_rest));
-    const size_t rest_chunk_bytes = round256(sizeof(ChunkDesc) * size_t(n_rest_chunks));
+    const size_t rest_chunk_bytes = round256(sizeof(int32_t) * size_t(n_rest_chunks));
     size_t seg_bytes[3], range_bytes[3];
     for (int k = 0; k < 3; ++k) {
         seg_bytes[k] = round256(sizeof(SegDesc) * host_segs[k].size());
@@ -730,9 +740,9 @@ lamb_status lamb_plan_create(const lamb_tensor *tensors, int32_t n_tensors,
     char *base = static_cast<char *>(plan->device_block);
     plan->tensors = reinterpret_cast<TensorDesc *>(base);
     base += tensors_bytes;
-    plan->chunks = reinterpret_cast<ChunkDesc *>(base);
+    plan->chunk_ids = reinterpret_cast<int32_t *>(base);
     base += chunks_bytes;
-    plan->coarse_chunks = reinterpret_cast<ChunkDesc *>(base);
+    plan->coarse_ids = reinterpret_cast<int32_t *>(base);
     base += coarse_bytes;
     plan->partials = reinterpret_cast<Partial *>(base);  // sized for the fine table
     base += partial_bytes;
@@ -748,7 +758,7 @@ lamb_status lamb_plan_create(const lamb_tensor *tensors, int32_t n_tensors,
     base += ctl_bytes;
     plan->rest_tensors = reinterpret_cast<TensorDesc *>(base);
     base += rest_bytes;
-    plan->rest_chunks = reinterpret_cast<ChunkDesc *>(base);
+    plan->rest_ids = reinterpret_cast<int32_t *>(base);
     base += rest_chunk_bytes;
     for (int k = 0; k < 3; ++k) {
         plan->segs[k] = reinterpret_cast<SegDesc *>(base);
@@ -764,11 +774,11 @@ lamb_status lamb_plan_create(const lamb_tensor *tensors, int32_t n_tensors,
     err = hipMemcpy(plan->tensors, host_tensors.data(), sizeof(TensorDesc) * size_t(n_tensors),
                     hipMemcpyHostToDevice);
     if (err == hipSuccess)
-        err = hipMemcpy(plan->chunks, host_chunks.data(), sizeof(ChunkDesc) * size_t(n_chunks),
-                        hipMemcpyHostToDevice);
+        err = hipMemcpy(plan->chunk_ids, ids_of(host_chunks).data(),
+                        sizeof(int32_t) * size_t(n_chunks), hipMemcpyHostToDevice);
     if (err == hipSuccess)
-        err = hipMemcpy(plan->coarse_chunks, host_coarse.data(),
-                        sizeof(ChunkDesc) * size_t(n_coarse), hipMemcpyHostToDevice);
+        err = hipMemcpy(plan->coarse_ids, ids_of(host_coarse).data(),
+                        sizeof(int32_t) * size_t(n_coarse), hipMemcpyHostToDevice);
     if (err == hipSuccess && n_tiles > 0)
         err = hipMemcpy(plan->tiles, host_tiles.data(), sizeof(ChunkDesc) * size_t(n_tiles),
                         hipMemcpyHostToDevice);
@@ -776,8 +786,8 @@ lamb_status lamb_plan_create(const lamb_tensor *tensors, int32_t n_tensors,
         err = hipMemcpy(plan->rest_tensors, host_rest.data(), sizeof(TensorDesc) * size_t(n_rest),
                         hipMemcpyHostToDevice);
     if (err == hipSuccess && n_rest > 0)
-        err = hipMemcpy(plan->rest_chunks, host_rest_chunks.data(),
-                        sizeof(ChunkDesc) * size_t(n_rest_chunks), hipMemcpyHostToDevice);
+        err = hipMemcpy(plan->rest_ids, ids_of(host_rest_chunks).data(),
+                        sizeof(int32_t) * size_t(n_rest_chunks), hipMemcpyHostToDevice);
     for (int k = 0; k < 3 && err == hipSuccess; ++k) {
         if (!host_segs[k].empty())
             err = hipMemcpy(plan->segs[k], host_segs[k].data(),
@@ -838,6 +848,7 @@ lamb_status lamb_plan_create(const lamb_tensor *tensors, int32_t n_tensors,
     for (const Range &r : ranges)
         plan->ranges.emplace_back(r.lo, r.hi);
     plan->chunk_elems = chunk;
+    plan->coarse_elems = coarse;
     *out = plan;
     return LAMB_OK;
 }
@@ -1063,19 +1074,16 @@ lamb_status lamb_step_ex(lamb_plan *plan, const lamb_hparams *hp, void *stream,
         const StepKind &k2 = single ? direct : kind;
         const TensorDesc *tensors = single ? plan->rest_tensors : plan->tensors;
         const int32_t n_tensors = single ? plan->n_rest : plan->n_tensors;
-        const ChunkDesc *chunks = single ? plan->rest_chunks : plan->chunks;
+        const int32_t *chunk_ids = single ? plan->rest_ids : plan->chunk_ids;
         const int32_t n_chunks = single ? plan->n_rest_chunks : plan->n_chunks;
         const uint32_t *guard_ctl = checked ? plan->ctl : nullptr;
         // Deferred moment passes only read, and use the coarse chunk table.
-        const ChunkDesc *moment_chunks = k2.deferred ? plan->coarse_chunks : chunks;
+        const int32_t *moment_ids = k2.deferred ? plan->coarse_ids : chunk_ids;
         const int32_t n_moment_chunks = k2.deferred ? plan->n_coarse : n_chunks;
-        const int64_t coarse_elems =
-            std::min<int64_t>(int64_t(plan->chunk_elems) * kCoarseFactor, kMaxChunkElems);
-        const int32_t moment_threads =
-            two_pass_threads(k2.deferred ? coarse_elems : plan->chunk_elems);
-        hipError_t err = launch_moments(k2, tensors, moment_chunks, plan->partials,
-                                        n_moment_chunks, moment_threads, plan->flags, guard_ctl,
-                                        a, s);
+        const int32_t moment_elems = k2.deferred ? plan->coarse_elems : plan->chunk_elems;
+        hipError_t err = launch_moments(k2, tensors, moment_ids, moment_elems, plan->partials,
+                                        n_moment_chunks, two_pass_threads(moment_elems),
+                                        plan->flags, guard_ctl, a, s);
         if (err != hipSuccess)
             return fail_hip(err, "launching the moment kernel");
         mark(plan, kTimedMoments, s);
@@ -1087,7 +1095,7 @@ lamb_status lamb_step_ex(lamb_plan *plan, const lamb_hparams *hp, void *stream,
         if (err != hipSuccess)
             return fail_hip(err, "launching the finalize kernel");
         mark(plan, kTimedFinalize, s);
-        err = launch_apply(k2, tensors, chunks, plan->scale, n_chunks,
+        err = launch_apply(k2, tensors, chunk_ids, plan->chunk_elems, plan->scale, n_chunks,
                            two_pass_threads(plan->chunk_elems), plan->flags, guard_ctl,
                            k2.deferred ? nonfinite_out : nullptr, a, s);
         if (err != hipSuccess)

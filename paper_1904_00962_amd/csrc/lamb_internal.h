@@ -191,11 +191,14 @@ constexpr int32_t kCheckElems = 16384;
 // flags[0], the apply pass reads flags[1]. Nothing depends on a host counter,
 // so a captured graph replays correctly. `nonfinite_out` may be null.
 // `guard_ctl` non-null (direct mode only): return at once when the verdict
-// word of the epoch in guard_ctl is raised.
+// word of the epoch in guard_ctl is raised. The moment and apply passes take
+// a chunk table as one tensor id per chunk (`chunk_ids`) and its chunk size;
+// the moment pass of deferred mode reads the coarse table (tensors'
+// first_coarse), every other pass a fine one (first_chunk).
 hipError_t launch_moments(const StepKind &kind, const TensorDesc *tensors,
-                          const ChunkDesc *chunks, Partial *partials, int32_t n_chunks,
-                          int32_t threads, uint32_t *flags, const uint32_t *guard_ctl,
-                          const StepArgs &args, hipStream_t stream);
+                          const int32_t *chunk_ids, int32_t chunk_elems, Partial *partials,
+                          int32_t n_chunks, int32_t threads, uint32_t *flags,
+                          const uint32_t *guard_ctl, const StepArgs &args, hipStream_t stream);
 // Both levels of the finalize: `segs` (n_segs entries) over `partials` into
 // `seg_partials`, then per tensor over its `ranges` entry of the segments.
 hipError_t launch_finalize(NormKind norm, const TensorDesc *tensors, int32_t n_tensors,
@@ -204,9 +207,10 @@ hipError_t launch_finalize(NormKind norm, const TensorDesc *tensors, int32_t n_t
                            const FinalizeArgs &args, float *scale, double *ratio_out,
                            double *norms_out, uint32_t *flags, hipStream_t stream);
 hipError_t launch_apply(const StepKind &kind, const TensorDesc *tensors,
-                        const ChunkDesc *chunks, const float *scale, int32_t n_chunks,
-                        int32_t threads, uint32_t *flags, const uint32_t *guard_ctl,
-                        int32_t *nonfinite_out, const StepArgs &args, hipStream_t stream);
+                        const int32_t *chunk_ids, int32_t chunk_elems, const float *scale,
+                        int32_t n_chunks, int32_t threads, uint32_t *flags,
+                        const uint32_t *guard_ctl, int32_t *nonfinite_out, const StepArgs &args,
+                        hipStream_t stream);
 // The finiteness check over `chunks` (all tensors, kCheckElems each).
 hipError_t launch_finite(bool bf16_grad, const TensorDesc *tensors, const ChunkDesc *chunks,
                          int32_t n_chunks, uint32_t *flags, const uint32_t *ctl, float grad_scale,

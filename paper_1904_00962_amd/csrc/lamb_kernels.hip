@@ -353,15 +353,32 @@ __device__ __forceinline__ bool verdict_raised(const uint32_t *flags, const uint
     return ctl && flags[kVerdictWord + (ctl[kCtlEpoch] & 1u)] != 0;
 }
 
+// Chunk k of a table of `chunk`-element chunks whose tensor ids are `ids`:
+// tensor i's chunks are consecutive from `first` (its first_chunk, or its
+// first_coarse in the coarse table), the last one ragged. A 4-byte id per
+// chunk instead of a 16-byte descriptor keeps the table's share of the
+// traffic small: consecutive chunks run on different XCDs, and each XCD's L2
+// fetches every line of the table.
+template <bool kCoarse>
+__device__ __forceinline__ ChunkDesc chunk_at(const TensorDesc *tensors, const int32_t *ids,
+                                              uint32_t k, int32_t chunk) {
+    const int32_t i = ids[k];
+    const TensorDesc &t = tensors[i];
+    const int32_t first = kCoarse ? t.first_coarse : t.first_chunk;
+    const int64_t start = int64_t(int32_t(k) - first) * chunk;
+    const int64_t left = t.numel - start;
+    return ChunkDesc{i, int32_t(left < chunk ? left : chunk), start};
+}
+
 template <int kAlgo, bool kBf16, int kNorm, bool kDeferred>
 __global__ __launch_bounds__(kBlock) void moments_kernel(
-    const TensorDesc *__restrict__ tensors, const ChunkDesc *__restrict__ chunks,
-    Partial *__restrict__ partials, uint32_t *__restrict__ flags, const uint32_t *__restrict__ ctl,
-    StepArgs a) {
+    const TensorDesc *__restrict__ tensors, const int32_t *__restrict__ chunk_ids,
+    int32_t chunk_elems, Partial *__restrict__ partials, uint32_t *__restrict__ flags,
+    const uint32_t *__restrict__ ctl, StepArgs a) {
     constexpr bool kV = kHasSecondMoment<kAlgo>;
     if (!kDeferred && verdict_raised(flags, ctl))
         return;
-    const ChunkDesc c = chunks[chunk_index()];
+    const ChunkDesc c = chunk_at<kDeferred>(tensors, chunk_ids, chunk_index(), chunk_elems);
     const TensorDesc &t = tensors[c.tensor];
     gcfloat *x = global_view(static_cast<const float *>(t.x) + c.start);
     gfloat *m = global_view(t.m + c.start);
@@ -444,9 +461,9 @@ __global__ __launch_bounds__(kBlock) void moments_kernel(
 
 template <int kAlgo, bool kBf16, bool kDeferred>
 __global__ __launch_bounds__(kBlock) void apply_kernel(
-    const TensorDesc *__restrict__ tensors, const ChunkDesc *__restrict__ chunks,
-    const float *__restrict__ scale, uint32_t *__restrict__ flags, const uint32_t *__restrict__ ctl,
-    int32_t *__restrict__ nonfinite_out, StepArgs a) {
+    const TensorDesc *__restrict__ tensors, const int32_t *__restrict__ chunk_ids,
+    int32_t chunk_elems, const float *__restrict__ scale, uint32_t *__restrict__ flags,
+    const uint32_t *__restrict__ ctl, int32_t *__restrict__ nonfinite_out, StepArgs a) {
     constexpr bool kV = kHasSecondMoment<kAlgo>;
     constexpr bool kReadsGrad = kDeferred || kDirectionNeedsGrad<kAlgo>;
     if (!kDeferred && verdict_raised(flags, ctl))
@@ -460,7 +477,7 @@ __global__ __launch_bounds__(kBlock) void apply_kernel(
         if (bad)
             return;
     }
-    const ChunkDesc c = chunks[apply_chunk_index()];
+    const ChunkDesc c = chunk_at<false>(tensors, chunk_ids, apply_chunk_index(), chunk_elems);
     const TensorDesc &t = tensors[c.tensor];
     gfloat *x = global_view(t.x + c.start);
     gfloat *m = global_view(t.m + c.start);
@@ -1123,13 +1140,13 @@ const void *fused_fn(const StepKind &k, int groups) {
 // ---------------------------------------------------------------------------
 
 hipError_t launch_moments(const StepKind &kind, const TensorDesc *tensors,
-                          const ChunkDesc *chunks, Partial *partials, int32_t n_chunks,
-                          int32_t threads, uint32_t *flags, const uint32_t *guard_ctl,
-                          const StepArgs &args, hipStream_t stream) {
+                          const int32_t *chunk_ids, int32_t chunk_elems, Partial *partials,
+                          int32_t n_chunks, int32_t threads, uint32_t *flags,
+                          const uint32_t *guard_ctl, const StepArgs &args, hipStream_t stream) {
     if (threads < 64 || threads > kBlock || threads % 64 != 0)
         return hipErrorInvalidValue;
     StepArgs a = args;
-    void *params[] = {&tensors, &chunks, &partials, &flags, &guard_ctl, &a};
+    void *params[] = {&tensors, &chunk_ids, &chunk_elems, &partials, &flags, &guard_ctl, &a};
     const void *fn;
     switch (kind.algo) {
     case kNLamb: fn = moments_fn<kNLamb>(kind); break;
@@ -1141,13 +1158,15 @@ hipError_t launch_moments(const StepKind &kind, const TensorDesc *tensors,
 }
 
 hipError_t launch_apply(const StepKind &kind, const TensorDesc *tensors,
-                        const ChunkDesc *chunks, const float *scale, int32_t n_chunks,
-                        int32_t threads, uint32_t *flags, const uint32_t *guard_ctl,
-                        int32_t *nonfinite_out, const StepArgs &args, hipStream_t stream) {
+                        const int32_t *chunk_ids, int32_t chunk_elems, const float *scale,
+                        int32_t n_chunks, int32_t threads, uint32_t *flags,
+                        const uint32_t *guard_ctl, int32_t *nonfinite_out, const StepArgs &args,
+                        hipStream_t stream) {
     if (threads < 64 || threads > kBlock || threads % 64 != 0)
         return hipErrorInvalidValue;
     StepArgs a = args;
-    void *params[] = {&tensors, &chunks, &scale, &flags, &guard_ctl, &nonfinite_out, &a};
+    void *params[] = {&tensors,  &chunk_ids,  &chunk_elems,   &scale,
+                      &flags,    &guard_ctl,  &nonfinite_out, &a};
     const void *fn;
     switch (kind.algo) {
     case kNLamb: fn = apply_fn<kNLamb>(kind); break;

@@ -7,9 +7,9 @@
 
 namespace lamb_mi355x {
 
-hipError_t launch_moments(const StepKind &, const TensorDesc *, const ChunkDesc *, Partial *,
-                          int32_t, int32_t, uint32_t *, const uint32_t *, const StepArgs &,
-                          hipStream_t) {
+hipError_t launch_moments(const StepKind &, const TensorDesc *, const int32_t *, int32_t,
+                          Partial *, int32_t, int32_t, uint32_t *, const uint32_t *,
+                          const StepArgs &, hipStream_t) {
     return hipErrorNotSupported;
 }
 
@@ -19,8 +19,8 @@ hipError_t launch_finalize(NormKind, const TensorDesc *, int32_t, const Partial 
     return hipErrorNotSupported;
 }
 
-hipError_t launch_apply(const StepKind &, const TensorDesc *, const ChunkDesc *, const float *,
-                        int32_t, int32_t, uint32_t *, const uint32_t *, int32_t *,
+hipError_t launch_apply(const StepKind &, const TensorDesc *, const int32_t *, int32_t,
+                        const float *, int32_t, int32_t, uint32_t *, const uint32_t *, int32_t *,
                         const StepArgs &, hipStream_t) {
     return hipErrorNotSupported;
 }
