@@ -9,7 +9,8 @@
 // The step needs every per-layer norm ||u_i|| before any x_i may move, so it
 // is two streaming passes over HBM with a tiny reduction between them:
 //
-//   moments  (one workgroup per chunk): read x, g, m (and v); form the new
+//   moments  (one workgroup per chunk, sized to it: one thread per float4 in
+//            whole waves, at most 256): read x, g, m (and v); form the new
 //            moments and the update direction u (m_t for LARS); write the
 //            chunk's partial norms of x and u to a fixed slot; store the new
 //            moments (direct mode) or nothing (deferred mode).
