@@ -23,6 +23,9 @@
  *    stream) and return without synchronising, allocating (beyond one HIP
  *    event per device, created by the first single-pass step) or copying to
  *    the host. Device faults surface at the caller's next synchronisation.
+ *    A step that returns LAMB_EHIP after validation may already have
+ *    enqueued the kernels before the failed launch, so the state of that
+ *    step is then undefined.
  *  - One step may be in flight per plan (its partials buffer is reused);
  *    a plan is not thread-safe. Distinct plans are independent.
  *  - NaN and Inf in the inputs propagate by IEEE rules; nothing is masked.
