@@ -199,10 +199,13 @@ class Pair:
         return self.oracle.lars_step(self.hx, hg, self.hm, [self.wd[i] for i in self.subset],
                                      **f32_scalars(hp))
 
-    def compare(self, ref: np.ndarray, label: str, ratio_tol: float = RATIO_TOL) -> Report:
+    def compare(self, ref: np.ndarray, label: str, ratio_tol: float = RATIO_TOL,
+                ratio_min_numel: int = 1) -> Report:
         """Element-wise state and per-tensor ratio/norm comparison for the subset
         (ratios and norms only when the oracle did not skip the step). First
-        checks that no single-pass wait of the plan was abandoned."""
+        checks that no single-pass wait of the plan was abandoned.
+        ratio_min_numel: compare the trust ratio and ||u|| only for tensors of
+        at least that many elements (||x|| and the state always)."""
         _lib.lamb_plan_check(self.plan, self.torch.cuda.current_stream().cuda_stream)
         self.torch.cuda.synchronize()
         rep = Report()
@@ -219,9 +222,10 @@ class Pair:
         idx = np.asarray(self.subset)
         if np.all(np.isnan(ref)):
             return rep
-        compare_ratios(ratio[idx], ref[:, 0], label + " trust ratio", ratio_tol)
+        big = np.asarray([self.X[i].numel() >= ratio_min_numel for i in self.subset])
+        compare_ratios(ratio[idx][big], ref[big, 0], label + " trust ratio", ratio_tol)
         compare_ratios(norms[idx, 0], ref[:, 1], label + " ||x||", ratio_tol)
-        compare_ratios(norms[idx, 1], ref[:, 2], label + " ||u||", ratio_tol)
+        compare_ratios(norms[idx, 1][big], ref[big, 2], label + " ||u||", ratio_tol)
         return rep
 
     def close(self) -> None:
