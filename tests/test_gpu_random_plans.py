@@ -1,8 +1,8 @@
 """Seeded random plans against the oracle: tensor counts and sizes (many of
 them on chunk, block and tile boundaries), chunk sizes, paths, algorithms,
-gradient dtypes, layer norms, the non-finite skip mode and hyperparameters
-drawn from their documented ranges; two steps each, compared element by
-element with the parity tolerances.
+gradient dtypes, layer norms, the non-finite skip mode, bf16 copies of x and
+hyperparameters drawn from their documented ranges; two steps each, compared
+element by element with the parity tolerances.
 
 The trust ratio and ||u|| are compared only for tensors of at least
 RATIO_MIN_NUMEL elements. With random moments and gradients, one element's
@@ -77,6 +77,14 @@ def test_random_plan(seed):
     wd = [bool(rng.random() < 0.7) for _ in c["sizes"]]
     pair = H.Pair(xs, wd, c["g_dtype"], "lars" if c["algo"] == "lars" else "lamb", c["chunk"],
                   path=c["path"])
+    # bf16 copies of x on some tensors of some plans (their own draws)
+    crng = np.random.default_rng(9000 + seed)
+    copies = [None] * len(xs)
+    if crng.random() < 0.4:
+        copies = [torch.full((n,), 12345, dtype=torch.int16, device="cuda").view(torch.bfloat16)
+                  if crng.random() < 0.7 else None for n in c["sizes"]]
+        _lib.lamb_plan_set_bf16_copies(pair.plan, [b.data_ptr() if b is not None else 0
+                                                   for b in copies])
     try:
         for t in (1, 2):
             gs = []
@@ -88,6 +96,22 @@ def test_random_plan(seed):
             ref = H.step_ex_both(pair, hp, hg)
             pair.compare(ref, "random plan %d step %d" % (seed, t),
                          ratio_min_numel=RATIO_MIN_NUMEL)
+            for i, b in enumerate(copies):
+                if b is None:
+                    continue
+                # torch's cast of the GPU's own x, bit for bit; within one bf16
+                # step of the oracle's rounding of the oracle's x wherever
+                # |x| >= rms/256: there a bf16 step (>= |x| 2^-8) exceeds the
+                # x tolerance of 1e-5 rms, below it the tolerance can exceed it
+                got = b.view(torch.int16).cpu().numpy()
+                assert np.array_equal(got, pair.X[i].to(torch.bfloat16).view(torch.int16)
+                                      .cpu().numpy()), (t, i)
+                hx = pair.hx[i]
+                rms = float(np.sqrt(np.mean(hx.astype(np.float64) ** 2)))
+                far = np.abs(hx) >= rms / 256
+                want = pair.oracle.round_bf16(hx).view(np.int16)
+                diff = np.abs(got.astype(np.int32) - want.astype(np.int32))
+                assert np.all(diff[far] <= 1), (t, i)
     finally:
         pair.close()
 
