@@ -260,9 +260,13 @@ LAMB_API lamb_status lamb_plan_tiles(const lamb_plan *plan, int32_t *tiles_per_t
  * exercise this path; a value that is not a positive integer makes
  * lamb_plan_create fail with LAMB_EINVAL, and values above 2^30 count as
  * 2^30).
- * That step's state is then undefined and the plan's single pass does no
- * further work: restore the state and build a new plan. Synchronises the
- * stream. Errors: LAMB_ENULL, LAMB_EHIP, LAMB_ESYNC.
+ * That step's state is then undefined (tiles that finished reading had
+ * written new moments without moving x), and from then on every kernel of
+ * the plan returns without changing anything, on both paths. To recover,
+ * restore x, m and v from a checkpoint and build a new plan (on
+ * LAMB_PATH_TWO_PASS if the device cannot be given to the single pass
+ * alone). Synchronises the stream. Errors: LAMB_ENULL, LAMB_EHIP,
+ * LAMB_ESYNC.
  */
 LAMB_API lamb_status lamb_plan_check(lamb_plan *plan, void *stream);
 
@@ -346,6 +350,80 @@ LAMB_API lamb_status lars_step(lamb_plan *plan, float lr, float momentum,
                       float weight_decay, float gamma_l, float gamma_u,
                       float trust_coef, void *stream, double *ratio_out,
                       double *norms_out);
+
+/*
+ * Split step, for optimizer state sharded over workers. Section 4.1 trains
+ * with synchronous data parallelism: every worker holds the step's averaged
+ * gradient g_t. When each worker keeps only a slice of every block's x, m
+ * and v, it runs the step on its slices (one plan over them); the layer norms
+ * ||x_i|| and ||u_i|| of Algorithms 1-2 then need every slice, so the step
+ * splits where those norms are formed:
+ *
+ *   lamb_step_partials   the moment pass over every block of the plan (the
+ *                        two-pass kernels, whatever the plan's path): with
+ *                        skip_nonfinite = 0 it writes the new m and v; with
+ *                        skip_nonfinite = 1 it only reads, since whether the
+ *                        step runs is known once every shard has reported.
+ *                        Then each block's partial norms over this plan's
+ *                        elements go to `totals`.
+ *   (the caller combines the totals of all shards, element by element)
+ *   lamb_step_finish     from the combined totals: each block's norms, phi,
+ *                        trust ratio and step scale (as lamb_step_ex), then
+ *                        the apply pass. With skip_nonfinite = 1 it writes x,
+ *                        m and v unless the combined verdict is nonzero, in
+ *                        which case nothing changes.
+ *
+ *   totals   device, 2 * n_tensors + 1 doubles. totals[2 i] and totals[2 i + 1]
+ *            are block i's partial norms of x and of the update direction u
+ *            (m_t for LARS) over this plan's elements, as raw accumulators:
+ *            sums of squares (L2), sums of magnitudes (L1) or maxima of
+ *            magnitudes (L-infinity). totals[2 n] is 1.0 when skip_nonfinite
+ *            is set and any scaled gradient element of this plan is NaN or
+ *            infinite, else 0.0. Combine shards with an element-wise sum (L2,
+ *            L1) or maximum that keeps NaN (L-infinity); either keeps
+ *            totals[2 n] nonzero when any shard saw a non-finite gradient.
+ *            lamb_step_finish only reads it (totals may be the buffer the
+ *            combine wrote in place).
+ *   hp       the same hyperparameters for both halves of one step, and for
+ *            every shard; validated on the host before any HIP call
+ *   ratio_out, norms_out, nonfinite_out   as lamb_step_ex (the combined,
+ *            whole-block values)
+ * Between the two halves the plan runs nothing else. Timing hooks do not
+ * record split steps. Errors: LAMB_ENULL (plan, totals), LAMB_EPLAN,
+ * LAMB_EINVAL, LAMB_EHIP.
+ */
+LAMB_API lamb_status lamb_step_partials(lamb_plan *plan, const lamb_hparams *hp, void *stream,
+                                        double *totals);
+LAMB_API lamb_status lamb_step_finish(lamb_plan *plan, const lamb_hparams *hp, void *stream,
+                                      const double *totals, double *ratio_out,
+                                      double *norms_out, int32_t *nonfinite_out);
+
+/*
+ * Check of the two-pass path's recomputation (Algorithm 2's last line uses
+ * one u for ||u_i|| and for the update; the apply pass recomputes u from the
+ * stored moments instead of storing it). enable = 1 allocates one partial-norm
+ * pair per chunk of the plan: from then on the apply pass of every step that
+ * takes the two-pass kernels without skip_nonfinite (lamb_step_ex on layers
+ * outside the single pass, lamb_step_finish) also sums the norms of the x it
+ * reads and of the u it recomputes, per chunk, in the moment pass's order,
+ * which must give the moment pass's partials bit for bit. enable = 0 frees
+ * the buffer. Do not call while a step runs. Errors: LAMB_ENULL, LAMB_EINVAL,
+ * LAMB_ENOMEM, LAMB_EHIP.
+ */
+LAMB_API lamb_status lamb_plan_set_u_check(lamb_plan *plan, int32_t enable);
+
+/*
+ * Wait for `stream` and copy, for the last step that ran the check, the
+ * moment pass's per-chunk partial norms and the apply pass's re-summed ones
+ * to the host: moment_out and apply_out receive *n_out pairs {x, u} each, in
+ * the order of that step's chunk table (*n_out = 0, and nothing is copied,
+ * when the last step did not run the check). capacity: pairs each array can
+ * hold. Errors: LAMB_ENULL, LAMB_EINVAL (capacity too small; *n_out is still
+ * set), LAMB_EHIP.
+ */
+LAMB_API lamb_status lamb_plan_u_partials(lamb_plan *plan, void *stream, int32_t capacity,
+                                          double *moment_out, double *apply_out,
+                                          int32_t *n_out);
 
 /*
  * The chunk table a plan would use (host only, no HIP call). Tensor i is cut

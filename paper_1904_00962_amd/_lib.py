@@ -56,7 +56,8 @@ EXPORTS = ("lamb_plan_create", "lamb_plan_destroy", "lamb_plan_info",
            "lamb_step_ex", "lamb_step", "nlamb_step", "lars_step", "lamb_lr_at",
            "lamb_sqrt_scaled_lr", "lamb_chunk_table", "lamb_plan_set_timing", "lamb_plan_timing",
            "lamb_plan_set_path", "lamb_plan_tiles", "lamb_plan_check", "lamb_tile_schedule",
-           "lamb_status_str", "lamb_last_error")
+           "lamb_step_partials", "lamb_step_finish", "lamb_plan_set_u_check",
+           "lamb_plan_u_partials", "lamb_status_str", "lamb_last_error")
 
 
 class LambError(RuntimeError):
@@ -125,6 +126,10 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
     lib.lamb_plan_check.argtypes = [vp, vp]
     lib.lamb_tile_schedule.argtypes = [P(i64), i32, i32, i32, i32, P(i32), P(i64), P(i32),
                                        P(i32), P(i32), P(i32), P(i32), P(i32)]
+    lib.lamb_step_partials.argtypes = [vp, P(lamb_hparams), vp, vp]
+    lib.lamb_step_finish.argtypes = [vp, P(lamb_hparams), vp, vp, vp, vp, vp]
+    lib.lamb_plan_set_u_check.argtypes = [vp, i32]
+    lib.lamb_plan_u_partials.argtypes = [vp, vp, i32, vp, vp, P(i32)]
     lib.lamb_status_str.argtypes = [i32]
     lib.lamb_status_str.restype = ctypes.c_char_p
     lib.lamb_last_error.argtypes = []
@@ -356,3 +361,44 @@ def lamb_plan_check(plan: Plan, stream: int = 0) -> None:
     """Synchronise `stream`; raise LambError (LAMB_ESYNC) if a single-pass step
     of the plan abandoned a wait."""
     _check(load().lamb_plan_check(_vp(plan.handle), _vp(stream)), "lamb_plan_check")
+
+
+def lamb_step_partials(plan: Plan, hp: lamb_hparams, stream: int = 0, totals: int = 0) -> None:
+    """First half of a split step: the moment pass over the plan's blocks and
+    each block's partial norms into ``totals`` (device, 2 n + 1 doubles)."""
+    _check(load().lamb_step_partials(_vp(plan.handle), ctypes.byref(hp), _vp(stream),
+                                     _vp(totals)), "lamb_step_partials")
+
+
+def lamb_step_finish(plan: Plan, hp: lamb_hparams, stream: int = 0, totals: int = 0,
+                     ratio_out: int = 0, norms_out: int = 0, nonfinite_out: int = 0) -> None:
+    """Second half of a split step, from the shards' combined ``totals``."""
+    _check(load().lamb_step_finish(_vp(plan.handle), ctypes.byref(hp), _vp(stream), _vp(totals),
+                                   _vp(ratio_out), _vp(norms_out), _vp(nonfinite_out)),
+           "lamb_step_finish")
+
+
+def lamb_plan_set_u_check(plan: Plan, enable: bool) -> None:
+    _check(load().lamb_plan_set_u_check(_vp(plan.handle), int(bool(enable))),
+           "lamb_plan_set_u_check")
+
+
+def lamb_plan_u_partials(plan: Plan, stream: int = 0):
+    """(moment, apply) per-chunk partial norms of the last checked step, each
+    an (n, 2) float64 array of {x, u} pairs (n = 0 when none was checked)."""
+    lib = load()
+    n = ctypes.c_int32()
+    # the count first: capacity 0 fails with LAMB_EINVAL but still sets it
+    status = lib.lamb_plan_u_partials(_vp(plan.handle), _vp(stream), 0, None, None,
+                                      ctypes.byref(n))
+    if status not in (LAMB_OK, LAMB_EINVAL):
+        _check(status, "lamb_plan_u_partials")
+    k = n.value
+    moment = np.zeros((k, 2), np.float64)
+    apply = np.zeros((k, 2), np.float64)
+    if k:
+        _check(lib.lamb_plan_u_partials(_vp(plan.handle), _vp(stream), k,
+                                        ctypes.c_void_p(moment.ctypes.data),
+                                        ctypes.c_void_p(apply.ctypes.data), ctypes.byref(n)),
+               "lamb_plan_u_partials")
+    return moment, apply

@@ -18,7 +18,8 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIBRARY = os.path.join(PKG, "liblamb_mi355x.so")
 SOURCES = [os.path.join(CSRC, "lamb_kernels.hip"), os.path.join(CSRC, "lamb_api.cpp")]
-HEADERS = [os.path.join(INCLUDE, "lamb_mi355x.h"), os.path.join(CSRC, "lamb_internal.h")]
+HEADERS = [os.path.join(INCLUDE, "lamb_mi355x.h"), os.path.join(CSRC, "lamb_internal.h"),
+           os.path.join(CSRC, "lamb_host.h")]
 # Measurement only: streams with the kernels' access patterns (bench.py).
 PROBE_LIBRARY = os.path.join(PKG, "libstream_probe.so")
 PROBE_SOURCES = [os.path.join(CSRC, "stream_probe.hip")]

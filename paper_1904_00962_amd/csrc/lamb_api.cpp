@@ -18,6 +18,7 @@
 #include <utility>
 #include <vector>
 
+#include "lamb_host.h"
 #include "lamb_internal.h"
 
 using namespace lamb_mi355x;
@@ -65,6 +66,10 @@ struct lamb_plan {
     // finiteness check of skip_nonfinite steps that take the single pass
     ChunkDesc *check_chunks = nullptr;
     int32_t n_check = 0;
+    // u-consistency check (lamb_plan_set_u_check): the apply pass's re-summed
+    // partial norms, and the chunk count of the last step that filled them
+    Partial *u_check = nullptr;
+    int32_t u_check_chunks = 0;
     // timing hooks: up to kEvents events per recorded step, in launch order,
     // with the kernel kind of each interval
     std::vector<hipEvent_t> events;
@@ -78,7 +83,7 @@ struct lamb_plan {
     bool timing_this_step = false;
 };
 
-namespace {
+namespace lamb_mi355x {
 
 // Kernel kinds of the timing hooks (the index in lamb_plan_timing's output).
 enum TimedKernel : uint8_t { kTimedMoments = 0, kTimedFinalize = 1, kTimedApply = 2,
@@ -103,8 +108,6 @@ bool aligned16(const void *p) {
     return (reinterpret_cast<uintptr_t>(p) & 15u) == 0;
 }
 
-constexpr int64_t kMaxChunkElems = int64_t(1) << 30;
-constexpr int64_t kMaxNumel = int64_t(1) << 40;  // elements per tensor
 
 // Every size in [1, kMaxNumel]: chunk and tile counts then stay far from
 // int64 overflow.
@@ -260,7 +263,7 @@ void release_events(lamb_plan *plan) {
     plan->timing_seen = 0;
 }
 
-}  // namespace
+}  // namespace lamb_mi355x
 
 extern "C" {
 
@@ -466,7 +469,7 @@ lamb_status lamb_tile_schedule(const int64_t *numel, int32_t n_tensors, int32_t 
 
 }  // extern "C"
 
-namespace {
+namespace lamb_mi355x {
 
 lamb_status build_chunks(const std::vector<int64_t> &numel, int32_t chunk, int32_t n_chunks,
                          std::vector<ChunkDesc> *out) {
@@ -480,6 +483,47 @@ lamb_status build_chunks(const std::vector<int64_t> &numel, int32_t chunk, int32
     out->resize(static_cast<size_t>(n_chunks));
     for (int32_t k = 0; k < n_chunks; ++k)
         (*out)[size_t(k)] = ChunkDesc{ct[size_t(k)], cl[size_t(k)], cs[size_t(k)]};
+    return LAMB_OK;
+}
+
+// Validates a table of blocks (as lamb_plan_create documents) using the
+// caller's room for 4 * n ranges, which it leaves sorted; allocates nothing.
+lamb_status check_table(const lamb_tensor *tensors, int32_t n_tensors, lamb_grad_dtype g_dtype,
+                        bool needs_v, BufferRange *ranges, int32_t *n_ranges) {
+    const size_t g_size = g_dtype == LAMB_GRAD_BF16 ? 2 : 4;
+    int32_t k = 0;
+    for (int32_t i = 0; i < n_tensors; ++i) {
+        const lamb_tensor &t = tensors[i];
+        if (!t.x || !t.g || !t.m || (needs_v && !t.v))
+            return fail(LAMB_ENULL, "tensor %d: x, g, m%s must not be NULL", i,
+                        needs_v ? ", v" : "");
+        if (t.numel < 1 || t.numel > kMaxNumel)
+            return fail(LAMB_EINVAL, "tensor %d: numel %lld, need 1 to 2^40", i,
+                        static_cast<long long>(t.numel));
+        if (t.wd != 0 && t.wd != 1)
+            return fail(LAMB_EINVAL, "tensor %d: wd must be 0 or 1", i);
+        if (t.reserved != 0)
+            return fail(LAMB_EINVAL, "tensor %d: reserved field must be 0", i);
+        if (!aligned16(t.x) || !aligned16(t.g) || !aligned16(t.m) || (needs_v && !aligned16(t.v)))
+            return fail(LAMB_EALIGN, "tensor %d: every buffer must be 16-byte aligned", i);
+        const uintptr_t f32_bytes = uintptr_t(t.numel) * 4u;
+        auto add = [&](const void *p, uintptr_t bytes, const char *what) {
+            const uintptr_t lo = reinterpret_cast<uintptr_t>(p);
+            ranges[k++] = BufferRange{lo, lo + bytes, i, what};
+        };
+        add(t.x, f32_bytes, "x");
+        add(t.g, uintptr_t(t.numel) * g_size, "g");
+        add(t.m, f32_bytes, "m");
+        if (needs_v)
+            add(t.v, f32_bytes, "v");
+    }
+    std::sort(ranges, ranges + k,
+              [](const BufferRange &a, const BufferRange &b) { return a.lo < b.lo; });
+    for (int32_t j = 1; j < k; ++j)
+        if (ranges[j].lo < ranges[j - 1].hi)
+            return fail(LAMB_EOVERLAP, "tensor %d %s overlaps tensor %d %s", ranges[j].tensor,
+                        ranges[j].what, ranges[j - 1].tensor, ranges[j - 1].what);
+    *n_ranges = k;
     return LAMB_OK;
 }
 
@@ -508,7 +552,7 @@ void build_segments(const std::vector<std::pair<int32_t, int32_t>> &tensor_chunk
     }
 }
 
-}  // namespace
+}  // namespace lamb_mi355x
 
 extern "C" {
 
@@ -534,48 +578,15 @@ lamb_status lamb_plan_create(const lamb_tensor *tensors, int32_t n_tensors,
         return st;
 
     const bool needs_v = algo == LAMB_ALGO_LAMB;
-    const size_t g_size = g_dtype == LAMB_GRAD_BF16 ? 2 : 4;
-    struct Range {
-        uintptr_t lo, hi;
-        int32_t tensor;
-        const char *what;
-    };
-    std::vector<Range> ranges;
     std::vector<int64_t> numel(size_t(n_tensors), 0);
-    ranges.reserve(size_t(n_tensors) * 4);
-    for (int32_t i = 0; i < n_tensors; ++i) {
-        const lamb_tensor &t = tensors[i];
-        if (!t.x || !t.g || !t.m || (needs_v && !t.v))
-            return fail(LAMB_ENULL, "tensor %d: x, g, m%s must not be NULL", i,
-                        needs_v ? ", v" : "");
-        st = check_numel(&t.numel, 1);
-        if (st != LAMB_OK)
-            return fail(LAMB_EINVAL, "tensor %d: numel %lld, need 1 to 2^40", i,
-                        static_cast<long long>(t.numel));
-        if (t.wd != 0 && t.wd != 1)
-            return fail(LAMB_EINVAL, "tensor %d: wd must be 0 or 1", i);
-        if (t.reserved != 0)
-            return fail(LAMB_EINVAL, "tensor %d: reserved field must be 0", i);
-        if (!aligned16(t.x) || !aligned16(t.g) || !aligned16(t.m) || (needs_v && !aligned16(t.v)))
-            return fail(LAMB_EALIGN, "tensor %d: every buffer must be 16-byte aligned", i);
-        numel[size_t(i)] = t.numel;
-        const uintptr_t f32_bytes = uintptr_t(t.numel) * 4u;
-        auto add = [&](const void *p, uintptr_t bytes, const char *what) {
-            const uintptr_t lo = reinterpret_cast<uintptr_t>(p);
-            ranges.push_back({lo, lo + bytes, i, what});
-        };
-        add(t.x, f32_bytes, "x");
-        add(t.g, uintptr_t(t.numel) * g_size, "g");
-        add(t.m, f32_bytes, "m");
-        if (needs_v)
-            add(t.v, f32_bytes, "v");
-    }
-    std::sort(ranges.begin(), ranges.end(),
-              [](const Range &a, const Range &b) { return a.lo < b.lo; });
-    for (size_t k = 1; k < ranges.size(); ++k)
-        if (ranges[k].lo < ranges[k - 1].hi)
-            return fail(LAMB_EOVERLAP, "tensor %d %s overlaps tensor %d %s", ranges[k].tensor,
-                        ranges[k].what, ranges[k - 1].tensor, ranges[k - 1].what);
+    std::vector<BufferRange> ranges(size_t(n_tensors) * 4);
+    int32_t n_ranges = 0;
+    st = check_table(tensors, n_tensors, g_dtype, needs_v, ranges.data(), &n_ranges);
+    if (st != LAMB_OK)
+        return st;
+    ranges.resize(size_t(n_ranges));
+    for (int32_t i = 0; i < n_tensors; ++i)
+        numel[size_t(i)] = tensors[i].numel;
 
     const int64_t total = count_chunks(numel.data(), n_tensors, chunk);
     if (total < 0)
@@ -845,7 +856,7 @@ lamb_status lamb_plan_create(const lamb_tensor *tensors, int32_t n_tensors,
     plan->n_rest_chunks = n_rest_chunks;
     plan->host_tensors = std::move(host_tensors);
     plan->host_rest = std::move(host_rest);
-    for (const Range &r : ranges)
+    for (const BufferRange &r : ranges)
         plan->ranges.emplace_back(r.lo, r.hi);
     plan->chunk_elems = chunk;
     plan->coarse_elems = coarse;
@@ -859,6 +870,11 @@ lamb_status lamb_plan_destroy(lamb_plan *plan) {
     DeviceGuard guard(plan->device);
     release_events(plan);
     hipError_t err = hipFree(plan->device_block);
+    if (plan->u_check) {
+        const hipError_t e2 = hipFree(plan->u_check);
+        if (err == hipSuccess)
+            err = e2;
+    }
     delete plan;
     if (err != hipSuccess)
         return fail_hip(err, "hipFree");
@@ -880,22 +896,23 @@ lamb_status lamb_plan_info(const lamb_plan *plan, int32_t *n_tensors, int32_t *n
 
 }  // extern "C"
 
-namespace {
+namespace lamb_mi355x {
 
 bool valid_beta(float beta) { return beta >= 0.0f && beta < 1.0f; }
 
-// Host-side validation of one step's hyperparameters (all before any HIP call).
+// Host-side validation of one step's hyperparameters (all before any HIP
+// call); `plan` may be null (a planless step).
 lamb_status check_hparams(const lamb_plan *plan, const lamb_hparams *hp,
                           const int32_t *nonfinite_out) {
-    if (!plan || !hp)
-        return fail(LAMB_ENULL, "plan and hparams must not be NULL");
+    if (!hp)
+        return fail(LAMB_ENULL, "hparams must not be NULL");
     if (hp->reserved != 0)
         return fail(LAMB_EINVAL, "hparams.reserved must be 0");
     const int32_t variant = hp->variant;
     if (variant < LAMB_VARIANT_LAMB || variant > LAMB_VARIANT_LARS)
         return fail(LAMB_EINVAL, "unknown variant %d", variant);
     const bool lars = variant == LAMB_VARIANT_LARS;
-    if (lars != (plan->algo == LAMB_ALGO_LARS))
+    if (plan && lars != (plan->algo == LAMB_ALGO_LARS))
         return fail(LAMB_EPLAN, "%s needs a plan created for %s", lars ? "LARS" : "the LAMB family",
                     lars ? "LARS" : "LAMB");
     if (hp->norm < LAMB_NORM_L2 || hp->norm > LAMB_NORM_LINF)
@@ -972,7 +989,23 @@ StepArgs step_args(const lamb_hparams &hp) {
     return a;
 }
 
-}  // namespace
+// What a validated step launches.
+StepKind step_kind(const lamb_hparams &hp, lamb_grad_dtype g_dtype) {
+    StepKind kind;
+    kind.algo = static_cast<Algo>(hp.variant);
+    kind.norm = static_cast<NormKind>(hp.norm);
+    kind.bf16_grad = g_dtype == LAMB_GRAD_BF16;
+    kind.deferred = hp.skip_nonfinite != 0;
+    return kind;
+}
+
+FinalizeArgs finalize_args(const lamb_hparams &hp) {
+    const bool lars = hp.variant == LAMB_VARIANT_LARS;
+    return FinalizeArgs{double(hp.lr), double(hp.gamma_l), double(hp.gamma_u),
+                        lars ? double(hp.trust_coef) : 1.0};
+}
+
+}  // namespace lamb_mi355x
 
 extern "C" {
 
@@ -1016,19 +1049,15 @@ lamb_status lamb_hparams_init(lamb_hparams *hp, int32_t variant) {
 
 lamb_status lamb_step_ex(lamb_plan *plan, const lamb_hparams *hp, void *stream,
                          double *ratio_out, double *norms_out, int32_t *nonfinite_out) {
+    if (!plan)
+        return fail(LAMB_ENULL, "plan must not be NULL");
     lamb_status st = check_hparams(plan, hp, nonfinite_out);
     if (st != LAMB_OK)
         return st;
-    StepKind kind;
-    kind.algo = static_cast<Algo>(hp->variant);
-    kind.norm = static_cast<NormKind>(hp->norm);
-    kind.bf16_grad = plan->g_dtype == LAMB_GRAD_BF16;
-    kind.deferred = hp->skip_nonfinite != 0;
+    const StepKind kind = step_kind(*hp, plan->g_dtype);
     StepArgs a = step_args(*hp);
     a.spin_limit = plan->spin_limit;
-    const bool lars = hp->variant == LAMB_VARIANT_LARS;
-    const FinalizeArgs f{double(hp->lr), double(hp->gamma_l), double(hp->gamma_u),
-                         lars ? double(hp->trust_coef) : 1.0};
+    const FinalizeArgs f = finalize_args(*hp);
     // The single pass serves the layers that fit; the two-pass kernels take
     // the rest (or everything on LAMB_PATH_TWO_PASS). A skip_nonfinite step
     // on the single pass first takes its verdict with a read-only check of g,
@@ -1076,14 +1105,13 @@ lamb_status lamb_step_ex(lamb_plan *plan, const lamb_hparams *hp, void *stream,
         const int32_t n_tensors = single ? plan->n_rest : plan->n_tensors;
         const int32_t *chunk_ids = single ? plan->rest_ids : plan->chunk_ids;
         const int32_t n_chunks = single ? plan->n_rest_chunks : plan->n_chunks;
-        const uint32_t *guard_ctl = checked ? plan->ctl : nullptr;
         // Deferred moment passes only read, and use the coarse chunk table.
         const int32_t *moment_ids = k2.deferred ? plan->coarse_ids : chunk_ids;
         const int32_t n_moment_chunks = k2.deferred ? plan->n_coarse : n_chunks;
         const int32_t moment_elems = k2.deferred ? plan->coarse_elems : plan->chunk_elems;
         hipError_t err = launch_moments(k2, tensors, moment_ids, moment_elems, plan->partials,
                                         n_moment_chunks, two_pass_threads(moment_elems),
-                                        plan->flags, guard_ctl, a, s);
+                                        plan->flags, plan->ctl, checked, a, s);
         if (err != hipSuccess)
             return fail_hip(err, "launching the moment kernel");
         mark(plan, kTimedMoments, s);
@@ -1095,12 +1123,16 @@ lamb_status lamb_step_ex(lamb_plan *plan, const lamb_hparams *hp, void *stream,
         if (err != hipSuccess)
             return fail_hip(err, "launching the finalize kernel");
         mark(plan, kTimedFinalize, s);
+        Partial *check = k2.deferred ? nullptr : plan->u_check;
         err = launch_apply(k2, tensors, chunk_ids, plan->chunk_elems, plan->scale, n_chunks,
-                           two_pass_threads(plan->chunk_elems), plan->flags, guard_ctl,
-                           k2.deferred ? nonfinite_out : nullptr, a, s);
+                           two_pass_threads(plan->chunk_elems), plan->flags, plan->ctl, checked,
+                           k2.deferred ? nonfinite_out : nullptr, check, a, s);
         if (err != hipSuccess)
             return fail_hip(err, "launching the apply kernel");
         mark(plan, kTimedApply, s);
+        plan->u_check_chunks = check ? n_chunks : 0;
+    } else {
+        plan->u_check_chunks = 0;
     }
     if (checked) {
         hipError_t err = gated_fused_launch(plan->device, s, direct, plan, grid, true,
@@ -1347,6 +1379,125 @@ lamb_status lamb_plan_timing(lamb_plan *plan, double *kernel_ms, int64_t *steps)
     }
     *steps = plan->timing_used;
     plan->timing_used = 0;
+    return LAMB_OK;
+}
+
+lamb_status lamb_step_partials(lamb_plan *plan, const lamb_hparams *hp, void *stream,
+                               double *totals) {
+    if (!plan || !totals)
+        return fail(LAMB_ENULL, "plan and totals must not be NULL");
+    lamb_status st = check_hparams(plan, hp, nullptr);
+    if (st != LAMB_OK)
+        return st;
+    const StepKind kind = step_kind(*hp, plan->g_dtype);
+    StepArgs a = step_args(*hp);
+    a.spin_limit = plan->spin_limit;
+    DeviceGuard guard(plan->device);
+    if (guard.status != hipSuccess)
+        return fail_hip(guard.status, "selecting the plan's device");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    // Every layer takes the moment pass: a deferred one (read only, coarse
+    // chunks) when the step may be skipped, since the verdict is only known
+    // once the shards' totals are combined.
+    const int32_t *ids = kind.deferred ? plan->coarse_ids : plan->chunk_ids;
+    const int32_t n = kind.deferred ? plan->n_coarse : plan->n_chunks;
+    const int32_t elems = kind.deferred ? plan->coarse_elems : plan->chunk_elems;
+    hipError_t err = launch_moments(kind, plan->tensors, ids, elems, plan->partials, n,
+                                    two_pass_threads(elems), plan->flags, plan->ctl, false, a, s);
+    if (err != hipSuccess)
+        return fail_hip(err, "launching the moment kernel");
+    const int seg = kind.deferred ? kSegCoarse : kSegFine;
+    err = launch_totals(kind.norm, plan->partials, plan->segs[seg], plan->n_segs[seg],
+                        plan->seg_ranges[seg], plan->n_tensors, plan->seg_partials, totals,
+                        plan->flags, kind.deferred, s);
+    if (err != hipSuccess)
+        return fail_hip(err, "launching the totals kernel");
+    plan->u_check_chunks = 0;
+    return LAMB_OK;
+}
+
+lamb_status lamb_step_finish(lamb_plan *plan, const lamb_hparams *hp, void *stream,
+                             const double *totals, double *ratio_out, double *norms_out,
+                             int32_t *nonfinite_out) {
+    if (!plan || !totals)
+        return fail(LAMB_ENULL, "plan and totals must not be NULL");
+    lamb_status st = check_hparams(plan, hp, nonfinite_out);
+    if (st != LAMB_OK)
+        return st;
+    const StepKind kind = step_kind(*hp, plan->g_dtype);
+    StepArgs a = step_args(*hp);
+    a.spin_limit = plan->spin_limit;
+    const FinalizeArgs f = finalize_args(*hp);
+    DeviceGuard guard(plan->device);
+    if (guard.status != hipSuccess)
+        return fail_hip(guard.status, "selecting the plan's device");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipError_t err = launch_scale(kind.norm, totals, plan->n_tensors, f, plan->scale, ratio_out,
+                                  norms_out, plan->flags, s);
+    if (err != hipSuccess)
+        return fail_hip(err, "launching the scale kernel");
+    Partial *check = kind.deferred ? nullptr : plan->u_check;
+    err = launch_apply(kind, plan->tensors, plan->chunk_ids, plan->chunk_elems, plan->scale,
+                       plan->n_chunks, two_pass_threads(plan->chunk_elems), plan->flags,
+                       plan->ctl, false, kind.deferred ? nonfinite_out : nullptr, check, a, s);
+    if (err != hipSuccess)
+        return fail_hip(err, "launching the apply kernel");
+    plan->u_check_chunks = check ? plan->n_chunks : 0;
+    return LAMB_OK;
+}
+
+lamb_status lamb_plan_set_u_check(lamb_plan *plan, int32_t enable) {
+    if (!plan)
+        return fail(LAMB_ENULL, "plan must not be NULL");
+    if (enable != 0 && enable != 1)
+        return fail(LAMB_EINVAL, "enable must be 0 or 1");
+    DeviceGuard guard(plan->device);
+    if (guard.status != hipSuccess)
+        return fail_hip(guard.status, "selecting the plan's device");
+    if (!enable) {
+        hipError_t err = plan->u_check ? hipFree(plan->u_check) : hipSuccess;
+        plan->u_check = nullptr;
+        plan->u_check_chunks = 0;
+        if (err != hipSuccess)
+            return fail_hip(err, "hipFree");
+        return LAMB_OK;
+    }
+    if (plan->u_check)
+        return LAMB_OK;
+    void *p = nullptr;
+    hipError_t err = hipMalloc(&p, sizeof(Partial) * size_t(plan->n_chunks));
+    if (err != hipSuccess)
+        return err == hipErrorOutOfMemory ? fail(LAMB_ENOMEM, "hipMalloc of the check buffer")
+                                          : fail_hip(err, "hipMalloc");
+    plan->u_check = static_cast<Partial *>(p);
+    plan->u_check_chunks = 0;
+    return LAMB_OK;
+}
+
+lamb_status lamb_plan_u_partials(lamb_plan *plan, void *stream, int32_t capacity,
+                                 double *moment_out, double *apply_out, int32_t *n_out) {
+    if (!plan || !n_out)
+        return fail(LAMB_ENULL, "plan and n_out must not be NULL");
+    const int32_t n = plan->u_check ? plan->u_check_chunks : 0;
+    *n_out = n;
+    if (n == 0)
+        return LAMB_OK;
+    if (capacity < n)
+        return fail(LAMB_EINVAL, "capacity %d < %d chunks", capacity, n);
+    if (!moment_out || !apply_out)
+        return fail(LAMB_ENULL, "moment_out and apply_out must not be NULL");
+    DeviceGuard guard(plan->device);
+    if (guard.status != hipSuccess)
+        return fail_hip(guard.status, "selecting the plan's device");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const size_t bytes = sizeof(Partial) * size_t(n);
+    hipError_t err = hipMemcpyAsync(moment_out, plan->partials, bytes, hipMemcpyDeviceToHost, s);
+    if (err == hipSuccess)
+        err = hipMemcpyAsync(apply_out, plan->u_check, bytes, hipMemcpyDeviceToHost, s);
+    if (err == hipSuccess)
+        err = hipStreamSynchronize(s);
+    if (err != hipSuccess)
+        return fail_hip(err, "copying the partial norms");
     return LAMB_OK;
 }
 

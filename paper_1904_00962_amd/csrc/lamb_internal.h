@@ -11,28 +11,16 @@ namespace lamb_mi355x {
 // Work is cut into chunks of at most `chunk_elems` elements of one tensor;
 // one workgroup of two_pass_threads(chunk_elems) threads (at most kBlock)
 // handles one chunk.
-#ifndef LAMB_BLOCK
-#define LAMB_BLOCK 256
-#endif
-#ifndef LAMB_DEFAULT_CHUNK
-#define LAMB_DEFAULT_CHUNK 256
-#endif
-constexpr int kBlock = LAMB_BLOCK;
+constexpr int kBlock = 256;
 constexpr int kWaves = kBlock / 64;
-constexpr int32_t kDefaultChunkElems = LAMB_DEFAULT_CHUNK;
+constexpr int32_t kDefaultChunkElems = 256;
 
 // Threads per workgroup of the moment and apply passes over chunks of `chunk`
-// elements: LAMB_TWO_PASS_F4 float4 groups per thread, whole waves, at least
-// one wave and at most kBlock threads (0: always kBlock). A default chunk is
-// one wave's float4 each: no thread of the workgroup idles.
-#ifndef LAMB_TWO_PASS_F4
-#define LAMB_TWO_PASS_F4 1
-#endif
+// elements: one float4 group per thread, whole waves, at least one wave and
+// at most kBlock threads. A default chunk is one wave's float4 each: no thread
+// of the workgroup idles.
 constexpr int32_t two_pass_threads(int64_t chunk) {
-    if (LAMB_TWO_PASS_F4 == 0)
-        return kBlock;
-    const int64_t groups = (chunk + 3) / 4;
-    const int64_t threads = (groups + LAMB_TWO_PASS_F4 - 1) / LAMB_TWO_PASS_F4;
+    const int64_t threads = (chunk + 3) / 4;
     const int64_t waves = (threads + 63) / 64;
     return int32_t(waves < 1 ? 64 : waves * 64 > kBlock ? kBlock : waves * 64);
 }
@@ -52,22 +40,13 @@ constexpr int32_t kCoarseFactor = 8;
 // every CU, so a layer of up to kFusedBlocksPerCu * (compute units) tiles can
 // have every tile resident at once. A plan uses kTileGroups, or kWideGroups
 // when the wider tile puts more parameters on the single pass.
-#ifndef LAMB_TILE_GROUPS
-#define LAMB_TILE_GROUPS 8
-#endif
-#ifndef LAMB_WIDE_GROUPS
-#define LAMB_WIDE_GROUPS 10
-#endif
-#ifndef LAMB_FUSED_WAVES
-#define LAMB_FUSED_WAVES 4
-#endif
-constexpr int kTileGroups = LAMB_TILE_GROUPS;
-constexpr int kWideGroups = LAMB_WIDE_GROUPS;
+constexpr int kTileGroups = 8;
+constexpr int kWideGroups = 10;
 constexpr int kLdsGroups = kTileGroups;
 static_assert(kWideGroups > kTileGroups, "the wide tile is the larger one");
 constexpr int32_t kBlockElems = kBlock * 4;  // one float4 per thread
 constexpr int64_t tile_elems(int groups) { return int64_t(groups) * kBlockElems; }
-constexpr int kFusedWaves = LAMB_FUSED_WAVES;
+constexpr int kFusedWaves = 4;  // waves per SIMD
 constexpr int kFusedBlocksPerCu = kFusedWaves * 4 / kWaves;  // 4 SIMDs per CU
 // Polls before a single-pass wait gives up (about a second); a plan reads an
 // override from the environment variable LAMB_MI355X_SPIN_LIMIT.
@@ -195,10 +174,16 @@ constexpr int32_t kCheckElems = 16384;
 // a chunk table as one tensor id per chunk (`chunk_ids`) and its chunk size;
 // the moment pass of deferred mode reads the coarse table (tensors'
 // first_coarse), every other pass a fine one (first_chunk).
+// `ctl` is the plan's FusedCtl words: every pass returns at once while the
+// sticky fault word is raised, so that after a single-pass give-up no layer
+// moves. `guarded` (direct mode only): also return when the verdict word of
+// the epoch in ctl is raised (a skip_nonfinite step whose verdict the
+// finiteness check took).
 hipError_t launch_moments(const StepKind &kind, const TensorDesc *tensors,
                           const int32_t *chunk_ids, int32_t chunk_elems, Partial *partials,
                           int32_t n_chunks, int32_t threads, uint32_t *flags,
-                          const uint32_t *guard_ctl, const StepArgs &args, hipStream_t stream);
+                          const uint32_t *ctl, bool guarded, const StepArgs &args,
+                          hipStream_t stream);
 // Both levels of the finalize: `segs` (n_segs entries) over `partials` into
 // `seg_partials`, then per tensor over its `ranges` entry of the segments.
 hipError_t launch_finalize(NormKind norm, const TensorDesc *tensors, int32_t n_tensors,
@@ -206,11 +191,27 @@ hipError_t launch_finalize(NormKind norm, const TensorDesc *tensors, int32_t n_t
                            const SegRange *ranges, Partial *seg_partials,
                            const FinalizeArgs &args, float *scale, double *ratio_out,
                            double *norms_out, uint32_t *flags, hipStream_t stream);
+// `check` non-null (direct mode only): also re-sum the partial norms of every
+// chunk from the x read and the u recomputed, into check[chunk].
 hipError_t launch_apply(const StepKind &kind, const TensorDesc *tensors,
                         const int32_t *chunk_ids, int32_t chunk_elems, const float *scale,
-                        int32_t n_chunks, int32_t threads, uint32_t *flags,
-                        const uint32_t *guard_ctl, int32_t *nonfinite_out, const StepArgs &args,
-                        hipStream_t stream);
+                        int32_t n_chunks, int32_t threads, uint32_t *flags, const uint32_t *ctl,
+                        bool guarded, int32_t *nonfinite_out, Partial *check,
+                        const StepArgs &args, hipStream_t stream);
+// Split step, first half: the segment level over `partials`, then per tensor
+// its combined partial norms into totals[2 i], totals[2 i + 1], and the
+// deferred moment pass's verdict (flags[0], then cleared) into totals[2 n]
+// (0 in direct mode).
+hipError_t launch_totals(NormKind norm, const Partial *partials, const SegDesc *segs,
+                         int32_t n_segs, const SegRange *ranges, int32_t n_tensors,
+                         Partial *seg_partials, double *totals, uint32_t *flags, bool deferred,
+                         hipStream_t stream);
+// Split step, second half: per tensor the norms, phi, ratio and scale from
+// combined totals; flags[1] receives the combined verdict for a deferred
+// apply pass.
+hipError_t launch_scale(NormKind norm, const double *totals, int32_t n_tensors,
+                        const FinalizeArgs &args, float *scale, double *ratio_out,
+                        double *norms_out, uint32_t *flags, hipStream_t stream);
 // The finiteness check over `chunks` (all tensors, kCheckElems each).
 hipError_t launch_finite(bool bf16_grad, const TensorDesc *tensors, const ChunkDesc *chunks,
                          int32_t n_chunks, uint32_t *flags, const uint32_t *ctl, float grad_scale,

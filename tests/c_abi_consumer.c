@@ -156,6 +156,14 @@ static void rejected_calls(void) {
     CHECK(lamb_hparams_init(&hp, LAMB_VARIANT_LAMB) == LAMB_OK);
     CHECK(lamb_step_ex(NULL, &hp, NULL, NULL, NULL, NULL) == LAMB_ENULL);
     CHECK(lamb_plan_check(NULL, NULL) == LAMB_ENULL);
+    {
+        double totals[3] = {0.0, 0.0, 0.0};
+        int32_t n = -1;
+        CHECK(lamb_step_partials(NULL, &hp, NULL, totals) == LAMB_ENULL);
+        CHECK(lamb_step_finish(NULL, &hp, NULL, totals, NULL, NULL, NULL) == LAMB_ENULL);
+        CHECK(lamb_plan_set_u_check(NULL, 1) == LAMB_ENULL);
+        CHECK(lamb_plan_u_partials(NULL, NULL, 0, NULL, NULL, &n) == LAMB_ENULL);
+    }
 }
 
 int main(void) {

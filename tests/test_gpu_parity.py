@@ -3,8 +3,8 @@
 Every step of every run is compared element by element (x, m, v) and per
 tensor (trust ratio, ||x||, ||u||) under the rule in ``gpu_harness``. The
 BERT-Large run uses the default chunk size, i.e. the launch configuration
-the benchmark times. The 1.5B set compares a sample of whole tensors with
-the oracle and checks a size-independent property on every tensor.
+the benchmark times. Every tensor of every set is compared, the 1.5B set one
+tensor at a time.
 """
 
 import numpy as np
@@ -74,42 +74,54 @@ def test_resnet50_nesterov_variants(algo):
 
 
 def test_bert_large_lars_bf16_grad():
-    ps = paramsets.get(2)
-    H.run_config(2, 2, "lars", oracle_subset=[0, 3, 4, 5, 6, ps.n_tensors - 1])
+    """All 391 tensors, two steps."""
+    H.run_config(2, 2, "lars")
 
 
-def test_gpt_1p5b_lamb_sampled():
-    """1.56e9 parameters: one step; whole-tensor parity on a sample (the 80M
-    token embedding, the first layer, the final norm), and on every tensor
-    the Section 3 identity ||x_{t+1} - x_t|| = eta * phi(||x_t||). The plan
-    takes 10240-element tiles, which put the 10.24M-element FFN layers on
-    the single pass."""
+def test_gpt_1p5b_lamb_every_tensor():
+    """1.56e9 parameters, one step, every one of the 580 tensors compared with
+    the oracle element by element (x, m, v) and per tensor (trust ratio,
+    ||x||, ||u||), one tensor at a time so that host memory stays bounded.
+    The plan takes 10240-element tiles, which put the 10.24M-element FFN
+    layers on the single pass; the 80M-element token embedding takes the
+    two-pass kernels."""
     torch = H.torch_cuda()
+    import oracle
     ps = paramsets.get(4)
-    sample = [0, 1, 2, 3, 4, 5, 6, 7, 8, 9, 10, 11, 12, 13, ps.n_tensors - 2, ps.n_tensors - 1]
-    H.log("parity cfg=4 sampled tensors %s" % sample)
+    H.log("parity cfg=4 (1.5B) every tensor, one step")
     pair = H.Pair(paramsets.draw_params(ps, device="cuda"), ps.wd_mask(), ps.g_dtype, "lamb",
-                  oracle_subset=sample)
+                  oracle_subset=[])
     try:
         per, _, groups = _lib.lamb_plan_tiles(pair.plan)
         assert groups == 10
         assert [i for i, k in enumerate(per) if k == 0] == [0]  # the token embedding only
         hp = H.lamb_hp(ps)
         x_old = [x.clone() for x in pair.X]
-        hg = pair.set_grads(paramsets.draw_grads(ps, 1, device="cuda"))
+        pair.set_grads(paramsets.draw_grads(ps, 1, device="cuda"))
         pair.gpu_lamb(hp, 1)
-        ref = pair.oracle_lamb(hg, hp, 1)
-        pair.compare(ref, "cfg4 step 1")
+        _lib.lamb_plan_check(pair.plan)
         torch.cuda.synchronize()
-        lr = float(np.float32(hp["lr"]))
-        worst = 0.0
+        ratio = pair.ratio.cpu().numpy()
+        norms = pair.norms.cpu().numpy().reshape(-1, 2)
+        o = oracle.load()
+        sc = H.f32_scalars(hp)
+        rep = H.Report()
+        worst_ratio = 0.0
         for i in range(ps.n_tensors):
-            xo = x_old[i].double()
-            length = float(torch.linalg.vector_norm(pair.X[i].double() - xo))
-            phi = min(max(float(torch.linalg.vector_norm(xo)), hp["gamma_l"]), hp["gamma_u"])
-            rel = abs(length - lr * phi) / (lr * phi)
-            worst = max(worst, rel)
-            assert rel < 1e-4, "tensor %d: step length %.9e vs eta*phi %.9e" % (i, length, lr * phi)
-        H.log("  step-length identity over all %d tensors: worst rel %.2e" % (ps.n_tensors, worst))
+            hx = paramsets.host_array(x_old[i]).copy()
+            x_old[i] = None  # free the device copy as the walk proceeds
+            hg = paramsets.host_array(pair.G[i]).copy()
+            hm = np.zeros_like(hx)
+            hv = np.zeros_like(hx)
+            ref = o.lamb_step([hx], [hg], [hm], [hv], [pair.wd[i]], step=1, **sc)
+            rep.merge(H.compare_state_device(pair.X[i], hx, "cfg4 x[%d]" % i))
+            rep.merge(H.compare_state_device(pair.M[i], hm, "cfg4 m[%d]" % i))
+            rep.merge(H.compare_state_device(pair.V[i], hv, "cfg4 v[%d]" % i))
+            worst_ratio = max(worst_ratio,
+                              H.compare_ratios(ratio[i:i + 1], ref[:, 0], "cfg4 ratio[%d]" % i),
+                              H.compare_ratios(norms[i:i + 1, 0], ref[:, 1], "cfg4 ||x||[%d]" % i),
+                              H.compare_ratios(norms[i:i + 1, 1], ref[:, 2], "cfg4 ||u||[%d]" % i))
+        H.log("  all %d tensors: max err %.3e, max abs %.3e, worst ratio/norm rel %.3e"
+              % (ps.n_tensors, rep.max_err, rep.max_abs, worst_ratio))
     finally:
         pair.close()

@@ -43,11 +43,14 @@ def test_every_kernel_variant_was_found(kernels):
     names = list(kernels)
     # 4 algorithms x 2 gradient dtypes x 3 norms, in both tile shapes
     assert sum("fused_kernel" in n for n in names) == 48
+    # 4 algorithms x 2 gradient dtypes x (direct, deferred) x 3 norms
     assert sum("moments_kernel" in n for n in names) == 48
-    assert sum("apply_kernel" in n for n in names) == 16
-    assert any("segment_kernel" in n for n in names)
-    assert any("finalize_kernel" in n for n in names)
-    assert any("finite_kernel" in n for n in names)
+    # 4 algorithms x 2 gradient dtypes x (deferred, direct, direct with the
+    # u re-sum in 3 norms)
+    assert sum("apply_kernel" in n for n in names) == 40
+    for kind in ("segment_kernel", "finalize_kernel", "totals_kernel", "scale_kernel"):
+        assert sum(kind in n for n in names) == 3, kind
+    assert sum("finite_kernel" in n for n in names) == 2
 
 
 def test_no_kernel_spills(kernels):
