@@ -426,6 +426,38 @@ LAMB_API lamb_status lamb_plan_u_partials(lamb_plan *plan, void *stream, int32_t
                                           int32_t *n_out);
 
 /*
+ * For callers that cannot allocate (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc): lamb_step_ex over a table
+ * of blocks without a plan. It runs the two-pass kernels (exactly those of a
+ * plan on LAMB_PATH_TWO_PASS with the same chunk_elems, with the same results
+ * bit for bit) and keeps their tables, per-chunk partial norms, scales and
+ * flags in a fixed device array of the library: 10.8 MiB, one per device,
+ * held from the library's load on that device until the process ends. A call
+ * allocates no device or host memory and copies nothing from the host: the
+ * tensor table reaches the device as kernel arguments of ceil(n_tensors / 48)
+ * small table kernels, which also clear the array's flag words.
+ *   tensors       host array of n_tensors blocks, as lamb_plan_create (v may
+ *                 be NULL for LARS); validated on every call
+ *   g_dtype       lamb_grad_dtype
+ *   chunk_elems   0 (the default) or as lamb_plan_create
+ *   hp, stream, ratio_out, norms_out, nonfinite_out   as lamb_step_ex (a
+ *                 LARS step is hp->variant = LAMB_VARIANT_LARS; hp selects
+ *                 the algorithm, there being no plan)
+ * Limits: n_tensors <= 4096, and at most 2^19 chunks of chunk_elems elements
+ * over the table (the sum of ceil(numel / chunk_elems)); a larger table fails
+ * with LAMB_EINVAL before any HIP call (a larger chunk_elems fits more).
+ * Every call on one device shares that device's array, which keeps the last
+ * call's contents: calls that overlap in time on one device (on different
+ * streams or host threads) race and give undefined results; calls ordered
+ * on one stream are safe. Runs on the current device.
+ * Errors: as lamb_plan_create and lamb_step_ex (LAMB_EPLAN does not occur).
+ */
+LAMB_API lamb_status lamb_step_static(const lamb_tensor *tensors, int32_t n_tensors,
+                                      int32_t g_dtype, int32_t chunk_elems,
+                                      const lamb_hparams *hp, void *stream, double *ratio_out,
+                                      double *norms_out, int32_t *nonfinite_out);
+
+/*
  * The chunk table a plan would use (host only, no HIP call). Tensor i is cut
  * into ceil(numel[i] / chunk_elems) chunks in table order; chunk k of it
  * starts at k * chunk_elems and holds min(chunk_elems, numel[i] - start)

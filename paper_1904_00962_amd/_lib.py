@@ -57,7 +57,7 @@ EXPORTS = ("lamb_plan_create", "lamb_plan_destroy", "lamb_plan_info",
            "lamb_sqrt_scaled_lr", "lamb_chunk_table", "lamb_plan_set_timing", "lamb_plan_timing",
            "lamb_plan_set_path", "lamb_plan_tiles", "lamb_plan_check", "lamb_tile_schedule",
            "lamb_step_partials", "lamb_step_finish", "lamb_plan_set_u_check",
-           "lamb_plan_u_partials", "lamb_status_str", "lamb_last_error")
+           "lamb_plan_u_partials", "lamb_step_static", "lamb_status_str", "lamb_last_error")
 
 
 class LambError(RuntimeError):
@@ -130,6 +130,8 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
     lib.lamb_step_finish.argtypes = [vp, P(lamb_hparams), vp, vp, vp, vp, vp]
     lib.lamb_plan_set_u_check.argtypes = [vp, i32]
     lib.lamb_plan_u_partials.argtypes = [vp, vp, i32, vp, vp, P(i32)]
+    lib.lamb_step_static.argtypes = [P(lamb_tensor), i32, i32, i32, P(lamb_hparams), vp, vp, vp,
+                                     vp]
     lib.lamb_status_str.argtypes = [i32]
     lib.lamb_status_str.restype = ctypes.c_char_p
     lib.lamb_last_error.argtypes = []
@@ -402,3 +404,19 @@ def lamb_plan_u_partials(plan: Plan, stream: int = 0):
                                         ctypes.c_void_p(apply.ctypes.data), ctypes.byref(n)),
                "lamb_plan_u_partials")
     return moment, apply
+
+
+def lamb_step_static(tensors: Sequence[Tuple[int, int, int, int, int, int]], g_dtype: int,
+                     hp: lamb_hparams, chunk_elems: int = 0, stream: int = 0, ratio_out: int = 0,
+                     norms_out: int = 0, nonfinite_out: int = 0) -> None:
+    """A step without a plan (the library's fixed device array holds its
+    tables): tensors as for lamb_plan_create, (x, g, m, v, numel, wd) device
+    pointers per block."""
+    n = len(tensors)
+    arr = (lamb_tensor * max(n, 1))()
+    for i, (x, g, m, v, numel, wd) in enumerate(tensors):
+        arr[i] = lamb_tensor(int(x) or None, int(g) or None, int(m) or None,
+                             int(v) if v else None, int(numel), int(wd), 0)
+    _check(load().lamb_step_static(arr, n, int(g_dtype), int(chunk_elems), ctypes.byref(hp),
+                                   _vp(stream), _vp(ratio_out), _vp(norms_out),
+                                   _vp(nonfinite_out)), "lamb_step_static")

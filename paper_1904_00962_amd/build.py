@@ -17,7 +17,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIBRARY = os.path.join(PKG, "liblamb_mi355x.so")
-SOURCES = [os.path.join(CSRC, "lamb_kernels.hip"), os.path.join(CSRC, "lamb_api.cpp")]
+SOURCES = [os.path.join(CSRC, "lamb_kernels.hip"), os.path.join(CSRC, "lamb_static.hip"),
+           os.path.join(CSRC, "lamb_api.cpp")]
 HEADERS = [os.path.join(INCLUDE, "lamb_mi355x.h"), os.path.join(CSRC, "lamb_internal.h"),
            os.path.join(CSRC, "lamb_host.h")]
 # Measurement only: streams with the kernels' access patterns (bench.py).

@@ -191,3 +191,30 @@ def test_stream_probe_library_validates_on_the_host():
     ]
     for args in bad:
         assert probe.stream_probe(*args, None) == -1, args
+
+
+def test_static_step_validation_before_any_hip_call(lib):
+    """lamb_step_static rejects bad tables and hyperparameters on the host
+    (these fail before it looks up its device array)."""
+    hp = _lib.lamb_hparams_init("lamb")
+    ok = (4096, 8192, 12288, 16384, 256, 1)  # fake, aligned, disjoint addresses
+    cases = [
+        ([], _lib.LAMB_GRAD_F32, 0, _lib.LAMB_EINVAL),                    # no tensors
+        ([ok] * 4097, _lib.LAMB_GRAD_F32, 0, _lib.LAMB_EINVAL),           # over 4096
+        ([ok], 5, 0, _lib.LAMB_EINVAL),                                   # gradient dtype
+        ([ok], _lib.LAMB_GRAD_F32, 12, _lib.LAMB_EINVAL),                 # chunk size
+        ([(0, 8192, 12288, 16384, 256, 1)], _lib.LAMB_GRAD_F32, 0, _lib.LAMB_ENULL),
+        ([(4100, 8192, 12288, 16384, 256, 1)], _lib.LAMB_GRAD_F32, 0, _lib.LAMB_EALIGN),
+        ([(4096, 4608, 12288, 16384, 256, 1)], _lib.LAMB_GRAD_F32, 0, _lib.LAMB_EOVERLAP),
+        # 2^22 elements in chunks of 8: 524,288 chunks fit, one element more does not
+        ([(1 << 30, 1 << 31, 3 << 30, 1 << 32, (1 << 22) + 1, 1)], _lib.LAMB_GRAD_F32, 8,
+         _lib.LAMB_EINVAL),
+    ]
+    for rows, g_dtype, chunk, status in cases:
+        with pytest.raises(_lib.LambError) as e:
+            _lib.lamb_step_static(rows, g_dtype, hp, chunk)
+        assert e.value.status == status, (rows[:1], g_dtype, chunk, _lib.last_error())
+    bad = _lib.lamb_hparams_init("lamb", beta1=1.5)
+    with pytest.raises(_lib.LambError) as e:
+        _lib.lamb_step_static([ok], _lib.LAMB_GRAD_F32, bad, 0)
+    assert e.value.status == _lib.LAMB_EINVAL

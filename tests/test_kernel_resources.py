@@ -1,5 +1,5 @@
 """The kernels' resource use, read from the gfx950 assembly hipcc writes for
-lamb_kernels.hip (on the CPU; no GPU involved): no kernel spills to scratch,
+lamb_kernels.hip and lamb_static.hip (on the CPU; no GPU involved): no kernel spills to scratch,
 and every single-pass variant fits the four workgroups per CU that its
 persistent grid needs resident (at most 128 VGPRs at four waves per SIMD, and
 LDS for four workgroups within the CU's 160 KB)."""
@@ -12,19 +12,22 @@ import pytest
 
 from paper_1904_00962_amd import build
 
-KERNELS = os.path.join(build.CSRC, "lamb_kernels.hip")
+KERNEL_SOURCES = [os.path.join(build.CSRC, name)
+                  for name in ("lamb_kernels.hip", "lamb_static.hip")]
 LDS_PER_CU = 160 * 1024
 
 
 @pytest.fixture(scope="module")
 def kernels(tmp_path_factory):
-    out = tmp_path_factory.mktemp("isa") / "lamb_kernels.s"
     flags = [f for f in build.HIPCC_FLAGS if f not in ("-shared", "-fPIC")]
-    r = subprocess.run([build.hipcc(), *flags, "-I", build.INCLUDE, "-I", build.CSRC,
-                        "--cuda-device-only", "-S", KERNELS, "-o", str(out)],
-                       capture_output=True, text=True, timeout=600)
-    assert r.returncode == 0, r.stderr[-2000:]
-    text = out.read_text()
+    text = ""
+    for src in KERNEL_SOURCES:
+        out = tmp_path_factory.mktemp("isa") / (os.path.basename(src) + ".s")
+        r = subprocess.run([build.hipcc(), *flags, "-I", build.INCLUDE, "-I", build.CSRC,
+                            "--cuda-device-only", "-S", src, "-o", str(out)],
+                           capture_output=True, text=True, timeout=600)
+        assert r.returncode == 0, r.stderr[-2000:]
+        text += out.read_text()
     found = {}
     for m in re.finditer(r"^\s*\.amdhsa_kernel\s+(\S+)\s*$(.*?)^\s*\.end_amdhsa_kernel",
                          text, re.M | re.S):
@@ -51,6 +54,7 @@ def test_every_kernel_variant_was_found(kernels):
     for kind in ("segment_kernel", "finalize_kernel", "totals_kernel", "scale_kernel"):
         assert sum(kind in n for n in names) == 3, kind
     assert sum("finite_kernel" in n for n in names) == 2
+    assert sum("table_kernel" in n for n in names) == 1
 
 
 def test_no_kernel_spills(kernels):
