@@ -377,10 +377,12 @@ def main() -> int:
     if args.bf16_copy:
         opt.attach_bf16_copies("allocate")
     n_tensors, n_chunks, chunk = _lib.lamb_plan_info(opt.plan)
-    tiles_per_tensor, n_tiles, tile_groups = _lib.lamb_plan_tiles(opt.plan)
+    tiles_per_tensor, n_tiles, tile_groups, single_elems = _lib.lamb_plan_tiles(opt.plan, True)
     single = args.path == "auto"
     P = sum(x.numel() for x in xs)
-    P_single = sum(x.numel() for x, k in zip(xs, tiles_per_tensor) if k) if single else 0
+    # elements on the single pass: whole layers, and the tails of layers
+    # larger than one round (their heads take the two-pass kernels)
+    P_single = sum(single_elems) if single else 0
     checked = single and args.skip_nonfinite and P_single > 0
 
     # The oracle's sample is copied out before the GPU steps move x; the

@@ -113,14 +113,19 @@ typedef enum lamb_norm {
  *                      m, v and writes x, m, v once: a persistent grid keeps
  *                      each tile's x and update direction on chip while the
  *                      layer's norms are combined. A tile holds 8192
- *                      elements, or 10240 when that puts more parameters on
- *                      the single pass (lamb_tile_schedule): layers of up to
- *                      8M or 10M elements on MI355X. The environment
- *                      variable LAMB_MI355X_TILE_GROUPS (8 or 10), read by
- *                      lamb_plan_create, fixes the tile instead; tests use
- *                      it to run the wider tile on small layers (any other
- *                      value fails with LAMB_EINVAL). Larger layers take the
- *                      two-pass kernels. Needs the device's full occupancy
+ *                      elements, or 10240 when that puts more whole layers'
+ *                      parameters on the single pass (lamb_tile_schedule):
+ *                      one round holds 8M or 10M elements on MI355X. The
+ *                      environment variable LAMB_MI355X_TILE_GROUPS (8 or
+ *                      10), read by lamb_plan_create, fixes the tile instead;
+ *                      tests use it to run the wider tile on small layers
+ *                      (any other value fails with LAMB_EINVAL). A larger
+ *                      layer puts its last elements, one round of tiles from
+ *                      a multiple of 1024, on the single pass and its head on
+ *                      the two-pass kernels: a moment pass and a totals
+ *                      kernel before the single pass, which adds the head's
+ *                      partial norms into the layer's, and an apply pass
+ *                      after it. Needs the device's full occupancy
  *                      for the length of that kernel: the library runs the
  *                      single-pass kernels of one process one at a time
  *                      (a step on another stream than the previous one
@@ -242,15 +247,19 @@ LAMB_API lamb_status lamb_plan_set_path(lamb_plan *plan, int32_t path);
 
 /*
  * The single-pass layout (host outputs; any may be NULL):
- *   tiles_per_tensor  n_tensors entries: the layer's tile count, or 0 when
- *                     the layer takes the two-pass kernels
+ *   tiles_per_tensor  n_tensors entries: the layer's tile count on the
+ *                     single pass (of its tail, for a layer of more than one
+ *                     round of tiles)
  *   n_tiles           total tiles of the single pass
  *   tile_groups       the tile shape lamb_tile_schedule chose: 8 (tiles of
  *                     8192 elements) or 10 (10240 elements)
+ *   single_elems      n_tensors entries: the layer's elements on the single
+ *                     pass; the rest (the head of a larger layer) take the
+ *                     two-pass kernels
  * Errors: LAMB_ENULL (plan).
  */
 LAMB_API lamb_status lamb_plan_tiles(const lamb_plan *plan, int32_t *tiles_per_tensor,
-                            int32_t *n_tiles, int32_t *tile_groups);
+                            int32_t *n_tiles, int32_t *tile_groups, int64_t *single_elems);
 
 /*
  * Wait for `stream` and report whether a single-pass step of the plan gave

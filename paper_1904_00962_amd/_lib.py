@@ -122,7 +122,7 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
     lib.lamb_plan_set_timing.argtypes = [vp, i32, i32]
     lib.lamb_plan_timing.argtypes = [vp, P(ctypes.c_double), P(i64)]
     lib.lamb_plan_set_path.argtypes = [vp, i32]
-    lib.lamb_plan_tiles.argtypes = [vp, P(i32), P(i32), P(i32)]
+    lib.lamb_plan_tiles.argtypes = [vp, P(i32), P(i32), P(i32), P(i64)]
     lib.lamb_plan_check.argtypes = [vp, vp]
     lib.lamb_tile_schedule.argtypes = [P(i64), i32, i32, i32, i32, P(i32), P(i64), P(i32),
                                        P(i32), P(i32), P(i32), P(i32), P(i32)]
@@ -326,14 +326,19 @@ def lamb_plan_set_path(plan: Plan, path="auto") -> None:
     _check(load().lamb_plan_set_path(_vp(plan.handle), code), "lamb_plan_set_path")
 
 
-def lamb_plan_tiles(plan: Plan) -> Tuple[list, int, int]:
-    """(tiles per tensor, 0 for a two-pass layer; total single-pass tiles;
-    tile shape in float4 groups per thread, 8 or 10)."""
+def lamb_plan_tiles(plan: Plan, with_elems: bool = False):
+    """(tiles per tensor on the single pass, total single-pass tiles, tile shape
+    in float4 groups per thread: 8 or 10), and with ``with_elems`` also the
+    elements of each tensor on the single pass (the rest of a layer larger
+    than one round takes the two-pass kernels)."""
     n = lamb_plan_info(plan)[0]
     per = (ctypes.c_int32 * n)()
+    elems = (ctypes.c_int64 * n)()
     total, groups = ctypes.c_int32(), ctypes.c_int32()
     _check(load().lamb_plan_tiles(_vp(plan.handle), per, ctypes.byref(total),
-                                  ctypes.byref(groups)), "lamb_plan_tiles")
+                                  ctypes.byref(groups), elems), "lamb_plan_tiles")
+    if with_elems:
+        return list(per), total.value, groups.value, list(elems)
     return list(per), total.value, groups.value
 
 

@@ -52,8 +52,12 @@ struct lamb_plan {
     ChunkDesc *tiles = nullptr;
     uint64_t *slots = nullptr;     // 2 x 3 x n_tiles slot words
     uint32_t *ctl = nullptr;       // FusedCtl words
+    // Layers of more than one round of tiles keep a head on the two-pass
+    // kernels (rest_tensors) and put their tail on the single pass.
     TensorDesc *rest_tensors = nullptr;
-    int32_t *rest_ids = nullptr;    // tensor id (in rest_tensors) of every fine chunk of those
+    int32_t *rest_ids = nullptr;    // tensor id (in rest_tensors) of every fine chunk of the heads
+    TensorDesc *fused_tensors = nullptr;  // the single pass's table: tails at their offsets
+    double *ext_totals = nullptr;   // the heads' partial-norm totals (2 per head, then a verdict)
     // Finalize segments of the fine, the coarse and the other-layers table.
     SegDesc *segs[3] = {};
     SegRange *seg_ranges[3] = {};
@@ -61,7 +65,9 @@ struct lamb_plan {
     Partial *seg_partials = nullptr;
     int fused_per_cu[4][2][3] = {};  // single-pass workgroups per CU by algo, bf16, norm
     std::vector<TensorDesc> host_tensors;  // host image of the tensor table
-    std::vector<TensorDesc> host_rest;     // host image of the other-layers table
+    std::vector<TensorDesc> host_rest;     // host image of the heads' table
+    std::vector<TensorDesc> host_fused;    // host image of the single pass's table
+    std::vector<int64_t> single_elems;     // elements of each layer on the single pass
     std::vector<std::pair<uintptr_t, uintptr_t>> ranges;  // sorted buffer ranges of the table
     // finiteness check of skip_nonfinite steps that take the single pass
     ChunkDesc *check_chunks = nullptr;
@@ -211,9 +217,10 @@ hipError_t gated_fused_launch(int device, hipStream_t stream, const StepKind &ki
     if (err != hipSuccess)
         return err;
     if (capture != hipStreamCaptureStatusNone)
-        return launch_fused(kind, plan->tile_groups, plan->tensors, plan->tiles, plan->n_tiles,
-                            grid, plan->slots, plan->ctl, plan->flags, guarded, nonfinite_out, a,
-                            f, ratio_out, norms_out, stream);
+        return launch_fused(kind, plan->tile_groups, plan->fused_tensors, plan->tiles,
+                            plan->n_tiles, grid, plan->slots, plan->ctl, plan->flags, guarded,
+                            nonfinite_out, a, f, ratio_out, norms_out, plan->ext_totals,
+                            plan->scale, stream);
     std::lock_guard<std::mutex> lock(g_gate_mutex);
     if (g_gates.size() <= size_t(device))
         g_gates.resize(size_t(device) + 1);
@@ -228,9 +235,9 @@ hipError_t gated_fused_launch(int device, hipStream_t stream, const StepKind &ki
         if (err != hipSuccess)
             return err;
     }
-    err = launch_fused(kind, plan->tile_groups, plan->tensors, plan->tiles, plan->n_tiles, grid,
-                       plan->slots, plan->ctl, plan->flags, guarded, nonfinite_out, a, f,
-                       ratio_out, norms_out, stream);
+    err = launch_fused(kind, plan->tile_groups, plan->fused_tensors, plan->tiles, plan->n_tiles,
+                       grid, plan->slots, plan->ctl, plan->flags, guarded, nonfinite_out, a, f,
+                       ratio_out, norms_out, plan->ext_totals, plan->scale, stream);
     if (err != hipSuccess)
         return err;
     err = hipEventRecord(gate.done, stream);
@@ -642,14 +649,31 @@ lamb_status lamb_plan_create(const lamb_tensor *tensors, int32_t n_tensors,
                         kTileGroups, kWideGroups);
         groups = int32_t(v);
     }
+    // The tile shape (lamb_tile_schedule's rule over whole layers), then the
+    // schedule: a layer of more tiles than a round keeps a head on the
+    // two-pass kernels and puts its last elements, at most one round of
+    // tiles from a multiple of kBlockElems, on the single pass.
     st = lamb_tile_schedule(numel.data(), n_tensors, max_round, groups, 0, nullptr, nullptr,
                             nullptr, first_tile.data(), tile_count.data(), &n_entries, &round,
                             &groups);
+    if (st != LAMB_OK)
+        return st;
+    const int64_t round_elems = int64_t(max_round) * tile_elems(groups);
+    std::vector<int64_t> head(size_t(n_tensors), 0), tail(size_t(n_tensors), 0);
+    for (int32_t i = 0; i < n_tensors; ++i) {
+        const int64_t n = numel[size_t(i)];
+        if (n > round_elems)
+            head[size_t(i)] = (n - round_elems + kBlockElems - 1) / kBlockElems * kBlockElems;
+        tail[size_t(i)] = n - head[size_t(i)];
+    }
+    st = lamb_tile_schedule(tail.data(), n_tensors, max_round, groups, 0, nullptr, nullptr,
+                            nullptr, first_tile.data(), tile_count.data(), &n_entries, &round,
+                            nullptr);
     std::vector<int32_t> entry_tensor(static_cast<size_t>(n_entries)),
         entry_len(static_cast<size_t>(n_entries));
     std::vector<int64_t> entry_start(static_cast<size_t>(n_entries));
     if (st == LAMB_OK)
-        st = lamb_tile_schedule(numel.data(), n_tensors, max_round, groups, n_entries,
+        st = lamb_tile_schedule(tail.data(), n_tensors, max_round, groups, n_entries,
                                 entry_tensor.data(), entry_start.data(), entry_len.data(),
                                 first_tile.data(), tile_count.data(), &n_entries, &round,
                                 nullptr);
@@ -659,8 +683,11 @@ lamb_status lamb_plan_create(const lamb_tensor *tensors, int32_t n_tensors,
     for (int32_t k = 0; k < n_entries; ++k)
         host_tiles[size_t(k)] =
             ChunkDesc{entry_tensor[size_t(k)], entry_len[size_t(k)], entry_start[size_t(k)]};
+    // Three tensor tables: every layer whole (the two-pass path and the split
+    // step), the single pass's (tails at their offsets), and the heads.
+    std::vector<TensorDesc> host_fused(static_cast<size_t>(n_tensors));
     std::vector<TensorDesc> host_rest;
-    std::vector<ChunkDesc> host_rest_chunks;
+    std::vector<int32_t> host_rest_ids;
     {
         int32_t first = 0, first_coarse = 0;
         for (int32_t i = 0; i < n_tensors; ++i) {
@@ -670,27 +697,37 @@ lamb_status lamb_plan_create(const lamb_tensor *tensors, int32_t n_tensors,
             TensorDesc d{t.x,          t.g,          t.m,   needs_v ? t.v : nullptr,
                          nullptr,      t.numel,      t.wd,  first,
                          nc,           first_coarse, ncc,   first_tile[size_t(i)],
-                         tile_count[size_t(i)], i};
-            if (d.n_tiles == 0) {
+                         tile_count[size_t(i)], i,   -1};
+            host_tensors[size_t(i)] = d;
+            const int64_t h = head[size_t(i)];
+            TensorDesc f = d;
+            f.first_chunk = f.n_chunks = f.first_coarse = f.n_coarse = 0;
+            if (h > 0) {
+                const size_t g_size = g_dtype == LAMB_GRAD_BF16 ? 2 : 4;
+                f.x = t.x + h;
+                f.g = static_cast<const char *>(t.g) + h * int64_t(g_size);
+                f.m = t.m + h;
+                f.v = needs_v ? t.v + h : nullptr;
+                f.numel = tail[size_t(i)];
+                f.ext = int32_t(host_rest.size());
                 TensorDesc r = d;
-                r.first_chunk = int32_t(host_rest_chunks.size());
+                r.numel = h;
+                r.first_chunk = int32_t(host_rest_ids.size());
+                r.n_chunks = int32_t((h + chunk - 1) / chunk);
                 r.first_coarse = r.n_coarse = 0;
-                const int32_t ri = int32_t(host_rest.size());
-                for (int32_t k = 0; k < nc; ++k) {
-                    ChunkDesc c = host_chunks[size_t(first + k)];
-                    c.tensor = ri;
-                    host_rest_chunks.push_back(c);
-                }
+                r.first_tile = r.n_tiles = 0;
+                for (int32_t k = 0; k < r.n_chunks; ++k)
+                    host_rest_ids.push_back(f.ext);
                 host_rest.push_back(r);
             }
-            host_tensors[size_t(i)] = d;
+            host_fused[size_t(i)] = f;
             first += nc;
             first_coarse += ncc;
         }
     }
     const int32_t n_tiles = int32_t(host_tiles.size());
     const int32_t n_rest = int32_t(host_rest.size());
-    const int32_t n_rest_chunks = int32_t(host_rest_chunks.size());
+    const int32_t n_rest_chunks = int32_t(host_rest_ids.size());
     std::vector<SegDesc> host_segs[3];
     std::vector<SegRange> host_ranges[3];
     {
@@ -729,6 +766,8 @@ lamb_status lamb_plan_create(const lamb_tensor *tensors, int32_t n_tensors,
     const size_t ctl_bytes = 256;
     const size_t rest_bytes = round256(sizeof(TensorDesc) * size_t(n_rest));
     const size_t rest_chunk_bytes = round256(sizeof(int32_t) * size_t(n_rest_chunks));
+    const size_t fused_bytes = round256(sizeof(TensorDesc) * size_t(n_tensors));
+    const size_t ext_bytes = round256(sizeof(double) * (2 * size_t(n_rest) + 1));
     size_t seg_bytes[3], range_bytes[3];
     for (int k = 0; k < 3; ++k) {
         seg_bytes[k] = round256(sizeof(SegDesc) * host_segs[k].size());
@@ -739,7 +778,8 @@ lamb_status lamb_plan_create(const lamb_tensor *tensors, int32_t n_tensors,
     err = hipMalloc(&plan->device_block,
                     tensors_bytes + chunks_bytes + coarse_bytes + partial_bytes + scale_bytes +
                         flag_bytes + tiles_bytes + slot_bytes + ctl_bytes + rest_bytes +
-                        rest_chunk_bytes + seg_bytes[0] + seg_bytes[1] + seg_bytes[2] +
+                        rest_chunk_bytes + fused_bytes + ext_bytes + seg_bytes[0] +
+                        seg_bytes[1] + seg_bytes[2] +
                         range_bytes[0] + range_bytes[1] + range_bytes[2] + seg_partial_bytes +
                         check_bytes);
     if (err != hipSuccess) {
@@ -771,6 +811,10 @@ lamb_status lamb_plan_create(const lamb_tensor *tensors, int32_t n_tensors,
     base += rest_bytes;
     plan->rest_ids = reinterpret_cast<int32_t *>(base);
     base += rest_chunk_bytes;
+    plan->fused_tensors = reinterpret_cast<TensorDesc *>(base);
+    base += fused_bytes;
+    plan->ext_totals = reinterpret_cast<double *>(base);
+    base += ext_bytes;
     for (int k = 0; k < 3; ++k) {
         plan->segs[k] = reinterpret_cast<SegDesc *>(base);
         base += seg_bytes[k];
@@ -797,8 +841,11 @@ lamb_status lamb_plan_create(const lamb_tensor *tensors, int32_t n_tensors,
         err = hipMemcpy(plan->rest_tensors, host_rest.data(), sizeof(TensorDesc) * size_t(n_rest),
                         hipMemcpyHostToDevice);
     if (err == hipSuccess && n_rest > 0)
-        err = hipMemcpy(plan->rest_ids, ids_of(host_rest_chunks).data(),
+        err = hipMemcpy(plan->rest_ids, host_rest_ids.data(),
                         sizeof(int32_t) * size_t(n_rest_chunks), hipMemcpyHostToDevice);
+    if (err == hipSuccess)
+        err = hipMemcpy(plan->fused_tensors, host_fused.data(),
+                        sizeof(TensorDesc) * size_t(n_tensors), hipMemcpyHostToDevice);
     for (int k = 0; k < 3 && err == hipSuccess; ++k) {
         if (!host_segs[k].empty())
             err = hipMemcpy(plan->segs[k], host_segs[k].data(),
@@ -855,7 +902,9 @@ lamb_status lamb_plan_create(const lamb_tensor *tensors, int32_t n_tensors,
     plan->n_rest = n_rest;
     plan->n_rest_chunks = n_rest_chunks;
     plan->host_tensors = std::move(host_tensors);
+    plan->host_fused = std::move(host_fused);
     plan->host_rest = std::move(host_rest);
+    plan->single_elems = std::move(tail);
     for (const BufferRange &r : ranges)
         plan->ranges.emplace_back(r.lo, r.hi);
     plan->chunk_elems = chunk;
@@ -1058,13 +1107,18 @@ lamb_status lamb_step_ex(lamb_plan *plan, const lamb_hparams *hp, void *stream,
     StepArgs a = step_args(*hp);
     a.spin_limit = plan->spin_limit;
     const FinalizeArgs f = finalize_args(*hp);
-    // The single pass serves the layers that fit; the two-pass kernels take
-    // the rest (or everything on LAMB_PATH_TWO_PASS). A skip_nonfinite step
-    // on the single pass first takes its verdict with a read-only check of g,
-    // then runs the direct-mode kernels, which skip when it is raised; the
-    // single pass goes last and reports it.
+    // On LAMB_PATH_AUTO the single pass serves every layer of at most one
+    // round of tiles and the tails of larger ones, whose heads take a moment
+    // pass and a totals kernel before it and an apply pass after it (the
+    // single pass adds the heads' totals into those layers' norms and writes
+    // their scales). LAMB_PATH_TWO_PASS runs everything on the two-pass
+    // kernels. A skip_nonfinite step on the single pass first takes its
+    // verdict with a read-only check of g; the kernels before the single pass
+    // obey the epoch's verdict word, the apply pass after it a copy the totals
+    // kernel takes (the single pass rewrites the epoch's words as it ends).
     const bool single = plan->path == LAMB_PATH_AUTO && plan->n_tiles > 0;
     const bool checked = single && kind.deferred;
+    const bool heads = single && plan->n_rest > 0;
     StepKind direct = kind;
     direct.deferred = false;
 
@@ -1085,61 +1139,75 @@ lamb_status lamb_step_ex(lamb_plan *plan, const lamb_hparams *hp, void *stream,
     }
     hipStream_t s = static_cast<hipStream_t>(stream);
     begin_timing(plan, s);
+    hipError_t err = hipSuccess;
     if (checked) {
-        hipError_t err = launch_finite(kind.bf16_grad, plan->tensors, plan->check_chunks,
-                                       plan->n_check, plan->flags, plan->ctl, a.grad_scale, s);
+        err = launch_finite(kind.bf16_grad, plan->tensors, plan->check_chunks, plan->n_check,
+                            plan->flags, plan->ctl, a.grad_scale, s);
         if (err != hipSuccess)
             return fail_hip(err, "launching the finiteness check");
         mark(plan, kTimedCheck, s);
     }
-    if (single && !checked) {
-        hipError_t err = gated_fused_launch(plan->device, s, direct, plan, grid, false, nullptr, a,
-                                            f, ratio_out, norms_out);
+    if (single) {
+        if (heads) {
+            err = launch_moments(direct, plan->rest_tensors, plan->rest_ids, plan->chunk_elems,
+                                 plan->partials, plan->n_rest_chunks,
+                                 two_pass_threads(plan->chunk_elems), plan->flags, plan->ctl,
+                                 checked ? kGuardEpoch : kGuardNone, a, s);
+            if (err != hipSuccess)
+                return fail_hip(err, "launching the moment kernel");
+            mark(plan, kTimedMoments, s);
+            err = launch_totals(direct.norm, plan->partials, plan->segs[kSegRest],
+                                plan->n_segs[kSegRest], plan->seg_ranges[kSegRest], plan->n_rest,
+                                plan->seg_partials, plan->ext_totals, plan->flags, plan->ctl,
+                                checked ? kVerdictCopy : kVerdictZero, s);
+            if (err != hipSuccess)
+                return fail_hip(err, "launching the totals kernel");
+            mark(plan, kTimedFinalize, s);
+        }
+        err = gated_fused_launch(plan->device, s, direct, plan, grid, checked,
+                                 checked ? nonfinite_out : nullptr, a, f, ratio_out, norms_out);
         if (err != hipSuccess)
             return fail_hip(err, "launching the single-pass kernel");
         mark(plan, kTimedSingle, s);
-    }
-    if (!single || plan->n_rest > 0) {
-        const StepKind &k2 = single ? direct : kind;
-        const TensorDesc *tensors = single ? plan->rest_tensors : plan->tensors;
-        const int32_t n_tensors = single ? plan->n_rest : plan->n_tensors;
-        const int32_t *chunk_ids = single ? plan->rest_ids : plan->chunk_ids;
-        const int32_t n_chunks = single ? plan->n_rest_chunks : plan->n_chunks;
+        plan->u_check_chunks = 0;
+        if (heads) {
+            err = launch_apply(direct, plan->rest_tensors, plan->rest_ids, plan->chunk_elems,
+                               plan->scale, plan->n_rest_chunks,
+                               two_pass_threads(plan->chunk_elems), plan->flags, plan->ctl,
+                               checked ? kGuardCopy : kGuardNone, nullptr, plan->u_check, a, s);
+            if (err != hipSuccess)
+                return fail_hip(err, "launching the apply kernel");
+            mark(plan, kTimedApply, s);
+            plan->u_check_chunks = plan->u_check ? plan->n_rest_chunks : 0;
+        }
+    } else {
         // Deferred moment passes only read, and use the coarse chunk table.
-        const int32_t *moment_ids = k2.deferred ? plan->coarse_ids : chunk_ids;
-        const int32_t n_moment_chunks = k2.deferred ? plan->n_coarse : n_chunks;
-        const int32_t moment_elems = k2.deferred ? plan->coarse_elems : plan->chunk_elems;
-        hipError_t err = launch_moments(k2, tensors, moment_ids, moment_elems, plan->partials,
-                                        n_moment_chunks, two_pass_threads(moment_elems),
-                                        plan->flags, plan->ctl, checked, a, s);
+        const int32_t *moment_ids = kind.deferred ? plan->coarse_ids : plan->chunk_ids;
+        const int32_t n_moment_chunks = kind.deferred ? plan->n_coarse : plan->n_chunks;
+        const int32_t moment_elems = kind.deferred ? plan->coarse_elems : plan->chunk_elems;
+        err = launch_moments(kind, plan->tensors, moment_ids, moment_elems, plan->partials,
+                             n_moment_chunks, two_pass_threads(moment_elems), plan->flags,
+                             plan->ctl, kGuardNone, a, s);
         if (err != hipSuccess)
             return fail_hip(err, "launching the moment kernel");
         mark(plan, kTimedMoments, s);
-        const int seg = k2.deferred ? kSegCoarse : single ? kSegRest : kSegFine;
-        err = launch_finalize(k2.norm, tensors, n_tensors, plan->partials, plan->segs[seg],
-                              plan->n_segs[seg], plan->seg_ranges[seg], plan->seg_partials, f,
-                              plan->scale, ratio_out, norms_out,
-                              k2.deferred ? plan->flags : nullptr, s);
+        const int seg = kind.deferred ? kSegCoarse : kSegFine;
+        err = launch_finalize(kind.norm, plan->tensors, plan->n_tensors, plan->partials,
+                              plan->segs[seg], plan->n_segs[seg], plan->seg_ranges[seg],
+                              plan->seg_partials, f, plan->scale, ratio_out, norms_out,
+                              kind.deferred ? plan->flags : nullptr, s);
         if (err != hipSuccess)
             return fail_hip(err, "launching the finalize kernel");
         mark(plan, kTimedFinalize, s);
-        Partial *check = k2.deferred ? nullptr : plan->u_check;
-        err = launch_apply(k2, tensors, chunk_ids, plan->chunk_elems, plan->scale, n_chunks,
-                           two_pass_threads(plan->chunk_elems), plan->flags, plan->ctl, checked,
-                           k2.deferred ? nonfinite_out : nullptr, check, a, s);
+        Partial *check = kind.deferred ? nullptr : plan->u_check;
+        err = launch_apply(kind, plan->tensors, plan->chunk_ids, plan->chunk_elems, plan->scale,
+                           plan->n_chunks, two_pass_threads(plan->chunk_elems), plan->flags,
+                           plan->ctl, kGuardNone, kind.deferred ? nonfinite_out : nullptr, check,
+                           a, s);
         if (err != hipSuccess)
             return fail_hip(err, "launching the apply kernel");
         mark(plan, kTimedApply, s);
-        plan->u_check_chunks = check ? n_chunks : 0;
-    } else {
-        plan->u_check_chunks = 0;
-    }
-    if (checked) {
-        hipError_t err = gated_fused_launch(plan->device, s, direct, plan, grid, true,
-                                            nonfinite_out, a, f, ratio_out, norms_out);
-        if (err != hipSuccess)
-            return fail_hip(err, "launching the single-pass kernel");
-        mark(plan, kTimedSingle, s);
+        plan->u_check_chunks = check ? plan->n_chunks : 0;
     }
     end_timing(plan);
     return LAMB_OK;
@@ -1221,11 +1289,21 @@ lamb_status lamb_plan_set_bf16_copies(lamb_plan *plan, void *const *copies) {
     std::vector<TensorDesc> next_rest = plan->host_rest;
     for (TensorDesc &r : next_rest)
         r.x_copy = next[size_t(r.out_index)].x_copy;
+    // the single pass's table holds the tails of split layers at an offset
+    std::vector<TensorDesc> next_fused = plan->host_fused;
+    for (int32_t i = 0; i < plan->n_tensors; ++i) {
+        uint16_t *c = next[size_t(i)].x_copy;
+        const int64_t head = next[size_t(i)].numel - next_fused[size_t(i)].numel;
+        next_fused[size_t(i)].x_copy = c ? c + head : nullptr;
+    }
     DeviceGuard guard(plan->device);
     if (guard.status != hipSuccess)
         return fail_hip(guard.status, "selecting the plan's device");
     hipError_t err = hipMemcpy(plan->tensors, next.data(),
                                sizeof(TensorDesc) * size_t(plan->n_tensors), hipMemcpyHostToDevice);
+    if (err == hipSuccess)
+        err = hipMemcpy(plan->fused_tensors, next_fused.data(),
+                        sizeof(TensorDesc) * size_t(plan->n_tensors), hipMemcpyHostToDevice);
     if (err == hipSuccess && plan->n_rest > 0)
         err = hipMemcpy(plan->rest_tensors, next_rest.data(),
                         sizeof(TensorDesc) * size_t(plan->n_rest), hipMemcpyHostToDevice);
@@ -1234,6 +1312,7 @@ lamb_status lamb_plan_set_bf16_copies(lamb_plan *plan, void *const *copies) {
     if (err != hipSuccess)
         return fail_hip(err, "hipMemcpy of the tensor table");
     plan->host_tensors = std::move(next);
+    plan->host_fused = std::move(next_fused);
     plan->host_rest = std::move(next_rest);
     return LAMB_OK;
 }
@@ -1248,12 +1327,15 @@ lamb_status lamb_plan_set_path(lamb_plan *plan, int32_t path) {
 }
 
 lamb_status lamb_plan_tiles(const lamb_plan *plan, int32_t *tiles_per_tensor, int32_t *n_tiles,
-                            int32_t *tile_groups) {
+                            int32_t *tile_groups, int64_t *single_elems) {
     if (!plan)
         return fail(LAMB_ENULL, "plan must not be NULL");
     if (tiles_per_tensor)
         for (int32_t i = 0; i < plan->n_tensors; ++i)
-            tiles_per_tensor[i] = plan->host_tensors[size_t(i)].n_tiles;
+            tiles_per_tensor[i] = plan->host_fused[size_t(i)].n_tiles;
+    if (single_elems)
+        for (int32_t i = 0; i < plan->n_tensors; ++i)
+            single_elems[i] = plan->single_elems[size_t(i)];
     if (n_tiles)
         *n_tiles = plan->n_tiles;
     if (tile_groups)
@@ -1403,13 +1485,14 @@ lamb_status lamb_step_partials(lamb_plan *plan, const lamb_hparams *hp, void *st
     const int32_t n = kind.deferred ? plan->n_coarse : plan->n_chunks;
     const int32_t elems = kind.deferred ? plan->coarse_elems : plan->chunk_elems;
     hipError_t err = launch_moments(kind, plan->tensors, ids, elems, plan->partials, n,
-                                    two_pass_threads(elems), plan->flags, plan->ctl, false, a, s);
+                                    two_pass_threads(elems), plan->flags, plan->ctl, kGuardNone,
+                                    a, s);
     if (err != hipSuccess)
         return fail_hip(err, "launching the moment kernel");
     const int seg = kind.deferred ? kSegCoarse : kSegFine;
     err = launch_totals(kind.norm, plan->partials, plan->segs[seg], plan->n_segs[seg],
                         plan->seg_ranges[seg], plan->n_tensors, plan->seg_partials, totals,
-                        plan->flags, kind.deferred, s);
+                        plan->flags, plan->ctl, kind.deferred ? kVerdictMove : kVerdictZero, s);
     if (err != hipSuccess)
         return fail_hip(err, "launching the totals kernel");
     plan->u_check_chunks = 0;
@@ -1439,7 +1522,8 @@ lamb_status lamb_step_finish(lamb_plan *plan, const lamb_hparams *hp, void *stre
     Partial *check = kind.deferred ? nullptr : plan->u_check;
     err = launch_apply(kind, plan->tensors, plan->chunk_ids, plan->chunk_elems, plan->scale,
                        plan->n_chunks, two_pass_threads(plan->chunk_elems), plan->flags,
-                       plan->ctl, false, kind.deferred ? nonfinite_out : nullptr, check, a, s);
+                       plan->ctl, kGuardNone, kind.deferred ? nonfinite_out : nullptr, check, a,
+                       s);
     if (err != hipSuccess)
         return fail_hip(err, "launching the apply kernel");
     plan->u_check_chunks = check ? plan->n_chunks : 0;

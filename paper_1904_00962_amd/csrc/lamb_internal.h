@@ -75,8 +75,11 @@ struct TensorDesc {
     int32_t first_tile;    // single-pass tiles [first_tile, first_tile + n_tiles);
     int32_t n_tiles;       //   n_tiles = 0: the layer takes the two-pass path
     int32_t out_index;     // the layer's index in ratio_out / norms_out
+    int32_t ext;           // single-pass table: the index of the layer's head in the
+                           // two-pass table (its partial-norm totals and its step
+                           // scale), or -1 when the whole layer is in the tiles
 };
-static_assert(sizeof(TensorDesc) == 80, "TensorDesc layout");
+static_assert(sizeof(TensorDesc) == 88, "TensorDesc layout");
 
 // One chunk: `len` elements of tensor `tensor` starting at element `start`.
 struct ChunkDesc {
@@ -174,15 +177,22 @@ constexpr int32_t kCheckElems = 16384;
 // a chunk table as one tensor id per chunk (`chunk_ids`) and its chunk size;
 // the moment pass of deferred mode reads the coarse table (tensors'
 // first_coarse), every other pass a fine one (first_chunk).
+// Which verdict a direct-mode pass of a skip_nonfinite step obeys (it returns
+// at once when that word is raised).
+enum Guard : int32_t {
+    kGuardNone = 0,   // not a skip_nonfinite step (or deferred mode)
+    kGuardEpoch = 1,  // the verdict word of the epoch in ctl (kVerdictWord + (epoch & 1))
+    kGuardCopy = 2,   // flags[1], the copy the totals kernel took before the single
+                      // pass (which rewrites the epoch's words as it ends)
+};
+
 // `ctl` is the plan's FusedCtl words: every pass returns at once while the
 // sticky fault word is raised, so that after a single-pass give-up no layer
-// moves. `guarded` (direct mode only): also return when the verdict word of
-// the epoch in ctl is raised (a skip_nonfinite step whose verdict the
-// finiteness check took).
+// moves; `guard` is a Guard value.
 hipError_t launch_moments(const StepKind &kind, const TensorDesc *tensors,
                           const int32_t *chunk_ids, int32_t chunk_elems, Partial *partials,
                           int32_t n_chunks, int32_t threads, uint32_t *flags,
-                          const uint32_t *ctl, bool guarded, const StepArgs &args,
+                          const uint32_t *ctl, int32_t guard, const StepArgs &args,
                           hipStream_t stream);
 // Both levels of the finalize: `segs` (n_segs entries) over `partials` into
 // `seg_partials`, then per tensor over its `ranges` entry of the segments.
@@ -196,16 +206,22 @@ hipError_t launch_finalize(NormKind norm, const TensorDesc *tensors, int32_t n_t
 hipError_t launch_apply(const StepKind &kind, const TensorDesc *tensors,
                         const int32_t *chunk_ids, int32_t chunk_elems, const float *scale,
                         int32_t n_chunks, int32_t threads, uint32_t *flags, const uint32_t *ctl,
-                        bool guarded, int32_t *nonfinite_out, Partial *check,
+                        int32_t guard, int32_t *nonfinite_out, Partial *check,
                         const StepArgs &args, hipStream_t stream);
-// Split step, first half: the segment level over `partials`, then per tensor
-// its combined partial norms into totals[2 i], totals[2 i + 1], and the
-// deferred moment pass's verdict (flags[0], then cleared) into totals[2 n]
-// (0 in direct mode).
+// What the totals kernel does with the step's non-finite verdict.
+enum VerdictMode : int32_t {
+    kVerdictZero = 0,   // totals[2 n] = 0 (a direct-mode step)
+    kVerdictMove = 1,   // totals[2 n] = the deferred moment pass's flags[0], then cleared
+    kVerdictCopy = 2,   // flags[1] = totals[2 n] = the epoch's verdict word (kGuardCopy)
+};
+// Per tensor its combined partial norms into totals[2 i], totals[2 i + 1]
+// after the segment level over `partials`, and the verdict into totals[2 n]
+// (a VerdictMode). The split step's first half, and the totals of the heads
+// of layers split between the two paths.
 hipError_t launch_totals(NormKind norm, const Partial *partials, const SegDesc *segs,
                          int32_t n_segs, const SegRange *ranges, int32_t n_tensors,
-                         Partial *seg_partials, double *totals, uint32_t *flags, bool deferred,
-                         hipStream_t stream);
+                         Partial *seg_partials, double *totals, uint32_t *flags,
+                         const uint32_t *ctl, int32_t verdict_mode, hipStream_t stream);
 // Split step, second half: per tensor the norms, phi, ratio and scale from
 // combined totals; flags[1] receives the combined verdict for a deferred
 // apply pass.
@@ -227,12 +243,17 @@ constexpr uint64_t kEmptySlot = ~uint64_t(0);
 // raised or not; the last workgroup writes it to `nonfinite_out` (may be
 // null). Every step's last workgroup clears the verdict word of the next
 // epoch.
-// `groups` is the plan's tile shape, kTileGroups or kWideGroups.
+// `groups` is the plan's tile shape, kTileGroups or kWideGroups. A layer
+// whose descriptor has ext >= 0 (the last part of a layer too large for one
+// round) combines the totals of its head, ext_totals[2 ext] and
+// ext_totals[2 ext + 1], before its own tiles' partials, and writes its step
+// scale to ext_scale[ext] for the apply pass over the head.
 hipError_t launch_fused(const StepKind &kind, int groups, const TensorDesc *tensors,
                         const ChunkDesc *tiles, int32_t n_tiles, int32_t grid, uint64_t *slots,
                         uint32_t *ctl, uint32_t *flags, bool guarded, int32_t *nonfinite_out,
                         const StepArgs &args, const FinalizeArgs &fargs, double *ratio_out,
-                        double *norms_out, hipStream_t stream);
+                        double *norms_out, const double *ext_totals, float *ext_scale,
+                        hipStream_t stream);
 // Workgroups of the single-pass kernel for `kind` and tile shape `groups`
 // that fit on one CU at once.
 hipError_t fused_blocks_per_cu(const StepKind &kind, int groups, int *blocks);

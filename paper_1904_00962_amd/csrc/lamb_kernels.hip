@@ -314,11 +314,14 @@ __device__ __forceinline__ uint32_t ctl_load(const uint32_t *p) {
 // Whether a two-pass kernel must do nothing: the plan's single pass gave up a
 // wait (`fault`, the sticky fault word, so that no layer moves after a
 // give-up), or, for a direct-mode pass of a step whose verdict the finiteness
-// check took (`guarded`), that verdict is raised. The kernels load the fault
-// word before their chunk-table entry, so its latency hides behind that load.
+// check took, that verdict (`guard`, a Guard value) is raised. The kernels
+// load the fault word before their chunk-table entry, so its latency hides
+// behind that load.
 __device__ __forceinline__ bool pass_stopped(uint32_t fault, const uint32_t *flags,
-                                             const uint32_t *ctl, int32_t guarded) {
-    if (guarded && flags[kVerdictWord + (ctl[kCtlEpoch] & 1u)] != 0)
+                                             const uint32_t *ctl, int32_t guard) {
+    if (guard == kGuardEpoch && flags[kVerdictWord + (ctl[kCtlEpoch] & 1u)] != 0)
+        return true;
+    if (guard == kGuardCopy && flags[1] != 0)
         return true;
     return fault != 0;
 }
@@ -344,11 +347,11 @@ template <int kAlgo, bool kBf16, int kNorm, bool kDeferred>
 __global__ __launch_bounds__(kBlock) void moments_kernel(
     const TensorDesc *__restrict__ tensors, const int32_t *__restrict__ chunk_ids,
     int32_t chunk_elems, Partial *__restrict__ partials, uint32_t *__restrict__ flags,
-    const uint32_t *__restrict__ ctl, int32_t guarded, StepArgs a) {
+    const uint32_t *__restrict__ ctl, int32_t guard, StepArgs a) {
     constexpr bool kV = kHasSecondMoment<kAlgo>;
     const uint32_t fault = ctl_load(ctl + kCtlFault);
     const ChunkDesc c = chunk_at<kDeferred>(tensors, chunk_ids, chunk_index(), chunk_elems);
-    if (pass_stopped(fault, flags, ctl, kDeferred ? 0 : guarded))
+    if (pass_stopped(fault, flags, ctl, kDeferred ? int32_t(kGuardNone) : guard))
         return;
     const TensorDesc &t = tensors[c.tensor];
     gcfloat *x = global_view(static_cast<const float *>(t.x) + c.start);
@@ -441,14 +444,14 @@ template <int kAlgo, bool kBf16, bool kDeferred, int kNorm, bool kCheck>
 __global__ __launch_bounds__(kBlock) void apply_kernel(
     const TensorDesc *__restrict__ tensors, const int32_t *__restrict__ chunk_ids,
     int32_t chunk_elems, const float *__restrict__ scale, uint32_t *__restrict__ flags,
-    const uint32_t *__restrict__ ctl, int32_t guarded, int32_t *__restrict__ nonfinite_out,
+    const uint32_t *__restrict__ ctl, int32_t guard, int32_t *__restrict__ nonfinite_out,
     Partial *__restrict__ check, StepArgs a) {
     static_assert(!(kCheck && kDeferred), "the check runs on direct-mode steps");
     constexpr bool kV = kHasSecondMoment<kAlgo>;
     constexpr bool kReadsGrad = kDeferred || kDirectionNeedsGrad<kAlgo>;
     const uint32_t fault = ctl_load(ctl + kCtlFault);
     const ChunkDesc c = chunk_at<false>(tensors, chunk_ids, apply_chunk_index(), chunk_elems);
-    if (pass_stopped(fault, flags, ctl, kDeferred ? 0 : guarded))
+    if (pass_stopped(fault, flags, ctl, kDeferred ? int32_t(kGuardNone) : guard))
         return;
     if constexpr (kDeferred) {
         // The finalize moved the moment pass's verdict (raised if any scaled
@@ -573,6 +576,24 @@ __device__ float finish_layer(const Partial &total, const FinalizeArgs &a, int32
     return static_cast<float>(a.lr * ratio);
 }
 
+// finish_layer for the single pass: a layer too large for one round keeps its
+// head on the two-pass kernels, whose totals (ext_totals[2 ext], [2 ext + 1])
+// come first in the layer's sum; its step scale also goes to ext_scale[ext]
+// for the apply pass over the head.
+template <int kNorm>
+__device__ float finish_split_layer(const Partial &tiles_total, int32_t ext,
+                                    const double *ext_totals, float *ext_scale,
+                                    const FinalizeArgs &a, int32_t out, double *ratio_out,
+                                    double *norms_out) {
+    if (ext < 0)
+        return finish_layer<kNorm>(tiles_total, a, out, ratio_out, norms_out);
+    const Partial total{norm_combine<kNorm>(ext_totals[2 * ext], tiles_total.sum_xx),
+                        norm_combine<kNorm>(ext_totals[2 * ext + 1], tiles_total.sum_uu)};
+    const float s = finish_layer<kNorm>(total, a, out, ratio_out, norms_out);
+    ext_scale[ext] = s;
+    return s;
+}
+
 // ---------------------------------------------------------------------------
 // Finiteness check: the verdict of a skip_nonfinite step taken before
 // anything is written (the step then runs the direct-mode kernels, which
@@ -688,16 +709,22 @@ template <int kNorm>
 __global__ __launch_bounds__(kSegBlock) void totals_kernel(
     const Partial *__restrict__ seg_partials, const SegRange *__restrict__ ranges,
     int32_t n_tensors, double *__restrict__ totals, uint32_t *__restrict__ flags,
-    int32_t deferred) {
+    const uint32_t *__restrict__ ctl, int32_t verdict_mode) {
     const int i = blockIdx.x;
     const Partial total = tensor_total<kNorm>(seg_partials, ranges[i]);
     if (threadIdx.x == 0) {
         totals[2 * i] = total.sum_xx;
         totals[2 * i + 1] = total.sum_uu;
         if (i == 0) {
-            totals[2 * n_tensors] = deferred && flags[0] != 0u ? 1.0 : 0.0;
-            if (deferred)
+            uint32_t bad = 0u;
+            if (verdict_mode == kVerdictMove) {
+                bad = flags[0];
                 flags[0] = 0u;
+            } else if (verdict_mode == kVerdictCopy) {
+                bad = flags[kVerdictWord + (ctl[kCtlEpoch] & 1u)];
+                flags[1] = bad;
+            }
+            totals[2 * n_tensors] = bad != 0u ? 1.0 : 0.0;
         }
     }
 }
@@ -809,7 +836,8 @@ void fused_kernel(const TensorDesc *__restrict__ tensors, const ChunkDesc *__res
                   uint32_t *__restrict__ flags, int32_t guarded,
                   int32_t *__restrict__ nonfinite_out,
                   StepArgs a, FinalizeArgs f, double *__restrict__ ratio_out,
-                  double *__restrict__ norms_out) {
+                  double *__restrict__ norms_out, const double *__restrict__ ext_totals,
+                  float *__restrict__ ext_scale) {
     constexpr bool kV = kHasSecondMoment<kAlgo>;
     constexpr int kUnrollF = kFusedUnroll<kAlgo>;
     __shared__ uint32_t sh_epoch, sh_fault, sh_skip;
@@ -961,7 +989,8 @@ void fused_kernel(const TensorDesc *__restrict__ tensors, const ChunkDesc *__res
         int give_up = 0;
         if (team == 1) {
             if (threadIdx.x == 0)
-                sh_scale = finish_layer<kNorm>(sh_tile, f, t.out_index, ratio_out, norms_out);
+                sh_scale = finish_split_layer<kNorm>(sh_tile, t.ext, ext_totals, ext_scale, f,
+                                                     t.out_index, ratio_out, norms_out);
         } else {
             if (threadIdx.x == 0) {
                 slot_store(cur + j, slot_word(sh_tile.sum_xx));
@@ -990,8 +1019,9 @@ void fused_kernel(const TensorDesc *__restrict__ tensors, const ChunkDesc *__res
                 give_up = __syncthreads_or(give_up);
                 if (!give_up) {
                     if (threadIdx.x == 0)
-                        sh_scale = finish_layer<kNorm>(sh_layer, f, t.out_index, ratio_out,
-                                                       norms_out);
+                        sh_scale = finish_split_layer<kNorm>(sh_layer, t.ext, ext_totals,
+                                                             ext_scale, f, t.out_index,
+                                                             ratio_out, norms_out);
                     __syncthreads();
                     const uint64_t w = __float_as_uint(sh_scale);
                     for (int k = threadIdx.x + 1; k < team; k += kBlock)
@@ -1159,12 +1189,12 @@ const void *fused_fn(const StepKind &k, int groups) {
 hipError_t launch_moments(const StepKind &kind, const TensorDesc *tensors,
                           const int32_t *chunk_ids, int32_t chunk_elems, Partial *partials,
                           int32_t n_chunks, int32_t threads, uint32_t *flags,
-                          const uint32_t *ctl, bool guarded, const StepArgs &args,
+                          const uint32_t *ctl, int32_t guard, const StepArgs &args,
                           hipStream_t stream) {
-    if (threads < 64 || threads > kBlock || threads % 64 != 0 || !ctl)
+    if (threads < 64 || threads > kBlock || threads % 64 != 0 || !ctl ||
+        guard < kGuardNone || guard > kGuardCopy)
         return hipErrorInvalidValue;
     StepArgs a = args;
-    int32_t guard = guarded ? 1 : 0;
     void *params[] = {&tensors, &chunk_ids, &chunk_elems, &partials, &flags, &ctl, &guard, &a};
     const void *fn;
     switch (kind.algo) {
@@ -1179,13 +1209,12 @@ hipError_t launch_moments(const StepKind &kind, const TensorDesc *tensors,
 hipError_t launch_apply(const StepKind &kind, const TensorDesc *tensors,
                         const int32_t *chunk_ids, int32_t chunk_elems, const float *scale,
                         int32_t n_chunks, int32_t threads, uint32_t *flags, const uint32_t *ctl,
-                        bool guarded, int32_t *nonfinite_out, Partial *check,
+                        int32_t guard, int32_t *nonfinite_out, Partial *check,
                         const StepArgs &args, hipStream_t stream) {
     if (threads < 64 || threads > kBlock || threads % 64 != 0 || !ctl ||
-        (check && kind.deferred))
+        (check && kind.deferred) || guard < kGuardNone || guard > kGuardCopy)
         return hipErrorInvalidValue;
     StepArgs a = args;
-    int32_t guard = guarded ? 1 : 0;
     void *params[] = {&tensors, &chunk_ids,     &chunk_elems, &scale, &flags,
                       &ctl,     &guard,         &nonfinite_out, &check, &a};
     const bool c = check != nullptr;
@@ -1231,13 +1260,15 @@ hipError_t launch_finalize(NormKind norm, const TensorDesc *tensors, int32_t n_t
 
 hipError_t launch_totals(NormKind norm, const Partial *partials, const SegDesc *segs,
                          int32_t n_segs, const SegRange *ranges, int32_t n_tensors,
-                         Partial *seg_partials, double *totals, uint32_t *flags, bool deferred,
-                         hipStream_t stream) {
+                         Partial *seg_partials, double *totals, uint32_t *flags,
+                         const uint32_t *ctl, int32_t verdict_mode, hipStream_t stream) {
+    if (verdict_mode < kVerdictZero || verdict_mode > kVerdictCopy ||
+        (verdict_mode == kVerdictCopy && !ctl))
+        return hipErrorInvalidValue;
     hipError_t err = launch_segments(norm, partials, segs, n_segs, seg_partials, stream);
     if (err != hipSuccess)
         return err;
-    int32_t d = deferred ? 1 : 0;
-    void *params[] = {&seg_partials, &ranges, &n_tensors, &totals, &flags, &d};
+    void *params[] = {&seg_partials, &ranges, &n_tensors, &totals, &flags, &ctl, &verdict_mode};
     const void *fn = norm == kL1     ? reinterpret_cast<const void *>(&totals_kernel<kL1>)
                      : norm == kLinf ? reinterpret_cast<const void *>(&totals_kernel<kLinf>)
                                      : reinterpret_cast<const void *>(&totals_kernel<kL2>);
@@ -1260,15 +1291,17 @@ hipError_t launch_fused(const StepKind &kind, int groups, const TensorDesc *tens
                         const ChunkDesc *tiles, int32_t n_tiles, int32_t grid, uint64_t *slots,
                         uint32_t *ctl, uint32_t *flags, bool guarded, int32_t *nonfinite_out,
                         const StepArgs &args, const FinalizeArgs &fargs, double *ratio_out,
-                        double *norms_out, hipStream_t stream) {
+                        double *norms_out, const double *ext_totals, float *ext_scale,
+                        hipStream_t stream) {
     const void *fn = fused_fn(kind, groups);
     if (!fn)
         return hipErrorInvalidValue;
     StepArgs a = args;
     FinalizeArgs f = fargs;
     int32_t guard = guarded ? 1 : 0;
-    void *params[] = {&tensors, &tiles, &n_tiles, &slots, &ctl, &flags, &guard, &nonfinite_out,
-                      &a, &f, &ratio_out, &norms_out};
+    void *params[] = {&tensors, &tiles,     &n_tiles,   &slots,      &ctl,
+                      &flags,   &guard,     &nonfinite_out, &a,      &f,
+                      &ratio_out, &norms_out, &ext_totals, &ext_scale};
     return hipLaunchKernel(fn, dim3(grid), dim3(kBlock), params, 0, stream);
 }
 

@@ -151,6 +151,7 @@ __global__ __launch_bounds__(kBlock) void table_kernel(TableBatch b, StaticTable
         d.first_tile = 0;
         d.n_tiles = 0;
         d.out_index = i;
+        d.ext = -1;
         t.tensors[i] = d;
         t.ranges[0][i] = SegRange{r.first_seg, ns};
         t.ranges[1][i] = SegRange{r.first_cseg, ncs};
@@ -313,7 +314,7 @@ lamb_status lamb_step_static(const lamb_tensor *tensors, int32_t n_tensors, int3
     const int32_t n_moment = kind.deferred ? int32_t(n_coarse) : int32_t(n_chunks);
     const int32_t moment_elems = kind.deferred ? coarse : chunk;
     err = launch_moments(kind, t.tensors, moment_ids, moment_elems, t.partials, n_moment,
-                         two_pass_threads(moment_elems), t.flags, t.ctl, false, a, s);
+                         two_pass_threads(moment_elems), t.flags, t.ctl, kGuardNone, a, s);
     if (err != hipSuccess)
         return fail_hip(err, "launching the moment kernel");
     const int seg = kind.deferred ? 1 : 0;
@@ -323,7 +324,7 @@ lamb_status lamb_step_static(const lamb_tensor *tensors, int32_t n_tensors, int3
     if (err != hipSuccess)
         return fail_hip(err, "launching the finalize kernel");
     err = launch_apply(kind, t.tensors, t.ids, chunk, t.scale, int32_t(n_chunks),
-                       two_pass_threads(chunk), t.flags, t.ctl, false,
+                       two_pass_threads(chunk), t.flags, t.ctl, kGuardNone,
                        kind.deferred ? nonfinite_out : nullptr, nullptr, a, s);
     if (err != hipSuccess)
         return fail_hip(err, "launching the apply kernel");

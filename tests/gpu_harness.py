@@ -452,9 +452,10 @@ def run_config(cfg: int, steps: int, algo: str = "lamb", chunk_elems: int = 0,
         % (cfg, ps.name, algo, steps, chunk_elems, path))
     pair = Pair(paramsets.draw_params(ps, device=device), ps.wd_mask(), ps.g_dtype, algo,
                 chunk_elems, oracle_subset, path)
-    per, total, groups = _lib.lamb_plan_tiles(pair.plan)
-    log("  single-pass layers %d of %d, %d tiles of %d groups"
-        % (sum(1 for k in per if k), len(per), total, groups))
+    per, total, groups, elems = _lib.lamb_plan_tiles(pair.plan, True)
+    whole = sum(1 for e, x in zip(elems, pair.X) if e == x.numel())
+    log("  single-pass layers %d whole, %d split, of %d; %d tiles of %d groups"
+        % (whole, len(per) - whole, len(per), total, groups))
     rep = Report()
     hp = {"lamb": lamb_hp, "lars": lars_hp, "nlamb": nlamb_hp, "nnlamb": nlamb_hp}[algo](ps)
     try:

@@ -8,7 +8,7 @@
 namespace lamb_mi355x {
 
 hipError_t launch_moments(const StepKind &, const TensorDesc *, const int32_t *, int32_t,
-                          Partial *, int32_t, int32_t, uint32_t *, const uint32_t *, bool,
+                          Partial *, int32_t, int32_t, uint32_t *, const uint32_t *, int32_t,
                           const StepArgs &, hipStream_t) {
     return hipErrorNotSupported;
 }
@@ -20,13 +20,14 @@ hipError_t launch_finalize(NormKind, const TensorDesc *, int32_t, const Partial 
 }
 
 hipError_t launch_apply(const StepKind &, const TensorDesc *, const int32_t *, int32_t,
-                        const float *, int32_t, int32_t, uint32_t *, const uint32_t *, bool,
+                        const float *, int32_t, int32_t, uint32_t *, const uint32_t *, int32_t,
                         int32_t *, Partial *, const StepArgs &, hipStream_t) {
     return hipErrorNotSupported;
 }
 
 hipError_t launch_totals(NormKind, const Partial *, const SegDesc *, int32_t, const SegRange *,
-                         int32_t, Partial *, double *, uint32_t *, bool, hipStream_t) {
+                         int32_t, Partial *, double *, uint32_t *, const uint32_t *, int32_t,
+                         hipStream_t) {
     return hipErrorNotSupported;
 }
 
@@ -42,7 +43,8 @@ hipError_t launch_finite(bool, const TensorDesc *, const ChunkDesc *, int32_t, u
 
 hipError_t launch_fused(const StepKind &, int, const TensorDesc *, const ChunkDesc *, int32_t,
                         int32_t, uint64_t *, uint32_t *, uint32_t *, bool, int32_t *,
-                        const StepArgs &, const FinalizeArgs &, double *, double *, hipStream_t) {
+                        const StepArgs &, const FinalizeArgs &, double *, double *,
+                        const double *, float *, hipStream_t) {
     return hipErrorNotSupported;
 }
 

@@ -161,7 +161,7 @@ def test_null_plan_and_outputs(lib):
     assert lib.lamb_plan_set_bf16_copies(None, None) == _lib.LAMB_ENULL
     assert lib.lamb_plan_create(None, 1, 0, 0, 0, None) == _lib.LAMB_ENULL
     assert lib.lamb_plan_set_path(None, 0) == _lib.LAMB_ENULL
-    assert lib.lamb_plan_tiles(None, None, None, None) == _lib.LAMB_ENULL
+    assert lib.lamb_plan_tiles(None, None, None, None, None) == _lib.LAMB_ENULL
     assert lib.lamb_plan_check(None, None) == _lib.LAMB_ENULL
     per = (ctypes.c_double * 5)()
     steps = ctypes.c_int64()

@@ -318,8 +318,9 @@ def test_subnormal_and_zero_gradients():
 @pytest.mark.parametrize("groups", [8, 10])
 def test_single_pass_layout_and_rounds(groups):
     """The single pass runs in rounds of one workgroup per tile, four per CU.
-    A layer of exactly one round of tiles takes it, a layer of one element
-    more than a round of the wider tile takes the two-pass kernels; layers
+    A layer of exactly one round of tiles takes it whole; a layer of one
+    element more than a round of the wider tile puts its last round (from a
+    multiple of 1024 elements) on it and its head on the two-pass kernels; layers
     that leave a gap in a round (padded with empty entries) and a layer that
     fills the last round still match the oracle on every element. With a
     layer that only the 10240-element tile fits in a round, the plan picks
@@ -337,10 +338,13 @@ def test_single_pass_layout_and_rounds(groups):
     H.log("single-pass rounds: R=%d groups=%d sizes=%s" % (R, groups, sizes))
     pair = H.Pair(xs, wd, "bf16", "lamb", path="auto")
     try:
-        per, total, got = _lib.lamb_plan_tiles(pair.plan)
+        per, total, got, elems = _lib.lamb_plan_tiles(pair.plan, True)
         assert got == groups
-        want = [(n + T - 1) // T for n in sizes]
-        want[1] = 0
+        head = -(-(sizes[1] - R * T) // 1024) * 1024
+        want_elems = list(sizes)
+        want_elems[1] = sizes[1] - head
+        assert elems == want_elems and 0 < want_elems[1] <= R * T
+        want = [(n + T - 1) // T for n in want_elems]
         assert per == want
         assert total >= sum(want)
         for t in range(1, 3):

@@ -155,9 +155,11 @@ def test_skip_nonfinite_sequence(algo, g_dtype, path):
 
 @pytest.mark.parametrize("path", ["auto", "wide"])
 def test_skip_nonfinite_with_two_pass_layer(path):
-    """The single-pass skip mode with a layer too large for the single pass
-    (with either tile): the check's verdict also stops that layer's moment
-    and apply passes."""
+    """The single-pass skip mode with a layer larger than one round (with
+    either tile): its head takes a moment pass before the single pass and an
+    apply pass after it, and the check's verdict stops both, the apply pass
+    through the copy the totals kernel takes (the single pass rewrites the
+    epoch's verdict words as it ends)."""
     torch = H.torch_cuda()
     cus = torch.cuda.get_device_properties(0).multi_processor_count
     big = 4 * cus * 10240 + 1029
@@ -166,8 +168,8 @@ def test_skip_nonfinite_with_two_pass_layer(path):
     pair = _pair(xs, [True, True, False], "bf16", "lamb", path=path)
     flag = torch.full((1,), -1, dtype=torch.int32, device="cuda")
     try:
-        per, _, _ = _lib.lamb_plan_tiles(pair.plan)
-        assert per[0] == 0 and per[1] > 0 and per[2] > 0
+        per, _, _, elems = _lib.lamb_plan_tiles(pair.plan, True)
+        assert 0 < elems[0] < big and elems[1:] == [3000, 7] and min(per) > 0
         for t, kind in enumerate(["ok", "nan_big", "ok", "inf_small", "ok"], start=1):
             gs = _grads(rng, pair.X, "bf16")
             if kind == "nan_big":

@@ -83,8 +83,8 @@ def test_gpt_1p5b_lamb_every_tensor():
     the oracle element by element (x, m, v) and per tensor (trust ratio,
     ||x||, ||u||), one tensor at a time so that host memory stays bounded.
     The plan takes 10240-element tiles, which put the 10.24M-element FFN
-    layers on the single pass; the 80M-element token embedding takes the
-    two-pass kernels."""
+    layers on the single pass; the 80M-element token embedding puts its last
+    round on the single pass and its head on the two-pass kernels."""
     torch = H.torch_cuda()
     import oracle
     ps = paramsets.get(4)
@@ -92,9 +92,10 @@ def test_gpt_1p5b_lamb_every_tensor():
     pair = H.Pair(paramsets.draw_params(ps, device="cuda"), ps.wd_mask(), ps.g_dtype, "lamb",
                   oracle_subset=[])
     try:
-        per, _, groups = _lib.lamb_plan_tiles(pair.plan)
+        per, _, groups, elems = _lib.lamb_plan_tiles(pair.plan, True)
         assert groups == 10
-        assert [i for i, k in enumerate(per) if k == 0] == [0]  # the token embedding only
+        # only the token embedding is split between the two paths
+        assert [i for i, e in enumerate(elems) if e < pair.X[i].numel()] == [0]
         hp = H.lamb_hp(ps)
         x_old = [x.clone() for x in pair.X]
         pair.set_grads(paramsets.draw_grads(ps, 1, device="cuda"))

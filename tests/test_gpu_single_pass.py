@@ -32,9 +32,9 @@ def _run_path(cfg, path, steps=2):
 
 @pytest.mark.parametrize("path", ["auto", "wide"])
 def test_single_pass_agrees_with_two_pass(path):
-    """BERT-Base: 198 layers on the single pass (with either tile), the token
-    embedding on the two-pass kernels, against the two-pass path for
-    everything."""
+    """BERT-Base: 198 layers on the single pass (with either tile) and the
+    token embedding split between the two paths, against the two-pass path
+    for everything."""
     torch = H.torch_cuda()
     x1, m1, v1, r1, n1 = _run_path(1, path)
     x2, m2, v2, r2, n2 = _run_path(1, "two-pass")
