@@ -408,6 +408,19 @@ LAMB_API lamb_status lamb_step_finish(lamb_plan *plan, const lamb_hparams *hp, v
                                       double *norms_out, int32_t *nonfinite_out);
 
 /*
+ * Per-tile timeline of the single pass, for measurement. With `trace` a
+ * device buffer of 4 * n_tiles 64-bit words (lamb_plan_tiles), every later
+ * single-pass step of the plan writes for tile j (its index in the schedule,
+ * lamb_tile_schedule): trace[4 j] when the tile starts, [4 j + 1] when its
+ * reads and partial norms are done, [4 j + 2] when its layer's step scale is
+ * known and [4 j + 3] when its writes are issued, in ticks of the device's
+ * constant 100 MHz clock (entries of empty tiles are left as they are). NULL
+ * turns it off. The caller owns the buffer and must keep it valid while
+ * traced steps run. Errors: LAMB_ENULL (plan), LAMB_EALIGN.
+ */
+LAMB_API lamb_status lamb_plan_set_trace(lamb_plan *plan, uint64_t *trace);
+
+/*
  * Check of the two-pass path's recomputation (Algorithm 2's last line uses
  * one u for ||u_i|| and for the update; the apply pass recomputes u from the
  * stored moments instead of storing it). enable = 1 allocates one partial-norm

@@ -57,7 +57,8 @@ EXPORTS = ("lamb_plan_create", "lamb_plan_destroy", "lamb_plan_info",
            "lamb_sqrt_scaled_lr", "lamb_chunk_table", "lamb_plan_set_timing", "lamb_plan_timing",
            "lamb_plan_set_path", "lamb_plan_tiles", "lamb_plan_check", "lamb_tile_schedule",
            "lamb_step_partials", "lamb_step_finish", "lamb_plan_set_u_check",
-           "lamb_plan_u_partials", "lamb_step_static", "lamb_status_str", "lamb_last_error")
+           "lamb_plan_u_partials", "lamb_step_static", "lamb_plan_set_trace", "lamb_status_str",
+           "lamb_last_error")
 
 
 class LambError(RuntimeError):
@@ -129,6 +130,7 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
     lib.lamb_step_partials.argtypes = [vp, P(lamb_hparams), vp, vp]
     lib.lamb_step_finish.argtypes = [vp, P(lamb_hparams), vp, vp, vp, vp, vp]
     lib.lamb_plan_set_u_check.argtypes = [vp, i32]
+    lib.lamb_plan_set_trace.argtypes = [vp, vp]
     lib.lamb_plan_u_partials.argtypes = [vp, vp, i32, vp, vp, P(i32)]
     lib.lamb_step_static.argtypes = [P(lamb_tensor), i32, i32, i32, P(lamb_hparams), vp, vp, vp,
                                      vp]
@@ -425,3 +427,9 @@ def lamb_step_static(tensors: Sequence[Tuple[int, int, int, int, int, int]], g_d
     _check(load().lamb_step_static(arr, n, int(g_dtype), int(chunk_elems), ctypes.byref(hp),
                                    _vp(stream), _vp(ratio_out), _vp(norms_out),
                                    _vp(nonfinite_out)), "lamb_step_static")
+
+
+def lamb_plan_set_trace(plan: Plan, trace: int = 0) -> None:
+    """Per-tile clock stamps of later single-pass steps into ``trace`` (device
+    pointer to 4 x n_tiles uint64), or off (0)."""
+    _check(load().lamb_plan_set_trace(_vp(plan.handle), _vp(trace)), "lamb_plan_set_trace")

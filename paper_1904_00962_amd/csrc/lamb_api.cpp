@@ -76,6 +76,7 @@ struct lamb_plan {
     // partial norms, and the chunk count of the last step that filled them
     Partial *u_check = nullptr;
     int32_t u_check_chunks = 0;
+    uint64_t *trace = nullptr;      // caller's per-tile clock stamps (lamb_plan_set_trace)
     // timing hooks: up to kEvents events per recorded step, in launch order,
     // with the kernel kind of each interval
     std::vector<hipEvent_t> events;
@@ -220,7 +221,7 @@ hipError_t gated_fused_launch(int device, hipStream_t stream, const StepKind &ki
         return launch_fused(kind, plan->tile_groups, plan->fused_tensors, plan->tiles,
                             plan->n_tiles, grid, plan->slots, plan->ctl, plan->flags, guarded,
                             nonfinite_out, a, f, ratio_out, norms_out, plan->ext_totals,
-                            plan->scale, stream);
+                            plan->scale, plan->trace, stream);
     std::lock_guard<std::mutex> lock(g_gate_mutex);
     if (g_gates.size() <= size_t(device))
         g_gates.resize(size_t(device) + 1);
@@ -237,7 +238,7 @@ hipError_t gated_fused_launch(int device, hipStream_t stream, const StepKind &ki
     }
     err = launch_fused(kind, plan->tile_groups, plan->fused_tensors, plan->tiles, plan->n_tiles,
                        grid, plan->slots, plan->ctl, plan->flags, guarded, nonfinite_out, a, f,
-                       ratio_out, norms_out, plan->ext_totals, plan->scale, stream);
+                       ratio_out, norms_out, plan->ext_totals, plan->scale, plan->trace, stream);
     if (err != hipSuccess)
         return err;
     err = hipEventRecord(gate.done, stream);
@@ -651,19 +652,28 @@ lamb_status lamb_plan_create(const lamb_tensor *tensors, int32_t n_tensors,
     }
     // The tile shape (lamb_tile_schedule's rule over whole layers), then the
     // schedule: a layer of more tiles than a round keeps a head on the
-    // two-pass kernels and puts its last elements, at most one round of
-    // tiles from a multiple of kBlockElems, on the single pass.
+    // two-pass kernels and puts its last elements on the single pass, from a
+    // multiple of kBlockElems, in as many tiles as the largest layer that
+    // fits whole (one round if none does). Every tile of a layer must be
+    // resident at once, and work on other streams can withhold residency; a
+    // tail no larger than the plan's largest layer keeps that demand as it
+    // was (a tail of a whole round, on a plan whose layers take half of one,
+    // gave up its waits beside fp32 matrix products on another stream).
     st = lamb_tile_schedule(numel.data(), n_tensors, max_round, groups, 0, nullptr, nullptr,
                             nullptr, first_tile.data(), tile_count.data(), &n_entries, &round,
                             &groups);
     if (st != LAMB_OK)
         return st;
+    int64_t largest = 0;
+    for (int32_t i = 0; i < n_tensors; ++i)
+        largest = std::max<int64_t>(largest, tile_count[size_t(i)]);
     const int64_t round_elems = int64_t(max_round) * tile_elems(groups);
+    const int64_t tail_elems = (largest > 0 ? largest : max_round) * tile_elems(groups);
     std::vector<int64_t> head(size_t(n_tensors), 0), tail(size_t(n_tensors), 0);
     for (int32_t i = 0; i < n_tensors; ++i) {
         const int64_t n = numel[size_t(i)];
         if (n > round_elems)
-            head[size_t(i)] = (n - round_elems + kBlockElems - 1) / kBlockElems * kBlockElems;
+            head[size_t(i)] = (n - tail_elems + kBlockElems - 1) / kBlockElems * kBlockElems;
         tail[size_t(i)] = n - head[size_t(i)];
     }
     st = lamb_tile_schedule(tail.data(), n_tensors, max_round, groups, 0, nullptr, nullptr,
@@ -1582,6 +1592,15 @@ lamb_status lamb_plan_u_partials(lamb_plan *plan, void *stream, int32_t capacity
         err = hipStreamSynchronize(s);
     if (err != hipSuccess)
         return fail_hip(err, "copying the partial norms");
+    return LAMB_OK;
+}
+
+lamb_status lamb_plan_set_trace(lamb_plan *plan, uint64_t *trace) {
+    if (!plan)
+        return fail(LAMB_ENULL, "plan must not be NULL");
+    if (trace && (reinterpret_cast<uintptr_t>(trace) & 7u) != 0)
+        return fail(LAMB_EALIGN, "the trace buffer must be 8-byte aligned");
+    plan->trace = trace;
     return LAMB_OK;
 }
 

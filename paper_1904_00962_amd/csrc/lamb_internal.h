@@ -243,6 +243,10 @@ constexpr uint64_t kEmptySlot = ~uint64_t(0);
 // raised or not; the last workgroup writes it to `nonfinite_out` (may be
 // null). Every step's last workgroup clears the verdict word of the next
 // epoch.
+// `trace` non-null: every tile j of the step writes trace[4 j .. 4 j + 3], the
+// device's constant 100 MHz clock when the tile starts, when its reads and
+// partial norms are done, when its layer's scale is known and when its writes
+// are issued.
 // `groups` is the plan's tile shape, kTileGroups or kWideGroups. A layer
 // whose descriptor has ext >= 0 (the last part of a layer too large for one
 // round) combines the totals of its head, ext_totals[2 ext] and
@@ -253,7 +257,7 @@ hipError_t launch_fused(const StepKind &kind, int groups, const TensorDesc *tens
                         uint32_t *ctl, uint32_t *flags, bool guarded, int32_t *nonfinite_out,
                         const StepArgs &args, const FinalizeArgs &fargs, double *ratio_out,
                         double *norms_out, const double *ext_totals, float *ext_scale,
-                        hipStream_t stream);
+                        uint64_t *trace, hipStream_t stream);
 // Workgroups of the single-pass kernel for `kind` and tile shape `groups`
 // that fit on one CU at once.
 hipError_t fused_blocks_per_cu(const StepKind &kind, int groups, int *blocks);

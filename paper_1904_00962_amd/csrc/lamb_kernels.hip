@@ -837,7 +837,7 @@ void fused_kernel(const TensorDesc *__restrict__ tensors, const ChunkDesc *__res
                   int32_t *__restrict__ nonfinite_out,
                   StepArgs a, FinalizeArgs f, double *__restrict__ ratio_out,
                   double *__restrict__ norms_out, const double *__restrict__ ext_totals,
-                  float *__restrict__ ext_scale) {
+                  float *__restrict__ ext_scale, uint64_t *__restrict__ trace) {
     constexpr bool kV = kHasSecondMoment<kAlgo>;
     constexpr int kUnrollF = kFusedUnroll<kAlgo>;
     __shared__ uint32_t sh_epoch, sh_fault, sh_skip;
@@ -876,6 +876,9 @@ void fused_kernel(const TensorDesc *__restrict__ tensors, const ChunkDesc *__res
         if (c.len == 0)
             continue;  // an empty entry that pads a round
         const TensorDesc &t = tensors[c.tensor];
+        uint64_t stamp[3] = {0, 0, 0};  // the trace's first three clocks of this tile
+        if (trace)
+            stamp[0] = __builtin_amdgcn_s_memrealtime();
         gfloat *x = global_view(t.x);
         gfloat *m = global_view(t.m);
         gfloat *v = kV ? global_view(t.v) : nullptr;
@@ -964,6 +967,8 @@ void fused_kernel(const TensorDesc *__restrict__ tensors, const ChunkDesc *__res
         }
         block_combine<kNorm, kWaves>(sum_xx, sum_uu, &sh_tile);
         __syncthreads();
+        if (trace)
+            stamp[1] = __builtin_amdgcn_s_memrealtime();
         __builtin_amdgcn_s_setprio(0);
         p_j = -1;
         if (j + grid < n_tiles) {
@@ -1039,6 +1044,8 @@ void fused_kernel(const TensorDesc *__restrict__ tensors, const ChunkDesc *__res
         stop = __syncthreads_or(give_up) != 0;
         if (stop)
             break;
+        if (trace)
+            stamp[2] = __builtin_amdgcn_s_memrealtime();
 
         __builtin_amdgcn_s_setprio(3);
         // x - scale * u from LDS and the registers.
@@ -1070,6 +1077,12 @@ void fused_kernel(const TensorDesc *__restrict__ tensors, const ChunkDesc *__res
                     }
                 }
             }
+        }
+        if (trace && threadIdx.x == 0) {
+            trace[4 * j] = stamp[0];
+            trace[4 * j + 1] = stamp[1];
+            trace[4 * j + 2] = stamp[2];
+            trace[4 * j + 3] = __builtin_amdgcn_s_memrealtime();
         }
     }
 
@@ -1292,7 +1305,7 @@ hipError_t launch_fused(const StepKind &kind, int groups, const TensorDesc *tens
                         uint32_t *ctl, uint32_t *flags, bool guarded, int32_t *nonfinite_out,
                         const StepArgs &args, const FinalizeArgs &fargs, double *ratio_out,
                         double *norms_out, const double *ext_totals, float *ext_scale,
-                        hipStream_t stream) {
+                        uint64_t *trace, hipStream_t stream) {
     const void *fn = fused_fn(kind, groups);
     if (!fn)
         return hipErrorInvalidValue;
@@ -1301,7 +1314,7 @@ hipError_t launch_fused(const StepKind &kind, int groups, const TensorDesc *tens
     int32_t guard = guarded ? 1 : 0;
     void *params[] = {&tensors, &tiles,     &n_tiles,   &slots,      &ctl,
                       &flags,   &guard,     &nonfinite_out, &a,      &f,
-                      &ratio_out, &norms_out, &ext_totals, &ext_scale};
+                      &ratio_out, &norms_out, &ext_totals, &ext_scale, &trace};
     return hipLaunchKernel(fn, dim3(grid), dim3(kBlock), params, 0, stream);
 }
 

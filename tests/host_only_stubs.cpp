@@ -44,7 +44,7 @@ hipError_t launch_finite(bool, const TensorDesc *, const ChunkDesc *, int32_t, u
 hipError_t launch_fused(const StepKind &, int, const TensorDesc *, const ChunkDesc *, int32_t,
                         int32_t, uint64_t *, uint32_t *, uint32_t *, bool, int32_t *,
                         const StepArgs &, const FinalizeArgs &, double *, double *,
-                        const double *, float *, hipStream_t) {
+                        const double *, float *, uint64_t *, hipStream_t) {
     return hipErrorNotSupported;
 }
 
