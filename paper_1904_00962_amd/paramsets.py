@@ -234,24 +234,3 @@ def host_array(t) -> np.ndarray:
         return t.view(torch.int16).cpu().numpy().view(np.uint16)
     return t.cpu().numpy()
 
-
-def bf16_bits_to_f32(bits: np.ndarray) -> np.ndarray:
-    """Exact widening of bf16 bit patterns to fp32 (for building test inputs)."""
-    return (bits.astype(np.uint32) << 16).view(np.float32)
-
-
-def f32_to_bf16_bits(a: np.ndarray) -> np.ndarray:
-    """Round-to-nearest-even cast of fp32 values to bf16 bit patterns."""
-    torch = _torch()
-    t = torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32))
-    return t.to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
-
-
-def random_case(rng: np.random.Generator, numels: Sequence[int], sigma_x: float = 0.02,
-                sigma_g: float = 1e-3, g_dtype: str = "f32"):
-    """Small ad-hoc case for edge tests: (x list, g list) drawn from ``rng``."""
-    xs = [(rng.standard_normal(n) * sigma_x).astype(np.float32) for n in numels]
-    gs = [(rng.standard_normal(n) * sigma_g).astype(np.float32) for n in numels]
-    if g_dtype == "bf16":
-        gs = [f32_to_bf16_bits(g) for g in gs]
-    return xs, gs

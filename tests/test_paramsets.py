@@ -54,7 +54,8 @@ def test_bf16_gradients_round_to_nearest_even():
     for spec in ps.tensors[:3]:
         torch.randn(spec.numel, generator=gen)
     ref = (torch.randn(1024, generator=gen) * ps.sigma_g).numpy()
-    widened = paramsets.bf16_bits_to_f32(bits)
+    widened = (bits.astype(np.uint32) << 16).view(np.float32)  # exact widening
     # nearest bf16: error at most half a bf16 ulp (2^-8 relative), never more
     assert np.all(np.abs(widened - ref) <= np.abs(ref) * 2.0 ** -8)
-    assert np.array_equal(paramsets.f32_to_bf16_bits(ref), bits)
+    rounded = torch.from_numpy(ref).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(rounded, bits)
