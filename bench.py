@@ -306,7 +306,7 @@ def main() -> int:
     ap.add_argument("--algo", choices=("lamb", "lars", "nlamb", "nnlamb"), default="lamb")
     ap.add_argument("--chunk", type=int, default=0, help="elements per chunk (0 = default)")
     ap.add_argument("--path", choices=("auto", "two-pass"), default="auto",
-                    help="auto: layers of up to 8M elements take the single-pass kernel")
+                    help="auto: the single-pass kernel for every layer that fits one round of tiles and for the last tiles of larger ones")
     ap.add_argument("--norm", choices=("l2", "l1", "linf"), default="l2",
                     help="layer norm (Appendix F)")
     ap.add_argument("--grad-scale", type=float, default=1.0)

@@ -120,8 +120,10 @@ typedef enum lamb_norm {
  *                      10), read by lamb_plan_create, fixes the tile instead;
  *                      tests use it to run the wider tile on small layers
  *                      (any other value fails with LAMB_EINVAL). A larger
- *                      layer puts its last elements, one round of tiles from
- *                      a multiple of 1024, on the single pass and its head on
+ *                      layer puts its last elements on the single pass (as
+ *                      many tiles as the plan's largest whole layer takes,
+ *                      or one round when no whole layer is on it; its head
+ *                      ends at a multiple of 1024 elements) and its head on
  *                      the two-pass kernels: a moment pass and a totals
  *                      kernel before the single pass, which adds the head's
  *                      partial norms into the layer's, and an apply pass

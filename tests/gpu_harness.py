@@ -47,12 +47,14 @@ class Report:
     max_abs: float = 0.0
     max_rel: float = 0.0
     n_rel_over: int = 0
+    max_ratio: float = 0.0  # worst relative error of a trust ratio or norm
 
     def merge(self, other: "Report") -> None:
         self.max_err = max(self.max_err, other.max_err)
         self.max_abs = max(self.max_abs, other.max_abs)
         self.max_rel = max(self.max_rel, other.max_rel)
         self.n_rel_over += other.n_rel_over
+        self.max_ratio = max(self.max_ratio, other.max_ratio)
 
 
 def compare_state(gpu: np.ndarray, ref: np.ndarray, what: str, tol: float = STATE_TOL) -> Report:
@@ -345,9 +347,10 @@ class Pair:
         idx = np.asarray(self.subset, dtype=np.int64)
         if idx.size == 0 or np.all(np.isnan(ref)):
             return rep
-        compare_ratios(ratio[idx], ref[:, 0], label + " trust ratio", ratio_tol)
-        compare_ratios(norms[idx, 0], ref[:, 1], label + " ||x||", RATIO_TOL)
-        compare_ratios(norms[idx, 1], ref[:, 2], label + " ||u||", ratio_tol)
+        rep.max_ratio = max(
+            compare_ratios(ratio[idx], ref[:, 0], label + " trust ratio", ratio_tol),
+            compare_ratios(norms[idx, 0], ref[:, 1], label + " ||x||", RATIO_TOL),
+            compare_ratios(norms[idx, 1], ref[:, 2], label + " ||u||", ratio_tol))
         return rep
 
     def ratio_tolerances(self, hp, hg) -> np.ndarray:
@@ -463,8 +466,9 @@ def run_config(cfg: int, steps: int, algo: str = "lamb", chunk_elems: int = 0,
             hg = pair.set_grads(paramsets.draw_grads(ps, t, device=device))
             ref = step_both(pair, algo, hg, hp, t)
             r = pair.compare(ref, "cfg%d %s step %d" % (cfg, algo, t))
-            log("  step %d: max err %.3e, max abs %.3e, max rel %.3e, rel>1e-5: %d"
-                % (t, r.max_err, r.max_abs, r.max_rel, r.n_rel_over))
+            log("  step %d: max err %.3e, max abs %.3e, max rel %.3e, rel>1e-5: %d, "
+                "ratio/norm rel %.3e" % (t, r.max_err, r.max_abs, r.max_rel, r.n_rel_over,
+                                         r.max_ratio))
             rep.merge(r)
     finally:
         pair.close()
