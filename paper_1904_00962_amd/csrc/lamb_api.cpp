@@ -668,6 +668,10 @@ lamb_status lamb_plan_create(const lamb_tensor *tensors, int32_t n_tensors,
     for (int32_t i = 0; i < n_tensors; ++i)
         largest = std::max<int64_t>(largest, tile_count[size_t(i)]);
     const int64_t round_elems = int64_t(max_round) * tile_elems(groups);
+    // the single pass addresses a layer's elements with 32-bit byte offsets
+    if (round_elems > (int64_t(1) << 29))
+        return fail(LAMB_EINVAL, "%d single-pass workgroups: a round of tiles exceeds 2^29 elements",
+                    max_round);
     const int64_t tail_elems = (largest > 0 ? largest : max_round) * tile_elems(groups);
     std::vector<int64_t> head(size_t(n_tensors), 0), tail(size_t(n_tensors), 0);
     for (int32_t i = 0; i < n_tensors; ++i) {

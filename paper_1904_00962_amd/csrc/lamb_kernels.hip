@@ -85,6 +85,17 @@ __device__ __forceinline__ void store4(gfloat *p, f32x4 v) {
     stream_store((LAMB_GLOBAL f32x4 *)p, v);
 }
 
+// Element i of a float array as a 32-bit byte offset from a uniform base, so
+// that the loads and stores take the base in scalar registers and one VGPR of
+// offset (arrays of the single pass stay far below 4 GiB).
+__device__ __forceinline__ f32x4 load4_at(gcfloat *base, uint32_t i) {
+    return stream_load((LAMB_GLOBAL const f32x4 *)((LAMB_GLOBAL const char *)base + i * 4u));
+}
+
+__device__ __forceinline__ void store4_at(gfloat *base, uint32_t i, f32x4 v) {
+    stream_store((LAMB_GLOBAL f32x4 *)((LAMB_GLOBAL char *)base + i * 4u), v);
+}
+
 // The gradient of one chunk: fp32, or bf16 bit patterns that widen exactly
 // (a bf16 is the top half of an fp32), multiplied by the step's grad_scale.
 template <bool kBf16>
@@ -102,6 +113,22 @@ struct GradView {
             r = __uint_as_float(uint32_t(((gcbf16 *)base)[i]) << 16);
         else
             r = ((gcfloat *)base)[i];
+        return r * scale;
+    }
+
+    // elements i..i+3 at a 32-bit byte offset, i a multiple of 4
+    __device__ __forceinline__ f32x4 at4_off(uint32_t i) const {
+        f32x4 r;
+        if constexpr (kBf16) {
+            const u32x2 w = stream_load(
+                (LAMB_GLOBAL const u32x2 *)((LAMB_GLOBAL const char *)base + i * 2u));
+            r.x = __uint_as_float(w.x << 16);
+            r.y = __uint_as_float(w.x & 0xffff0000u);
+            r.z = __uint_as_float(w.y << 16);
+            r.w = __uint_as_float(w.y & 0xffff0000u);
+        } else {
+            r = load4_at((gcfloat *)base, i);
+        }
         return r * scale;
     }
 
@@ -785,10 +812,15 @@ constexpr int kPollSleep = 8;
 // faster on BERT-Large, 0.5-0.6% on LARS; within 0.5% on the other sets).
 // Before it waits, a workgroup loads group 0 of its next tile, so that HBM
 // keeps streaming through the wait (0.2-0.55% faster; 16 more VGPRs).
-// Float4 groups each thread of the single pass loads per trip: one for the
-// LAMB family (four streams; two were 0.3-1% slower, a round's resident tiles
-// already keep enough loads in flight), two for LARS (three streams; one was
-// 3-5% slower).
+// Float4 groups each thread of the single pass uses per trip: one for the
+// LAMB family (four streams; two were 0.3-1% slower), two for LARS (three
+// streams; one was 3-5% slower). On a full tile the next trip's groups are
+// loaded before this trip's are used, so a wave always has loads in flight
+// (same-box A/B against loading each trip after the last: BERT-Large 0.25%
+// faster, its LARS step 3.9%, BERT-Base 1.1%, ResNet-50 1.7% and 0.75% for
+// LARS, the 1.5B set 0.8%; two trips ahead was slower on all but ResNet-50).
+// Every load and store of the single pass addresses its array as a uniform
+// base plus a 32-bit byte offset (one VGPR instead of a 64-bit address).
 template <int kAlgo>
 constexpr int kFusedUnroll = kAlgo == kLars ? 2 : 1;
 static_assert(kTileGroups % 2 == 0 && kWideGroups % 2 == 0,
@@ -863,9 +895,9 @@ void fused_kernel(const TensorDesc *__restrict__ tensors, const ChunkDesc *__res
     bool stop = sh_fault != 0 || sh_skip != 0;
 
     const int32_t grid = static_cast<int32_t>(gridDim.x);
-    // Group 0 of this workgroup's next tile, loaded before the current tile
-    // waits for its layer's scale, so that HBM keeps streaming through the
-    // wait. p_j: the entry it belongs to (-1: none for this thread).
+    // Group 0 of this workgroup's next tile (when that tile is full), loaded
+    // before the current tile waits for its layer's scale, so that HBM keeps
+    // streaming through the wait. p_j: the entry it belongs to (-1: none).
     f32x4 px = {0.0f, 0.0f, 0.0f, 0.0f}, pg = px, pm = px, pv = px;
     int32_t p_j = -1;
     for (int32_t r = 0; !stop; ++r) {
@@ -886,13 +918,13 @@ void fused_kernel(const TensorDesc *__restrict__ tensors, const ChunkDesc *__res
         const float lam = t.wd ? a.weight_decay : 0.0f;
         // Group k of this thread: 4 elements from `first`, `valid` (0-4) of them
         // inside the layer.
-        auto group = [&](int k, int64_t &first, int &valid) {
+        auto group = [&](int k, uint32_t &first, int &valid) {
             // Tile i of a layer of T tiles holds its 1024-element blocks i, i + T,
             // i + 2T, ...: at any moment the layer's tiles stream one dense
             // stretch of it.
-            const int64_t block = int64_t(k) * t.n_tiles + (j - t.first_tile);
-            first = block * (4 * kBlock) + 4 * threadIdx.x;
-            const int64_t left = t.numel - first;
+            const uint32_t block = uint32_t(k) * uint32_t(t.n_tiles) + uint32_t(j - t.first_tile);
+            first = block * (4u * kBlock) + 4u * threadIdx.x;
+            const int64_t left = t.numel - int64_t(first);
             valid = left >= 4 ? 4 : left > 0 ? int(left) : 0;
         };
 
@@ -900,69 +932,141 @@ void fused_kernel(const TensorDesc *__restrict__ tensors, const ChunkDesc *__res
         f32x4 us[kGroups];
         f32x4 x_keep[kInRegs > 0 ? kInRegs : 1];
         double sum_xx = 0.0, sum_uu = 0.0;
+        if (c.len == kGroups * 4 * kBlock) {
+            // A full tile: every group is whole, so every load is issued
+            // unconditionally and the next trip's groups are in flight while
+            // this trip's are used.
+            auto fetch = [&](int k, f32x4 &xr, f32x4 &gr, f32x4 &mr, f32x4 &vr, uint32_t &at) {
+                int whole;
+                group(k, at, whole);
+                xr = load4_at(x, at);
+                gr = g.at4_off(at);
+                mr = load4_at(m, at);
+                vr = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+                if constexpr (kV)
+                    vr = load4_at(v, at);
+            };
+            // A ring of two trips' groups: the next trip's loads are issued before
+            // this trip's groups are used.
+            constexpr int kAhead = kUnrollF;
+            constexpr int kRing = kAhead + kUnrollF;
+            f32x4 bx[kRing], bg[kRing], bm[kRing], bv[kRing];
+            uint32_t bat[kRing];
 #pragma unroll
-        for (int k0 = 0; k0 < kGroups; k0 += kUnrollF) {
-            f32x4 xr[kUnrollF], gr[kUnrollF], mr[kUnrollF], vr[kUnrollF];
-            int64_t at[kUnrollF];
-            int ok[kUnrollF];
-#pragma unroll
-            for (int k = 0; k < kUnrollF; ++k) {
-                group(k0 + k, at[k], ok[k]);
-                xr[k] = gr[k] = mr[k] = vr[k] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-                if (k0 + k == 0 && p_j == j) {
-                    xr[k] = px;
-                    gr[k] = pg;
-                    mr[k] = pm;
-                    vr[k] = pv;
-                } else if (ok[k] == 4) {
-                    xr[k] = load4(x + at[k]);
-                    gr[k] = g.at4(at[k]);
-                    mr[k] = load4(m + at[k]);
-                    if constexpr (kV)
-                        vr[k] = load4(v + at[k]);
-                } else if (ok[k] > 0) {  // the layer's last, partial group
-                    for (int e = 0; e < ok[k]; ++e) {
-                        xr[k][e] = x[at[k] + e];
-                        gr[k][e] = g.at(at[k] + e);
-                        mr[k][e] = m[at[k] + e];
-                        if constexpr (kV)
-                            vr[k][e] = v[at[k] + e];
-                    }
+            for (int k = 0; k < kAhead && k < kGroups; ++k) {
+                if (k == 0 && p_j == j) {
+                    int whole;
+                    group(0, bat[0], whole);
+                    bx[0] = px;
+                    bg[0] = pg;
+                    bm[0] = pm;
+                    bv[0] = pv;
+                } else {
+                    fetch(k, bx[k % kRing], bg[k % kRing], bm[k % kRing], bv[k % kRing],
+                          bat[k % kRing]);
                 }
             }
 #pragma unroll
-            for (int k = 0; k < kUnrollF; ++k) {
-                f32x4 ur = {0.0f, 0.0f, 0.0f, 0.0f};
-                if (ok[k] > 0) {
+            for (int k0 = 0; k0 < kGroups; k0 += kUnrollF) {
+#pragma unroll
+                for (int k = 0; k < kUnrollF; ++k) {
+                    const int q = k0 + kAhead + k;
+                    if (q < kGroups)
+                        fetch(q, bx[q % kRing], bg[q % kRing], bm[q % kRing], bv[q % kRing],
+                              bat[q % kRing]);
+                }
+#pragma unroll
+                for (int k = 0; k < kUnrollF; ++k) {
+                    const int q = (k0 + k) % kRing;
+                    f32x4 xr = bx[q], gr = bg[q], mr = bm[q], vr = bv[q];
+                    f32x4 ur;
 #pragma unroll
                     for (int e = 0; e < 4; ++e) {
-                        if (e < ok[k]) {
-                            float me = mr[k][e], ve = vr[k][e];
-                            new_moments<kAlgo>(xr[k][e], gr[k][e], lam, me, ve, a);
-                            ur[e] = direction<kAlgo>(xr[k][e], gr[k][e], me, ve, lam, a);
-                            sum_xx = norm_add<kNorm>(sum_xx, xr[k][e]);
-                            sum_uu = norm_add<kNorm>(sum_uu, ur[e]);
-                            mr[k][e] = me;
-                            vr[k][e] = ve;
-                        }
+                        float me = mr[e], ve = vr[e];
+                        new_moments<kAlgo>(xr[e], gr[e], lam, me, ve, a);
+                        ur[e] = direction<kAlgo>(xr[e], gr[e], me, ve, lam, a);
+                        sum_xx = norm_add<kNorm>(sum_xx, xr[e]);
+                        sum_uu = norm_add<kNorm>(sum_uu, ur[e]);
+                        mr[e] = me;
+                        vr[e] = ve;
                     }
-                    if (ok[k] == 4) {
-                        store4(m + at[k], mr[k]);
+                    store4_at(m, bat[q], mr);
+                    if constexpr (kV)
+                        store4_at(v, bat[q], vr);
+                    if (k0 + k < kInLds)
+                        sh_x[k0 + k][threadIdx.x] = xr;
+                    else
+                        x_keep[k0 + k - kInLds] = xr;
+                    us[k0 + k] = ur;
+                }
+            }
+        } else {
+            // A tile that is not full (the layer ends inside it): groups past
+            // the layer's end hold nothing, and one group may be partial.
+#pragma unroll
+            for (int k0 = 0; k0 < kGroups; k0 += kUnrollF) {
+                f32x4 xr[kUnrollF], gr[kUnrollF], mr[kUnrollF], vr[kUnrollF];
+                uint32_t at[kUnrollF];
+                int ok[kUnrollF];
+#pragma unroll
+                for (int k = 0; k < kUnrollF; ++k) {
+                    group(k0 + k, at[k], ok[k]);
+                    xr[k] = gr[k] = mr[k] = vr[k] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+                    if (k0 + k == 0 && p_j == j) {
+                        xr[k] = px;
+                        gr[k] = pg;
+                        mr[k] = pm;
+                        vr[k] = pv;
+                    } else if (ok[k] == 4) {
+                        xr[k] = load4_at(x, at[k]);
+                        gr[k] = g.at4_off(at[k]);
+                        mr[k] = load4_at(m, at[k]);
                         if constexpr (kV)
-                            store4(v + at[k], vr[k]);
-                    } else {
+                            vr[k] = load4_at(v, at[k]);
+                    } else if (ok[k] > 0) {  // the layer's last, partial group
                         for (int e = 0; e < ok[k]; ++e) {
-                            m[at[k] + e] = mr[k][e];
+                            xr[k][e] = x[at[k] + e];
+                            gr[k][e] = g.at(at[k] + e);
+                            mr[k][e] = m[at[k] + e];
                             if constexpr (kV)
-                                v[at[k] + e] = vr[k][e];
+                                vr[k][e] = v[at[k] + e];
                         }
                     }
                 }
-                if (k0 + k < kInLds)
-                    sh_x[k0 + k][threadIdx.x] = xr[k];
-                else
-                    x_keep[k0 + k - kInLds] = xr[k];
-                us[k0 + k] = ur;
+#pragma unroll
+                for (int k = 0; k < kUnrollF; ++k) {
+                    f32x4 ur = {0.0f, 0.0f, 0.0f, 0.0f};
+                    if (ok[k] > 0) {
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            if (e < ok[k]) {
+                                float me = mr[k][e], ve = vr[k][e];
+                                new_moments<kAlgo>(xr[k][e], gr[k][e], lam, me, ve, a);
+                                ur[e] = direction<kAlgo>(xr[k][e], gr[k][e], me, ve, lam, a);
+                                sum_xx = norm_add<kNorm>(sum_xx, xr[k][e]);
+                                sum_uu = norm_add<kNorm>(sum_uu, ur[e]);
+                                mr[k][e] = me;
+                                vr[k][e] = ve;
+                            }
+                        }
+                        if (ok[k] == 4) {
+                            store4_at(m, at[k], mr[k]);
+                            if constexpr (kV)
+                                store4_at(v, at[k], vr[k]);
+                        } else {
+                            for (int e = 0; e < ok[k]; ++e) {
+                                m[at[k] + e] = mr[k][e];
+                                if constexpr (kV)
+                                    v[at[k] + e] = vr[k][e];
+                            }
+                        }
+                    }
+                    if (k0 + k < kInLds)
+                        sh_x[k0 + k][threadIdx.x] = xr[k];
+                    else
+                        x_keep[k0 + k - kInLds] = xr[k];
+                    us[k0 + k] = ur;
+                }
             }
         }
         block_combine<kNorm, kWaves>(sum_xx, sum_uu, &sh_tile);
@@ -974,18 +1078,16 @@ void fused_kernel(const TensorDesc *__restrict__ tensors, const ChunkDesc *__res
         if (j + grid < n_tiles) {
             const int32_t jn = j + grid;
             const ChunkDesc cn = tiles[jn];
-            if (cn.len != 0) {
+            if (cn.len == kGroups * 4 * kBlock) {  // a full tile: block 0 is whole
                 const TensorDesc &tn = tensors[cn.tensor];
                 // block 0 of tile jn - first_tile of its layer
-                const int64_t at0 = int64_t(jn - tn.first_tile) * (4 * kBlock) + 4 * threadIdx.x;
-                if (tn.numel - at0 >= 4) {
-                    px = load4(global_view(tn.x) + at0);
-                    pg = GradView<kBf16>(tn.g, 0, a.grad_scale).at4(at0);
-                    pm = load4(global_view(tn.m) + at0);
-                    if constexpr (kV)
-                        pv = load4(global_view(tn.v) + at0);
-                    p_j = jn;
-                }
+                const uint32_t at0 = uint32_t(jn - tn.first_tile) * (4u * kBlock) + 4u * threadIdx.x;
+                px = load4_at(global_view(tn.x), at0);
+                pg = GradView<kBf16>(tn.g, 0, a.grad_scale).at4_off(at0);
+                pm = load4_at(global_view(tn.m), at0);
+                if constexpr (kV)
+                    pv = load4_at(global_view(tn.v), at0);
+                p_j = jn;
             }
         }
 
@@ -1053,7 +1155,7 @@ void fused_kernel(const TensorDesc *__restrict__ tensors, const ChunkDesc *__res
         gbf16 *copy = t.x_copy ? (gbf16 *)t.x_copy : nullptr;
 #pragma unroll
         for (int k = 0; k < kGroups; ++k) {
-            int64_t at;
+            uint32_t at;
             int valid;
             group(k, at, valid);
             if (valid > 0) {
@@ -1063,11 +1165,12 @@ void fused_kernel(const TensorDesc *__restrict__ tensors, const ChunkDesc *__res
                 for (int e = 0; e < 4; ++e)
                     xn[e] = fmaf(-s, us[k][e], xo[e]);
                 if (valid == 4) {
-                    store4(x + at, xn);
+                    store4_at(x, at, xn);
                     if (copy) {
                         const u32x2 packed = {bf16_bits(xn[0]) | (bf16_bits(xn[1]) << 16),
                                               bf16_bits(xn[2]) | (bf16_bits(xn[3]) << 16)};
-                        stream_store((LAMB_GLOBAL u32x2 *)(copy + at), packed);
+                        stream_store((LAMB_GLOBAL u32x2 *)((LAMB_GLOBAL char *)copy + at * 2u),
+                                     packed);
                     }
                 } else {
                     for (int e = 0; e < valid; ++e) {
