@@ -1012,12 +1012,7 @@ void fused_kernel(const TensorDesc *__restrict__ tensors, const ChunkDesc *__res
                 for (int k = 0; k < kUnrollF; ++k) {
                     group(k0 + k, at[k], ok[k]);
                     xr[k] = gr[k] = mr[k] = vr[k] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-                    if (k0 + k == 0 && p_j == j) {
-                        xr[k] = px;
-                        gr[k] = pg;
-                        mr[k] = pm;
-                        vr[k] = pv;
-                    } else if (ok[k] == 4) {
+                    if (ok[k] == 4) {
                         xr[k] = load4_at(x, at[k]);
                         gr[k] = g.at4_off(at[k]);
                         mr[k] = load4_at(m, at[k]);
