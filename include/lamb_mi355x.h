@@ -213,8 +213,10 @@ typedef struct lamb_hparams {
  *                given chunk size and agree across sizes to rounding.
  *   out          receives the plan
  * Errors: LAMB_ENULL (tensors/out/x/g/m, or v for LAMB), LAMB_EINVAL (sizes,
- * dtype, algo, reserved != 0), LAMB_EALIGN, LAMB_EOVERLAP, LAMB_ENOMEM,
- * LAMB_EHIP (device allocation or copy failed).
+ * dtype, algo, reserved != 0, or a device whose round of single-pass tiles
+ * would exceed 2^29 elements, which the kernel's 32-bit offsets cannot
+ * address), LAMB_EALIGN, LAMB_EOVERLAP, LAMB_ENOMEM, LAMB_EHIP (device
+ * allocation or copy failed).
  */
 LAMB_API lamb_status lamb_plan_create(const lamb_tensor *tensors, int32_t n_tensors,
                              int32_t g_dtype, int32_t algo,
