@@ -142,7 +142,8 @@ typedef enum lamb_norm {
  * skip_nonfinite = 1 on LAMB_PATH_AUTO (with any layer on the single pass)
  * first reads every g once to take the step's verdict, then runs the same
  * kernels as a direct step, which change nothing when the verdict is
- * raised; the single pass runs last and reports the verdict. On
+ * raised; the single pass reports the verdict (the heads' apply pass after
+ * it reads a copy the totals kernel took). On
  * LAMB_PATH_TWO_PASS it takes the deferred two-pass kernels: a read-only
  * moment pass, then an apply pass that writes x, m, v unless the verdict
  * is raised.
